@@ -1,0 +1,141 @@
+"""Plain CPU oracle for the TVL GEMV path (ctypes over ``oracle.c``).
+
+TEST INFRASTRUCTURE.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+benchmark's ``cpu_baseline`` leg may import this package.  It shares no code
+with the HIP library and never imports it.
+
+Every function here marshals numpy arrays into the C oracle; the arithmetic is
+in ``oracle.c``.  The definitions cited there are from Kilictas & Alpay,
+arXiv 2601.03324: the GEMV of Sec. 6.1 (naive loop and the GEMV listing,
+row-major ``w + i*n + j``), its traffic/FLOP model in Sec. 3.1, and the
+accepted summation-order drift of Sec. 5.2.
+"""
+from __future__ import annotations
+
+import contextlib
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+CFLAGS = ["-std=c99", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
+
+
+def build(force: bool = True) -> str:
+    """Compile ``oracle.c`` with gcc into ``liboracle.so`` next to it."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def load(path: str) -> ctypes.CDLL:
+    """Open an oracle shared library at ``path`` and declare its signatures."""
+    L = ctypes.CDLL(path)
+    P, I64, D = ctypes.c_void_p, ctypes.c_int64, ctypes.c_double
+    L.oracle_f16_to_f64.argtypes = [ctypes.c_uint16]
+    L.oracle_f16_to_f64.restype = D
+    for name in ("oracle_gemv_f32", "oracle_gemv_f16"):
+        fn = getattr(L, name)
+        fn.argtypes = [P, I64, P, I64, I64, P, P]
+        fn.restype = None
+    L.oracle_check.argtypes = [P, P, P, I64, D, P, P, P]
+    L.oracle_check.restype = I64
+    return L
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        _lib = load(_LIB)
+    return _lib
+
+
+@contextlib.contextmanager
+def using(path: str):
+    """Temporarily route every call of this module to the library at ``path``
+    (the pin suite uses it to show that a deliberately broken oracle fails)."""
+    global _lib
+    saved = _lib
+    _lib = load(path)
+    try:
+        yield _lib
+    finally:
+        _lib = saved
+
+
+def _ptr(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+def _rows(W: np.ndarray, K: int | None):
+    if W.ndim != 2 or not W.flags.c_contiguous:
+        raise ValueError("W must be a C-contiguous 2-D array [M, ldw]")
+    M, ldw = W.shape
+    K = ldw if K is None else int(K)
+    if not (0 <= K <= ldw):
+        raise ValueError("need 0 <= K <= ldw")
+    return M, ldw, K
+
+
+def gemv_f32(W: np.ndarray, x: np.ndarray, K: int | None = None):
+    """Return (y, S) in float64 for fp32 W [M, ldw] (first K columns used)."""
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    M, ldw, K = _rows(W, K)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.shape[0] < K:
+        raise ValueError("x shorter than K")
+    y = np.empty(M, dtype=np.float64)
+    S = np.empty(M, dtype=np.float64)
+    lib().oracle_gemv_f32(_ptr(W), ldw, _ptr(x), M, K, _ptr(y), _ptr(S))
+    return y, S
+
+
+def gemv_f16(W_bits: np.ndarray, x: np.ndarray, K: int | None = None):
+    """Return (y, S) in float64 for binary16 W given as uint16 bit patterns."""
+    W_bits = np.ascontiguousarray(W_bits)
+    if W_bits.dtype == np.float16:
+        W_bits = W_bits.view(np.uint16)
+    if W_bits.dtype != np.uint16:
+        raise ValueError("W_bits must be uint16 (binary16 bit patterns)")
+    M, ldw, K = _rows(W_bits, K)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.shape[0] < K:
+        raise ValueError("x shorter than K")
+    y = np.empty(M, dtype=np.float64)
+    S = np.empty(M, dtype=np.float64)
+    lib().oracle_gemv_f16(_ptr(W_bits), ldw, _ptr(x), M, K, _ptr(y), _ptr(S))
+    return y, S
+
+
+def f16_to_f64(bits: int) -> float:
+    return lib().oracle_f16_to_f64(int(bits) & 0xFFFF)
+
+
+def check(y_gpu: np.ndarray, y_ref: np.ndarray, S: np.ndarray, tol: float):
+    """Normalised parity check.  Returns dict(bad, max_err, argmax, mean_err)."""
+    y_gpu = np.ascontiguousarray(y_gpu, dtype=np.float32)
+    y_ref = np.ascontiguousarray(y_ref, dtype=np.float64)
+    S = np.ascontiguousarray(S, dtype=np.float64)
+    M = y_gpu.shape[0]
+    if y_ref.shape[0] != M or S.shape[0] != M:
+        raise ValueError("length mismatch")
+    mx = ctypes.c_double()
+    am = ctypes.c_int64()
+    mean = ctypes.c_double()
+    bad = lib().oracle_check(_ptr(y_gpu), _ptr(y_ref), _ptr(S), M, float(tol),
+                             ctypes.addressof(mx), ctypes.addressof(am),
+                             ctypes.addressof(mean))
+    return {"bad": int(bad), "max_err": mx.value, "argmax": am.value,
+            "mean_err": mean.value}

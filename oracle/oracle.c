@@ -1,0 +1,136 @@
+/*
+ * oracle.c -- the plain CPU oracle for the TVL GEMV path.
+ *
+ * TEST INFRASTRUCTURE.  Only the test suite, the package smoke check and the
+ * benchmark's CPU-baseline leg may load or call this file.  The product path
+ * (the HIP library under paper_2601_03324_amd/) never includes, links or calls
+ * it, and this file includes no HIP header and no product source.
+ *
+ * What it computes (Kilictas & Alpay, "Bare-Metal Tensor Virtualization",
+ * arXiv 2601.03324):
+ *
+ *   y = W x, W row-major with row i at W + i*ldw  (Sec. 6.1, the naive loop
+ *   y[i] += W[i][j] * x[j] and the GEMV listing xout = W @ x with the weight
+ *   for (i, j) at w + i*n + j; Sec. 3.1 Roofline: one product and one add per
+ *   weight).
+ *
+ * The paper's NEON kernel only reorders this sum (Sec. 5.2 says reordered
+ * fused multiply-add accumulation drifts from scalar accumulation and that
+ * this drift is accepted).  So the oracle is the plain definition, written as
+ * the naive loop, in double precision:
+ *
+ *   - each product w*x of an fp32 (24-bit significand) or fp16 (11-bit) weight
+ *     and an fp32 x is exact in double (at most 48 significand bits < 53);
+ *   - the only rounding is the sequential double sum over ascending j, so
+ *     |acc - exact| <= (K-1) * 2^-53 * S_i, with S_i = sum_j |W_ij x_j|.
+ *
+ * The oracle also returns S_i, the normaliser of the parity norm
+ * err_i = |y_gpu_i - y_ref_i| / S_i (the textbook forward error bound of a
+ * dot product is a multiple of S_i).
+ *
+ * Readings of the paper taken here (each listed in the design notes):
+ *   - layout is row-major with a row stride ldw >= K; entries j >= K of a row
+ *     are padding and never read;
+ *   - the output is overwritten (xout = W @ x), not accumulated into;
+ *   - all K terms are included (the printed vector loop has no remainder loop;
+ *     the result here is the mathematical one over every column);
+ *   - fp16 weights are decoded exactly (binary16 definition, subnormals kept)
+ *     and accumulated in double; x stays fp32.
+ *
+ * Build: gcc -std=c99 -O2 -ffp-contract=off -fPIC -shared (no -ffast-math).
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+
+/* ------------------------------------------------------------------------ */
+/* IEEE 754 binary16 -> double, exact (IEEE 754-2008 Sec. 3.4 definition).   */
+/* ------------------------------------------------------------------------ */
+double oracle_f16_to_f64(uint16_t h)
+{
+    const int sign = (h >> 15) & 1;
+    const int e = (h >> 10) & 0x1f;
+    const int m = h & 0x3ff;
+    double v;
+    if (e == 0) {
+        /* zero or subnormal: m * 2^-24 */
+        v = ldexp((double)m, -24);
+    } else if (e == 31) {
+        v = (m == 0) ? INFINITY : NAN;
+    } else {
+        /* normal: (1 + m/1024) * 2^(e-15) = (1024 + m) * 2^(e-25) */
+        v = ldexp((double)(1024 + m), e - 25);
+    }
+    return sign ? -v : v;
+}
+
+/* ------------------------------------------------------------------------ */
+/* y_i = sum_{j<K} W[i*ldw + j] * x[j], in double, j ascending (Sec. 6.1).   */
+/* S_i = sum_{j<K} |W[i*ldw + j] * x[j]|.  S may be NULL.                    */
+/* ------------------------------------------------------------------------ */
+void oracle_gemv_f32(const float *W, int64_t ldw, const float *x,
+                     int64_t M, int64_t K, double *y, double *S)
+{
+    for (int64_t i = 0; i < M; ++i) {
+        const float *row = W + i * ldw;
+        double acc = 0.0, s = 0.0;
+        for (int64_t j = 0; j < K; ++j) {
+            const double p = (double)row[j] * (double)x[j]; /* exact */
+            acc += p;
+            s += fabs(p);
+        }
+        y[i] = acc;
+        if (S) S[i] = s;
+    }
+}
+
+/* Same definition with binary16 weights (bit patterns), fp32 x. */
+void oracle_gemv_f16(const uint16_t *W, int64_t ldw, const float *x,
+                     int64_t M, int64_t K, double *y, double *S)
+{
+    for (int64_t i = 0; i < M; ++i) {
+        const uint16_t *row = W + i * ldw;
+        double acc = 0.0, s = 0.0;
+        for (int64_t j = 0; j < K; ++j) {
+            const double p = oracle_f16_to_f64(row[j]) * (double)x[j]; /* exact */
+            acc += p;
+            s += fabs(p);
+        }
+        y[i] = acc;
+        if (S) S[i] = s;
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Parity norm.  err_i = |y_i - ref_i| / S_i; a non-finite y_i, or a nonzero */
+/* y_i where S_i == 0 (zero row or zero x), counts as an infinite error.     */
+/* Returns the number of outputs with err_i > tol.                           */
+/* ------------------------------------------------------------------------ */
+int64_t oracle_check(const float *y, const double *ref, const double *S,
+                     int64_t M, double tol, double *max_err,
+                     int64_t *argmax, double *mean_err)
+{
+    double worst = 0.0, sum = 0.0;
+    int64_t where = -1, bad = 0;
+    for (int64_t i = 0; i < M; ++i) {
+        const double yi = (double)y[i];
+        double e;
+        if (!isfinite(yi)) {
+            e = INFINITY;
+        } else if (S[i] == 0.0) {
+            e = (yi == 0.0) ? 0.0 : INFINITY;
+        } else {
+            e = fabs(yi - ref[i]) / S[i];
+        }
+        if (e > tol) ++bad;
+        if (where < 0 || e > worst) {
+            worst = e;
+            where = i;
+        }
+        sum += e;
+    }
+    if (max_err) *max_err = worst;
+    if (argmax) *argmax = where;
+    if (mean_err) *mean_err = (M > 0) ? sum / (double)M : 0.0;
+    return bad;
+}

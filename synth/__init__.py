@@ -1,0 +1,209 @@
+"""Seeded synthetic inputs for the TVL GEMV path (ctypes over ``synth.c``).
+
+This module is shared by the oracle side and the HIP side.  It draws numbers
+and rounds them to storage types; it holds none of the GEMV arithmetic.
+
+The workloads stand in for the paper's Llama-2 checkpoints (Kilictas & Alpay,
+arXiv 2601.03324, Sec. 7.1 runs the 110M "stories" model; Sec. 1 motivates the
+70B case): the decode-step weight shapes of Llama-2 110M, 7B and an 8-layer
+70B-shaped stack, with N(0, 0.02^2) weights (uniform for the single 768x768
+case) and N(0, 1) activations, every matrix with its own seeded x.  GEMV time
+does not depend on the values, so nothing about speed hinges on them.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass, field
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "synth.c")
+_LIB = os.path.join(_HERE, "libsynth.so")
+
+
+def build(force: bool = True) -> str:
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-std=c99", "-O2", "-fopenmp", "-fPIC", "-shared",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        L = ctypes.CDLL(_LIB)
+        P, I64, U64, D = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_double
+        L.synth_u64.argtypes = [U64, U64]
+        L.synth_u64.restype = U64
+        L.synth_key.argtypes = [U64, P, ctypes.c_int]
+        L.synth_key.restype = U64
+        L.synth_f32_to_f16_bits.argtypes = [ctypes.c_float]
+        L.synth_f32_to_f16_bits.restype = ctypes.c_uint16
+        L.synth_f32_to_f16.argtypes = [P, P, I64]
+        L.synth_uniform_f32.argtypes = [P, I64, U64, U64, D, D]
+        L.synth_normal_f32.argtypes = [P, I64, U64, U64, D]
+        L.synth_normal_f16.argtypes = [P, I64, U64, U64, D]
+        L.synth_int_f32.argtypes = [P, I64, U64, U64, I64, I64]
+        L.synth_int_f16.argtypes = [P, I64, U64, U64, I64, I64]
+        for n in ("synth_f32_to_f16", "synth_uniform_f32", "synth_normal_f32",
+                  "synth_normal_f16", "synth_int_f32", "synth_int_f16"):
+            getattr(L, n).restype = None
+        _lib = L
+    return _lib
+
+
+# ----------------------------------------------------------------- primitives
+def u64(key: int, k: int) -> int:
+    return int(lib().synth_u64(key, k))
+
+
+def key(*fields: int, root: int = 0) -> int:
+    arr = (ctypes.c_uint64 * len(fields))(*[int(f) for f in fields])
+    return int(lib().synth_key(root, arr, len(fields)))
+
+
+def uniform_f32(n: int, k: int, a: float, b: float, offset: int = 0, out=None):
+    out = np.empty(n, np.float32) if out is None else out
+    lib().synth_uniform_f32(out.ctypes.data, n, k, offset, a, b)
+    return out
+
+
+def normal_f32(n: int, k: int, sigma: float = 1.0, offset: int = 0, out=None):
+    out = np.empty(n, np.float32) if out is None else out
+    lib().synth_normal_f32(out.ctypes.data, n, k, offset, sigma)
+    return out
+
+
+def normal_f16(n: int, k: int, sigma: float, offset: int = 0, out=None):
+    """binary16 bit patterns (uint16) of the RNE-rounded N(0, sigma^2) fp32 values."""
+    out = np.empty(n, np.uint16) if out is None else out
+    lib().synth_normal_f16(out.ctypes.data, n, k, offset, sigma)
+    return out
+
+
+def int_f32(n: int, k: int, lo: int, hi: int, offset: int = 0):
+    out = np.empty(n, np.float32)
+    lib().synth_int_f32(out.ctypes.data, n, k, offset, lo, hi)
+    return out
+
+
+def int_f16(n: int, k: int, lo: int, hi: int, offset: int = 0):
+    out = np.empty(n, np.uint16)
+    lib().synth_int_f16(out.ctypes.data, n, k, offset, lo, hi)
+    return out
+
+
+def f32_to_f16_bits(a: np.ndarray) -> np.ndarray:
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    out = np.empty(a.shape, np.uint16)
+    lib().synth_f32_to_f16(a.ctypes.data, out.ctypes.data, a.size)
+    return out
+
+
+# ----------------------------------------------------------------- workloads
+MATRIX_IDS = {"wq": 0, "wk": 1, "wv": 2, "wo": 3, "w1": 4, "w3": 5, "w2": 6, "cls": 7}
+KIND_W, KIND_X = 0, 1
+
+
+@dataclass(frozen=True)
+class MatSpec:
+    """One weight matrix of a workload and the recipe of its inputs."""
+    name: str
+    M: int
+    K: int
+    dtype: str  # "f32" or "f16" (weights); x and y are fp32
+    dist: tuple  # ("normal", sigma) or ("uniform", a, b)
+    cfg: int
+    layer: int
+    mat: int
+
+    @property
+    def w_key(self) -> int:
+        return key(self.cfg, self.layer, self.mat, KIND_W, 0)
+
+    def x_key(self, rep: int = 0) -> int:
+        return key(self.cfg, self.layer, self.mat, KIND_X, rep)
+
+    @property
+    def wbytes(self) -> int:
+        return self.M * self.K * (4 if self.dtype == "f32" else 2)
+
+    def algo_bytes(self) -> int:
+        """Algorithmic bytes of one GEMV: |W| + |x| + |y| (paper Sec. 3.1)."""
+        return self.wbytes + 4 * self.K + 4 * self.M
+
+    def weights(self, row0: int = 0, nrows: int | None = None) -> np.ndarray:
+        """Rows [row0, row0+nrows) as a dense [nrows, K] array (fp32, or uint16 bits)."""
+        nrows = self.M - row0 if nrows is None else nrows
+        n, off = nrows * self.K, row0 * self.K
+        if self.dist[0] == "uniform":
+            w = uniform_f32(n, self.w_key, self.dist[1], self.dist[2], off)
+            if self.dtype == "f16":
+                w = f32_to_f16_bits(w)
+        elif self.dtype == "f32":
+            w = normal_f32(n, self.w_key, self.dist[1], off)
+        else:
+            w = normal_f16(n, self.w_key, self.dist[1], off)
+        return w.reshape(nrows, self.K)
+
+    def x(self, rep: int = 0) -> np.ndarray:
+        return normal_f32(self.K, self.x_key(rep), 1.0)
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    cfg: int
+    mats: tuple = field(default_factory=tuple)
+    reps: int = 1  # x vectors per matrix (the classifier case draws 100)
+
+    def algo_bytes(self) -> int:
+        return sum(m.algo_bytes() for m in self.mats)
+
+    def weight_bytes(self) -> int:
+        return sum(m.wbytes for m in self.mats)
+
+    def flops(self) -> int:
+        return sum(2 * m.M * m.K for m in self.mats)
+
+
+def _llama(cfg: int, layers: int, dim: int, hidden: int, vocab: int | None,
+           dtype: str, kv: int | None = None, sigma: float = 0.02) -> tuple:
+    kv = dim if kv is None else kv
+    shapes = [("wq", dim, dim), ("wk", kv, dim), ("wv", kv, dim), ("wo", dim, dim),
+              ("w1", hidden, dim), ("w3", hidden, dim), ("w2", dim, hidden)]
+    mats = []
+    for l in range(layers):
+        for nm, M, K in shapes:
+            mats.append(MatSpec(f"L{l}.{nm}", M, K, dtype, ("normal", sigma), cfg, l,
+                                MATRIX_IDS[nm]))
+    if vocab:
+        mats.append(MatSpec("cls", vocab, dim, dtype, ("normal", sigma), cfg, 0,
+                            MATRIX_IDS["cls"]))
+    return tuple(mats)
+
+
+WORKLOADS = {
+    # a single fp32 GEMV, W U(-0.05, 0.05), x N(0, 1), seed 0
+    "gemv768": Workload("gemv768", 1, (MatSpec("w", 768, 768, "f32", ("uniform", -0.05, 0.05),
+                                               1, 0, 0),)),
+    # one decode token of Llama-2 110M ("stories"), fp32: 12 layers + tied classifier
+    "sweep110m": Workload("sweep110m", 2, _llama(2, 12, 768, 2048, 32000, "f32")),
+    # the 110M classifier alone, 100 fresh x
+    "cls32000": Workload("cls32000", 3, (MatSpec("cls", 32000, 768, "f32", ("normal", 0.02),
+                                                 3, 0, MATRIX_IDS["cls"]),), reps=100),
+    # one decode token of Llama-2 7B, fp32: 32 layers + classifier
+    "sweep7b": Workload("sweep7b", 4, _llama(4, 32, 4096, 11008, 32000, "f32")),
+    # 8 layers of a Llama-2 70B-shaped stack, fp16 weights (GQA: wk, wv are 1024 x 8192)
+    "stack70b8": Workload("stack70b8", 5, _llama(5, 8, 8192, 28672, None, "f16", kv=1024)),
+}

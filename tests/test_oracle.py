@@ -1,0 +1,320 @@
+"""Pins of the CPU oracle against what the mathematics fixes (CPU only).
+
+The oracle computes the GEMV of Kilictas & Alpay, arXiv 2601.03324, Sec. 6.1
+(y = W x, row-major, every column summed) in double.  The paper prints no
+numeric GEMV example, so the oracle is pinned by:
+
+  * hand-worked cases (tests/golden/gemv_small.json),
+  * exact rational arithmetic (fractions.Fraction) on tiny inputs, within the
+    bound the oracle's only rounding (a sequential double sum) allows,
+  * closed forms: identity W, all-ones rows (against math.fsum), one-hot x,
+    zero rows, integer-valued W and x (exact), linearity,
+  * the binary16 definition over all 65,536 bit patterns (against numpy),
+  * the parity norm's rules (S = 0, non-finite outputs, the tolerance edge).
+
+Each pin is a plain function so that ``test_mutants_are_caught`` can run the
+whole suite against deliberately broken copies of the oracle and show that
+every plausible mistake is caught by at least one pin.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+import shutil
+import subprocess
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+
+U = 2.0 ** -53  # unit roundoff of double
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "gemv_small.json")
+
+
+def _fr(v) -> Fraction:
+    return Fraction(float(v))
+
+
+def _mixed_f32(rng, n, lo=-40, hi=40):
+    """fp32 values with random signs and exponents spread over 2^lo .. 2^hi."""
+    v = rng.standard_normal(n) * np.exp2(rng.integers(lo, hi, n).astype(np.float64))
+    return v.astype(np.float32)
+
+
+# --------------------------------------------------------------------- pins
+def pin_golden():
+    cases = json.load(open(GOLDEN))["cases"]
+    for c in cases:
+        M, K, ldw = c["M"], c["K"], c["ldw"]
+        x = np.array(c["x"], np.float32)
+        if c["dtype"] == "f32":
+            W = np.array([float(v) for v in c["W"]], np.float32).reshape(M, ldw)
+            y, S = oracle.gemv_f32(W, x, K)
+        else:
+            W = np.array(c["W_bits"], np.uint16).reshape(M, ldw)
+            y, S = oracle.gemv_f16(W, x, K)
+        assert list(y) == c["y"], (c["name"], y)
+        assert list(S) == c["S"], (c["name"], S)
+
+
+def pin_products_exact():
+    """Each product is exact in double: K = 1 GEMVs against Fraction products."""
+    rng = np.random.default_rng(11)
+    w = _mixed_f32(rng, 2000, -60, 60)
+    for xv in _mixed_f32(rng, 12, -60, 60):
+        y, S = oracle.gemv_f32(w.reshape(-1, 1), np.array([xv], np.float32))
+        for i in range(len(w)):
+            p = _fr(w[i]) * _fr(xv)
+            assert Fraction(y[i]) == p
+            assert Fraction(S[i]) == abs(p)
+    # binary16 weights: every finite pattern times a few x
+    bits = np.arange(0, 65536, dtype=np.uint16)
+    fin = np.isfinite(bits.view(np.float16))
+    bits = bits[fin]
+    for xv in (np.float32(1.0), np.float32(-3.0517578e-05), np.float32(1234.5677)):
+        y, _ = oracle.gemv_f16(bits.reshape(-1, 1), np.array([xv], np.float32))
+        ref = bits.view(np.float16).astype(np.float64) * np.float64(xv)
+        # exact: 11 x 24 significand bits fit in 53
+        assert np.array_equal(y, ref)
+
+
+def pin_brute_force_exact():
+    """Tiny random GEMVs against exact rational sums:
+    |y - exact| <= (K-1) u S and |S - S_exact| <= (K-1) u S_exact."""
+    rng = np.random.default_rng(12)
+    for trial in range(40):
+        M = int(rng.integers(1, 9))
+        K = int(rng.integers(1, 33))
+        ldw = K + int(rng.integers(0, 5))
+        W = np.full((M, ldw), np.nan, np.float32)
+        W[:, :K] = _mixed_f32(rng, M * K, -20, 20).reshape(M, K)
+        x = _mixed_f32(rng, K, -20, 20)
+        y, S = oracle.gemv_f32(W, x, K)
+        for i in range(M):
+            prods = [_fr(W[i, j]) * _fr(x[j]) for j in range(K)]
+            ex = sum(prods, Fraction(0))
+            sx = sum((abs(p) for p in prods), Fraction(0))
+            bound = (K - 1) * U * float(sx)
+            assert abs(float(Fraction(y[i]) - ex)) <= bound, (trial, i)
+            assert abs(float(Fraction(S[i]) - sx)) <= bound, (trial, i)
+
+
+def pin_brute_force_exact_f16():
+    rng = np.random.default_rng(13)
+    for trial in range(30):
+        M = int(rng.integers(1, 7))
+        K = int(rng.integers(1, 40))
+        ldw = K + int(rng.integers(0, 3))
+        bits = rng.integers(0, 65536, (M, ldw)).astype(np.uint16)
+        # keep finite weights only (replace Inf/NaN exponent patterns by zero)
+        bits[(bits & 0x7C00) == 0x7C00] = 0
+        x = _mixed_f32(rng, K, -10, 10)
+        y, S = oracle.gemv_f16(bits, x, K)
+        wf = bits.view(np.float16)
+        for i in range(M):
+            prods = [_fr(wf[i, j]) * _fr(x[j]) for j in range(K)]
+            ex = sum(prods, Fraction(0))
+            sx = sum((abs(p) for p in prods), Fraction(0))
+            bound = (K - 1) * U * float(sx)
+            assert abs(float(Fraction(y[i]) - ex)) <= bound
+            assert abs(float(Fraction(S[i]) - sx)) <= bound
+
+
+def pin_index_and_stride():
+    """Non-square integer W in a padded row stride against Python integers."""
+    rng = np.random.default_rng(14)
+    for M, K, ldw in ((5, 7, 9), (7, 5, 32), (1, 13, 13), (9, 1, 4)):
+        Wi = rng.integers(-9, 10, (M, K))
+        xi = rng.integers(-9, 10, K)
+        W = np.full((M, ldw), np.nan, np.float32)
+        W[:, :K] = Wi
+        y, S = oracle.gemv_f32(W, xi.astype(np.float32), K)
+        for i in range(M):
+            assert y[i] == sum(int(Wi[i, j]) * int(xi[j]) for j in range(K))
+            assert S[i] == sum(abs(int(Wi[i, j]) * int(xi[j])) for j in range(K))
+        Wb = np.full((M, ldw), 0x7E00, np.uint16)  # NaN padding
+        Wb[:, :K] = Wi.astype(np.float16).view(np.uint16)
+        y16, _ = oracle.gemv_f16(Wb, xi.astype(np.float32), K)
+        assert np.array_equal(y16, y)
+
+
+def pin_identity():
+    rng = np.random.default_rng(15)
+    for K in (1, 17, 256):
+        x = _mixed_f32(rng, K)
+        y, _ = oracle.gemv_f32(np.eye(K, dtype=np.float32), x)
+        assert np.array_equal(y, x.astype(np.float64))
+        y16, _ = oracle.gemv_f16(np.eye(K, dtype=np.float16).view(np.uint16), x)
+        assert np.array_equal(y16, x.astype(np.float64))
+
+
+def pin_all_ones_rows():
+    """y_i = sum_j x_j: against math.fsum (correctly rounded)."""
+    rng = np.random.default_rng(16)
+    for K in (1, 3, 768, 4099):
+        x = _mixed_f32(rng, K, -30, 30)
+        y, S = oracle.gemv_f32(np.ones((2, K), np.float32), x)
+        ref = math.fsum(float(v) for v in x)
+        tol = max(K - 1, 0) * U * math.fsum(abs(float(v)) for v in x) + abs(ref) * U
+        assert abs(y[0] - ref) <= tol and abs(y[1] - ref) <= tol
+
+
+def pin_integer_exact():
+    """Integer W in [-3, 3], x in [-8, 8], K <= 4096: every partial sum is an
+    integer below 2^53, so the result is exact; compare with numpy int64."""
+    rng = np.random.default_rng(17)
+    for M, K in ((32, 4096), (3, 1000)):
+        Wi = rng.integers(-3, 4, (M, K))
+        xi = rng.integers(-8, 9, K)
+        ref = Wi.astype(np.int64) @ xi.astype(np.int64)
+        y, S = oracle.gemv_f32(Wi.astype(np.float32), xi.astype(np.float32))
+        assert np.array_equal(y, ref.astype(np.float64))
+        assert np.array_equal(S, (np.abs(Wi) @ np.abs(xi)).astype(np.float64))
+        y16, _ = oracle.gemv_f16(Wi.astype(np.float16).view(np.uint16), xi.astype(np.float32))
+        assert np.array_equal(y16, ref.astype(np.float64))
+
+
+def pin_linearity():
+    """W(a x + b z) = a W x + b W z, exactly, with integer data."""
+    rng = np.random.default_rng(18)
+    M, K = 16, 300
+    W = rng.integers(-5, 6, (M, K)).astype(np.float32)
+    x = rng.integers(-7, 8, K)
+    z = rng.integers(-7, 8, K)
+    a, b = 3, -2
+    lhs, _ = oracle.gemv_f32(W, (a * x + b * z).astype(np.float32))
+    yx, _ = oracle.gemv_f32(W, x.astype(np.float32))
+    yz, _ = oracle.gemv_f32(W, z.astype(np.float32))
+    assert np.array_equal(lhs, a * yx + b * yz)
+
+
+def pin_one_hot():
+    """x = e_j picks column j of W exactly."""
+    rng = np.random.default_rng(19)
+    M, K = 37, 29
+    W = _mixed_f32(rng, M * K).reshape(M, K)
+    Wb = rng.integers(0, 0x7C00, (M, K)).astype(np.uint16)  # finite, nonnegative
+    for j in (0, 5, K - 1):
+        e = np.zeros(K, np.float32)
+        e[j] = 1.0
+        y, S = oracle.gemv_f32(W, e)
+        assert np.array_equal(y, W[:, j].astype(np.float64))
+        assert np.array_equal(S, np.abs(W[:, j]).astype(np.float64))
+        y16, _ = oracle.gemv_f16(Wb, e)
+        assert np.array_equal(y16, Wb[:, j].view(np.float16).astype(np.float64))
+
+
+def pin_zero_row():
+    W = np.zeros((3, 10), np.float32)
+    W[1] = 1.0
+    x = np.arange(10, dtype=np.float32) - 4.5
+    y, S = oracle.gemv_f32(W, x)
+    assert y[0] == 0.0 and S[0] == 0.0 and y[2] == 0.0 and S[2] == 0.0
+    assert y[1] == float(x.astype(np.float64).sum())
+
+
+def pin_f16_decode_all_patterns():
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    ref = bits.view(np.float16).astype(np.float64)
+    got = np.array([oracle.f16_to_f64(int(b)) for b in bits])
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    # signs of zero and of every finite value match (bitwise on non-NaN)
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+
+
+def pin_f16_subnormal_gemv():
+    """W = 2^-24 (smallest binary16 subnormal) everywhere: y = 2^-24 sum x."""
+    rng = np.random.default_rng(20)
+    K = 777
+    xi = rng.integers(-50, 51, K).astype(np.float32)
+    y, _ = oracle.gemv_f16(np.full((4, K), 1, np.uint16), xi)
+    assert np.all(y == math.ldexp(float(xi.astype(np.int64).sum()), -24))
+
+
+def pin_check_rules():
+    y_ref = np.array([1.0, 0.0, 0.0, 2.0, -3.0])
+    S = np.array([2.0, 0.0, 0.0, 4.0, 6.0])
+    y = np.array([1.0, 0.0, -0.0, 2.0, -3.0], np.float32)
+    r = oracle.check(y, y_ref, S, 1e-5)
+    assert r["bad"] == 0 and r["max_err"] == 0.0
+    # S = 0 requires an exact zero
+    r = oracle.check(np.array([1.0, 1e-30, 0, 2.0, -3.0], np.float32), y_ref, S, 1e-5)
+    assert r["bad"] == 1 and r["argmax"] == 1 and math.isinf(r["max_err"])
+    # non-finite outputs always fail
+    for bad in (np.nan, np.inf, -np.inf):
+        r = oracle.check(np.array([bad, 0, 0, 2.0, -3.0], np.float32), y_ref, S, 1e-5)
+        assert r["bad"] == 1 and r["argmax"] == 0 and math.isinf(r["max_err"])
+    # normalised error and the tolerance edge (err == tol passes)
+    y = np.array([1.0, 0, 0, 2.0 + 0.5, -3.0], np.float32)  # err = 0.5/4
+    r = oracle.check(y, y_ref, S, 0.125)
+    assert r["bad"] == 0 and r["max_err"] == 0.125 and r["argmax"] == 3
+    r = oracle.check(y, y_ref, S, 0.124)
+    assert r["bad"] == 1
+    assert r["mean_err"] == pytest.approx(0.125 / 5)
+
+
+PINS = [pin_golden, pin_products_exact, pin_brute_force_exact, pin_brute_force_exact_f16,
+        pin_index_and_stride, pin_identity, pin_all_ones_rows, pin_integer_exact,
+        pin_linearity, pin_one_hot, pin_zero_row, pin_f16_decode_all_patterns,
+        pin_f16_subnormal_gemv, pin_check_rules]
+
+
+@pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
+def test_oracle_pin(pin):
+    pin()
+
+
+# ------------------------------------------------------------------ mutants
+# Plausible mistakes, each applied to a private copy of oracle.c.  None of
+# them may survive the pins above.  (Mutants that could read out of bounds
+# are not used: they would crash the test process rather than fail a pin.)
+MUTANTS = {
+    "dropped_last_term_f32": ("for (int64_t j = 0; j < K; ++j) {\n            const double p = (double)row[j]",
+                              "for (int64_t j = 0; j < K - 1; ++j) {\n            const double p = (double)row[j]"),
+    "dropped_last_term_f16": ("for (int64_t j = 0; j < K; ++j) {\n            const double p = oracle_f16",
+                              "for (int64_t j = 1; j < K; ++j) {\n            const double p = oracle_f16"),
+    "stride_K_not_ldw_f32": ("const float *row = W + i * ldw;", "const float *row = W + i * K;"),
+    "stride_K_not_ldw_f16": ("const uint16_t *row = W + i * ldw;", "const uint16_t *row = W + i * K;"),
+    "product_rounded_to_f32": ("(double)row[j] * (double)x[j]", "(double)(row[j] * x[j])"),
+    "float_accumulator": ("double acc = 0.0, s = 0.0;", "float acc = 0.0f; double s = 0.0;"),
+    "sign_flip": ("            acc += p;", "            acc -= p;"),
+    "S_not_absolute": ("            s += fabs(p);", "            s += p;"),
+    "f16_subnormal_scale": ("ldexp((double)m, -24)", "ldexp((double)m, -25)"),
+    "f16_exponent_bias": ("e - 25);", "e - 24);"),
+    "f16_sign_dropped": ("return sign ? -v : v;", "return v;"),
+    "f16_mantissa_width": ("ldexp((double)(1024 + m)", "ldexp((double)(512 + m)"),
+    "check_S0_rule": ("e = (yi == 0.0) ? 0.0 : INFINITY;", "e = 0.0;"),
+    "check_nonfinite": ("if (!isfinite(yi)) {", "if (0) {"),
+    "check_tol_strict": ("if (e > tol) ++bad;", "if (e >= tol) ++bad;"),
+}
+
+
+def test_mutants_are_caught(tmp_path):
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    src = open(oracle._SRC).read()
+    survivors = []
+    for name, (old, new) in MUTANTS.items():
+        assert old in src, name
+        msrc = src.replace(old, new, 1)
+        cpath = tmp_path / f"{name}.c"
+        cpath.write_text(msrc)
+        so = tmp_path / f"lib{name}.so"
+        subprocess.check_call(["gcc", *oracle.CFLAGS, "-o", str(so), str(cpath), "-lm"])
+        caught = []
+        with oracle.using(str(so)):
+            for pin in PINS:
+                try:
+                    pin()
+                except (AssertionError, ValueError, OverflowError):
+                    # a pin that cannot even evaluate the mutant's output
+                    # (NaN or Inf where an exact value belongs) catches it too
+                    caught.append(pin.__name__)
+        if not caught:
+            survivors.append(name)
+    assert not survivors, f"mutants not caught by any pin: {survivors}"
