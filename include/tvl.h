@@ -1,0 +1,211 @@
+/*
+ * tvl.h -- C ABI of the TVL GEMV library for AMD Instinct MI355X (gfx950).
+ *
+ * The operation is the per-token matrix-vector product of a Llama-2 decode
+ * step (Kilictas & Alpay, "Bare-Metal Tensor Virtualization", arXiv
+ * 2601.03324): Sec. 6.1 defines it by the naive loop y[i] += W[i][j] * x[j]
+ * and the GEMV listing "xout = W @ x" with the weight for (i, j) at
+ * w + i*n + j; Sec. 1 and Sec. 3.1 state that every token streams every
+ * weight matrix once, so the traffic is |W| + |x| + |y| bytes.  Here:
+ *
+ *     y[i] = sum_{j < K} W[i*ldw + j] * x[j],      0 <= i < M
+ *
+ *   - W is row-major with a row stride of ldw elements (ldw >= K), fp32 or
+ *     binary16 (fp16); x and y are fp32; products are accumulated in fp32.
+ *     An fp16 weight is converted to fp32 exactly (subnormals kept).
+ *   - Tensor Virtualization Layout (TVL, Sec. 3.2 and the abstract: every
+ *     buffer starts on a cache line and every vector load touches one line):
+ *     here every row starts on a 128-byte boundary, i.e. W is 128-byte
+ *     aligned and ldw * sizeof(weight) is a multiple of 128.  W spans M
+ *     whole rows (M * ldw elements, the last row's padding included: a
+ *     16-byte load may touch it).  Elements K..ldw-1 of a row are padding;
+ *     their values are never used (they may even hold NaN).
+ *   - y is overwritten ("xout = W @ x"); its previous contents are ignored.
+ *   - Summation order differs from the sequential loop (Sec. 5.2 accepts the
+ *     drift of reordered fused multiply-add accumulation).  Each output is
+ *     the sum of 256 interleaved fp32 partial sums (64 lanes x 4) joined by
+ *     a fixed tree, so |y_i - exact| <= (K/256 + 8) * 2^-24 * sum_j |W_ij x_j|
+ *     up to second-order terms, and reruns of one variant are bitwise equal.
+ *
+ * Memory and ownership.  All W, x, y pointers are device pointers owned by
+ * the caller; the library never allocates, frees or retains them.  The same
+ * W or x may appear in several items (a tied classifier, Sec. 5.1; a shared
+ * activation).  The library owns only what it allocates itself: plan objects
+ * and the K-split workspace (see tvl_gemv).
+ *
+ * Streams.  Every compute call enqueues work on `stream` (0 = the null
+ * stream) and returns without synchronising; results are valid once the
+ * caller has synchronised with that stream.
+ *
+ * Errors.  Calls return a tvl_status and never abort or throw.  Arguments are
+ * validated before anything is enqueued; a batch with one bad item enqueues
+ * nothing.  Launch failures are reported as TVL_ERR_HIP with the HIP error
+ * text in tvl_last_error(); faults during execution surface at the caller's
+ * next synchronisation, as for any HIP kernel.
+ *
+ * Threading.  All calls may be made from several host threads.  A plan must
+ * not run on two streams at once.  K-split calls that share a stream share
+ * one workspace and are ordered by the stream; different streams get
+ * different workspaces.
+ */
+#ifndef TVL_H
+#define TVL_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#if defined(__GNUC__)
+#define TVL_API __attribute__((visibility("default")))
+#else
+#define TVL_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TVL_VERSION 100 /* 1.0.0 */
+
+/* Weight element type.  x and y are always fp32. */
+typedef enum tvl_dtype {
+    TVL_F32 = 0, /* IEEE binary32 weights */
+    TVL_F16 = 1  /* IEEE binary16 weights, converted exactly to fp32 */
+} tvl_dtype;
+
+typedef enum tvl_status {
+    TVL_OK = 0,
+    TVL_ERR_NULL = -1,  /* a required pointer is NULL                        */
+    TVL_ERR_SHAPE = -2, /* M < 1 or > 2^31-1, K < 1 or > 2^30, ldw < K, ... */
+    TVL_ERR_ALIGN = -3, /* W not 128-B aligned, ldw*size % 128 != 0,
+                           x not 16-B aligned, y not 4-B aligned             */
+    TVL_ERR_DTYPE = -4, /* unknown weight dtype                              */
+    TVL_ERR_ALIAS = -5, /* an output overlaps an input or another output     */
+    TVL_ERR_HIP = -6,   /* a HIP runtime call or a launch failed             */
+    TVL_ERR_NOMEM = -7, /* host or device allocation failed                  */
+    TVL_ERR_ARG = -8    /* an unsupported tuning value or other argument     */
+} tvl_status;
+
+/* One GEMV of a batch: y = W x with the same meaning as tvl_gemv's
+ * arguments.  56 bytes, no implicit padding. */
+typedef struct tvl_item {
+    const void *W;  /* device, M whole rows of ldw elements of `dtype`    */
+    int64_t ldw;    /* row stride in elements                              */
+    const float *x; /* device, K floats                                    */
+    float *y;       /* device, M floats, overwritten                       */
+    int64_t M;      /* rows                                                */
+    int64_t K;      /* columns used                                        */
+    int32_t dtype;  /* tvl_dtype                                           */
+    int32_t reserved; /* must be 0                                         */
+} tvl_item;
+
+/* Launch shape override.  A zero field means "choose by shape".
+ *   rows_per_wave   R in {1, 2, 4, 8}: rows one wavefront computes at once
+ *   waves_per_block W in {2, 4, 8}: wavefronts per workgroup
+ *   unroll          U in {2, 4, 8, 16}: 16-byte loads per row kept in flight
+ *                   per lane (only the pairs (R,U) the library instantiates
+ *                   are accepted: (1,8) (1,16) (2,4) (2,8) (4,2) (4,4) (8,2))
+ *   ksplit          S >= 1: K slices per row tile (tvl_gemv only; 1 = row split)
+ *   grid            workgroups of a sweep launch (0 = one per tile); a smaller
+ *                   grid makes each workgroup loop over tiles
+ *   flags           bit 0: plain (cached) weight loads instead of streaming
+ *                   (non-temporal) loads */
+typedef struct tvl_tuning {
+    int32_t rows_per_wave;
+    int32_t waves_per_block;
+    int32_t unroll;
+    int32_t ksplit;
+    int32_t grid;
+    int32_t flags;
+} tvl_tuning;
+
+#define TVL_FLAG_CACHED_LOADS 1
+
+/* Opaque sweep plan. */
+typedef struct tvl_plan tvl_plan;
+
+/* Library version (TVL_VERSION of the built library). */
+TVL_API int32_t tvl_version(void);
+
+/* Row stride, in elements, of the TVL layout for K columns of `dtype`:
+ * roundup(K * size, 128) / size.  Returns -1 for K < 1 or an unknown dtype.
+ * Pure host function. */
+TVL_API int64_t tvl_row_stride(int64_t K, int32_t dtype);
+
+/* TVL pack (Sec. 3.2 alignment): copy a dense row-major [M x K] matrix
+ * `src` (device) into `dst` (device, M rows of stride ldw, 128-byte aligned)
+ * and zero elements K..ldw-1 of every row.  One kernel launch on `stream`.
+ * `src` is only required to be element aligned; `dst` must not overlap `src`. */
+TVL_API tvl_status tvl_pack_rows(void *dst, int64_t ldw, const void *src,
+                                 int64_t M, int64_t K, int32_t dtype,
+                                 hipStream_t stream);
+
+/* y = W x (Sec. 6.1), one launch.  The library picks the variant by shape:
+ * row split (each wavefront owns R whole rows) when there are enough rows to
+ * fill the GPU, else K split (S workgroups share a row tile, each sums one
+ * slice of K into an fp32 partial; the last workgroup to finish adds the S
+ * partials in the fixed order 0..S-1, so results stay deterministic).  The
+ * K-split workspace (S*M floats and one counter per row tile) is allocated by
+ * the library on first use per (device, stream) and kept until
+ * tvl_release_workspaces() or process exit. */
+TVL_API tvl_status tvl_gemv(const void *W, int64_t ldw, int32_t dtype,
+                            const float *x, float *y, int64_t M, int64_t K,
+                            hipStream_t stream);
+
+/* tvl_gemv with an explicit launch shape (NULL = choose by shape). */
+TVL_API tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype,
+                               const float *x, float *y, int64_t M, int64_t K,
+                               const tvl_tuning *tuning, hipStream_t stream);
+
+/* All n GEMVs of `items` (e.g. every weight matrix of one decode token,
+ * Sec. 1: each token streams every matrix once) in ONE launch.  The host
+ * array `items` is read during the call only.  The first call with a given
+ * item list builds a device tile table (one synchronous upload) and caches
+ * it; later calls with an identical list launch at once.  The cache holds 64
+ * lists; when it is full the device is synchronised and the cache emptied.
+ * No output y may overlap any W, x or other y of the batch. */
+TVL_API tvl_status tvl_gemv_batch_sweep(const tvl_item *items, int32_t n,
+                                        hipStream_t stream);
+
+/* Sweep plan: validate `items`, build the tile table (tiles of R*W rows,
+ * ordered by bytes per tile, largest first) and upload it once.  The item
+ * list is copied; the W, x, y buffers it names must stay valid for every
+ * run.  `tuning` may be NULL.  The plan belongs to the device current at
+ * creation. */
+TVL_API tvl_status tvl_sweep_plan_create(const tvl_item *items, int32_t n,
+                                         const tvl_tuning *tuning,
+                                         tvl_plan **plan);
+/* Run a plan: exactly one kernel launch on `stream`. */
+TVL_API tvl_status tvl_sweep_plan_run(const tvl_plan *plan, hipStream_t stream);
+/* Number of tiles and the launch grid of a plan (either pointer may be NULL). */
+TVL_API tvl_status tvl_sweep_plan_info(const tvl_plan *plan, int64_t *ntiles,
+                                       int64_t *grid, int32_t *rows_per_tile);
+/* Free a plan (synchronises its device first).  NULL is a no-op. */
+TVL_API tvl_status tvl_sweep_plan_destroy(tvl_plan *plan);
+
+/* Free the K-split workspaces and the batch-sweep cache (synchronises every
+ * device that holds one). */
+TVL_API tvl_status tvl_release_workspaces(void);
+
+/* Diagnostics (not part of the GEMV path; used to calibrate measurements).
+ * tvl_util_read_stream: read `bytes` (a multiple of 16) at `src` (16-byte
+ *   aligned) with the same streaming loads as the GEMV and write one float
+ *   per workgroup to `sink` (at least `sink_len` floats, >= the grid it
+ *   reports through *grid_out, which may be NULL).
+ * tvl_util_copy: copy `bytes` (multiple of 16, both 16-byte aligned, no
+ *   overlap) from src to dst. */
+TVL_API tvl_status tvl_util_read_stream(const void *src, int64_t bytes,
+                                        float *sink, int64_t sink_len,
+                                        int64_t *grid_out, hipStream_t stream);
+TVL_API tvl_status tvl_util_copy(void *dst, const void *src, int64_t bytes,
+                                 hipStream_t stream);
+
+/* Static text for a status code. */
+TVL_API const char *tvl_status_str(int32_t status);
+/* Detail of the last failure on the calling thread ("" if none). */
+TVL_API const char *tvl_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TVL_H */

@@ -1,0 +1,604 @@
+// tvl_abi.cpp -- the C ABI declared in include/tvl.h: argument validation,
+// variant choice by shape, sweep plans, K-split workspaces, error reporting.
+//
+// Every entry point validates all of its arguments before it makes any HIP
+// call, so the validation paths run (and are tested) on a host without a GPU.
+#include "tvl.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <new>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "tvl_internal.h"
+
+using tvl::DevItem;
+using tvl::DevTile;
+using tvl::Shape;
+
+struct tvl_plan {
+    int device = -1;
+    Shape shape{4, 4, 4, false};
+    int ks_cap = 0;
+    int ntiles = 0;
+    int grid = 0;
+    DevItem *d_items = nullptr;
+    DevTile *d_tiles = nullptr;
+    std::vector<tvl_item> items;
+};
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+tvl_status fail(tvl_status st, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+tvl_status fail_hip(hipError_t e, const char *what)
+{
+    return fail(TVL_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
+}
+
+constexpr int64_t kMaxDim = 2147483647LL; // M and tile counts fit in int32
+constexpr int64_t kMaxK = 1LL << 30;       // K plus one LDS slice still fits in int32
+
+int elem_size(int32_t dt) { return dt == TVL_F16 ? 2 : 4; }
+
+bool dtype_ok(int32_t dt) { return dt == TVL_F32 || dt == TVL_F16; }
+
+struct Range {
+    uintptr_t b, e; // [b, e)
+};
+
+// Validate one GEMV's arguments (no HIP calls).
+tvl_status check_one(const void *W, int64_t ldw, int32_t dt, const float *x, const float *y,
+                     int64_t M, int64_t K, const char *who)
+{
+    if (!W || !x || !y) return fail(TVL_ERR_NULL, "%s: W, x and y must be non-NULL", who);
+    if (!dtype_ok(dt)) return fail(TVL_ERR_DTYPE, "%s: unknown weight dtype %d", who, (int)dt);
+    if (M < 1 || K < 1 || M > kMaxDim || K > kMaxK)
+        return fail(TVL_ERR_SHAPE, "%s: need 1 <= M <= 2^31-1 and 1 <= K <= 2^30 (M=%lld K=%lld)",
+                    who, (long long)M, (long long)K);
+    if (ldw < K) return fail(TVL_ERR_SHAPE, "%s: ldw (%lld) < K (%lld)", who, (long long)ldw,
+                             (long long)K);
+    const int s = elem_size(dt);
+    // the weight span must be addressable: ((M-1)*ldw + K) * s < 2^62
+    if (ldw > (int64_t(1) << 62) / s / M)
+        return fail(TVL_ERR_SHAPE, "%s: M * ldw overflows", who);
+    if (reinterpret_cast<uintptr_t>(W) % tvl::kLineBytes != 0)
+        return fail(TVL_ERR_ALIGN, "%s: W must be 128-byte aligned", who);
+    if ((ldw * s) % tvl::kLineBytes != 0)
+        return fail(TVL_ERR_ALIGN, "%s: ldw * %d bytes (=%lld) must be a multiple of 128", who, s,
+                    (long long)(ldw * s));
+    if (reinterpret_cast<uintptr_t>(x) % 16 != 0)
+        return fail(TVL_ERR_ALIGN, "%s: x must be 16-byte aligned", who);
+    if (reinterpret_cast<uintptr_t>(y) % 4 != 0)
+        return fail(TVL_ERR_ALIGN, "%s: y must be 4-byte aligned", who);
+    return TVL_OK;
+}
+
+// A TVL matrix spans M whole rows of ldw elements: the kernels' 16-byte loads
+// may touch the padding of the last row (its values are never used).
+Range w_range(const void *W, int64_t ldw, int32_t dt, int64_t M)
+{
+    const uintptr_t b = reinterpret_cast<uintptr_t>(W);
+    return {b, b + (uintptr_t)(M * ldw * elem_size(dt))};
+}
+Range f_range(const float *p, int64_t n)
+{
+    const uintptr_t b = reinterpret_cast<uintptr_t>(p);
+    return {b, b + (uintptr_t)(n * 4)};
+}
+bool overlap(const Range &a, const Range &b) { return a.b < b.e && b.b < a.e; }
+
+// Outputs must not overlap each other or any input of the batch.
+tvl_status check_alias(const tvl_item *items, int32_t n)
+{
+    std::vector<Range> wr(n);
+    for (int32_t i = 0; i < n; ++i)
+        wr[i] = f_range(items[i].y, items[i].M);
+    std::vector<int32_t> ord(n);
+    for (int32_t i = 0; i < n; ++i)
+        ord[i] = i;
+    std::sort(ord.begin(), ord.end(), [&](int32_t a, int32_t b) { return wr[a].b < wr[b].b; });
+    for (int32_t i = 1; i < n; ++i)
+        if (overlap(wr[ord[i - 1]], wr[ord[i]]))
+            return fail(TVL_ERR_ALIAS, "items %d and %d: outputs overlap", (int)ord[i - 1],
+                        (int)ord[i]);
+    std::vector<Range> sorted(n);
+    for (int32_t i = 0; i < n; ++i)
+        sorted[i] = wr[ord[i]];
+    auto hits = [&](const Range &r) -> int32_t {
+        // last output starting before r ends; outputs are disjoint and sorted
+        auto it = std::lower_bound(sorted.begin(), sorted.end(), r.e,
+                                   [](const Range &a, uintptr_t v) { return a.b < v; });
+        if (it == sorted.begin()) return -1;
+        --it;
+        return overlap(*it, r) ? ord[it - sorted.begin()] : -1;
+    };
+    for (int32_t i = 0; i < n; ++i) {
+        const tvl_item &t = items[i];
+        int32_t h = hits(w_range(t.W, t.ldw, t.dtype, t.M));
+        if (h >= 0)
+            return fail(TVL_ERR_ALIAS, "output of item %d overlaps W of item %d", (int)h, (int)i);
+        h = hits(f_range(t.x, t.K));
+        if (h >= 0)
+            return fail(TVL_ERR_ALIAS, "output of item %d overlaps x of item %d", (int)h, (int)i);
+    }
+    return TVL_OK;
+}
+
+tvl_status check_items(const tvl_item *items, int32_t n)
+{
+    if (n < 0) return fail(TVL_ERR_SHAPE, "sweep: n < 0");
+    if (n > 0 && !items) return fail(TVL_ERR_NULL, "sweep: items is NULL");
+    for (int32_t i = 0; i < n; ++i) {
+        const tvl_item &t = items[i];
+        char who[48];
+        snprintf(who, sizeof who, "sweep item %d", (int)i);
+        const tvl_status st = check_one(t.W, t.ldw, t.dtype, t.x, t.y, t.M, t.K, who);
+        if (st != TVL_OK) return st;
+        if (t.reserved != 0) return fail(TVL_ERR_ARG, "%s: reserved must be 0", who);
+    }
+    return check_alias(items, n);
+}
+
+tvl_status check_tuning(const tvl_tuning *t, bool allow_ksplit)
+{
+    if (!t) return TVL_OK;
+    if (t->rows_per_wave < 0 || t->waves_per_block < 0 || t->unroll < 0 || t->ksplit < 0 ||
+        t->grid < 0 || (t->flags & ~TVL_FLAG_CACHED_LOADS) != 0)
+        return fail(TVL_ERR_ARG, "tuning: negative field or unknown flag");
+    if (!allow_ksplit && t->ksplit > 1)
+        return fail(TVL_ERR_ARG, "tuning: ksplit applies to tvl_gemv only");
+    if (t->ksplit > 1024) return fail(TVL_ERR_ARG, "tuning: ksplit > 1024");
+    return TVL_OK;
+}
+
+// ---------------------------------------------------------------- devices
+struct DevInfo {
+    int cus = 256;
+};
+
+std::mutex g_mu;
+std::map<int, DevInfo> g_dev;
+
+tvl_status current_device(int *dev, DevInfo *info)
+{
+    hipError_t e = hipGetDevice(dev);
+    if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_dev.find(*dev);
+    if (it == g_dev.end()) {
+        DevInfo d;
+        int cus = 0;
+        e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, *dev);
+        if (e != hipSuccess) return fail_hip(e, "hipDeviceGetAttribute");
+        if (cus > 0) d.cus = cus;
+        it = g_dev.emplace(*dev, d).first;
+    }
+    *info = it->second;
+    return TVL_OK;
+}
+
+// Shape from a tuning override, else the default.
+tvl_status pick_shape(const tvl_tuning *t, Shape def, Shape *out)
+{
+    Shape s = def;
+    if (t) {
+        if (t->rows_per_wave) s.R = t->rows_per_wave;
+        if (t->waves_per_block) s.W = t->waves_per_block;
+        if (t->unroll) s.U = t->unroll;
+        s.cached = (t->flags & TVL_FLAG_CACHED_LOADS) != 0;
+        if (t->rows_per_wave && !t->unroll) {
+            // keep about 16 KB of weights in flight per wavefront by default
+            s.U = s.R >= 8 ? 2 : s.R == 4 ? 4 : 8;
+        }
+    }
+    if (!tvl::shape_supported(s))
+        return fail(TVL_ERR_ARG, "tuning: (rows_per_wave %d, waves_per_block %d, unroll %d) is "
+                                 "not an instantiated shape",
+                    s.R, s.W, s.U);
+    *out = s;
+    return TVL_OK;
+}
+
+// ---------------------------------------------------------- K-split workspace
+struct Workspace {
+    float *partials = nullptr;
+    int64_t partial_cap = 0; // floats
+    int *counters = nullptr;
+    int64_t counter_cap = 0; // ints
+};
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+
+tvl_status get_workspace(int dev, hipStream_t st, int64_t nfloat, int64_t ncnt, Workspace *out)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    Workspace &w = g_ws[{dev, st}];
+    if (w.partial_cap < nfloat || w.counter_cap < ncnt) {
+        hipError_t e;
+        if (w.partials || w.counters) {
+            // earlier launches on this stream may still use the old buffers
+            e = hipStreamSynchronize(st);
+            if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
+            (void)hipFree(w.partials);
+            (void)hipFree(w.counters);
+            w = Workspace{};
+        }
+        const int64_t pf = std::max<int64_t>(nfloat, 1 << 16);
+        const int64_t pc = std::max<int64_t>(ncnt, 1 << 12);
+        e = hipMalloc(&w.partials, pf * sizeof(float));
+        if (e != hipSuccess) return fail(TVL_ERR_NOMEM, "K-split workspace: %s", hipGetErrorString(e));
+        e = hipMalloc(&w.counters, pc * sizeof(int));
+        if (e != hipSuccess) {
+            (void)hipFree(w.partials);
+            w = Workspace{};
+            return fail(TVL_ERR_NOMEM, "K-split workspace: %s", hipGetErrorString(e));
+        }
+        e = tvl::launch_zero_i32(w.counters, pc, st);
+        if (e != hipSuccess) return fail_hip(e, "counter reset launch");
+        w.partial_cap = pf;
+        w.counter_cap = pc;
+    }
+    *out = w;
+    return TVL_OK;
+}
+
+// -------------------------------------------------------------- plans
+tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning, tvl_plan **out)
+{
+    Shape shape;
+    tvl_status st = pick_shape(tuning, Shape{4, 4, 4, false}, &shape);
+    if (st != TVL_OK) return st;
+    int dev = 0;
+    DevInfo info;
+    st = current_device(&dev, &info);
+    if (st != TVL_OK) return st;
+
+    tvl_plan *p = new (std::nothrow) tvl_plan;
+    if (!p) return fail(TVL_ERR_NOMEM, "plan: host allocation");
+    p->device = dev;
+    p->shape = shape;
+    p->items.assign(items, items + n);
+
+    const int rows_per_tile = shape.R * shape.W;
+    // bytes per tile, largest first, so the longest tiles start first
+    std::vector<int32_t> ord(n);
+    for (int32_t i = 0; i < n; ++i)
+        ord[i] = i;
+    std::stable_sort(ord.begin(), ord.end(), [&](int32_t a, int32_t b) {
+        return items[a].K * elem_size(items[a].dtype) > items[b].K * elem_size(items[b].dtype);
+    });
+    std::vector<DevItem> hitems(n);
+    std::vector<DevTile> htiles;
+    int64_t ntiles = 0;
+    int64_t kmax = 1;
+    for (int32_t i = 0; i < n; ++i) {
+        const tvl_item &t = items[i];
+        hitems[i] = DevItem{t.W, t.ldw, t.x, t.y, (int32_t)t.M, (int32_t)t.K, t.dtype, 0};
+        ntiles += (t.M + rows_per_tile - 1) / rows_per_tile;
+        kmax = std::max<int64_t>(kmax, t.K);
+    }
+    if (ntiles > kMaxDim) {
+        delete p;
+        return fail(TVL_ERR_SHAPE, "plan: %lld tiles exceed 2^31-1", (long long)ntiles);
+    }
+    htiles.reserve((size_t)ntiles);
+    for (int32_t k = 0; k < n; ++k) {
+        const int32_t i = ord[k];
+        for (int64_t r = 0; r < items[i].M; r += rows_per_tile)
+            htiles.push_back(DevTile{i, (int32_t)r});
+    }
+    p->ntiles = (int)ntiles;
+    p->ks_cap = tvl::slice_cap(kmax);
+    p->grid = (tuning && tuning->grid) ? std::min<int>(tuning->grid, std::max(p->ntiles, 1))
+                                       : p->ntiles;
+    if (n > 0) {
+        hipError_t e = hipMalloc(&p->d_items, sizeof(DevItem) * n);
+        if (e == hipSuccess) e = hipMalloc(&p->d_tiles, sizeof(DevTile) * htiles.size());
+        if (e == hipSuccess)
+            e = hipMemcpy(p->d_items, hitems.data(), sizeof(DevItem) * n, hipMemcpyHostToDevice);
+        if (e == hipSuccess)
+            e = hipMemcpy(p->d_tiles, htiles.data(), sizeof(DevTile) * htiles.size(),
+                          hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            (void)hipFree(p->d_items);
+            (void)hipFree(p->d_tiles);
+            delete p;
+            return fail(e == hipErrorOutOfMemory ? TVL_ERR_NOMEM : TVL_ERR_HIP,
+                        "plan upload: %s", hipGetErrorString(e));
+        }
+    }
+    *out = p;
+    return TVL_OK;
+}
+
+tvl_status plan_launch(const tvl_plan *p, hipStream_t st)
+{
+    if (p->ntiles == 0) return TVL_OK;
+    const hipError_t e =
+        tvl::launch_sweep(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid, p->ks_cap, st);
+    if (e != hipSuccess) return fail_hip(e, "sweep launch");
+    return TVL_OK;
+}
+
+void plan_free(tvl_plan *p)
+{
+    if (!p) return;
+    int cur = -1;
+    if (hipGetDevice(&cur) == hipSuccess && cur != p->device) (void)hipSetDevice(p->device);
+    (void)hipDeviceSynchronize();
+    (void)hipFree(p->d_items);
+    (void)hipFree(p->d_tiles);
+    if (cur >= 0 && cur != p->device) (void)hipSetDevice(cur);
+    delete p;
+}
+
+// batch-sweep cache: item list bytes + device -> plan
+std::map<std::string, tvl_plan *> g_cache;
+constexpr size_t kCacheMax = 64;
+
+}  // namespace
+
+// ================================================================== ABI
+extern "C" {
+
+int32_t tvl_version(void) { return TVL_VERSION; }
+
+int64_t tvl_row_stride(int64_t K, int32_t dtype)
+{
+    if (K < 1 || !dtype_ok(dtype)) return -1;
+    const int s = elem_size(dtype);
+    if (K > (INT64_MAX - tvl::kLineBytes) / s) return -1;
+    return (K * s + tvl::kLineBytes - 1) / tvl::kLineBytes * tvl::kLineBytes / s;
+}
+
+tvl_status tvl_pack_rows(void *dst, int64_t ldw, const void *src, int64_t M, int64_t K,
+                         int32_t dtype, hipStream_t stream)
+{
+    g_err[0] = 0;
+    if (!dst || !src) return fail(TVL_ERR_NULL, "tvl_pack_rows: dst and src must be non-NULL");
+    if (!dtype_ok(dtype)) return fail(TVL_ERR_DTYPE, "tvl_pack_rows: unknown dtype %d", (int)dtype);
+    if (M < 1 || K < 1 || M > kMaxDim || K > kMaxK || ldw < K)
+        return fail(TVL_ERR_SHAPE, "tvl_pack_rows: need 1 <= M <= 2^31-1, 1 <= K <= 2^30, "
+                                   "ldw >= K");
+    const int s = elem_size(dtype);
+    if (ldw > (int64_t(1) << 62) / s / M) return fail(TVL_ERR_SHAPE, "tvl_pack_rows: overflow");
+    if (reinterpret_cast<uintptr_t>(dst) % tvl::kLineBytes != 0 || (ldw * s) % tvl::kLineBytes)
+        return fail(TVL_ERR_ALIGN, "tvl_pack_rows: dst rows must start on 128-byte boundaries");
+    if (reinterpret_cast<uintptr_t>(src) % s != 0)
+        return fail(TVL_ERR_ALIGN, "tvl_pack_rows: src must be element aligned");
+    const Range d = w_range(dst, ldw, dtype, M);
+    const Range r = w_range(src, K, dtype, M);
+    if (overlap(d, r)) return fail(TVL_ERR_ALIAS, "tvl_pack_rows: dst overlaps src");
+    const hipError_t e = tvl::launch_pack(dtype, dst, ldw, src, M, K, stream);
+    if (e != hipSuccess) return fail_hip(e, "pack launch");
+    return TVL_OK;
+}
+
+tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype, const float *x, float *y,
+                       int64_t M, int64_t K, const tvl_tuning *tuning, hipStream_t stream)
+{
+    g_err[0] = 0;
+    tvl_status st = check_one(W, ldw, dtype, x, y, M, K, "tvl_gemv");
+    if (st != TVL_OK) return st;
+    tvl_item it{W, ldw, x, y, M, K, dtype, 0};
+    st = check_alias(&it, 1);
+    if (st != TVL_OK) return st;
+    st = check_tuning(tuning, true);
+    if (st != TVL_OK) return st;
+
+    // Variant by shape.  Row split when there are enough row tiles to give
+    // every CU several workgroups; otherwise split K so that small-M GEMVs
+    // still spread over the whole GPU.
+    Shape shape;
+    int S = 1;
+    const bool user_shape =
+        tuning && (tuning->rows_per_wave || tuning->waves_per_block || tuning->unroll);
+    if (user_shape || (tuning && tuning->flags)) {
+        st = pick_shape(tuning, Shape{4, 4, 4, false}, &shape);
+        if (st != TVL_OK) return st;
+    }
+
+    int dev = 0;
+    DevInfo info;
+    st = current_device(&dev, &info);
+    if (st != TVL_OK) return st;
+    if (!(user_shape || (tuning && tuning->flags))) {
+        shape = Shape{4, 4, 4, false};
+        if ((M + 15) / 16 < 2 * info.cus) shape = Shape{1, 4, 8, false};
+    }
+    const int rows_per_tile = shape.R * shape.W;
+    const int64_t tiles = (M + rows_per_tile - 1) / rows_per_tile;
+    if (tuning && tuning->ksplit) {
+        S = tuning->ksplit;
+    } else if (!user_shape && tiles < 2 * info.cus) {
+        // aim for ~4 workgroups per CU; each slice keeps >= 2 LDS chunks
+        const int64_t want = (4LL * info.cus + tiles - 1) / tiles;
+        const int64_t most = std::max<int64_t>(1, K / (2 * tvl::kChunkElems));
+        S = (int)std::max<int64_t>(1, std::min<int64_t>(want, most));
+    }
+    hipError_t e;
+    if (S <= 1) {
+        e = tvl::launch_gemv_rows(shape, dtype, W, ldw, x, y, (int)M, (int)K, stream);
+    } else {
+        if ((int64_t)tiles * S > kMaxDim) return fail(TVL_ERR_ARG, "tvl_gemv: grid too large");
+        Workspace ws;
+        st = get_workspace(dev, stream, (int64_t)S * M, tiles, &ws);
+        if (st != TVL_OK) return st;
+        e = tvl::launch_gemv_ksplit(shape, dtype, W, ldw, x, y, (int)M, (int)K, S, ws.partials,
+                                    ws.counters, stream);
+    }
+    if (e != hipSuccess) return fail_hip(e, "gemv launch");
+    return TVL_OK;
+}
+
+tvl_status tvl_gemv(const void *W, int64_t ldw, int32_t dtype, const float *x, float *y,
+                    int64_t M, int64_t K, hipStream_t stream)
+{
+    return tvl_gemv_ex(W, ldw, dtype, x, y, M, K, nullptr, stream);
+}
+
+tvl_status tvl_sweep_plan_create(const tvl_item *items, int32_t n, const tvl_tuning *tuning,
+                                 tvl_plan **plan)
+{
+    g_err[0] = 0;
+    if (!plan) return fail(TVL_ERR_NULL, "tvl_sweep_plan_create: plan is NULL");
+    *plan = nullptr;
+    tvl_status st = check_items(items, n);
+    if (st != TVL_OK) return st;
+    st = check_tuning(tuning, false);
+    if (st != TVL_OK) return st;
+    return plan_build(items, n, tuning, plan);
+}
+
+tvl_status tvl_sweep_plan_run(const tvl_plan *plan, hipStream_t stream)
+{
+    g_err[0] = 0;
+    if (!plan) return fail(TVL_ERR_NULL, "tvl_sweep_plan_run: plan is NULL");
+    int dev = -1;
+    const hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail_hip(e, "hipGetDevice");
+    if (dev != plan->device)
+        return fail(TVL_ERR_ARG, "tvl_sweep_plan_run: plan belongs to device %d, current is %d",
+                    plan->device, dev);
+    return plan_launch(plan, stream);
+}
+
+tvl_status tvl_sweep_plan_info(const tvl_plan *plan, int64_t *ntiles, int64_t *grid,
+                               int32_t *rows_per_tile)
+{
+    if (!plan) return fail(TVL_ERR_NULL, "tvl_sweep_plan_info: plan is NULL");
+    if (ntiles) *ntiles = plan->ntiles;
+    if (grid) *grid = plan->grid;
+    if (rows_per_tile) *rows_per_tile = plan->shape.R * plan->shape.W;
+    return TVL_OK;
+}
+
+tvl_status tvl_sweep_plan_destroy(tvl_plan *plan)
+{
+    plan_free(plan);
+    return TVL_OK;
+}
+
+tvl_status tvl_gemv_batch_sweep(const tvl_item *items, int32_t n, hipStream_t stream)
+{
+    g_err[0] = 0;
+    tvl_status st = check_items(items, n);
+    if (st != TVL_OK) return st;
+    if (n == 0) return TVL_OK;
+    int dev = 0;
+    DevInfo info;
+    st = current_device(&dev, &info);
+    if (st != TVL_OK) return st;
+    std::string key(reinterpret_cast<const char *>(&dev), sizeof dev);
+    key.append(reinterpret_cast<const char *>(items), sizeof(tvl_item) * (size_t)n);
+    tvl_plan *p = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        auto it = g_cache.find(key);
+        if (it != g_cache.end()) p = it->second;
+    }
+    if (!p) {
+        st = plan_build(items, n, nullptr, &p);
+        if (st != TVL_OK) return st;
+        std::lock_guard<std::mutex> lk(g_mu);
+        if (g_cache.size() >= kCacheMax) {
+            for (auto &kv : g_cache)
+                plan_free(kv.second);
+            g_cache.clear();
+        }
+        auto ins = g_cache.emplace(key, p);
+        if (!ins.second) { // another thread built the same list meanwhile
+            plan_free(p);
+            p = ins.first->second;
+        }
+    }
+    return plan_launch(p, stream);
+}
+
+tvl_status tvl_release_workspaces(void)
+{
+    g_err[0] = 0;
+    std::lock_guard<std::mutex> lk(g_mu);
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    for (auto &kv : g_ws) {
+        (void)hipSetDevice(kv.first.first);
+        (void)hipDeviceSynchronize();
+        (void)hipFree(kv.second.partials);
+        (void)hipFree(kv.second.counters);
+    }
+    g_ws.clear();
+    for (auto &kv : g_cache)
+        plan_free(kv.second);
+    g_cache.clear();
+    if (cur >= 0) (void)hipSetDevice(cur);
+    return TVL_OK;
+}
+
+tvl_status tvl_util_read_stream(const void *src, int64_t bytes, float *sink, int64_t sink_len,
+                                int64_t *grid_out, hipStream_t stream)
+{
+    g_err[0] = 0;
+    if (!src || !sink) return fail(TVL_ERR_NULL, "tvl_util_read_stream: NULL pointer");
+    if (bytes < 16 || bytes % 16 || sink_len < 1 || sink_len > (1 << 20))
+        return fail(TVL_ERR_SHAPE, "tvl_util_read_stream: bytes must be a positive multiple of "
+                                   "16 and 1 <= sink_len <= 2^20");
+    if (reinterpret_cast<uintptr_t>(src) % 16 || reinterpret_cast<uintptr_t>(sink) % 4)
+        return fail(TVL_ERR_ALIGN, "tvl_util_read_stream: src 16-byte, sink 4-byte aligned");
+    if (grid_out) *grid_out = sink_len;
+    const hipError_t e = tvl::launch_read_stream(src, bytes, sink, (int)sink_len, stream);
+    if (e != hipSuccess) return fail_hip(e, "read_stream launch");
+    return TVL_OK;
+}
+
+tvl_status tvl_util_copy(void *dst, const void *src, int64_t bytes, hipStream_t stream)
+{
+    g_err[0] = 0;
+    if (!src || !dst) return fail(TVL_ERR_NULL, "tvl_util_copy: NULL pointer");
+    if (bytes < 16 || bytes % 16) return fail(TVL_ERR_SHAPE, "tvl_util_copy: bytes % 16 != 0");
+    if (reinterpret_cast<uintptr_t>(src) % 16 || reinterpret_cast<uintptr_t>(dst) % 16)
+        return fail(TVL_ERR_ALIGN, "tvl_util_copy: 16-byte alignment required");
+    if (overlap(Range{(uintptr_t)src, (uintptr_t)src + (uintptr_t)bytes},
+                Range{(uintptr_t)dst, (uintptr_t)dst + (uintptr_t)bytes}))
+        return fail(TVL_ERR_ALIAS, "tvl_util_copy: overlap");
+    const hipError_t e = tvl::launch_copy(dst, src, bytes, stream);
+    if (e != hipSuccess) return fail_hip(e, "copy launch");
+    return TVL_OK;
+}
+
+const char *tvl_status_str(int32_t status)
+{
+    switch (status) {
+    case TVL_OK: return "TVL_OK";
+    case TVL_ERR_NULL: return "TVL_ERR_NULL: a required pointer is NULL";
+    case TVL_ERR_SHAPE: return "TVL_ERR_SHAPE: invalid M, K, ldw or count";
+    case TVL_ERR_ALIGN: return "TVL_ERR_ALIGN: TVL alignment violated";
+    case TVL_ERR_DTYPE: return "TVL_ERR_DTYPE: unknown weight dtype";
+    case TVL_ERR_ALIAS: return "TVL_ERR_ALIAS: an output overlaps an input or output";
+    case TVL_ERR_HIP: return "TVL_ERR_HIP: HIP runtime error";
+    case TVL_ERR_NOMEM: return "TVL_ERR_NOMEM: allocation failed";
+    case TVL_ERR_ARG: return "TVL_ERR_ARG: unsupported argument";
+    default: return "unknown tvl_status";
+    }
+}
+
+const char *tvl_last_error(void) { return g_err; }
+
+}  // extern "C"

@@ -1,0 +1,74 @@
+// tvl_internal.h -- declarations shared by the C-ABI layer (tvl_abi.cpp) and
+// the gfx950 kernels (tvl_kernels.hip).  Not installed, not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace tvl {
+
+constexpr int kWave = 64;          // CDNA wavefront width
+constexpr int kLineBytes = 128;    // TVL row alignment: one gfx950 L2 cache line
+constexpr int kChunkElems = 512;   // LDS slice granularity: 64 lanes x 8 fp16 = 2 x (64 x 4 fp32)
+constexpr int kSliceCap = 8192;    // x elements staged per pass: 32 KB of LDS
+
+// One GEMV as the kernels read it (48 bytes).  M and K fit in int32 (the
+// ABI rejects larger), ldw stays 64-bit.
+struct DevItem {
+    const void *W;
+    int64_t ldw;
+    const float *x;
+    float *y;
+    int32_t M;
+    int32_t K;
+    int32_t dtype;
+    int32_t pad;
+};
+static_assert(sizeof(DevItem) == 48, "DevItem layout");
+
+// One row tile of a sweep: item index and first row.
+struct DevTile {
+    int32_t item;
+    int32_t row0;
+};
+static_assert(sizeof(DevTile) == 8, "DevTile layout");
+
+// Launch shape: rows per wave, waves per block, loads in flight per row,
+// streaming (non-temporal) or cached weight loads.
+struct Shape {
+    int R;
+    int W;
+    int U;
+    bool cached;
+};
+
+bool shape_supported(const Shape &s);
+
+// Elements of x staged per LDS pass for a row of K columns.
+inline int slice_cap(int64_t K)
+{
+    const int64_t r = (K + kChunkElems - 1) / kChunkElems * kChunkElems;
+    return (int)(r < kSliceCap ? r : kSliceCap);
+}
+
+hipError_t launch_gemv_rows(const Shape &s, int dtype, const void *W, int64_t ldw,
+                            const float *x, float *y, int M, int K, hipStream_t st);
+
+hipError_t launch_gemv_ksplit(const Shape &s, int dtype, const void *W, int64_t ldw,
+                              const float *x, float *y, int M, int K, int S,
+                              float *partials, int *counters, hipStream_t st);
+
+hipError_t launch_sweep(const Shape &s, const DevItem *items, const DevTile *tiles,
+                        int ntiles, int grid, int ks_cap, hipStream_t st);
+
+hipError_t launch_pack(int dtype, void *dst, int64_t ldw, const void *src, int64_t M,
+                       int64_t K, hipStream_t st);
+
+hipError_t launch_zero_i32(int *p, int64_t n, hipStream_t st);
+
+hipError_t launch_read_stream(const void *src, int64_t bytes, float *sink, int grid,
+                              hipStream_t st);
+
+hipError_t launch_copy(void *dst, const void *src, int64_t bytes, hipStream_t st);
+
+}  // namespace tvl

@@ -1,0 +1,544 @@
+// tvl_kernels.hip -- gfx950 (MI355X) kernels of the TVL GEMV path.
+//
+// y = W x over row-major weights (Kilictas & Alpay, arXiv 2601.03324,
+// Sec. 6.1).  A GEMV moves |W| + |x| + |y| bytes for 2|W| flops (Sec. 3.1):
+// 0.5 flop per byte at fp32, far below the fp32 vector ridge of MI355X, so
+// these kernels are built around HBM streaming, not arithmetic:
+//
+//   * every weight byte is read exactly once, with 16-byte per-lane loads
+//     (one wavefront load = 1 KB contiguous = 8 full 128-byte lines, the
+//     GPU form of the paper's "one vector load touches one cache line",
+//     Sec. 3.2); rows start on 128-byte boundaries (TVL layout);
+//   * x is staged once per workgroup in LDS (in slices of up to 8192
+//     elements) and each x vector read from LDS is reused for R rows held by
+//     the same wavefront;
+//   * each lane keeps 4 independent fp32 accumulators per row (the paper's
+//     four-accumulator ILP, Sec. 11.1) and U loads per row in flight, so a
+//     wavefront has R*U KB of weights outstanding;
+//   * a wavefront reduces its R rows jointly: R values per lane are halved
+//     across lanes in log2(R) exchange steps, then summed over the rest (the
+//     horizontal add at the end of the GEMV listing, Sec. 6.1, done across
+//     64 lanes); the order is fixed, so results are bitwise reproducible.
+//
+// No MFMA: a GEMV is not a dense contraction.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tvl_internal.h"
+
+namespace tvl {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+
+template <typename T>
+struct Vec;
+template <>
+struct Vec<float> {
+    using type = f4;
+    static constexpr int N = 4;
+};
+template <>
+struct Vec<_Float16> {
+    using type = h8;
+    static constexpr int N = 8;
+};
+
+// Global (address space 1) pointers: the weights and x arrive as generic
+// pointers inside descriptors, and a generic access would compile to a flat
+// load, which shares its wait counter with LDS reads and serialises the
+// stream.  A global load keeps its own in-order counter.
+#define TVL_GLOBAL __attribute__((address_space(1)))
+
+template <typename T, bool CACHED>
+__device__ __forceinline__ typename Vec<T>::type load_w(const T *p)
+{
+    using V = typename Vec<T>::type;
+    const TVL_GLOBAL V *g = (const TVL_GLOBAL V *)(p);
+    if constexpr (CACHED)
+        return *g;
+    else
+        return __builtin_nontemporal_load(g);
+}
+
+__device__ __forceinline__ void fma4(f4 &a, const f4 w, const f4 x)
+{
+    a.x = __builtin_fmaf(w.x, x.x, a.x);
+    a.y = __builtin_fmaf(w.y, x.y, a.y);
+    a.z = __builtin_fmaf(w.z, x.z, a.z);
+    a.w = __builtin_fmaf(w.w, x.w, a.w);
+}
+
+// One 16-byte weight vector times its x values from LDS.
+// fp32: vector v holds columns 4v..4v+3, x at xs4[v].
+// fp16: vector v holds columns 8v..8v+7; LDS keeps x in two planes so that
+//       both reads are unit-stride across lanes: xs4[v] = 8v..8v+3 and
+//       xs4[plane + v] = 8v+4..8v+7.  The conversion is exact.
+__device__ __forceinline__ void mac(f4 &a, const f4 w, const f4 *xs4, int v, int)
+{
+    fma4(a, w, xs4[v]);
+}
+__device__ __forceinline__ void mac(f4 &a, const h8 w, const f4 *xs4, int v, int plane)
+{
+    const f8 wf = __builtin_convertvector(w, f8);
+    const f4 lo = {wf[0], wf[1], wf[2], wf[3]};
+    const f4 hi = {wf[4], wf[5], wf[6], wf[7]};
+    fma4(a, lo, xs4[v]);
+    fma4(a, hi, xs4[plane + v]);
+}
+
+template <typename V, int N>
+__device__ __forceinline__ V mask_from(V w, int valid)
+{
+#pragma unroll
+    for (int e = 0; e < N; ++e)
+        if (e >= valid) w[e] = 0;
+    return w;
+}
+
+// Stage x[0..kn) of the current slice into LDS, zero-filled to a whole
+// number of weight vectors (so masked tail products are exactly 0 * 0).
+template <typename T>
+__device__ __forceinline__ void stage_x(const float *__restrict__ xg, int kn, f4 *__restrict__ xs4,
+                                        int plane)
+{
+    constexpr int N = Vec<T>::N;
+    const int nq = (kn + N - 1) / N * (N / 4);
+    for (int q = threadIdx.x; q < nq; q += blockDim.x) {
+        const int j = q * 4;
+        f4 val;
+        if (j + 4 <= kn) {
+            val = *(const TVL_GLOBAL f4 *)(xg + j);
+        } else {
+            val = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (j + e < kn) val[e] = *(const TVL_GLOBAL float *)(xg + j + e);
+        }
+        if constexpr (N == 4)
+            xs4[q] = val;
+        else
+            xs4[(q & 1) * plane + (q >> 1)] = val;
+    }
+}
+
+// Accumulate columns [0, kn) of one LDS slice for R rows of one wavefront.
+// w0 points at column 0 of the slice in the wavefront's first row; rows
+// r >= nrows re-read row nrows-1 (their results are discarded).
+template <typename T, int R, int U, bool CACHED>
+__device__ __forceinline__ void dot_slice(const T *__restrict__ w0, int64_t ldw, int nrows,
+                                          const f4 *__restrict__ xs4, int plane, int kn,
+                                          int lane, f4 (&acc)[R])
+{
+    using V = typename Vec<T>::type;
+    constexpr int N = Vec<T>::N;
+    constexpr int CH = kWave * N; // elements per wavefront load
+    const int nv = (kn + N - 1) / N;
+    const int nfull = kn / CH;
+    const T *rows[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        rows[r] = w0 + (int64_t)(r < nrows ? r : nrows - 1) * ldw + lane * N;
+
+    int c = 0;
+    for (; c + U <= nfull; c += U) {
+        V w[U][R];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                w[u][r] = load_w<T, CACHED>(rows[r] + (c + u) * CH);
+        // keep all U*R loads ahead of the first multiply: left alone, the
+        // scheduler interleaves them with the FMAs to save registers and
+        // only two or three loads stay in flight
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                mac(acc[r], w[u][r], xs4, (c + u) * kWave + lane, plane);
+    }
+    for (; c < nfull; ++c) {
+        V w[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            w[r] = load_w<T, CACHED>(rows[r] + c * CH);
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            mac(acc[r], w[r], xs4, c * kWave + lane, plane);
+    }
+    if (c * kWave < nv) { // ragged last chunk
+        const int v = c * kWave + lane;
+        if (v < nv) {
+            const int valid = kn - v * N;
+            V w[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                w[r] = load_w<T, CACHED>(rows[r] + c * CH);
+            if (valid < N) {
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    w[r] = mask_from<V, N>(w[r], valid);
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                mac(acc[r], w[r], xs4, v, plane);
+        }
+    }
+}
+
+// Exchange step of the joint reduction: lanes with bit O set keep the upper
+// H values, the others the lower H, each adding its partner's copy.
+template <int H, int O>
+__device__ __forceinline__ void halve(float *v, int lane)
+{
+    const bool up = (lane & O) != 0;
+#pragma unroll
+    for (int i = 0; i < H; ++i) {
+        const float send = up ? v[i] : v[i + H];
+        const float keep = up ? v[i + H] : v[i];
+        v[i] = keep + __shfl_xor(send, O);
+    }
+}
+
+// Reduce R rows of per-lane float4 partials over the wavefront.  On return
+// every lane holds the total of row lane / (64 / R).
+template <int R>
+__device__ __forceinline__ float reduce_rows(const f4 (&acc)[R], int lane)
+{
+    float v[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        v[r] = (acc[r].x + acc[r].y) + (acc[r].z + acc[r].w);
+    if constexpr (R == 8) {
+        halve<4, 32>(v, lane);
+        halve<2, 16>(v, lane);
+        halve<1, 8>(v, lane);
+    } else if constexpr (R == 4) {
+        halve<2, 32>(v, lane);
+        halve<1, 16>(v, lane);
+    } else if constexpr (R == 2) {
+        halve<1, 32>(v, lane);
+    }
+#pragma unroll
+    for (int o = 32 / R; o >= 1; o >>= 1)
+        v[0] += __shfl_xor(v[0], o);
+    return v[0];
+}
+
+// One row tile: WV wavefronts x R rows, columns [kbeg, kend).  out[row] gets
+// the tile's sum for each row < M.
+template <typename T, int R, int WV, int U, bool CACHED>
+__device__ __forceinline__ void gemv_tile(const T *__restrict__ W, int64_t ldw,
+                                          const float *__restrict__ x, int M, int row0, int kbeg,
+                                          int kend, int ks_cap, f4 *__restrict__ xs4,
+                                          float *__restrict__ out)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wrow0 = row0 + wave * R;
+    const int nrows = M - wrow0;
+    const int plane = ks_cap / 8;
+    f4 acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        acc[r] = f4{0.f, 0.f, 0.f, 0.f};
+
+    for (int k0 = kbeg; k0 < kend; k0 += ks_cap) {
+        const int kn = min(ks_cap, kend - k0);
+        __syncthreads(); // the previous slice (or tile) is no longer read
+        stage_x<T>(x + k0, kn, xs4, plane);
+        __syncthreads();
+        if (nrows > 0)
+            dot_slice<T, R, U, CACHED>(W + (int64_t)wrow0 * ldw + k0, ldw, min(nrows, R), xs4,
+                                       plane, kn, lane, acc);
+    }
+    const float v = reduce_rows<R>(acc, lane);
+    constexpr int G = kWave / R;
+    if (nrows > 0 && (lane % G) == 0) {
+        const int row = wrow0 + lane / G;
+        if (row < M) out[row] = v;
+    }
+}
+
+// ---------------------------------------------------------------- kernels
+template <typename T, int R, int WV, int U, bool CACHED>
+__global__ __launch_bounds__(WV *kWave) void k_gemv_rows(const T *__restrict__ W, int64_t ldw,
+                                                          const float *__restrict__ x,
+                                                          float *__restrict__ y, int M, int K,
+                                                          int ks_cap)
+{
+    extern __shared__ f4 smem4[];
+    gemv_tile<T, R, WV, U, CACHED>(W, ldw, x, M, (int)blockIdx.x * (R * WV), 0, K, ks_cap, smem4,
+                                   y);
+}
+
+// K split: workgroup b handles row tile b / S and K slice b % S.  Partials go
+// to partials[split * M + row]; the last workgroup of a tile to arrive (an
+// agent-scope counter) adds the S partials in the order 0..S-1 and resets
+// the counter to 0 for the next launch.
+template <typename T, int R, int WV, int U, bool CACHED>
+__global__ __launch_bounds__(WV *kWave) void k_gemv_ksplit(
+    const T *__restrict__ W, int64_t ldw, const float *__restrict__ x, float *__restrict__ y,
+    int M, int K, int ks_cap, int S, int kspan, float *__restrict__ partials,
+    int *__restrict__ counters)
+{
+    extern __shared__ f4 smem4[];
+    __shared__ int is_last;
+    const int tile = (int)blockIdx.x / S;
+    const int split = (int)blockIdx.x - tile * S;
+    const int row0 = tile * (R * WV);
+    const int kbeg = split * kspan;
+    const int kend = min(K, kbeg + kspan);
+    gemv_tile<T, R, WV, U, CACHED>(W, ldw, x, M, row0, kbeg, kend, ks_cap, smem4,
+                                   partials + (int64_t)split * M);
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int prev = __hip_atomic_fetch_add(counters + tile, 1, __ATOMIC_ACQ_REL,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+        is_last = (prev == S - 1);
+    }
+    __syncthreads();
+    if (is_last) {
+        __threadfence();
+        const int rows = min(R * WV, M - row0);
+        for (int r = threadIdx.x; r < rows; r += blockDim.x) {
+            float s = 0.f;
+            for (int p = 0; p < S; ++p)
+                s += __hip_atomic_load(partials + (int64_t)p * M + row0 + r, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+            y[row0 + r] = s;
+        }
+        if (threadIdx.x == 0)
+            __hip_atomic_store(counters + tile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// Grouped sweep: every GEMV of a decode token in one launch.  Workgroup b
+// takes tiles b, b + grid, ... of the plan's tile table (grid = number of
+// tiles gives one tile per workgroup and leaves the balancing to the
+// hardware dispatcher).
+template <int R, int WV, int U, bool CACHED>
+__global__ __launch_bounds__(WV *kWave) void k_sweep(const DevItem *__restrict__ items,
+                                                      const DevTile *__restrict__ tiles,
+                                                      int ntiles, int ks_cap)
+{
+    extern __shared__ f4 smem4[];
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const DevTile tl = tiles[t];
+        const DevItem it = items[tl.item];
+        if (it.dtype == 1)
+            gemv_tile<_Float16, R, WV, U, CACHED>(static_cast<const _Float16 *>(it.W), it.ldw,
+                                                  it.x, it.M, tl.row0, 0, it.K, ks_cap, smem4,
+                                                  it.y);
+        else
+            gemv_tile<float, R, WV, U, CACHED>(static_cast<const float *>(it.W), it.ldw, it.x,
+                                               it.M, tl.row0, 0, it.K, ks_cap, smem4, it.y);
+        // Drain this tile's y stores before the next tile's loads.  With a
+        // store still counted, the compiler's wait-count tracking treats the
+        // memory counter as out of order and waits for *all* loads before
+        // the first multiply of every chunk (vmcnt field 0; expcnt and
+        // lgkmcnt fields at their maxima, i.e. not waited on).
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+    }
+}
+
+template <typename E>
+__global__ __launch_bounds__(256) void k_pack(E *__restrict__ dst, int64_t ldw,
+                                              const E *__restrict__ src, int64_t M, int64_t K)
+{
+    for (int64_t row = blockIdx.x; row < M; row += gridDim.x)
+        for (int64_t j = threadIdx.x; j < ldw; j += blockDim.x)
+            dst[row * ldw + j] = (j < K) ? src[row * K + j] : E(0);
+}
+
+__global__ __launch_bounds__(256) void k_zero_i32(int *p, int64_t n)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = 0;
+}
+
+// Read-only streaming with the GEMV's load kind; one float per workgroup so
+// the loads cannot be optimised away.
+__global__ __launch_bounds__(256) void k_read_stream(const f4 *__restrict__ src, int64_t nvec,
+                                                     float *__restrict__ sink)
+{
+    __shared__ float red[4];
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (; i + 7 * stride < nvec; i += 8 * stride) {
+        f4 a[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            a[u] = __builtin_nontemporal_load(src + i + u * stride);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            acc += a[u];
+    }
+    for (; i < nvec; i += stride)
+        acc += __builtin_nontemporal_load(src + i);
+    float v = (acc.x + acc.y) + (acc.z + acc.w);
+    for (int o = 32; o >= 1; o >>= 1)
+        v += __shfl_xor(v, o);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x / 64] = v;
+    __syncthreads();
+    if (threadIdx.x == 0) sink[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__global__ __launch_bounds__(256) void k_copy(f4 *__restrict__ dst, const f4 *__restrict__ src,
+                                              int64_t nvec)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nvec;
+         i += (int64_t)gridDim.x * blockDim.x)
+        dst[i] = __builtin_nontemporal_load(src + i);
+}
+
+// ------------------------------------------------------ shape dispatch
+// (R, waves per block, U) triples the library instantiates.
+#define TVL_SHAPES(X)                                                                             \
+    X(1, 4, 8) X(1, 4, 16) X(2, 4, 4) X(2, 4, 8) X(4, 4, 2) X(4, 4, 4) X(8, 4, 2) X(1, 8, 8)      \
+        X(1, 8, 16) X(2, 8, 4) X(2, 8, 8) X(4, 8, 2) X(4, 8, 4) X(8, 8, 2) X(1, 2, 8) X(2, 2, 8)  \
+            X(4, 2, 4) X(8, 2, 2)
+
+template <int R, int WV, int U, bool C>
+struct Inst {
+    static hipError_t rows(int dtype, const void *W, int64_t ldw, const float *x, float *y, int M,
+                           int K, hipStream_t st)
+    {
+        const int ks = slice_cap(K);
+        const dim3 grid((M + R * WV - 1) / (R * WV)), block(WV * kWave);
+        if (dtype == 1)
+            hipLaunchKernelGGL((k_gemv_rows<_Float16, R, WV, U, C>), grid, block, ks * 4, st,
+                               static_cast<const _Float16 *>(W), ldw, x, y, M, K, ks);
+        else
+            hipLaunchKernelGGL((k_gemv_rows<float, R, WV, U, C>), grid, block, ks * 4, st,
+                               static_cast<const float *>(W), ldw, x, y, M, K, ks);
+        return hipGetLastError();
+    }
+    static hipError_t ksplit(int dtype, const void *W, int64_t ldw, const float *x, float *y,
+                             int M, int K, int S, float *partials, int *counters, hipStream_t st)
+    {
+        // slice width: a whole number of LDS chunks, S' = ceil(K / kspan) <= S
+        const int per = (K + S - 1) / S;
+        const int kspan = (per + kChunkElems - 1) / kChunkElems * kChunkElems;
+        const int Se = (K + kspan - 1) / kspan;
+        const int ks = slice_cap(kspan);
+        const int tiles = (M + R * WV - 1) / (R * WV);
+        const dim3 grid(tiles * Se), block(WV * kWave);
+        if (dtype == 1)
+            hipLaunchKernelGGL((k_gemv_ksplit<_Float16, R, WV, U, C>), grid, block, ks * 4, st,
+                               static_cast<const _Float16 *>(W), ldw, x, y, M, K, ks, Se, kspan,
+                               partials, counters);
+        else
+            hipLaunchKernelGGL((k_gemv_ksplit<float, R, WV, U, C>), grid, block, ks * 4, st,
+                               static_cast<const float *>(W), ldw, x, y, M, K, ks, Se, kspan,
+                               partials, counters);
+        return hipGetLastError();
+    }
+    static hipError_t sweep(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
+                            int ks_cap, hipStream_t st)
+    {
+        hipLaunchKernelGGL((k_sweep<R, WV, U, C>), dim3(grid), dim3(WV * kWave), ks_cap * 4, st,
+                           items, tiles, ntiles, ks_cap);
+        return hipGetLastError();
+    }
+};
+
+}  // namespace
+
+bool shape_supported(const Shape &s)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return true;
+    TVL_SHAPES(X)
+#undef X
+    return false;
+}
+
+hipError_t launch_gemv_rows(const Shape &s, int dtype, const void *W, int64_t ldw,
+                            const float *x, float *y, int M, int K, hipStream_t st)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return s.cached ? Inst<R_, W_, U_, true>::rows(dtype, W, ldw, x, y, M, K, st)             \
+                        : Inst<R_, W_, U_, false>::rows(dtype, W, ldw, x, y, M, K, st);
+    TVL_SHAPES(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemv_ksplit(const Shape &s, int dtype, const void *W, int64_t ldw,
+                              const float *x, float *y, int M, int K, int S, float *partials,
+                              int *counters, hipStream_t st)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return s.cached                                                                           \
+                   ? Inst<R_, W_, U_, true>::ksplit(dtype, W, ldw, x, y, M, K, S, partials,       \
+                                                    counters, st)                                 \
+                   : Inst<R_, W_, U_, false>::ksplit(dtype, W, ldw, x, y, M, K, S, partials,      \
+                                                     counters, st);
+    TVL_SHAPES(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_sweep(const Shape &s, const DevItem *items, const DevTile *tiles, int ntiles,
+                        int grid, int ks_cap, hipStream_t st)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return s.cached ? Inst<R_, W_, U_, true>::sweep(items, tiles, ntiles, grid, ks_cap, st)   \
+                        : Inst<R_, W_, U_, false>::sweep(items, tiles, ntiles, grid, ks_cap, st);
+    TVL_SHAPES(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_pack(int dtype, void *dst, int64_t ldw, const void *src, int64_t M, int64_t K,
+                       hipStream_t st)
+{
+    const int grid = (int)(M < 65536 ? M : 65536);
+    if (dtype == 1)
+        hipLaunchKernelGGL(k_pack<uint16_t>, dim3(grid), dim3(256), 0, st,
+                           static_cast<uint16_t *>(dst), ldw, static_cast<const uint16_t *>(src),
+                           M, K);
+    else
+        hipLaunchKernelGGL(k_pack<uint32_t>, dim3(grid), dim3(256), 0, st,
+                           static_cast<uint32_t *>(dst), ldw, static_cast<const uint32_t *>(src),
+                           M, K);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero_i32(int *p, int64_t n, hipStream_t st)
+{
+    int64_t g = (n + 255) / 256;
+    const int grid = (int)(g < 4096 ? (g > 0 ? g : 1) : 4096);
+    hipLaunchKernelGGL(k_zero_i32, dim3(grid), dim3(256), 0, st, p, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_read_stream(const void *src, int64_t bytes, float *sink, int grid,
+                              hipStream_t st)
+{
+    hipLaunchKernelGGL(k_read_stream, dim3(grid), dim3(256), 0, st,
+                       static_cast<const f4 *>(src), bytes / 16, sink);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy(void *dst, const void *src, int64_t bytes, hipStream_t st)
+{
+    const int64_t nvec = bytes / 16;
+    int64_t g = (nvec + 255) / 256;
+    const int grid = (int)(g < 8192 ? (g > 0 ? g : 1) : 8192);
+    hipLaunchKernelGGL(k_copy, dim3(grid), dim3(256), 0, st, static_cast<f4 *>(dst),
+                       static_cast<const f4 *>(src), nvec);
+    return hipGetLastError();
+}
+
+}  // namespace tvl

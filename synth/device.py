@@ -1,0 +1,72 @@
+"""Put a synthetic workload on the GPU (torch allocations, TVL row layout).
+
+Input plumbing shared by the GPU tests and the benchmark: draws each matrix
+with the generator of this package, uploads it, and gives every GEMV its own
+x and y buffers.  No GEMV arithmetic happens here.
+"""
+from __future__ import annotations
+
+import sys
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import MatSpec, Workload
+
+
+@dataclass
+class DevGemv:
+    spec: MatSpec
+    W: object  # TvlMatrix
+    x: object  # torch fp32 [K]
+    y: object  # torch fp32 [M]
+
+    def item(self):
+        from paper_2601_03324_amd import tvl
+        return (self.W.ptr, self.W.ldw, self.x, self.y, self.spec.M, self.spec.K, self.W.dtype)
+
+
+def dtype_code(spec: MatSpec) -> int:
+    return 0 if spec.dtype == "f32" else 1
+
+
+def load(wl: Workload, device="cuda", rep: int = 0, progress: bool = False,
+         share_from: list | None = None) -> list:
+    """Upload every matrix of ``wl``.  ``share_from`` reuses the weight buffers
+    of an earlier load (fresh x and y only)."""
+    import torch
+    from paper_2601_03324_amd import tvl
+    out = []
+    for i, m in enumerate(wl.mats):
+        if share_from is not None:
+            Wd = share_from[i].W
+        else:
+            Wd = tvl.upload_matrix(m.weights(), dtype_code(m), device)
+        x = torch.from_numpy(m.x(rep)).to(device)
+        y = torch.full((m.M,), float("nan"), dtype=torch.float32, device=device)
+        out.append(DevGemv(m, Wd, x, y))
+        if progress and (i % 16 == 0 or i == len(wl.mats) - 1):
+            print(f"  loaded {wl.name} {i + 1}/{len(wl.mats)}", flush=True, file=sys.stderr)
+    return out
+
+
+def clone_weights(gemvs: list, device="cuda") -> list:
+    """A second copy of every weight matrix (same values, new addresses) with
+    its own x and y: lets a benchmark alternate between copies so that the
+    256 MB last-level cache cannot serve a sweep from the previous one."""
+    import torch
+    from paper_2601_03324_amd import tvl
+    out = []
+    for g in gemvs:
+        buf = g.W.buf.clone()
+        Wd = tvl.TvlMatrix(buf, g.W.M, g.W.K, g.W.ldw, g.W.dtype)
+        out.append(DevGemv(g.spec, Wd, g.x.clone(), torch.empty_like(g.y)))
+    return out
+
+
+def sample_rows(M: int, n: int, seed: int) -> np.ndarray:
+    """First, last and n-2 seeded random rows of an M-row matrix (sorted, unique)."""
+    rng = np.random.default_rng(seed)
+    rows = {0, M - 1}
+    rows.update(int(r) for r in rng.integers(0, M, max(n - 2, 0)))
+    return np.array(sorted(rows), dtype=np.int64)

@@ -1,0 +1,166 @@
+"""The C-ABI library on a host without a GPU (CPU only).
+
+The library must load, export every entry point ``include/tvl.h`` declares,
+and reject every bad argument with the documented status before it makes any
+HIP call (fake pointers are passed; none is ever dereferenced).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tvl.h")
+
+tvl = pytest.importorskip("paper_2601_03324_amd.tvl",
+                          reason="libtvl.so not built (run __graft_entry__.build())")
+L = tvl.lib
+
+OK, NULL, SHAPE, ALIGN, DTYPE, ALIAS, HIP, NOMEM, ARG = 0, -1, -2, -3, -4, -5, -6, -7, -8
+A = 1 << 40  # fake, 128-byte aligned device addresses far apart
+B = 2 << 40
+C = 3 << 40
+
+
+def declared_symbols():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"TVL_API\s+[\w\s\*]+?\b(tvl_\w+)\s*\(", txt)))
+
+
+def test_exports_every_declared_symbol():
+    syms = declared_symbols()
+    assert len(syms) >= 15
+    for s in syms:
+        assert hasattr(L, s), s
+    assert set(syms) == set(tvl.EXPORTS)
+    assert tvl.tvl_version() == 100
+
+
+def test_missing_library_fails_loudly(tmp_path, monkeypatch):
+    monkeypatch.setattr(tvl, "LIB_PATH", str(tmp_path / "libtvl.so"))
+    with pytest.raises(ImportError):
+        tvl._load()
+
+
+def test_item_layout_matches_header():
+    assert ctypes.sizeof(tvl.tvl_item) == 56
+    assert tvl.tvl_item.dtype.offset == 48
+    assert ctypes.sizeof(tvl.tvl_tuning) == 24
+
+
+@pytest.mark.parametrize("K,dt,ldw", [(1, 0, 32), (32, 0, 32), (33, 0, 64), (768, 0, 768),
+                                      (11008, 0, 11008), (1, 1, 64), (64, 1, 64), (65, 1, 128),
+                                      (28672, 1, 28672), (100, 0, 128), (100, 1, 128)])
+def test_row_stride(K, dt, ldw):
+    assert tvl.tvl_row_stride(K, dt) == ldw
+
+
+def test_row_stride_rejects():
+    assert tvl.tvl_row_stride(0, 0) == -1
+    assert tvl.tvl_row_stride(5, 7) == -1
+    assert tvl.tvl_row_stride(-3, 1) == -1
+
+
+def gemv(W=A, ldw=768, dt=0, x=B, y=C, M=768, K=768, tuning=None):
+    t = None if tuning is None else ctypes.byref(tvl.tvl_tuning(**tuning))
+    return L.tvl_gemv_ex(W, ldw, dt, x, y, M, K, t, None)
+
+
+@pytest.mark.parametrize("kw,st", [
+    (dict(W=0), NULL), (dict(x=0), NULL), (dict(y=0), NULL),
+    (dict(dt=2), DTYPE), (dict(dt=-1), DTYPE),
+    (dict(M=0), SHAPE), (dict(K=0), SHAPE), (dict(M=-5), SHAPE), (dict(M=1 << 31), SHAPE),
+    (dict(K=(1 << 30) + 1, ldw=(1 << 30) + 32), SHAPE), (dict(ldw=767), SHAPE),
+    (dict(W=A + 64), ALIGN), (dict(ldw=770), ALIGN), (dict(dt=1, ldw=800), ALIGN),
+    (dict(x=B + 8), ALIGN), (dict(y=C + 2), ALIGN),
+    (dict(y=A + 4096), ALIAS), (dict(y=B - 4), ALIAS), (dict(x=C + 1024), ALIAS),
+    (dict(tuning=dict(rows_per_wave=3)), ARG), (dict(tuning=dict(unroll=-1)), ARG),
+    (dict(tuning=dict(rows_per_wave=8, unroll=16)), ARG), (dict(tuning=dict(flags=2)), ARG),
+    (dict(tuning=dict(ksplit=5000)), ARG),
+])
+def test_gemv_rejects(kw, st):
+    assert gemv(**kw) == st
+    assert tvl.tvl_last_error() != ""
+    assert tvl.tvl_status_str(st).startswith(tvl.STATUS[st])
+
+
+def test_alias_boundaries_are_exact():
+    # y ends exactly where W starts: no overlap, so validation passes and the
+    # call gets as far as the device query (which fails without a GPU)
+    M = 768
+    st = gemv(W=A, y=A - 4 * M)
+    assert st in (OK, HIP)
+    assert gemv(W=A, y=A - 4 * M + 4) == ALIAS
+    # the matrix spans M whole rows of ldw = 1024 > K elements
+    end = A + M * 1024 * 4
+    assert gemv(W=A, ldw=1024, y=end) in (OK, HIP)
+    assert gemv(W=A, ldw=1024, y=end - 4) == ALIAS
+
+
+def items(*specs):
+    arr, n = tvl.make_items(specs)
+    return arr, n
+
+
+def test_sweep_rejects_and_enqueues_nothing():
+    good = (A, 768, B, C, 768, 768, 0)
+    bad_align = (A + 8, 768, B, C + (1 << 20), 768, 768, 0)
+    arr, n = items(good, bad_align)
+    assert L.tvl_gemv_batch_sweep(arr, n, None) == ALIGN
+    assert "item 1" in tvl.tvl_last_error()
+    # two outputs overlapping
+    arr, n = items(good, (A + (1 << 30), 768, B, C + 100 * 4, 768, 768, 0))
+    assert L.tvl_gemv_batch_sweep(arr, n, None) == ALIAS
+    # output of one item over the x of another
+    arr, n = items(good, (A + (1 << 30), 768, C + 16, C + (1 << 24), 768, 768, 0))
+    assert L.tvl_gemv_batch_sweep(arr, n, None) == ALIAS
+    # reserved field must be zero
+    arr, n = items(good)
+    arr[0].reserved = 1
+    assert L.tvl_gemv_batch_sweep(arr, n, None) == ARG
+    assert L.tvl_gemv_batch_sweep(None, 3, None) == NULL
+    assert L.tvl_gemv_batch_sweep(None, -1, None) == SHAPE
+    # an empty sweep is a no-op that needs no device
+    assert L.tvl_gemv_batch_sweep(None, 0, None) == OK
+
+
+def test_shared_inputs_are_not_aliases():
+    # tied weights and a shared x are legal: only outputs may not overlap
+    arr, n = items((A, 768, B, C, 768, 768, 0), (A, 768, B, C + 4096, 768, 768, 0))
+    st = L.tvl_gemv_batch_sweep(arr, n, None)
+    assert st in (OK, HIP)
+
+
+def test_plan_api_rejects():
+    h = ctypes.c_void_p()
+    arr, n = items((A, 768, B, C, 768, 768, 0))
+    assert L.tvl_sweep_plan_create(arr, n, None, None) == NULL
+    t = tvl.tvl_tuning(ksplit=2)
+    assert L.tvl_sweep_plan_create(arr, n, ctypes.byref(t), ctypes.byref(h)) == ARG
+    assert h.value is None
+    assert L.tvl_sweep_plan_run(None, None) == NULL
+    assert L.tvl_sweep_plan_info(None, None, None, None) == NULL
+    assert L.tvl_sweep_plan_destroy(None) == OK  # idempotent on NULL
+    assert L.tvl_sweep_plan_destroy(None) == OK
+
+
+def test_pack_and_utils_reject():
+    assert L.tvl_pack_rows(0, 32, B, 4, 4, 0, None) == NULL
+    assert L.tvl_pack_rows(A, 4, B, 4, 4, 0, None) == ALIGN
+    assert L.tvl_pack_rows(A, 32, B, 4, 40, 0, None) == SHAPE
+    assert L.tvl_pack_rows(A, 32, A + 64, 4, 4, 0, None) == ALIAS
+    assert L.tvl_pack_rows(A, 32, B + 2, 4, 4, 0, None) == ALIGN
+    assert L.tvl_pack_rows(A, 32, B, 4, 4, 9, None) == DTYPE
+    assert L.tvl_util_copy(A, A + 16, 64, None) == ALIAS
+    assert L.tvl_util_copy(A, B, 60, None) == SHAPE
+    assert L.tvl_util_read_stream(A, 64, B, 0, None, None) == SHAPE
+    assert L.tvl_util_read_stream(A + 8, 64, B, 4, None, None) == ALIGN
+
+
+def test_status_strings():
+    for code, name in tvl.STATUS.items():
+        assert tvl.tvl_status_str(code).startswith(name)
+    assert tvl.tvl_status_str(42) == "unknown tvl_status"
