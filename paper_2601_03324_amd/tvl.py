@@ -49,10 +49,26 @@ class tvl_tuning(ctypes.Structure):
 assert ctypes.sizeof(tvl_item) == 56
 
 
+def _bind_hip_runtime() -> None:
+    """One HIP runtime per process.  torch ships its own libamdhip64 (same
+    soname as the system one); device pointers and stream handles from torch
+    are only valid in that runtime instance.  Loading it globally before
+    libtvl.so makes the library's libamdhip64.so.7 dependency resolve to the
+    already-loaded copy instead of a second runtime from /opt/rocm."""
+    try:
+        import torch
+    except ImportError:
+        return
+    hip = os.path.join(os.path.dirname(torch.__file__), "lib", "libamdhip64.so")
+    if os.path.exists(hip):
+        ctypes.CDLL(hip, mode=ctypes.RTLD_GLOBAL)
+
+
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run paper_2601_03324_amd.build.build() "
                           f"(hipcc --offload-arch=gfx950)")
+    _bind_hip_runtime()
     L = ctypes.CDLL(LIB_PATH)
     P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
     sig = {
