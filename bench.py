@@ -89,7 +89,8 @@ def main() -> int:
     ap.add_argument("--waves-per-block", type=int, default=0)
     ap.add_argument("--unroll", type=int, default=0)
     ap.add_argument("--grid", type=int, default=0)
-    ap.add_argument("--cached-loads", action="store_true")
+    ap.add_argument("--x-mode", choices=("auto", "lds", "direct"), default="auto",
+                    help="how wavefronts get x (default: the library's choice)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain copy of this many MiB before timing (counter calibration)")
     args = ap.parse_args()
@@ -122,7 +123,8 @@ def main() -> int:
         gemvs_a.append(sdev.DevGemv(m, Wd, x, y))
     copies = [gemvs_a] if args.warm else [gemvs_a, sdev.clone_weights(gemvs_a)]
     tuning = dict(rows_per_wave=args.rows_per_wave, waves_per_block=args.waves_per_block,
-                  unroll=args.unroll, grid=args.grid, flags=1 if args.cached_loads else 0)
+                  unroll=args.unroll, grid=args.grid,
+                  flags={"auto": 0, "lds": 1, "direct": 2}[args.x_mode])
     plans = [tvl.tvl_sweep_plan_create([g.item() for g in c], tuning) for c in copies]
     info = plans[0].info()
     torch.cuda.synchronize()

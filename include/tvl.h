@@ -100,15 +100,24 @@ typedef struct tvl_item {
 
 /* Launch shape override.  A zero field means "choose by shape".
  *   rows_per_wave   R in {1, 2, 4, 8}: rows one wavefront computes at once
- *   waves_per_block W in {2, 4, 8}: wavefronts per workgroup
- *   unroll          U in {2, 4, 8, 16}: 16-byte loads per row kept in flight
- *                   per lane (only the pairs (R,U) the library instantiates
- *                   are accepted: (1,8) (1,16) (2,4) (2,8) (4,2) (4,4) (8,2))
- *   ksplit          S >= 1: K slices per row tile (tvl_gemv only; 1 = row split)
+ *   waves_per_block W in {1, 2, 4, 8}: wavefronts per workgroup
+ *   unroll          U in {1, 2, 3, 4, 8}: 16-byte weight loads per row kept in
+ *                   flight per lane
+ *   ksplit          S >= 1: K slices per row tile (tvl_gemv only; 1 = row
+ *                   split; LDS-x mode only)
  *   grid            workgroups of a sweep launch (0 = one per tile); a smaller
  *                   grid makes each workgroup loop over tiles
- *   flags           bit 0: plain (cached) weight loads instead of streaming
- *                   (non-temporal) loads */
+ *   flags           TVL_FLAG_X_LDS: stage x once per workgroup in LDS;
+ *                   TVL_FLAG_X_DIRECT: each wavefront reads x from global
+ *                   memory (L1/L2-cached) next to its weights; neither: the
+ *                   library's default mode.
+ * Only the triples (R, W, U) the library instantiates for the chosen x mode
+ * are accepted (others give TVL_ERR_ARG):
+ *   LDS-x:    W=4: (1,4) (1,8) (2,2) (2,3) (2,4) (2,8) (4,1) (4,2) (4,3) (4,4)
+ *                  (8,1) (8,2);  W=8: (2,4) (2,8) (4,2);
+ *             W=2: (1,8) (2,8) (4,4) (8,2)
+ *   direct-x: W=1 and W=4: (1,4) (1,8) (2,2) (2,3) (2,4) (2,8) (4,1) (4,2)
+ *                  (4,3) (4,4) (8,1) (8,2) */
 typedef struct tvl_tuning {
     int32_t rows_per_wave;
     int32_t waves_per_block;
@@ -118,7 +127,8 @@ typedef struct tvl_tuning {
     int32_t flags;
 } tvl_tuning;
 
-#define TVL_FLAG_CACHED_LOADS 1
+#define TVL_FLAG_X_LDS 1
+#define TVL_FLAG_X_DIRECT 2
 
 /* Opaque sweep plan. */
 typedef struct tvl_plan tvl_plan;

@@ -26,7 +26,7 @@ using tvl::Shape;
 
 struct tvl_plan {
     int device = -1;
-    Shape shape{4, 4, 4, false};
+    Shape shape{4, 4, 2, tvl::kXLds};
     int ks_cap = 0;
     int ntiles = 0;
     int grid = 0;
@@ -161,8 +161,10 @@ tvl_status check_tuning(const tvl_tuning *t, bool allow_ksplit)
 {
     if (!t) return TVL_OK;
     if (t->rows_per_wave < 0 || t->waves_per_block < 0 || t->unroll < 0 || t->ksplit < 0 ||
-        t->grid < 0 || (t->flags & ~TVL_FLAG_CACHED_LOADS) != 0)
+        t->grid < 0 || (t->flags & ~(TVL_FLAG_X_LDS | TVL_FLAG_X_DIRECT)) != 0)
         return fail(TVL_ERR_ARG, "tuning: negative field or unknown flag");
+    if ((t->flags & TVL_FLAG_X_LDS) && (t->flags & TVL_FLAG_X_DIRECT))
+        return fail(TVL_ERR_ARG, "tuning: TVL_FLAG_X_LDS and TVL_FLAG_X_DIRECT exclude each other");
     if (!allow_ksplit && t->ksplit > 1)
         return fail(TVL_ERR_ARG, "tuning: ksplit applies to tvl_gemv only");
     if (t->ksplit > 1024) return fail(TVL_ERR_ARG, "tuning: ksplit > 1024");
@@ -195,6 +197,36 @@ tvl_status current_device(int *dev, DevInfo *info)
     return TVL_OK;
 }
 
+// Default launch shape for a set of GEMVs, from the bytes they stream
+// (measured on MI355X over every instantiated shape, both x modes):
+//   mostly fp16 weights                  -> direct-x, R=4, W=1, U=4
+//   fp32, rows of <= 8 KB (K <= 2048)    -> direct-x, R=2, W=4, U=4
+//   fp32, longer rows                    -> direct-x, R=1, W=4, U=8
+// Direct-x reads x next to the weights, so no wavefront waits on a staging
+// round trip; with fp16 weights each 16-byte load needs 32 bytes of x, so
+// more rows per wavefront (R=4) share each x read.
+Shape default_shape(double bytes_f16, double bytes_f32, double f32_row_bytes_weighted)
+{
+    if (bytes_f16 > bytes_f32) return Shape{4, 1, 4, tvl::kXDirect};
+    if (f32_row_bytes_weighted <= 8192.0) return Shape{2, 4, 4, tvl::kXDirect};
+    return Shape{1, 4, 8, tvl::kXDirect};
+}
+
+Shape default_shape_items(const tvl_item *items, int32_t n)
+{
+    double b16 = 0, b32 = 0, row32 = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        const double b = (double)items[i].M * (double)items[i].K * elem_size(items[i].dtype);
+        if (items[i].dtype == TVL_F16) {
+            b16 += b;
+        } else {
+            b32 += b;
+            row32 += b * (double)items[i].K * 4.0;
+        }
+    }
+    return default_shape(b16, b32, b32 > 0 ? row32 / b32 : 0.0);
+}
+
 // Shape from a tuning override, else the default.
 tvl_status pick_shape(const tvl_tuning *t, Shape def, Shape *out)
 {
@@ -203,16 +235,23 @@ tvl_status pick_shape(const tvl_tuning *t, Shape def, Shape *out)
         if (t->rows_per_wave) s.R = t->rows_per_wave;
         if (t->waves_per_block) s.W = t->waves_per_block;
         if (t->unroll) s.U = t->unroll;
-        s.cached = (t->flags & TVL_FLAG_CACHED_LOADS) != 0;
+        if (t->flags & TVL_FLAG_X_LDS) s.xmode = tvl::kXLds;
+        if (t->flags & TVL_FLAG_X_DIRECT) s.xmode = tvl::kXDirect;
+        if (!t->rows_per_wave && !t->waves_per_block && !t->unroll && s.xmode != def.xmode) {
+            // x mode forced, shape left to the library: the mode's all-rounder
+            s.R = 2;
+            s.W = 4;
+            s.U = 4;
+        }
         if (t->rows_per_wave && !t->unroll) {
             // keep about 16 KB of weights in flight per wavefront by default
-            s.U = s.R >= 8 ? 2 : s.R == 4 ? 4 : 8;
+            s.U = s.R >= 4 ? 2 : s.R == 2 ? 4 : 8;
         }
     }
     if (!tvl::shape_supported(s))
         return fail(TVL_ERR_ARG, "tuning: (rows_per_wave %d, waves_per_block %d, unroll %d) is "
-                                 "not an instantiated shape",
-                    s.R, s.W, s.U);
+                                 "not an instantiated %s shape",
+                    s.R, s.W, s.U, s.xmode == tvl::kXLds ? "LDS-x" : "direct-x");
     *out = s;
     return TVL_OK;
 }
@@ -263,7 +302,7 @@ tvl_status get_workspace(int dev, hipStream_t st, int64_t nfloat, int64_t ncnt, 
 tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning, tvl_plan **out)
 {
     Shape shape;
-    tvl_status st = pick_shape(tuning, Shape{4, 4, 4, false}, &shape);
+    tvl_status st = pick_shape(tuning, default_shape_items(items, n), &shape);
     if (st != TVL_OK) return st;
     int dev = 0;
     DevInfo info;
@@ -410,24 +449,34 @@ tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype, const float *x
     int S = 1;
     const bool user_shape =
         tuning && (tuning->rows_per_wave || tuning->waves_per_block || tuning->unroll);
-    if (user_shape || (tuning && tuning->flags)) {
-        st = pick_shape(tuning, Shape{4, 4, 4, false}, &shape);
+    const bool user_ksplit = tuning && tuning->ksplit > 1;
+    if (user_shape || (tuning && tuning->flags) || user_ksplit) {
+        // an explicit K split stages x in LDS unless told otherwise
+        const Shape base = user_ksplit ? Shape{1, 4, 8, tvl::kXLds}
+                                       : default_shape(dtype == TVL_F16 ? 1.0 : 0.0,
+                                                       dtype == TVL_F16 ? 0.0 : 1.0,
+                                                       (double)K * 4.0);
+        st = pick_shape(tuning, base, &shape);
         if (st != TVL_OK) return st;
+        if (user_ksplit && shape.xmode != tvl::kXLds)
+            return fail(TVL_ERR_ARG, "tuning: the K split stages x in LDS (no direct-x form)");
     }
 
     int dev = 0;
     DevInfo info;
     st = current_device(&dev, &info);
     if (st != TVL_OK) return st;
-    if (!(user_shape || (tuning && tuning->flags))) {
-        shape = Shape{4, 4, 4, false};
-        if ((M + 15) / 16 < 2 * info.cus) shape = Shape{1, 4, 8, false};
+    if (!(user_shape || (tuning && tuning->flags) || user_ksplit)) {
+        shape = default_shape(dtype == TVL_F16 ? 1.0 : 0.0, dtype == TVL_F16 ? 0.0 : 1.0,
+                              (double)K * 4.0);
+        // too few row tiles to fill every CU twice: split K instead (LDS-x)
+        if ((M + 15) / 16 < 2 * info.cus) shape = Shape{1, 4, 8, tvl::kXLds};
     }
     const int rows_per_tile = shape.R * shape.W;
     const int64_t tiles = (M + rows_per_tile - 1) / rows_per_tile;
     if (tuning && tuning->ksplit) {
         S = tuning->ksplit;
-    } else if (!user_shape && tiles < 2 * info.cus) {
+    } else if (!user_shape && shape.xmode == tvl::kXLds && tiles < 2 * info.cus) {
         // aim for ~4 workgroups per CU; each slice keeps >= 2 LDS chunks
         const int64_t want = (4LL * info.cus + tiles - 1) / tiles;
         const int64_t most = std::max<int64_t>(1, K / (2 * tvl::kChunkElems));

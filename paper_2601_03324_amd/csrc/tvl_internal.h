@@ -33,13 +33,18 @@ struct DevTile {
 };
 static_assert(sizeof(DevTile) == 8, "DevTile layout");
 
+// How a wavefront gets x: staged once per workgroup in LDS, or read
+// directly from global memory (L1/L2-cached) next to the weights.
+constexpr int kXLds = 0;
+constexpr int kXDirect = 1;
+
 // Launch shape: rows per wave, waves per block, loads in flight per row,
-// streaming (non-temporal) or cached weight loads.
+// x mode.
 struct Shape {
     int R;
     int W;
     int U;
-    bool cached;
+    int xmode;
 };
 
 bool shape_supported(const Shape &s);

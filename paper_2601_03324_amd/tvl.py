@@ -16,10 +16,19 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtvl.so")
 
 TVL_F32, TVL_F16 = 0, 1
-TVL_FLAG_CACHED_LOADS = 1
+TVL_FLAG_X_LDS = 1
+TVL_FLAG_X_DIRECT = 2
 STATUS = {0: "TVL_OK", -1: "TVL_ERR_NULL", -2: "TVL_ERR_SHAPE", -3: "TVL_ERR_ALIGN",
           -4: "TVL_ERR_DTYPE", -5: "TVL_ERR_ALIAS", -6: "TVL_ERR_HIP", -7: "TVL_ERR_NOMEM",
           -8: "TVL_ERR_ARG"}
+
+# (rows per wave, waves per block, unroll) triples the library instantiates
+LDS_SHAPES = ((1, 4, 4), (1, 4, 8), (2, 4, 2), (2, 4, 3), (2, 4, 4), (2, 4, 8), (4, 4, 1),
+              (4, 4, 2), (4, 4, 3), (4, 4, 4), (8, 4, 1), (8, 4, 2), (2, 8, 4), (2, 8, 8),
+              (4, 8, 2), (1, 2, 8), (2, 2, 8), (4, 2, 4), (8, 2, 2))
+DIRECT_SHAPES = tuple((r, w, u) for w in (1, 4)
+                      for (r, u) in ((1, 4), (1, 8), (2, 2), (2, 3), (2, 4), (2, 8), (4, 1),
+                                     (4, 2), (4, 3), (4, 4), (8, 1), (8, 2)))
 
 # every symbol include/tvl.h declares
 EXPORTS = ("tvl_version", "tvl_row_stride", "tvl_pack_rows", "tvl_gemv", "tvl_gemv_ex",

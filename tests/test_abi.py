@@ -78,7 +78,8 @@ def gemv(W=A, ldw=768, dt=0, x=B, y=C, M=768, K=768, tuning=None):
     (dict(x=B + 8), ALIGN), (dict(y=C + 2), ALIGN),
     (dict(y=A + 4096), ALIAS), (dict(y=B - 4), ALIAS), (dict(x=C + 1024), ALIAS),
     (dict(tuning=dict(rows_per_wave=3)), ARG), (dict(tuning=dict(unroll=-1)), ARG),
-    (dict(tuning=dict(rows_per_wave=8, unroll=16)), ARG), (dict(tuning=dict(flags=2)), ARG),
+    (dict(tuning=dict(rows_per_wave=8, unroll=16)), ARG), (dict(tuning=dict(flags=4)), ARG),
+    (dict(tuning=dict(flags=3)), ARG), (dict(tuning=dict(flags=2, ksplit=2)), ARG),
     (dict(tuning=dict(ksplit=5000)), ARG),
 ])
 def test_gemv_rejects(kw, st):
@@ -158,6 +159,21 @@ def test_pack_and_utils_reject():
     assert L.tvl_util_copy(A, B, 60, None) == SHAPE
     assert L.tvl_util_read_stream(A, 64, B, 0, None, None) == SHAPE
     assert L.tvl_util_read_stream(A + 8, 64, B, 4, None, None) == ALIGN
+
+
+@pytest.mark.parametrize("flag,shapes", [(1, "LDS_SHAPES"), (2, "DIRECT_SHAPES")])
+def test_instantiated_shapes_match_binding(flag, shapes):
+    """Probe every (R, W, U) in each x mode: the instantiated ones pass
+    validation (and then fail at the device query on a host without a GPU),
+    the rest are rejected."""
+    seen = set()
+    for R in (1, 2, 3, 4, 8, 16):
+        for W in (1, 2, 4, 8, 16):
+            for U in range(1, 17):
+                st = gemv(tuning=dict(rows_per_wave=R, waves_per_block=W, unroll=U, flags=flag))
+                if st != ARG:
+                    seen.add((R, W, U))
+    assert seen == set(getattr(tvl, shapes))
 
 
 def test_status_strings():

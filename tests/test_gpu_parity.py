@@ -29,12 +29,12 @@ TOL = {0: 1e-5, 1: 2e-3}
 DEV = "cuda"
 
 # every (R, waves, U) the library instantiates, plus K-split and cached loads
-SHAPES = [(1, 4, 8), (1, 4, 16), (2, 4, 4), (2, 4, 8), (4, 4, 2), (4, 4, 4), (8, 4, 2),
-          (1, 8, 8), (1, 8, 16), (2, 8, 4), (2, 8, 8), (4, 8, 2), (4, 8, 4), (8, 8, 2),
-          (1, 2, 8), (2, 2, 8), (4, 2, 4), (8, 2, 2)]
-VARIANTS = ([None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u) for r, w, u in SHAPES]
-            + [dict(rows_per_wave=4, waves_per_block=4, unroll=4, flags=1),
-               dict(ksplit=2), dict(ksplit=3), dict(ksplit=7),
+# every (R, waves, U) the library instantiates in both x modes, plus K splits
+SHAPES = ([(r, w, u, 1) for r, w, u in tvl.LDS_SHAPES]
+          + [(r, w, u, 2) for r, w, u in tvl.DIRECT_SHAPES])
+VARIANTS = ([None, dict(flags=1), dict(flags=2)]
+            + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=f) for r, w, u, f in SHAPES]
+            + [dict(ksplit=2), dict(ksplit=3), dict(ksplit=7),
                dict(rows_per_wave=1, waves_per_block=4, unroll=8, ksplit=4),
                dict(rows_per_wave=8, waves_per_block=2, unroll=2, ksplit=5)])
 
@@ -295,13 +295,14 @@ def test_sweep110m_plan_batch_and_grid():
             assert torch.equal(g.y, b), (grid, g.spec.name)
         p2.destroy()
     # every sweep launch shape
-    for r, w, u in SHAPES:
-        p3 = tvl.tvl_sweep_plan_create(items, dict(rows_per_wave=r, waves_per_block=w, unroll=u))
+    for r, w, u, f in SHAPES:
+        p3 = tvl.tvl_sweep_plan_create(items, dict(rows_per_wave=r, waves_per_block=w, unroll=u,
+                                                   flags=f))
         for g in gemvs:
             g.y.fill_(float("nan"))
         p3.run()
         torch.cuda.synchronize()
-        _check_gemvs(gemvs[:8] + gemvs[-1:], f"sweep110m R{r}W{w}U{u}")
+        _check_gemvs(gemvs[:8] + gemvs[-1:], f"sweep110m R{r}W{w}U{u}F{f}")
         p3.destroy()
     plan.destroy()
 
@@ -322,8 +323,11 @@ def test_sweep_mixed_dtypes_and_ragged():
     xd = [torch.from_numpy(x).to(DEV) for x in xs]
     items = [(mats[i][0], mats[i][1], xd[i], ys[i], M, K, dt)
              for i, (M, K, dt) in enumerate(specs)]
-    for tuning in (None, dict(rows_per_wave=8, waves_per_block=8, unroll=2),
-                   dict(rows_per_wave=1, waves_per_block=2, unroll=8, grid=7)):
+    for tuning in (None, dict(flags=1), dict(flags=2),
+                   dict(rows_per_wave=4, waves_per_block=8, unroll=2, flags=1),
+                   dict(rows_per_wave=1, waves_per_block=2, unroll=8, grid=7, flags=1),
+                   dict(rows_per_wave=8, waves_per_block=1, unroll=2, flags=2),
+                   dict(rows_per_wave=2, waves_per_block=4, unroll=3, grid=5, flags=2)):
         plan = tvl.tvl_sweep_plan_create(items, tuning)
         plan.run()
         torch.cuda.synchronize()
