@@ -273,7 +273,8 @@ def test_sweep110m_plan_batch_and_grid():
     items = [g.item() for g in gemvs]
     plan = tvl.tvl_sweep_plan_create(items)
     info = plan.info()
-    assert info["ntiles"] == sum((m.M + 15) // 16 for m in wl.mats)
+    rpt = info["rows_per_tile"]
+    assert info["ntiles"] == sum((m.M + rpt - 1) // rpt for m in wl.mats)
     plan.run()
     torch.cuda.synchronize()
     worst = _check_gemvs(gemvs, "sweep110m")
