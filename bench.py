@@ -10,11 +10,15 @@ y buffers are resident in HBM before timing starts.
 
 Two copies of the weights (877 MB together) are alternated step by step, so
 the 256 MB last-level cache cannot hand one sweep's weights to the next: the
-figure is HBM streaming.  ``--warm`` times a single copy instead (reported as
-context only).
+figure is HBM streaming.  ``--warm`` times a single copy instead.
 
-Prints ONE JSON line (rank 0) with the metric, a roofline object for the
-sweep kernel and the CPU oracle's throughput on the same workload.
+``--workload`` measures the other workloads the same way (not the headline):
+sweep7b (Llama-2 7B token, fp32), stack70b8 (8 layers of a 70B-shaped stack,
+fp16 weights), cls32000 (the 110M classifier alone, 100 fresh x, 6 weight
+copies rotated) and gemv768 (one 768x768 fp32 GEMV, cache-resident).
+
+Prints ONE JSON line with the metric, a roofline object for the dominant
+kernel and the CPU oracle's throughput on a bounded sample of the workload.
 """
 from __future__ import annotations
 
@@ -31,9 +35,19 @@ sys.path.insert(0, ROOT)
 
 PEAK_GBS = 8000.0  # MI355X HBM3E, decimal GB/s
 METRIC = "achieved HBM GB/s (% of peak) + µs per full-model GEMV sweep (tok/s equiv)"
-WORKLOAD = "sweep110m"
-TRAFFIC_JSON = os.path.join(ROOT, "profiles", "sweep110m_fp32_traffic.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2601_03324_amd", "csrc", "tvl_kernels.hip")
+
+DESCRIBE = {
+    "sweep110m": "sweep110m: one decode token of Llama-2 110M, 85 fp32 GEMVs "
+                 "(12 x {768x768 x4, 2048x768 x2, 768x2048} + 32000x768), one launch",
+    "sweep7b": "sweep7b: one decode token of Llama-2 7B, 225 fp32 GEMVs "
+               "(32 x {4096x4096 x4, 11008x4096 x2, 4096x11008} + 32000x4096), one launch",
+    "stack70b8": "stack70b8: 8 layers of a Llama-2 70B-shaped stack, 56 GEMVs, fp16 weights "
+                 "(8 x {8192x8192 x2, 1024x8192 x2, 28672x8192 x2, 8192x28672}), one launch",
+    "cls32000": "cls32000: the 110M classifier 32000x768 fp32, one GEMV per step, "
+                "100 seeded x and 6 weight copies rotated",
+    "gemv768": "gemv768: one 768x768 fp32 GEMV per step (cache-resident, launch-bound)",
+}
 
 
 def log(msg: str) -> None:
@@ -44,11 +58,12 @@ def kernel_hash() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def measured_traffic(algo_bytes: int):
+def measured_traffic(workload: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
     None when there is none or the kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_traffic.json")
     try:
-        t = json.load(open(TRAFFIC_JSON))
+        t = json.load(open(path))
     except (OSError, ValueError):
         return None
     if t.get("kernel_src_sha256_16") != kernel_hash():
@@ -56,25 +71,28 @@ def measured_traffic(algo_bytes: int):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(wl, hosts, seconds: float) -> dict:
-    """The oracle as it stands (single-threaded naive double GEMV) over whole
-    110M sweeps on this host, for about ``seconds`` of CPU time."""
+def cpu_baseline(samples, seconds: float, what: str) -> dict:
+    """The oracle as it stands (single-threaded naive double GEMV), cycling over
+    (spec, W, x) samples of the workload for about ``seconds`` of CPU time."""
     import oracle
-    xs = [m.x() for m in wl.mats]
     t0 = time.perf_counter()
-    reps = 0
+    nbytes, ngemv = 0, 0
     while True:
-        for m, W, x in zip(wl.mats, hosts, xs):
-            oracle.gemv_f32(W, x)
-        reps += 1
+        for m, W, x in samples:
+            if m.dtype == "f32":
+                oracle.gemv_f32(W, x)
+            else:
+                oracle.gemv_f16(W, x)
+            nbytes += m.algo_bytes()
+            ngemv += 1
         el = time.perf_counter() - t0
         if el >= seconds:
             break
-    gbs = wl.algo_bytes() * reps / el / 1e9
+    gbs = nbytes / el / 1e9
     return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{reps} full 110M sweeps (85 fp32 GEMVs, double accumulation) in "
-                      f"{el:.1f} s on one host thread ({platform.processor() or platform.machine()}"
-                      f"); {el / reps * 1e6:.0f} us per sweep"}
+            "sample": f"{ngemv} GEMVs of {what} ({nbytes / 1e9:.2f} GB algorithmic) in "
+                      f"{el:.1f} s on one host thread "
+                      f"({platform.processor() or platform.machine()})"}
 
 
 def main() -> int:
@@ -82,13 +100,15 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--warm", action="store_true", help="time one weight copy (cache-warm)")
+    ap.add_argument("--workload", choices=sorted(DESCRIBE), default="sweep110m")
+    ap.add_argument("--warm", action="store_true", help="one weight copy (cache-warm)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--rows-per-wave", type=int, default=0)
     ap.add_argument("--waves-per-block", type=int, default=0)
     ap.add_argument("--unroll", type=int, default=0)
     ap.add_argument("--grid", type=int, default=0)
+    ap.add_argument("--ksplit", type=int, default=0, help="single-GEMV workloads only")
     ap.add_argument("--x-mode", choices=("auto", "lds", "direct"), default="auto",
                     help="how wavefronts get x (default: the library's choice)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -102,6 +122,7 @@ def main() -> int:
 
     import numpy as np
     import torch
+    import oracle
     import synth
     import synth.device as sdev
     from paper_2601_03324_amd import tvl
@@ -110,23 +131,62 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     torch.cuda.set_device(0)
-    wl = synth.WORKLOADS[WORKLOAD]
-    algo = wl.algo_bytes()
+    wl = synth.WORKLOADS[args.workload]
+    single = args.workload in ("cls32000", "gemv768")
+    algo = wl.mats[0].algo_bytes() if single else wl.algo_bytes()
+    tuning = dict(rows_per_wave=args.rows_per_wave, waves_per_block=args.waves_per_block,
+                  unroll=args.unroll, grid=args.grid, ksplit=args.ksplit,
+                  flags={"auto": 0, "lds": 1, "direct": 2}[args.x_mode])
+    if not single and args.ksplit:
+        print("--ksplit applies to single-GEMV workloads", file=sys.stderr)
+        return 2
+    use_tuning = any(tuning.values())
 
     log(f"generating {wl.name}: {len(wl.mats)} GEMVs, {wl.weight_bytes() / 1e6:.1f} MB of weights")
-    hosts = [m.weights() for m in wl.mats]
-    gemvs_a = []
-    for m, W in zip(wl.mats, hosts):
-        Wd = tvl.upload_matrix(W, 0, "cuda")
-        x = torch.from_numpy(m.x()).cuda()
+    big = wl.weight_bytes() > 4e9
+    cpu_samples = []  # (spec, host W, x) for the CPU baseline and the spot check
+    gemvs = []
+    for i, m in enumerate(wl.mats):
+        W = m.weights()
+        dt = sdev.dtype_code(m)
+        Wd = tvl.upload_matrix(W, dt, "cuda")
+        x = m.x()
+        gemvs.append(sdev.DevGemv(m, Wd, torch.from_numpy(x).cuda(),
+                                  torch.empty(m.M, dtype=torch.float32, device="cuda")))
+        if not big or i < 7:
+            cpu_samples.append((m, W, x))
+        if big and i % 16 == 0:
+            log(f"  uploaded {i + 1}/{len(wl.mats)}")
+    stream = torch.cuda.current_stream()
+
+    if single:
+        m, g = wl.mats[0], gemvs[0]
+        ncopy = 1 if (args.warm or args.workload == "gemv768") else 6
+        Ws = [g.W] + [tvl.TvlMatrix(g.W.buf.clone(), m.M, m.K, g.W.ldw, g.W.dtype)
+                      for _ in range(ncopy - 1)]
+        xs = [torch.from_numpy(m.x(r)).cuda() for r in range(wl.reps)]
         y = torch.empty(m.M, dtype=torch.float32, device="cuda")
-        gemvs_a.append(sdev.DevGemv(m, Wd, x, y))
-    copies = [gemvs_a] if args.warm else [gemvs_a, sdev.clone_weights(gemvs_a)]
-    tuning = dict(rows_per_wave=args.rows_per_wave, waves_per_block=args.waves_per_block,
-                  unroll=args.unroll, grid=args.grid,
-                  flags={"auto": 0, "lds": 1, "direct": 2}[args.x_mode])
-    plans = [tvl.tvl_sweep_plan_create([g.item() for g in c], tuning) for c in copies]
-    info = plans[0].info()
+
+        def step(i):
+            Wc, xc = Ws[i % ncopy], xs[i % len(xs)]
+            if use_tuning:
+                tvl.tvl_gemv_ex(Wc.ptr, Wc.ldw, Wc.dtype, xc, y, m.M, m.K, tuning)
+            else:
+                tvl.tvl_gemv(Wc.ptr, Wc.ldw, Wc.dtype, xc, y, m.M, m.K)
+
+        copies_used = ncopy
+        plan_info = {}
+    else:
+        ncopy = 1 if (args.warm or big) else 2
+        copies = [gemvs] + [sdev.clone_weights(gemvs) for _ in range(ncopy - 1)]
+        plans = [tvl.tvl_sweep_plan_create([g.item() for g in c], tuning if use_tuning else None)
+                 for c in copies]
+        plan_info = plans[0].info()
+
+        def step(i):
+            plans[i % ncopy].run()
+
+        copies_used = ncopy
     torch.cuda.synchronize()
 
     if args.calib_copy_mib:
@@ -142,14 +202,15 @@ def main() -> int:
     try:
         nb = 2 << 30
         src = torch.ones(nb // 4, dtype=torch.float32, device="cuda")
-        sink = torch.empty(4096, dtype=torch.float32, device="cuda")
+        sink = torch.empty(1 << 16, dtype=torch.float32, device="cuda")
+        grid = 1 << 15
         for _ in range(3):
-            tvl.tvl_util_read_stream(src, nb, sink, 4096)
+            tvl.tvl_util_read_stream(src, nb, sink, grid)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
+        e0.record(stream)
         for _ in range(10):
-            tvl.tvl_util_read_stream(src, nb, sink, 4096)
-        e1.record()
+            tvl.tvl_util_read_stream(src, nb, sink, grid)
+        e1.record(stream)
         torch.cuda.synchronize()
         ceil_gbs = nb * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9
         del src, sink
@@ -157,48 +218,51 @@ def main() -> int:
         log(f"read ceiling skipped: {exc}")
 
     for i in range(args.warmup):
-        plans[i % len(plans)].run()
+        step(i)
     torch.cuda.synchronize()
 
-    # timed region: K back-to-back sweeps on torch's current stream, the
+    # timed region: K back-to-back steps on torch's current stream, the
     # stream every launch goes to; events bracket the whole region
-    stream = torch.cuda.current_stream()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
     for i in range(args.steps):
-        plans[i % len(plans)].run()
+        step(i)
     end.record(stream)
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / args.steps
 
-    # per-sweep latency distribution (separate pass, not the headline)
+    # per-step latency distribution (separate pass, not the headline)
     n_lat = min(args.steps, 200)
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(n_lat + 1)]
     evs[0].record(stream)
     for i in range(n_lat):
-        plans[i % len(plans)].run()
+        step(i)
         evs[i + 1].record(stream)
     torch.cuda.synchronize()
     lat = np.array([evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(n_lat)])
 
-    # spot parity of the last sweep of copy 0 against the oracle (5 matrices)
-    import oracle
-    plans[0].run()
-    torch.cuda.synchronize()
+    # spot parity against the oracle: sampled outputs of the first copy
     worst = 0.0
-    for j in (0, 4, 6, 83, 84):
-        g = copies[0][j]
-        yref, S = oracle.gemv_f32(hosts[j], g.x.cpu().numpy())
-        r = oracle.check(g.y.cpu().numpy(), yref, S, 1e-5)
+    step(0)  # copy 0 (and x rep 0 for single GEMVs)
+    torch.cuda.synchronize()
+    checks = cpu_samples[:3] + ([] if single else [(gemvs[-1].spec, None, None)])
+    for m, W, x in checks:
+        g = next(gg for gg in gemvs if gg.spec is m)
+        ydev = (y if single else g.y).cpu().numpy()
+        rows = sdev.sample_rows(m.M, 64, 7)
+        Wr = np.stack([m.weights(int(r), 1)[0] for r in rows]) if W is None else W[rows]
+        xr = m.x(0)
+        yref, S = (oracle.gemv_f32 if m.dtype == "f32" else oracle.gemv_f16)(Wr, xr)
+        r = oracle.check(ydev[rows], yref, S, 1e-5 if m.dtype == "f32" else 2e-3)
         worst = max(worst, r["max_err"])
         if r["bad"]:
-            log(f"PARITY FAILURE in {g.spec.name}: {r}")
+            log(f"PARITY FAILURE in {m.name}: {r}")
             return 1
 
     us = ms * 1e3
     gbs = algo / (ms * 1e-3) / 1e9
-    traffic = measured_traffic(algo)
+    dtype = "f16 weights, f32 x/accumulation" if wl.mats[0].dtype == "f16" else "f32"
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -210,20 +274,17 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": dtype,
         "data": "synthetic (seeded SplitMix64; W ~ N(0, 0.02^2), x ~ N(0, 1) per matrix)",
         "config": {
-            "workload": "sweep110m: one decode token of Llama-2 110M, 85 fp32 GEMVs "
-                        "(12 x {768x768 x4, 2048x768 x2, 768x2048} + 32000x768), one launch",
-            "algorithmic_bytes": algo,
-            "weight_copies_alternated": len(copies),
-            "tiles": info["ntiles"],
-            "rows_per_tile": info["rows_per_tile"],
-            "grid": info["grid"],
+            "workload": DESCRIBE[args.workload],
+            "algorithmic_bytes_per_step": algo,
+            "weight_copies_rotated": copies_used,
+            **({"tiles": plan_info["ntiles"], "rows_per_tile": plan_info["rows_per_tile"],
+                "grid": plan_info["grid"]} if plan_info else {}),
         },
         "pct_of_peak": round(100.0 * gbs / PEAK_GBS, 2),
-        "us_per_sweep": round(us, 3),
-        "tok_s_equiv": round(1e6 / us, 1),
+        ("us_per_gemv" if single else "us_per_sweep"): round(us, 3),
         "latency_us": {"p5": round(float(np.percentile(lat, 5)), 3),
                        "p50": round(float(np.percentile(lat, 50)), 3),
                        "p95": round(float(np.percentile(lat, 95)), 3),
@@ -236,16 +297,20 @@ def main() -> int:
             "peak": PEAK_GBS,
             "unit": "GB/s",
             "frac": round(gbs / PEAK_GBS, 4),
-            "traffic": traffic,
+            "traffic": measured_traffic(args.workload),
         },
-        "paper_context": "paper: >60 tok/s for the 110M model, one thread on Apple M2 Pro "
-                         "(whole decode step, not this GEMV sweep alone)",
     }
+    if not single:
+        out["tok_s_equiv"] = round(1e6 / us, 1)
+    if args.workload == "sweep110m":
+        out["paper_context"] = ("paper: >60 tok/s for the 110M model, one thread on Apple M2 Pro "
+                                "(whole decode step, not this GEMV sweep alone)")
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")
-        out["cpu_baseline"] = cpu_baseline(wl, hosts, args.cpu_seconds)
-    for p in plans:
-        p.destroy()
+        out["cpu_baseline"] = cpu_baseline(cpu_samples, args.cpu_seconds, wl.name)
+    if not single:
+        for p in plans:
+            p.destroy()
     print(json.dumps(out), flush=True)
     return 0
 

@@ -198,9 +198,10 @@ TVL_API tvl_status tvl_release_workspaces(void);
 
 /* Diagnostics (not part of the GEMV path; used to calibrate measurements).
  * tvl_util_read_stream: read `bytes` (a multiple of 16) at `src` (16-byte
- *   aligned) with the same streaming loads as the GEMV and write one float
- *   per workgroup to `sink` (at least `sink_len` floats, >= the grid it
- *   reports through *grid_out, which may be NULL).
+ *   aligned) with the same streaming loads as the GEMV, in `sink_len`
+ *   workgroups each reading one contiguous span, and write one float per
+ *   workgroup to `sink` (`sink_len` floats).  *grid_out (may be NULL)
+ *   receives the grid, which equals sink_len.
  * tvl_util_copy: copy `bytes` (multiple of 16, both 16-byte aligned, no
  *   overlap) from src to dst. */
 TVL_API tvl_status tvl_util_read_stream(const void *src, int64_t bytes,

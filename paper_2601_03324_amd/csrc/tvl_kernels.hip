@@ -529,26 +529,30 @@ __global__ __launch_bounds__(256) void k_zero_i32(int *p, int64_t n)
         p[i] = 0;
 }
 
-// Read-only streaming with the GEMV's load kind; one float per workgroup so
-// the loads cannot be optimised away.
+// Read-only streaming with the GEMV's load kind: workgroup b reads the
+// contiguous span [b*per, (b+1)*per) of 16-byte vectors, eight loads in
+// flight per lane, and writes one float so the loads cannot be optimised away.
 __global__ __launch_bounds__(256) void k_read_stream(const f4 *__restrict__ src, int64_t nvec,
-                                                     float *__restrict__ sink)
+                                                     int64_t per, float *__restrict__ sink)
 {
     __shared__ float red[4];
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t beg = (int64_t)blockIdx.x * per;
+    const int64_t end = min(beg + per, nvec);
+    const TVL_GLOBAL f4 *g = (const TVL_GLOBAL f4 *)(src);
     f4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (; i + 7 * stride < nvec; i += 8 * stride) {
+    int64_t i = beg + threadIdx.x;
+    for (; i + 7 * 256 < end; i += 8 * 256) {
         f4 a[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-            a[u] = __builtin_nontemporal_load(src + i + u * stride);
+            a[u] = __builtin_nontemporal_load(g + i + u * 256);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int u = 0; u < 8; ++u)
             acc += a[u];
     }
-    for (; i < nvec; i += stride)
-        acc += __builtin_nontemporal_load(src + i);
+    for (; i < end; i += 256)
+        acc += __builtin_nontemporal_load(g + i);
     float v = (acc.x + acc.y) + (acc.z + acc.w);
     for (int o = 32; o >= 1; o >>= 1)
         v += __shfl_xor(v, o);
@@ -735,8 +739,10 @@ hipError_t launch_zero_i32(int *p, int64_t n, hipStream_t st)
 hipError_t launch_read_stream(const void *src, int64_t bytes, float *sink, int grid,
                               hipStream_t st)
 {
+    const int64_t nvec = bytes / 16;
+    const int64_t per = (nvec + grid - 1) / grid;
     hipLaunchKernelGGL(k_read_stream, dim3(grid), dim3(256), 0, st,
-                       static_cast<const f4 *>(src), bytes / 16, sink);
+                       static_cast<const f4 *>(src), nvec, per, sink);
     return hipGetLastError();
 }
 
