@@ -104,7 +104,7 @@ typedef struct tvl_item {
  *   unroll          U in {1, 2, 3, 4, 8}: 16-byte weight loads per row kept in
  *                   flight per lane
  *   ksplit          S >= 1: K slices per row tile (tvl_gemv only; 1 = row
- *                   split; LDS-x mode only)
+ *                   split)
  *   grid            workgroups of a sweep launch (0 = one per tile); a smaller
  *                   grid makes each workgroup loop over tiles
  *   flags           TVL_FLAG_X_LDS: stage x once per workgroup in LDS;
@@ -149,14 +149,17 @@ TVL_API tvl_status tvl_pack_rows(void *dst, int64_t ldw, const void *src,
                                  int64_t M, int64_t K, int32_t dtype,
                                  hipStream_t stream);
 
-/* y = W x (Sec. 6.1), one launch.  The library picks the variant by shape:
- * row split (each wavefront owns R whole rows) when there are enough rows to
- * fill the GPU, else K split (S workgroups share a row tile, each sums one
- * slice of K into an fp32 partial; the last workgroup to finish adds the S
- * partials in the fixed order 0..S-1, so results stay deterministic).  The
- * K-split workspace (S*M floats and one counter per row tile) is allocated by
- * the library on first use per (device, stream) and kept until
- * tvl_release_workspaces() or process exit. */
+/* y = W x (Sec. 6.1), one launch.  The library picks the variant by shape
+ * (from timings on MI355X): a row split (each wavefront owns R whole rows;
+ * one row per single-wavefront workgroup when M is small), or, for very few
+ * long rows (M <= 128, rows >= 32 KB), a K split: S workgroups share a row
+ * tile, each sums one slice of K into an fp32 partial, and the last
+ * workgroup to finish adds the S partials in the fixed order 0..S-1, so
+ * results stay deterministic.  The K-split workspace (S*M floats and one
+ * counter per row tile) is allocated by the library on first use per
+ * (device, stream) and kept until tvl_release_workspaces() or process exit;
+ * a first K-split call on a stream that is being captured into a graph
+ * fails with TVL_ERR_NOMEM (make one call before capturing). */
 TVL_API tvl_status tvl_gemv(const void *W, int64_t ldw, int32_t dtype,
                             const float *x, float *y, int64_t M, int64_t K,
                             hipStream_t stream);

@@ -200,6 +200,8 @@ tvl_status current_device(int *dev, DevInfo *info)
 // Default launch shape for a set of GEMVs, from the bytes they stream
 // (measured on MI355X over every instantiated shape, both x modes):
 //   mostly fp16 weights                  -> direct-x, R=4, W=1, U=4
+//   fp32, rows of <= 3 KB (K <= 768)     -> direct-x, R=2, W=4, U=3 (one batch
+//                                           covers the row)
 //   fp32, rows of <= 8 KB (K <= 2048)    -> direct-x, R=2, W=4, U=4
 //   fp32, longer rows                    -> direct-x, R=1, W=4, U=8
 // Direct-x reads x next to the weights, so no wavefront waits on a staging
@@ -208,6 +210,7 @@ tvl_status current_device(int *dev, DevInfo *info)
 Shape default_shape(double bytes_f16, double bytes_f32, double f32_row_bytes_weighted)
 {
     if (bytes_f16 > bytes_f32) return Shape{4, 1, 4, tvl::kXDirect};
+    if (f32_row_bytes_weighted <= 3072.0) return Shape{2, 4, 3, tvl::kXDirect};
     if (f32_row_bytes_weighted <= 8192.0) return Shape{2, 4, 4, tvl::kXDirect};
     return Shape{1, 4, 8, tvl::kXDirect};
 }
@@ -271,6 +274,12 @@ tvl_status get_workspace(int dev, hipStream_t st, int64_t nfloat, int64_t ncnt, 
     Workspace &w = g_ws[{dev, st}];
     if (w.partial_cap < nfloat || w.counter_cap < ncnt) {
         hipError_t e;
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(st, &cap) == hipSuccess && cap != hipStreamCaptureStatusNone)
+            return fail(TVL_ERR_NOMEM, "K-split workspace: stream %p is being captured and its "
+                                       "workspace (%lld floats) is not allocated yet; run the "
+                                       "same K-split call once on this stream before capture",
+                        (void *)st, (long long)nfloat);
         if (w.partials || w.counters) {
             // earlier launches on this stream may still use the old buffers
             e = hipStreamSynchronize(st);
@@ -449,39 +458,36 @@ tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype, const float *x
     int S = 1;
     const bool user_shape =
         tuning && (tuning->rows_per_wave || tuning->waves_per_block || tuning->unroll);
-    const bool user_ksplit = tuning && tuning->ksplit > 1;
-    if (user_shape || (tuning && tuning->flags) || user_ksplit) {
-        // an explicit K split stages x in LDS unless told otherwise
-        const Shape base = user_ksplit ? Shape{1, 4, 8, tvl::kXLds}
-                                       : default_shape(dtype == TVL_F16 ? 1.0 : 0.0,
-                                                       dtype == TVL_F16 ? 0.0 : 1.0,
-                                                       (double)K * 4.0);
-        st = pick_shape(tuning, base, &shape);
+    const Shape def = default_shape(dtype == TVL_F16 ? 1.0 : 0.0, dtype == TVL_F16 ? 0.0 : 1.0,
+                                    (double)K * 4.0);
+    shape = def;
+    if (user_shape || (tuning && tuning->flags)) {
+        st = pick_shape(tuning, def, &shape);
         if (st != TVL_OK) return st;
-        if (user_ksplit && shape.xmode != tvl::kXLds)
-            return fail(TVL_ERR_ARG, "tuning: the K split stages x in LDS (no direct-x form)");
     }
 
     int dev = 0;
     DevInfo info;
     st = current_device(&dev, &info);
     if (st != TVL_OK) return st;
-    if (!(user_shape || (tuning && tuning->flags) || user_ksplit)) {
-        shape = default_shape(dtype == TVL_F16 ? 1.0 : 0.0, dtype == TVL_F16 ? 0.0 : 1.0,
-                              (double)K * 4.0);
-        // too few row tiles to fill every CU twice: split K instead (LDS-x)
-        if ((M + 15) / 16 < 2 * info.cus) shape = Shape{1, 4, 8, tvl::kXLds};
+    const bool auto_shape = !(user_shape || (tuning && tuning->flags));
+    if (auto_shape) {
+        // Few rows of more than 4 KB (measured on MI355X for M = 16 .. 1024):
+        // one row per single-wavefront workgroup, 8 loads in flight, beats
+        // both the large-M shapes and a K split: the split's publish-and-
+        // combine step costs more than it saves unless rows are long and
+        // very few.  Rows of <= 4 KB take one batch of loads anyway.
+        const int64_t blocks = (M + def.R * def.W - 1) / (def.R * def.W);
+        const int64_t row_bytes = K * elem_size(dtype);
+        if (blocks < 2LL * info.cus && row_bytes > 4096) shape = Shape{1, 1, 8, tvl::kXDirect};
+        if (!(tuning && tuning->ksplit) && M <= 128 && row_bytes >= 32768) {
+            shape = Shape{1, 1, 4, tvl::kXDirect};
+            S = (int)std::min<int64_t>(4, std::max<int64_t>(2, 256 / M));
+        }
     }
     const int rows_per_tile = shape.R * shape.W;
     const int64_t tiles = (M + rows_per_tile - 1) / rows_per_tile;
-    if (tuning && tuning->ksplit) {
-        S = tuning->ksplit;
-    } else if (!user_shape && shape.xmode == tvl::kXLds && tiles < 2 * info.cus) {
-        // aim for ~4 workgroups per CU; each slice keeps >= 2 LDS chunks
-        const int64_t want = (4LL * info.cus + tiles - 1) / tiles;
-        const int64_t most = std::max<int64_t>(1, K / (2 * tvl::kChunkElems));
-        S = (int)std::max<int64_t>(1, std::min<int64_t>(want, most));
-    }
+    if (tuning && tuning->ksplit) S = tuning->ksplit;
     hipError_t e;
     if (S <= 1) {
         e = tvl::launch_gemv_rows(shape, dtype, W, ldw, x, y, (int)M, (int)K, stream);

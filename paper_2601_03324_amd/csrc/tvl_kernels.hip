@@ -226,6 +226,18 @@ struct SliceRows {
     }
 };
 
+// Row results: plain stores for y; for K-split partials, agent-scope
+// (device-coherent) stores, which bypass the XCD-local L2 so that the
+// workgroup that combines them, on any XCD, reads what was written.
+template <bool COHERENT>
+__device__ __forceinline__ void store_out(float *p, float v)
+{
+    if constexpr (COHERENT)
+        __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+        *p = v;
+}
+
 // Exchange step of the joint reduction: lanes with bit O set keep the upper
 // H values, the others the lower H, each adding its partner's copy.
 template <int H, int O>
@@ -267,7 +279,7 @@ __device__ __forceinline__ float reduce_rows(const f4 (&acc)[R], int lane)
 
 // One row tile, x staged in LDS: WV wavefronts x R rows, columns
 // [kbeg, kend).  out[row] gets the tile's sum for each row < M.
-template <typename T, int R, int WV, int U>
+template <typename T, int R, int WV, int U, bool COHERENT = false>
 __device__ __forceinline__ void gemv_tile(const T *__restrict__ W, int64_t ldw,
                                           const float *__restrict__ x, int M, int row0, int kbeg,
                                           int kend, int ks_cap, f4 *__restrict__ xs4,
@@ -298,7 +310,7 @@ __device__ __forceinline__ void gemv_tile(const T *__restrict__ W, int64_t ldw,
     constexpr int G = kWave / R;
     if (nrows > 0 && (lane % G) == 0) {
         const int row = wrow0 + lane / G;
-        if (row < M) out[row] = v;
+        if (row < M) store_out<COHERENT>(out + row, v);
     }
 }
 
@@ -380,27 +392,28 @@ struct DirectRows {
     }
 };
 
-template <typename T, int R, int WV, int U>
+template <typename T, int R, int WV, int U, bool COHERENT = false>
 __device__ __forceinline__ void gemv_tile_direct(const T *__restrict__ W, int64_t ldw,
                                                  const float *__restrict__ x, int M, int row0,
-                                                 int K, float *__restrict__ out)
+                                                 int kbeg, int kend, float *__restrict__ out)
 {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int wrow0 = row0 + wave * R;
     const int nrows = M - wrow0;
-    if (nrows <= 0) return; // no barrier in this mode: idle wavefronts leave
+    if (nrows <= 0) return; // direct-x tiles have no barrier to reach
     f4 acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r)
         acc[r] = f4{0.f, 0.f, 0.f, 0.f};
-    const DirectRows<T, R, U> dr(W + (int64_t)wrow0 * ldw, ldw, min(nrows, R), x, K, lane);
+    const DirectRows<T, R, U> dr(W + (int64_t)wrow0 * ldw + kbeg, ldw, min(nrows, R), x + kbeg,
+                                 kend - kbeg, lane);
     dr.run(acc, lane);
     const float v = reduce_rows<R>(acc, lane);
     constexpr int G = kWave / R;
     if ((lane % G) == 0) {
         const int row = wrow0 + lane / G;
-        if (row < M) out[row] = v;
+        if (row < M) store_out<COHERENT>(out + row, v);
     }
 }
 
@@ -422,14 +435,22 @@ __global__ __launch_bounds__(WV *kWave) void k_gemv_rows_direct(const T *__restr
                                                                  float *__restrict__ y, int M,
                                                                  int K)
 {
-    gemv_tile_direct<T, R, WV, U>(W, ldw, x, M, (int)blockIdx.x * (R * WV), K, y);
+    gemv_tile_direct<T, R, WV, U>(W, ldw, x, M, (int)blockIdx.x * (R * WV), 0, K, y);
 }
 
-// K split: workgroup b handles row tile b / S and K slice b % S.  Partials go
-// to partials[split * M + row]; the last workgroup of a tile to arrive (an
-// agent-scope counter) adds the S partials in the order 0..S-1 and resets
-// the counter to 0 for the next launch.
-template <typename T, int R, int WV, int U>
+// K split: workgroup b handles row tile b / S and K slice b % S.  Each
+// slice's row sums go to partials[split * M + row] with device-coherent
+// stores; every thread waits for its stores to be acknowledged, the
+// workgroup meets at a barrier, and one thread bumps the tile's counter.  The
+// workgroup that brings the counter to S adds the S partials in the order
+// 0..S-1 (device-coherent loads) and resets the counter for the next launch.
+//
+// An agent-scope release/acquire fence would be the textbook way to publish
+// the partials, but on a multi-XCD part it compiles to a write-back and an
+// invalidation of the whole L2, once per workgroup: measured 20-100x slower
+// than the row split.  Coherent stores plus the store wait give the same
+// guarantee for exactly the data that needs it.
+template <typename T, int R, int WV, int U, int XM>
 __global__ __launch_bounds__(WV *kWave) void k_gemv_ksplit(
     const T *__restrict__ W, int64_t ldw, const float *__restrict__ x, float *__restrict__ y,
     int M, int K, int ks_cap, int S, int kspan, float *__restrict__ partials,
@@ -442,18 +463,21 @@ __global__ __launch_bounds__(WV *kWave) void k_gemv_ksplit(
     const int row0 = tile * (R * WV);
     const int kbeg = split * kspan;
     const int kend = min(K, kbeg + kspan);
-    gemv_tile<T, R, WV, U>(W, ldw, x, M, row0, kbeg, kend, ks_cap, smem4,
-                           partials + (int64_t)split * M);
-    __threadfence();
+    if constexpr (XM == kXLds)
+        gemv_tile<T, R, WV, U, true>(W, ldw, x, M, row0, kbeg, kend, ks_cap, smem4,
+                                     partials + (int64_t)split * M);
+    else
+        gemv_tile_direct<T, R, WV, U, true>(W, ldw, x, M, row0, kbeg, kend,
+                                            partials + (int64_t)split * M);
+    __builtin_amdgcn_s_waitcnt(0x0F70); // this thread's partial stores acknowledged
     __syncthreads();
     if (threadIdx.x == 0) {
-        const int prev = __hip_atomic_fetch_add(counters + tile, 1, __ATOMIC_ACQ_REL,
-                                                __HIP_MEMORY_SCOPE_AGENT);
+        const int prev =
+            __hip_atomic_fetch_add(counters + tile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         is_last = (prev == S - 1);
     }
     __syncthreads();
     if (is_last) {
-        __threadfence();
         const int rows = min(R * WV, M - row0);
         for (int r = threadIdx.x; r < rows; r += blockDim.x) {
             float s = 0.f;
@@ -505,10 +529,10 @@ __global__ __launch_bounds__(WV *kWave) void k_sweep_direct(const DevItem *__res
         const DevItem it = items[tl.item];
         if (it.dtype == 1)
             gemv_tile_direct<_Float16, R, WV, U>(static_cast<const _Float16 *>(it.W), it.ldw,
-                                                 it.x, it.M, tl.row0, it.K, it.y);
+                                                 it.x, it.M, tl.row0, 0, it.K, it.y);
         else
             gemv_tile_direct<float, R, WV, U>(static_cast<const float *>(it.W), it.ldw, it.x,
-                                              it.M, tl.row0, it.K, it.y);
+                                              it.M, tl.row0, 0, it.K, it.y);
         __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
     }
 }
@@ -580,6 +604,28 @@ __global__ __launch_bounds__(256) void k_copy(f4 *__restrict__ dst, const f4 *__
     X(4, 1, 3) X(4, 1, 4) X(8, 1, 1) X(8, 1, 2) X(1, 4, 4) X(1, 4, 8) X(2, 4, 2) X(2, 4, 3)       \
     X(2, 4, 4) X(2, 4, 8) X(4, 4, 1) X(4, 4, 2) X(4, 4, 3) X(4, 4, 4) X(8, 4, 1) X(8, 4, 2)
 
+template <int R, int WV, int U, int XM>
+hipError_t launch_ksplit(int dtype, const void *W, int64_t ldw, const float *x, float *y, int M,
+                         int K, int S, float *partials, int *counters, hipStream_t st)
+{
+    // slice width: a whole number of LDS chunks, S' = ceil(K / kspan) <= S
+    const int per = (K + S - 1) / S;
+    const int kspan = (per + kChunkElems - 1) / kChunkElems * kChunkElems;
+    const int Se = (K + kspan - 1) / kspan;
+    const int ks = XM == kXLds ? slice_cap(kspan) : 0;
+    const int tiles = (M + R * WV - 1) / (R * WV);
+    const dim3 grid(tiles * Se), block(WV * kWave);
+    if (dtype == 1)
+        hipLaunchKernelGGL((k_gemv_ksplit<_Float16, R, WV, U, XM>), grid, block, ks * 4, st,
+                           static_cast<const _Float16 *>(W), ldw, x, y, M, K, ks, Se, kspan,
+                           partials, counters);
+    else
+        hipLaunchKernelGGL((k_gemv_ksplit<float, R, WV, U, XM>), grid, block, ks * 4, st,
+                           static_cast<const float *>(W), ldw, x, y, M, K, ks, Se, kspan,
+                           partials, counters);
+    return hipGetLastError();
+}
+
 template <int R, int WV, int U>
 struct Inst {
     static hipError_t rows(int dtype, const void *W, int64_t ldw, const float *x, float *y, int M,
@@ -598,22 +644,8 @@ struct Inst {
     static hipError_t ksplit(int dtype, const void *W, int64_t ldw, const float *x, float *y,
                              int M, int K, int S, float *partials, int *counters, hipStream_t st)
     {
-        // slice width: a whole number of LDS chunks, S' = ceil(K / kspan) <= S
-        const int per = (K + S - 1) / S;
-        const int kspan = (per + kChunkElems - 1) / kChunkElems * kChunkElems;
-        const int Se = (K + kspan - 1) / kspan;
-        const int ks = slice_cap(kspan);
-        const int tiles = (M + R * WV - 1) / (R * WV);
-        const dim3 grid(tiles * Se), block(WV * kWave);
-        if (dtype == 1)
-            hipLaunchKernelGGL((k_gemv_ksplit<_Float16, R, WV, U>), grid, block, ks * 4, st,
-                               static_cast<const _Float16 *>(W), ldw, x, y, M, K, ks, Se, kspan,
-                               partials, counters);
-        else
-            hipLaunchKernelGGL((k_gemv_ksplit<float, R, WV, U>), grid, block, ks * 4, st,
-                               static_cast<const float *>(W), ldw, x, y, M, K, ks, Se, kspan,
-                               partials, counters);
-        return hipGetLastError();
+        return launch_ksplit<R, WV, U, kXLds>(dtype, W, ldw, x, y, M, K, S, partials, counters,
+                                              st);
     }
     static hipError_t sweep(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
                             int ks_cap, hipStream_t st)
@@ -637,6 +669,12 @@ struct InstDirect {
             hipLaunchKernelGGL((k_gemv_rows_direct<float, R, WV, U>), grid, block, 0, st,
                                static_cast<const float *>(W), ldw, x, y, M, K);
         return hipGetLastError();
+    }
+    static hipError_t ksplit(int dtype, const void *W, int64_t ldw, const float *x, float *y,
+                             int M, int K, int S, float *partials, int *counters, hipStream_t st)
+    {
+        return launch_ksplit<R, WV, U, kXDirect>(dtype, W, ldw, x, y, M, K, S, partials,
+                                                 counters, st);
     }
     static hipError_t sweep(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
                             hipStream_t st)
@@ -687,10 +725,17 @@ hipError_t launch_gemv_ksplit(const Shape &s, int dtype, const void *W, int64_t 
 #define X(R_, W_, U_)                                                                             \
     if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
         return Inst<R_, W_, U_>::ksplit(dtype, W, ldw, x, y, M, K, S, partials, counters, st);
+#define Y(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return InstDirect<R_, W_, U_>::ksplit(dtype, W, ldw, x, y, M, K, S, partials, counters,   \
+                                              st);
     if (s.xmode == kXLds) {
         TVL_LDS_SHAPES(X)
+    } else {
+        TVL_DIRECT_SHAPES(Y)
     }
 #undef X
+#undef Y
     return hipErrorInvalidValue;
 }
 

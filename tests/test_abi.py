@@ -79,7 +79,7 @@ def gemv(W=A, ldw=768, dt=0, x=B, y=C, M=768, K=768, tuning=None):
     (dict(y=A + 4096), ALIAS), (dict(y=B - 4), ALIAS), (dict(x=C + 1024), ALIAS),
     (dict(tuning=dict(rows_per_wave=3)), ARG), (dict(tuning=dict(unroll=-1)), ARG),
     (dict(tuning=dict(rows_per_wave=8, unroll=16)), ARG), (dict(tuning=dict(flags=4)), ARG),
-    (dict(tuning=dict(flags=3)), ARG), (dict(tuning=dict(flags=2, ksplit=2)), ARG),
+    (dict(tuning=dict(flags=3)), ARG),
     (dict(tuning=dict(ksplit=5000)), ARG),
 ])
 def test_gemv_rejects(kw, st):

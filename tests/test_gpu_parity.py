@@ -35,8 +35,13 @@ SHAPES = ([(r, w, u, 1) for r, w, u in tvl.LDS_SHAPES]
 VARIANTS = ([None, dict(flags=1), dict(flags=2)]
             + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=f) for r, w, u, f in SHAPES]
             + [dict(ksplit=2), dict(ksplit=3), dict(ksplit=7),
-               dict(rows_per_wave=1, waves_per_block=4, unroll=8, ksplit=4),
-               dict(rows_per_wave=8, waves_per_block=2, unroll=2, ksplit=5)])
+               dict(rows_per_wave=1, waves_per_block=4, unroll=8, ksplit=4, flags=1),
+               dict(rows_per_wave=8, waves_per_block=2, unroll=2, ksplit=5, flags=1),
+               dict(rows_per_wave=2, waves_per_block=4, unroll=4, ksplit=3, flags=1),
+               dict(rows_per_wave=1, waves_per_block=1, unroll=4, ksplit=4, flags=2),
+               dict(rows_per_wave=4, waves_per_block=1, unroll=4, ksplit=2, flags=2),
+               dict(rows_per_wave=2, waves_per_block=4, unroll=3, ksplit=6, flags=2),
+               dict(rows_per_wave=8, waves_per_block=4, unroll=1, ksplit=16, flags=2)])
 
 
 def vname(v):
