@@ -50,6 +50,12 @@ def load(path: str) -> ctypes.CDLL:
         fn.restype = None
     L.oracle_check.argtypes = [P, P, P, I64, D, P, P, P]
     L.oracle_check.restype = I64
+    L.oracle_rmsnorm.argtypes = [P, P, I64, D, P]
+    L.oracle_rmsnorm.restype = None
+    L.oracle_gemv_dx.argtypes = [P, ctypes.c_int32, I64, P, I64, I64, P, P]
+    L.oracle_gemv_dx.restype = None
+    L.oracle_swiglu.argtypes = [P, P, I64, P]
+    L.oracle_swiglu.restype = None
     return L
 
 
@@ -139,3 +145,73 @@ def check(y_gpu: np.ndarray, y_ref: np.ndarray, S: np.ndarray, tol: float):
                              ctypes.addressof(mean))
     return {"bad": int(bad), "max_err": mx.value, "argmax": am.value,
             "mean_err": mean.value}
+
+
+def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
+    """RMSNorm of fp32 x with fp32 weight g, in double (Sec. 11.2 listing order)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    g = np.ascontiguousarray(g, dtype=np.float32)
+    K = x.shape[0]
+    if g.shape[0] != K:
+        raise ValueError("g and x lengths differ")
+    out = np.empty(K, dtype=np.float64)
+    lib().oracle_rmsnorm(_ptr(x), _ptr(g), K, float(eps), _ptr(out))
+    return out
+
+
+def gemv_dx(W: np.ndarray, xd: np.ndarray, K: int | None = None):
+    """(y, S) for fp32 W or binary16 bits W and a double x."""
+    W = np.ascontiguousarray(W)
+    if W.dtype == np.float16:
+        W = W.view(np.uint16)
+    if W.dtype not in (np.float32, np.uint16):
+        raise ValueError("W must be float32 or uint16 (binary16 bits)")
+    M, ldw, K = _rows(W, K)
+    xd = np.ascontiguousarray(xd, dtype=np.float64)
+    if xd.shape[0] < K:
+        raise ValueError("x shorter than K")
+    y = np.empty(M, dtype=np.float64)
+    S = np.empty(M, dtype=np.float64)
+    lib().oracle_gemv_dx(_ptr(W), 1 if W.dtype == np.uint16 else 0, ldw, _ptr(xd), M, K,
+                         _ptr(y), _ptr(S))
+    return y, S
+
+
+def rmsnorm_gemv(W: np.ndarray, x: np.ndarray, g: np.ndarray, eps: float,
+                 K: int | None = None):
+    """y = W rmsnorm(x; g, eps): (y, S) with S_i = sum_j |W_ij xn_j|."""
+    return gemv_dx(W, rmsnorm(x, g, eps), K)
+
+
+def swiglu(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """h = silu(a) * b elementwise, in double."""
+    a = np.ascontiguousarray(a, dtype=np.float64)
+    b = np.ascontiguousarray(b, dtype=np.float64)
+    if a.shape != b.shape:
+        raise ValueError("a and b shapes differ")
+    h = np.empty_like(a)
+    lib().oracle_swiglu(_ptr(a), _ptr(b), a.shape[0], _ptr(h))
+    return h
+
+
+def swiglu_ffn_in(W1: np.ndarray, W3: np.ndarray, x: np.ndarray, g: np.ndarray | None = None,
+                  eps: float = 1e-5, K: int | None = None):
+    """The FFN input half of a Llama-2 layer: h = silu(W1 xn) * (W3 xn), with
+    xn = rmsnorm(x; g, eps) when g is given, else x.  Returns
+    (h, a, b, Sa, Sb): the gate, both GEMVs and their normalisers."""
+    xd = rmsnorm(x, g, eps) if g is not None else np.asarray(x, np.float32).astype(np.float64)
+    a, Sa = gemv_dx(W1, xd, K)
+    b, Sb = gemv_dx(W3, xd, K)
+    return swiglu(a, b), a, b, Sa, Sb
+
+
+def swiglu_bound(a: np.ndarray, b: np.ndarray, Sa: np.ndarray, Sb: np.ndarray,
+                 h: np.ndarray) -> np.ndarray:
+    """First-order normaliser of the gate's error: a GPU result whose a and b
+    are within tau*Sa and tau*Sb (the GEMV parity norm) moves h by at most
+    tau * (|silu'(a)| |b| Sa + |silu(a)| Sb); 2^-20 |h| covers the fp32
+    evaluation of silu itself.  err_i = |h_gpu - h_ref| / bound_i."""
+    a = np.asarray(a, np.float64)
+    sig = 1.0 / (1.0 + np.exp(-a))
+    dsilu = sig * (1.0 + a * (1.0 - sig))
+    return np.abs(dsilu) * np.abs(b) * Sa + np.abs(a * sig) * Sb + np.abs(h) * 2.0 ** -20

@@ -134,3 +134,51 @@ int64_t oracle_check(const float *y, const double *ref, const double *S,
     if (mean_err) *mean_err = (M > 0) ? sum / (double)M : 0.0;
     return bad;
 }
+
+/* ------------------------------------------------------------------------ */
+/* RMSNorm (Sec. 2.1: pre-normalisation; Sec. 6.2 and the Sec. 11.2 listing): */
+/*   ms = (1/K) sum_j x_j^2 ;  inv = 1 / sqrt(ms + eps) ;  o_j = x_j g_j inv  */
+/* in double; epsilon is added to the mean square inside the root, as in the */
+/* listing.  Output in double (the GEMV below takes it as its x).            */
+/* ------------------------------------------------------------------------ */
+void oracle_rmsnorm(const float *x, const float *g, int64_t K, double eps, double *out)
+{
+    double ss = 0.0;
+    for (int64_t j = 0; j < K; ++j)
+        ss += (double)x[j] * (double)x[j];
+    const double ms = ss / (double)K;
+    const double inv = 1.0 / sqrt(ms + eps);
+    for (int64_t j = 0; j < K; ++j)
+        out[j] = (double)x[j] * (double)g[j] * inv;
+}
+
+/* y = W xd with x given in double (e.g. an RMSNorm output), fp32 or binary16
+ * weights; same loop as oracle_gemv_f32/_f16.  S_i = sum_j |W_ij xd_j|. */
+void oracle_gemv_dx(const void *W, int32_t is_f16, int64_t ldw, const double *xd,
+                    int64_t M, int64_t K, double *y, double *S)
+{
+    for (int64_t i = 0; i < M; ++i) {
+        double acc = 0.0, s = 0.0;
+        for (int64_t j = 0; j < K; ++j) {
+            const double w = is_f16 ? oracle_f16_to_f64(((const uint16_t *)W)[i * ldw + j])
+                                    : (double)((const float *)W)[i * ldw + j];
+            const double p = w * xd[j];
+            acc += p;
+            s += fabs(p);
+        }
+        y[i] = acc;
+        if (S) S[i] = s;
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* SwiGLU gate (Sec. 2.1: the FFN uses three matrices W1, W2, W3; with the   */
+/* gated linear unit of Shazeer, "GLU Variants Improve Transformer", 2020):  */
+/*   h_i = silu(a_i) * b_i,  silu(z) = z / (1 + e^-z),                      */
+/* where a = W1 xn and b = W3 xn are given (e.g. from oracle_gemv_dx).       */
+/* ------------------------------------------------------------------------ */
+void oracle_swiglu(const double *a, const double *b, int64_t M, double *h)
+{
+    for (int64_t i = 0; i < M; ++i)
+        h[i] = a[i] / (1.0 + exp(-a[i])) * b[i];
+}

@@ -258,10 +258,94 @@ def pin_check_rules():
     assert r["mean_err"] == pytest.approx(0.125 / 5)
 
 
+# ------------------------------------------------------------ RMSNorm pins
+def pin_rmsnorm_closed_forms():
+    """Sec. 11.2 listing: o_j = x_j g_j / sqrt(mean(x^2) + eps)."""
+    # constant x = 2^-1, g = 1, eps = 0: mean square 1/4, inverse root 2, o = 1
+    o = oracle.rmsnorm(np.full(8, 0.5, np.float32), np.ones(8, np.float32), 0.0)
+    assert np.array_equal(o, np.ones(8))
+    # a single nonzero entry: mean square x0^2 / K
+    x = np.zeros(4, np.float32)
+    x[0] = 2.0
+    o = oracle.rmsnorm(x, np.full(4, 3.0, np.float32), 0.0)
+    assert np.array_equal(o, np.array([6.0, 0, 0, 0]))
+    # (3, 4): mean square 12.5 (eps inside the root)
+    o = oracle.rmsnorm(np.array([3, 4], np.float32), np.array([1, -2], np.float32), 0.5)
+    r = 1.0 / math.sqrt(13.0)
+    assert abs(o[0] - 3 * r) <= 4 * U and abs(o[1] + 8 * r) <= 8 * U
+    # zero x stays zero for any eps > 0
+    assert np.array_equal(oracle.rmsnorm(np.zeros(5, np.float32), np.ones(5, np.float32), 1e-5),
+                          np.zeros(5))
+
+
+def pin_rmsnorm_invariances():
+    rng = np.random.default_rng(21)
+    for K in (1, 7, 768, 4096):
+        x = rng.standard_normal(K).astype(np.float32)
+        g = rng.standard_normal(K).astype(np.float32)
+        base = oracle.rmsnorm(x, g, 0.0)
+        # scale invariance (eps = 0): exact for powers of two
+        for k in (-3, 5):
+            xs = (x * np.float32(2.0 ** k)).astype(np.float32)
+            assert np.array_equal(oracle.rmsnorm(xs, g, 0.0), base)
+        # linear in g, exactly for a factor of 2
+        assert np.array_equal(oracle.rmsnorm(x, (2 * g).astype(np.float32), 0.0), 2 * base)
+        # against numpy's float64 formula (fsum of squares)
+        ms = math.fsum(float(v) * float(v) for v in x) / K
+        for eps in (0.0, 1e-5, 0.25):
+            ref = x.astype(np.float64) * g.astype(np.float64) / math.sqrt(ms + eps)
+            got = oracle.rmsnorm(x, g, eps)
+            assert np.allclose(got, ref, rtol=(K + 8) * U, atol=0)
+
+
+def pin_rmsnorm_gemv():
+    """y = W rmsnorm(x): exact rational check on a dyadic case and the
+    column-sum identity for an all-ones W."""
+    x = np.array([1.0, -1.0, 1.0, -1.0], np.float32)  # mean square 1
+    g = np.array([1.0, 2.0, 3.0, 4.0], np.float32)
+    W = np.array([[1, 1, 1, 1], [0.5, 0, -2, 0], [0, 0, 0, 0]], np.float32)
+    y, S = oracle.rmsnorm_gemv(W, x, g, 0.0)
+    assert list(y) == [1 - 2 + 3 - 4, 0.5 - 6, 0.0]
+    assert list(S) == [10.0, 6.5, 0.0]
+    rng = np.random.default_rng(22)
+    xr = rng.standard_normal(300).astype(np.float32)
+    gr = rng.standard_normal(300).astype(np.float32)
+    y, S = oracle.rmsnorm_gemv(np.ones((2, 300), np.float32), xr, gr, 1e-5)
+    xn = oracle.rmsnorm(xr, gr, 1e-5)
+    assert abs(y[0] - math.fsum(xn)) <= 300 * U * float(np.abs(xn).sum())
+    # fp16 weights give the same as their fp32 values
+    Wb = rng.integers(-3, 4, (5, 300)).astype(np.float16)
+    y16, _ = oracle.rmsnorm_gemv(Wb.view(np.uint16), xr, gr, 1e-5)
+    y32, _ = oracle.rmsnorm_gemv(Wb.astype(np.float32), xr, gr, 1e-5)
+    assert np.array_equal(y16, y32)
+    # padded rows: the stride is honoured
+    Wp = np.full((5, 320), np.nan, np.float32)
+    Wp[:, :300] = Wb.astype(np.float32)
+    yp, _ = oracle.rmsnorm_gemv(Wp, xr, gr, 1e-5, K=300)
+    assert np.array_equal(yp, y32)
+
+
+# ------------------------------------------------------------- SwiGLU pins
+def pin_swiglu():
+    """h = silu(a) b with silu(z) = z / (1 + e^-z)."""
+    from scipy.special import expit
+    a = np.array([0.0, 1.0, -1.0, 2.5, -3.0, 40.0, -800.0, 1e-300])
+    b = np.array([2.0, 3.0, -0.5, 1.0, 7.0, 0.5, 5.0, 1.0])
+    h = oracle.swiglu(a, b)
+    ref = a * expit(a) * b
+    assert h[0] == 0.0 and h[5] == 20.0 and h[6] == 0.0 and np.all(np.isfinite(h))
+    assert np.allclose(h, ref, rtol=4 * U, atol=0)
+    assert abs(h[1] - 3.0 / (1.0 + math.exp(-1.0))) <= 4 * U * 3
+    # zero gate input or zero b gives zero
+    assert np.all(oracle.swiglu(np.zeros(3), np.array([1.0, -2.0, 3.0])) == 0.0)
+    assert np.all(oracle.swiglu(np.array([1.0, -2.0, 3.0]), np.zeros(3)) == 0.0)
+
+
 PINS = [pin_golden, pin_products_exact, pin_brute_force_exact, pin_brute_force_exact_f16,
         pin_index_and_stride, pin_identity, pin_all_ones_rows, pin_integer_exact,
         pin_linearity, pin_one_hot, pin_zero_row, pin_f16_decode_all_patterns,
-        pin_f16_subnormal_gemv, pin_check_rules]
+        pin_f16_subnormal_gemv, pin_check_rules, pin_rmsnorm_closed_forms,
+        pin_rmsnorm_invariances, pin_rmsnorm_gemv, pin_swiglu]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
@@ -291,6 +375,17 @@ MUTANTS = {
     "check_S0_rule": ("e = (yi == 0.0) ? 0.0 : INFINITY;", "e = 0.0;"),
     "check_nonfinite": ("if (!isfinite(yi)) {", "if (0) {"),
     "check_tol_strict": ("if (e > tol) ++bad;", "if (e >= tol) ++bad;"),
+    "rms_eps_outside_root": ("1.0 / sqrt(ms + eps)", "1.0 / sqrt(ms) + eps"),
+    "rms_sum_not_mean": ("const double ms = ss / (double)K;", "const double ms = ss;"),
+    "rms_g_dropped": ("(double)x[j] * (double)g[j] * inv", "(double)x[j] * inv"),
+    "rms_no_root": ("1.0 / sqrt(ms + eps)", "1.0 / (ms + eps)"),
+    "rms_abs_not_square": ("ss += (double)x[j] * (double)x[j];", "ss += fabs((double)x[j]);"),
+    "gemvdx_stride": ("((const float *)W)[i * ldw + j]", "((const float *)W)[i * K + j]"),
+    "gemvdx_f16_bits_as_int": ("is_f16 ? oracle_f16_to_f64(((const uint16_t *)W)[i * ldw + j])",
+                               "is_f16 ? (double)(((const uint16_t *)W)[i * ldw + j])"),
+    "swiglu_sign": ("a[i] / (1.0 + exp(-a[i])) * b[i]", "a[i] / (1.0 + exp(a[i])) * b[i]"),
+    "swiglu_sigmoid_only": ("a[i] / (1.0 + exp(-a[i])) * b[i]", "1.0 / (1.0 + exp(-a[i])) * b[i]"),
+    "swiglu_no_b": ("a[i] / (1.0 + exp(-a[i])) * b[i]", "a[i] / (1.0 + exp(-a[i]))"),
 }
 
 
