@@ -85,17 +85,36 @@ typedef enum tvl_status {
     TVL_ERR_ARG = -8    /* an unsupported tuning value or other argument     */
 } tvl_status;
 
+/* Item operations. */
+#define TVL_OP_GEMV 0   /* y = W x                                                */
+#define TVL_OP_SWIGLU 1 /* y = silu(W x) * (W3 x), silu(z) = z / (1 + e^-z): the
+                           gated FFN input of Sec. 2.1 (W = w1, W3 = w3)          */
+
 /* One GEMV of a batch: y = W x with the same meaning as tvl_gemv's
- * arguments.  56 bytes, no implicit padding. */
+ * arguments, optionally with its input normalised and/or as a SwiGLU pair.
+ * 80 bytes, no implicit padding.
+ *
+ *   RMSNorm (g != NULL; Sec. 2.1 pre-normalisation, Sec. 11.2 listing):
+ *     x is replaced by x_j * g_j / sqrt(mean_j(x_j^2) + eps) before the
+ *     product.  eps is added to the mean square inside the root, as in the
+ *     listing; the root is exact (no reciprocal-root estimate).
+ *   SwiGLU (op == TVL_OP_SWIGLU): y_i = silu(a_i) * b_i with a = W x and
+ *     b = W3 x over the (normalised) x; W3 has W's M, K, ldw and dtype.
+ * Items with g != NULL or op != TVL_OP_GEMV run in direct-x mode and cannot
+ * be K-split. */
 typedef struct tvl_item {
-    const void *W;  /* device, M whole rows of ldw elements of `dtype`    */
-    int64_t ldw;    /* row stride in elements                              */
-    const float *x; /* device, K floats                                    */
-    float *y;       /* device, M floats, overwritten                       */
-    int64_t M;      /* rows                                                */
-    int64_t K;      /* columns used                                        */
-    int32_t dtype;  /* tvl_dtype                                           */
-    int32_t reserved; /* must be 0                                         */
+    const void *W;      /* device, M whole rows of ldw elements of `dtype`   */
+    int64_t ldw;        /* row stride in elements                             */
+    const float *x;     /* device, K floats                                   */
+    float *y;           /* device, M floats, overwritten                      */
+    int64_t M;          /* rows                                               */
+    int64_t K;          /* columns used                                       */
+    int32_t dtype;      /* tvl_dtype                                          */
+    int32_t op;         /* TVL_OP_GEMV or TVL_OP_SWIGLU                       */
+    const void *W3;     /* TVL_OP_SWIGLU: second matrix (same layout), else NULL */
+    const float *g;     /* RMSNorm weight, K floats, 16-byte aligned; NULL = none */
+    float eps;          /* RMSNorm epsilon (finite, >= 0; ignored when g == NULL) */
+    int32_t reserved;   /* must be 0                                          */
 } tvl_item;
 
 /* Launch shape override.  A zero field means "choose by shape".
@@ -168,6 +187,12 @@ TVL_API tvl_status tvl_gemv(const void *W, int64_t ldw, int32_t dtype,
 TVL_API tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype,
                                const float *x, float *y, int64_t M, int64_t K,
                                const tvl_tuning *tuning, hipStream_t stream);
+
+/* One item (any op, with or without RMSNorm) in one launch.  A plain GEMV
+ * item is the same as tvl_gemv_ex; fused items use the direct-x row split.
+ * `tuning` may be NULL. */
+TVL_API tvl_status tvl_gemv_item(const tvl_item *item, const tvl_tuning *tuning,
+                                 hipStream_t stream);
 
 /* All n GEMVs of `items` (e.g. every weight matrix of one decode token,
  * Sec. 1: each token streams every matrix once) in ONE launch.  The host

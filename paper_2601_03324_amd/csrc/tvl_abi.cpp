@@ -10,6 +10,7 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cmath>
 #include <cstring>
 #include <map>
 #include <mutex>
@@ -26,6 +27,7 @@ using tvl::Shape;
 
 struct tvl_plan {
     int device = -1;
+    bool fused = false;
     Shape shape{4, 4, 2, tvl::kXLds};
     int ks_cap = 0;
     int ntiles = 0;
@@ -138,6 +140,42 @@ tvl_status check_alias(const tvl_item *items, int32_t n)
         h = hits(f_range(t.x, t.K));
         if (h >= 0)
             return fail(TVL_ERR_ALIAS, "output of item %d overlaps x of item %d", (int)h, (int)i);
+        if (t.op == TVL_OP_SWIGLU) {
+            h = hits(w_range(t.W3, t.ldw, t.dtype, t.M));
+            if (h >= 0)
+                return fail(TVL_ERR_ALIAS, "output of item %d overlaps W3 of item %d", (int)h,
+                            (int)i);
+        }
+        if (t.g) {
+            h = hits(f_range(t.g, t.K));
+            if (h >= 0)
+                return fail(TVL_ERR_ALIAS, "output of item %d overlaps g of item %d", (int)h,
+                            (int)i);
+        }
+    }
+    return TVL_OK;
+}
+
+// The item's GEMV arguments plus its RMSNorm / SwiGLU fields.
+tvl_status check_fused(const tvl_item &t, const char *who)
+{
+    tvl_status st = check_one(t.W, t.ldw, t.dtype, t.x, t.y, t.M, t.K, who);
+    if (st != TVL_OK) return st;
+    if (t.reserved != 0) return fail(TVL_ERR_ARG, "%s: reserved must be 0", who);
+    if (t.op != TVL_OP_GEMV && t.op != TVL_OP_SWIGLU)
+        return fail(TVL_ERR_ARG, "%s: unknown op %d", who, (int)t.op);
+    if (t.op == TVL_OP_SWIGLU) {
+        if (!t.W3) return fail(TVL_ERR_NULL, "%s: a SwiGLU item needs W3", who);
+        if (reinterpret_cast<uintptr_t>(t.W3) % tvl::kLineBytes != 0)
+            return fail(TVL_ERR_ALIGN, "%s: W3 must be 128-byte aligned", who);
+    } else if (t.W3) {
+        return fail(TVL_ERR_ARG, "%s: W3 is only for SwiGLU items", who);
+    }
+    if (t.g) {
+        if (reinterpret_cast<uintptr_t>(t.g) % 16 != 0)
+            return fail(TVL_ERR_ALIGN, "%s: g must be 16-byte aligned", who);
+        if (!std::isfinite(t.eps) || t.eps < 0.f)
+            return fail(TVL_ERR_ARG, "%s: eps must be finite and >= 0", who);
     }
     return TVL_OK;
 }
@@ -150,12 +188,13 @@ tvl_status check_items(const tvl_item *items, int32_t n)
         const tvl_item &t = items[i];
         char who[48];
         snprintf(who, sizeof who, "sweep item %d", (int)i);
-        const tvl_status st = check_one(t.W, t.ldw, t.dtype, t.x, t.y, t.M, t.K, who);
+        const tvl_status st = check_fused(t, who);
         if (st != TVL_OK) return st;
-        if (t.reserved != 0) return fail(TVL_ERR_ARG, "%s: reserved must be 0", who);
     }
     return check_alias(items, n);
 }
+
+bool is_fused(const tvl_item &t) { return t.op != TVL_OP_GEMV || t.g != nullptr; }
 
 tvl_status check_tuning(const tvl_tuning *t, bool allow_ksplit)
 {
@@ -215,6 +254,13 @@ Shape default_shape(double bytes_f16, double bytes_f32, double f32_row_bytes_wei
     return Shape{1, 4, 8, tvl::kXDirect};
 }
 
+// Default shape for items with a fused RMSNorm or SwiGLU (direct-x only,
+// an even R so a SwiGLU pair fits in one wavefront).
+Shape default_fused_shape(double bytes_f16, double bytes_f32)
+{
+    return bytes_f16 > bytes_f32 ? Shape{4, 1, 4, tvl::kXDirect} : Shape{2, 4, 4, tvl::kXDirect};
+}
+
 Shape default_shape_items(const tvl_item *items, int32_t n)
 {
     double b16 = 0, b32 = 0, row32 = 0;
@@ -227,8 +273,14 @@ Shape default_shape_items(const tvl_item *items, int32_t n)
             row32 += b * (double)items[i].K * 4.0;
         }
     }
+    bool fused = false;
+    for (int32_t i = 0; i < n; ++i)
+        fused = fused || is_fused(items[i]);
+    if (fused) return default_fused_shape(b16, b32);
     return default_shape(b16, b32, b32 > 0 ? row32 / b32 : 0.0);
 }
+
+int64_t item_bytes_factor(const tvl_item &t) { return t.op == TVL_OP_SWIGLU ? 2 : 1; }
 
 // Shape from a tuning override, else the default.
 tvl_status pick_shape(const tvl_tuning *t, Shape def, Shape *out)
@@ -323,14 +375,26 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
     p->device = dev;
     p->shape = shape;
     p->items.assign(items, items + n);
-
-    const int rows_per_tile = shape.R * shape.W;
+    for (int32_t i = 0; i < n; ++i)
+        p->fused = p->fused || is_fused(items[i]);
+    if (p->fused && !tvl::fused_shape_supported(shape)) {
+        delete p;
+        return fail(TVL_ERR_ARG, "plan: items with RMSNorm or SwiGLU need a direct-x shape with "
+                                 "fused support; (%d, %d, %d) %s has none",
+                    shape.R, shape.W, shape.U, shape.xmode == tvl::kXLds ? "LDS-x" : "direct-x");
+    }
+    // output rows per tile: a SwiGLU tile streams R rows of W and of W3 per
+    // wavefront, i.e. R/2 output rows
+    auto rows_of = [&](const tvl_item &t) {
+        return (t.op == TVL_OP_SWIGLU ? shape.R / 2 : shape.R) * shape.W;
+    };
     // bytes per tile, largest first, so the longest tiles start first
     std::vector<int32_t> ord(n);
     for (int32_t i = 0; i < n; ++i)
         ord[i] = i;
     std::stable_sort(ord.begin(), ord.end(), [&](int32_t a, int32_t b) {
-        return items[a].K * elem_size(items[a].dtype) > items[b].K * elem_size(items[b].dtype);
+        return items[a].K * elem_size(items[a].dtype) * item_bytes_factor(items[a]) >
+               items[b].K * elem_size(items[b].dtype) * item_bytes_factor(items[b]);
     });
     std::vector<DevItem> hitems(n);
     std::vector<DevTile> htiles;
@@ -338,8 +402,9 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
     int64_t kmax = 1;
     for (int32_t i = 0; i < n; ++i) {
         const tvl_item &t = items[i];
-        hitems[i] = DevItem{t.W, t.ldw, t.x, t.y, (int32_t)t.M, (int32_t)t.K, t.dtype, 0};
-        ntiles += (t.M + rows_per_tile - 1) / rows_per_tile;
+        hitems[i] = DevItem{t.W,     t.ldw, t.x, t.y, (int32_t)t.M, (int32_t)t.K, t.dtype,
+                            t.op,    t.W3,  t.g, t.eps, 0};
+        ntiles += (t.M + rows_of(t) - 1) / rows_of(t);
         kmax = std::max<int64_t>(kmax, t.K);
     }
     if (ntiles > kMaxDim) {
@@ -349,7 +414,7 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
     htiles.reserve((size_t)ntiles);
     for (int32_t k = 0; k < n; ++k) {
         const int32_t i = ord[k];
-        for (int64_t r = 0; r < items[i].M; r += rows_per_tile)
+        for (int64_t r = 0; r < items[i].M; r += rows_of(items[i]))
             htiles.push_back(DevTile{i, (int32_t)r});
     }
     p->ntiles = (int)ntiles;
@@ -380,7 +445,9 @@ tvl_status plan_launch(const tvl_plan *p, hipStream_t st)
 {
     if (p->ntiles == 0) return TVL_OK;
     const hipError_t e =
-        tvl::launch_sweep(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid, p->ks_cap, st);
+        p->fused ? tvl::launch_sweep_fused(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid, st)
+                 : tvl::launch_sweep(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid,
+                                     p->ks_cap, st);
     if (e != hipSuccess) return fail_hip(e, "sweep launch");
     return TVL_OK;
 }
@@ -445,7 +512,7 @@ tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype, const float *x
     g_err[0] = 0;
     tvl_status st = check_one(W, ldw, dtype, x, y, M, K, "tvl_gemv");
     if (st != TVL_OK) return st;
-    tvl_item it{W, ldw, x, y, M, K, dtype, 0};
+    tvl_item it{W, ldw, x, y, M, K, dtype, TVL_OP_GEMV, nullptr, nullptr, 0.f, 0};
     st = check_alias(&it, 1);
     if (st != TVL_OK) return st;
     st = check_tuning(tuning, true);
@@ -507,6 +574,40 @@ tvl_status tvl_gemv(const void *W, int64_t ldw, int32_t dtype, const float *x, f
                     int64_t M, int64_t K, hipStream_t stream)
 {
     return tvl_gemv_ex(W, ldw, dtype, x, y, M, K, nullptr, stream);
+}
+
+tvl_status tvl_gemv_item(const tvl_item *item, const tvl_tuning *tuning, hipStream_t stream)
+{
+    g_err[0] = 0;
+    if (!item) return fail(TVL_ERR_NULL, "tvl_gemv_item: item is NULL");
+    tvl_status st = check_fused(*item, "tvl_gemv_item");
+    if (st != TVL_OK) return st;
+    if (!is_fused(*item))
+        return tvl_gemv_ex(item->W, item->ldw, item->dtype, item->x, item->y, item->M, item->K,
+                           tuning, stream);
+    st = check_alias(item, 1);
+    if (st != TVL_OK) return st;
+    st = check_tuning(tuning, false);
+    if (st != TVL_OK) return st;
+    const bool f16 = item->dtype == TVL_F16;
+    Shape shape;
+    st = pick_shape(tuning, default_fused_shape(f16 ? 1.0 : 0.0, f16 ? 0.0 : 1.0), &shape);
+    if (st != TVL_OK) return st;
+    if (!tvl::fused_shape_supported(shape))
+        return fail(TVL_ERR_ARG, "tvl_gemv_item: RMSNorm/SwiGLU items need a direct-x shape with "
+                                 "fused support");
+    if (tuning && tuning->grid)
+        return fail(TVL_ERR_ARG, "tvl_gemv_item: grid applies to sweeps");
+    int dev = 0;
+    DevInfo info;
+    st = current_device(&dev, &info);
+    if (st != TVL_OK) return st;
+    const tvl_item &t = *item;
+    const DevItem d{t.W,  t.ldw, t.x, t.y,   (int32_t)t.M, (int32_t)t.K, t.dtype,
+                    t.op, t.W3,  t.g, t.eps, 0};
+    const hipError_t e = tvl::launch_item(shape, d, stream);
+    if (e != hipSuccess) return fail_hip(e, "item launch");
+    return TVL_OK;
 }
 
 tvl_status tvl_sweep_plan_create(const tvl_item *items, int32_t n, const tvl_tuning *tuning,

@@ -12,8 +12,13 @@ constexpr int kLineBytes = 128;    // TVL row alignment: one gfx950 L2 cache lin
 constexpr int kChunkElems = 512;   // LDS slice granularity: 64 lanes x 8 fp16 = 2 x (64 x 4 fp32)
 constexpr int kSliceCap = 8192;    // x elements staged per pass: 32 KB of LDS
 
-// One GEMV as the kernels read it (48 bytes).  M and K fit in int32 (the
-// ABI rejects larger), ldw stays 64-bit.
+// Item operations (mirrors tvl_item.op).
+constexpr int kOpGemv = 0;
+constexpr int kOpSwiglu = 1;
+
+// One GEMV as the kernels read it (72 bytes).  M and K fit in int32 (the
+// ABI rejects larger), ldw stays 64-bit.  W3 is the second matrix of a
+// SwiGLU item; g (or NULL) the RMSNorm weight applied to x first.
 struct DevItem {
     const void *W;
     int64_t ldw;
@@ -22,9 +27,13 @@ struct DevItem {
     int32_t M;
     int32_t K;
     int32_t dtype;
+    int32_t op;
+    const void *W3;
+    const float *g;
+    float eps;
     int32_t pad;
 };
-static_assert(sizeof(DevItem) == 48, "DevItem layout");
+static_assert(sizeof(DevItem) == 72, "DevItem layout");
 
 // One row tile of a sweep: item index and first row.
 struct DevTile {
@@ -65,6 +74,13 @@ hipError_t launch_gemv_ksplit(const Shape &s, int dtype, const void *W, int64_t 
 
 hipError_t launch_sweep(const Shape &s, const DevItem *items, const DevTile *tiles,
                         int ntiles, int grid, int ks_cap, hipStream_t st);
+
+// Sweep with fused RMSNorm / SwiGLU items (direct-x mode, R even).
+bool fused_shape_supported(const Shape &s);
+hipError_t launch_sweep_fused(const Shape &s, const DevItem *items, const DevTile *tiles,
+                              int ntiles, int grid, hipStream_t st);
+// One item (any op) as one launch: grid = its row tiles, item by value.
+hipError_t launch_item(const Shape &s, const DevItem &item, hipStream_t st);
 
 hipError_t launch_pack(int dtype, void *dst, int64_t ldw, const void *src, int64_t M,
                        int64_t K, hipStream_t st);

@@ -318,79 +318,223 @@ __device__ __forceinline__ void gemv_tile(const T *__restrict__ W, int64_t ldw,
 // memory (cached: every wavefront of the matrix reads the same x) together
 // with the weights.  No LDS, no barrier: wavefronts are independent, so none
 // waits for a staging round trip before its first weight load.
-template <typename T, int R, int U>
+//
+// NORM (fused RMSNorm, Sec. 2.1 / Sec. 11.2 listing): the RMSNorm weight g is
+// read next to x, the products use x*g, and each lane also accumulates x^2
+// over its columns.  The scalar 1/sqrt(mean(x^2) + eps) factors out of the
+// dot product, so it is applied to the row sums at the end: the normalised
+// vector is never materialised and the fusion costs no extra pass over x.
+template <typename T, int R, int U, bool NORM = false>
 struct DirectRows {
     using V = typename Vec<T>::type;
     static constexpr int N = Vec<T>::N;
     static constexpr int CH = kWave * N;
     const T *rows[R];
     const float *xl; // x at this lane's first column
+    const float *gl; // RMSNorm weight at this lane's first column (NORM)
     int kn, nv, nfull;
 
     __device__ __forceinline__ DirectRows(const T *w0, int64_t ldw, int nrows, const float *x,
-                                          int kn_, int lane)
-        : xl(x + lane * N), kn(kn_), nv((kn_ + N - 1) / N), nfull(kn_ / CH)
+                                          int kn_, int lane, const float *g = nullptr)
+        : xl(x + lane * N), gl(g + lane * N), kn(kn_), nv((kn_ + N - 1) / N), nfull(kn_ / CH)
     {
 #pragma unroll
         for (int r = 0; r < R; ++r)
             rows[r] = w0 + (int64_t)(r < nrows ? r : nrows - 1) * ldw + lane * N;
     }
+    // explicit row starts (column 0 of each row, this lane's offset added here)
+    __device__ __forceinline__ DirectRows(const T *const (&starts)[R], const float *x, int kn_,
+                                          int lane, const float *g = nullptr)
+        : xl(x + lane * N), gl(g + lane * N), kn(kn_), nv((kn_ + N - 1) / N), nfull(kn_ / CH)
+    {
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            rows[r] = starts[r] + lane * N;
+    }
 
-    __device__ __forceinline__ void run(f4 (&acc)[R], int lane) const
+    __device__ __forceinline__ void xg(f4 &xa, f4 &xb, f4 &ssq, const f4 ga, const f4 gb) const
+    {
+        if constexpr (NORM) {
+            fma4(ssq, xa, xa);
+            xa *= ga;
+            if constexpr (N == 8) {
+                fma4(ssq, xb, xb);
+                xb *= gb;
+            }
+        }
+    }
+
+    __device__ __forceinline__ void run(f4 (&acc)[R], int lane, f4 &ssq) const
     {
         int c = 0;
         for (; c + U <= nfull; c += U) {
             V w[U][R];
-            f4 xa[U], xb[U];
+            f4 xa[U], xb[U], ga[U], gb[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 xa[u] = load_x4(xl + (c + u) * CH);
                 xb[u] = (N == 8) ? load_x4(xl + (c + u) * CH + 4) : xa[u];
+                if constexpr (NORM) {
+                    ga[u] = load_x4(gl + (c + u) * CH);
+                    gb[u] = (N == 8) ? load_x4(gl + (c + u) * CH + 4) : ga[u];
+                }
 #pragma unroll
                 for (int r = 0; r < R; ++r)
                     w[u][r] = load_w<T>(rows[r] + (c + u) * CH);
             }
             __builtin_amdgcn_sched_barrier(0); // all loads of the batch first
 #pragma unroll
-            for (int u = 0; u < U; ++u)
+            for (int u = 0; u < U; ++u) {
+                xg(xa[u], xb[u], ssq, ga[u], gb[u]);
 #pragma unroll
                 for (int r = 0; r < R; ++r)
                     mac_x(acc[r], w[u][r], xa[u], xb[u]);
+            }
         }
         for (; c < nfull; ++c) {
             V w[R];
-            const f4 xa = load_x4(xl + c * CH);
-            const f4 xb = (N == 8) ? load_x4(xl + c * CH + 4) : xa;
+            f4 xa = load_x4(xl + c * CH);
+            f4 xb = (N == 8) ? load_x4(xl + c * CH + 4) : xa;
+            f4 ga = xa, gb = xb;
+            if constexpr (NORM) {
+                ga = load_x4(gl + c * CH);
+                gb = (N == 8) ? load_x4(gl + c * CH + 4) : ga;
+            }
 #pragma unroll
             for (int r = 0; r < R; ++r)
                 w[r] = load_w<T>(rows[r] + c * CH);
+            xg(xa, xb, ssq, ga, gb);
 #pragma unroll
             for (int r = 0; r < R; ++r)
                 mac_x(acc[r], w[r], xa, xb);
         }
-        if (c * kWave < nv) { // ragged last chunk: mask W and x past kn
+        if (c * kWave < nv) { // ragged last chunk: mask W, x and g past kn
             const int v = c * kWave + lane;
             if (v < nv) {
                 const int valid = kn - v * N; // >= 1
-                // an f4 of x is read only when it starts before kn; it then
-                // lies in the same 16-byte block as a valid element
+                // an f4 of x (or g) is read only when it starts before kn; it
+                // then lies in the same 16-byte block as a valid element
                 f4 xa = mask_from<f4, 4>(load_x4(xl + c * CH), valid);
-                f4 xb = xa;
+                f4 xb = xa, ga = xa, gb = xa;
                 if constexpr (N == 8) {
                     xb = f4{0.f, 0.f, 0.f, 0.f};
                     if (valid > 4) xb = mask_from<f4, 4>(load_x4(xl + c * CH + 4), valid - 4);
+                }
+                if constexpr (NORM) {
+                    ga = mask_from<f4, 4>(load_x4(gl + c * CH), valid);
+                    gb = ga;
+                    if constexpr (N == 8) {
+                        gb = f4{0.f, 0.f, 0.f, 0.f};
+                        if (valid > 4) gb = mask_from<f4, 4>(load_x4(gl + c * CH + 4), valid - 4);
+                    }
                 }
                 V w[R];
 #pragma unroll
                 for (int r = 0; r < R; ++r)
                     w[r] = mask_from<V, N>(load_w<T>(rows[r] + c * CH), valid);
+                xg(xa, xb, ssq, ga, gb);
 #pragma unroll
                 for (int r = 0; r < R; ++r)
                     mac_x(acc[r], w[r], xa, xb);
             }
         }
     }
+    __device__ __forceinline__ void run(f4 (&acc)[R], int lane) const
+    {
+        f4 unused = {0.f, 0.f, 0.f, 0.f};
+        run(acc, lane, unused);
+    }
 };
+
+__device__ __forceinline__ float wave_sum(float v)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1)
+        v += __shfl_xor(v, o);
+    return v;
+}
+
+// silu(z) = z / (1 + e^-z) (the SwiGLU gate of the FFN, Sec. 2.1), fp32 with
+// the accurate expf; z -> -inf gives -0, NaN stays NaN.
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+
+// One row tile of any item (GEMV or SwiGLU, with or without RMSNorm),
+// direct-x.  A wavefront streams R weight rows: R output rows of a GEMV, or
+// R/2 output rows of a SwiGLU item (R/2 rows of W1 and the same rows of W3;
+// the pairs meet across lane halves after the joint reduction).
+template <typename T, int R, int WV, int U, bool NORM, bool SWIGLU>
+__device__ __forceinline__ void tile_fused(const DevItem &it, int row0)
+{
+    constexpr int RO = SWIGLU ? R / 2 : R; // output rows per wavefront
+    static_assert(!SWIGLU || (R % 2 == 0), "SwiGLU pairs rows across lane halves");
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wrow0 = row0 + wave * RO;
+    const int nrows = it.M - wrow0;
+    if (nrows <= 0) return;
+    const int nv = min(nrows, RO);
+    const T *W = static_cast<const T *>(it.W);
+    const T *W3 = static_cast<const T *>(it.W3);
+    const T *starts[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int rr = r % RO;
+        const T *base = (SWIGLU && r >= RO) ? W3 : W;
+        starts[r] = base + (int64_t)(wrow0 + (rr < nv ? rr : nv - 1)) * it.ldw;
+    }
+    f4 acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        acc[r] = f4{0.f, 0.f, 0.f, 0.f};
+    f4 ssq = {0.f, 0.f, 0.f, 0.f};
+    const DirectRows<T, R, U, NORM> dr(starts, it.x, it.K, lane, it.g);
+    dr.run(acc, lane, ssq);
+    float v = reduce_rows<R>(acc, lane);
+    if constexpr (NORM) {
+        const float ss = wave_sum((ssq.x + ssq.y) + (ssq.z + ssq.w));
+        const float inv = 1.0f / sqrtf(ss / (float)it.K + it.eps);
+        v *= inv;
+    }
+    constexpr int G = kWave / R;
+    if constexpr (SWIGLU) {
+        const float b = __shfl_xor(v, 32); // row r + R/2 (W3) meets row r (W1)
+        if (lane < 32 && (lane % G) == 0) {
+            const int row = wrow0 + lane / G;
+            if (row < it.M) it.y[row] = silu(v) * b;
+        }
+    } else {
+        if ((lane % G) == 0) {
+            const int row = wrow0 + lane / G;
+            if (row < it.M) it.y[row] = v;
+        }
+    }
+}
+
+template <typename T, int R, int WV, int U>
+__device__ __forceinline__ void tile_any(const DevItem &it, int row0)
+{
+    const bool norm = it.g != nullptr;
+    if (it.op == kOpSwiglu) {
+        if constexpr (R % 2 == 0) {
+            if (norm)
+                tile_fused<T, R, WV, U, true, true>(it, row0);
+            else
+                tile_fused<T, R, WV, U, false, true>(it, row0);
+        }
+    } else {
+        if (norm)
+            tile_fused<T, R, WV, U, true, false>(it, row0);
+        else
+            tile_fused<T, R, WV, U, false, false>(it, row0);
+    }
+}
+
+// Output rows one tile of `it` covers.
+template <int R, int WV>
+__host__ __device__ __forceinline__ int tile_rows(int op)
+{
+    return (op == kOpSwiglu ? R / 2 : R) * WV;
+}
 
 template <typename T, int R, int WV, int U, bool COHERENT = false>
 __device__ __forceinline__ void gemv_tile_direct(const T *__restrict__ W, int64_t ldw,
@@ -537,6 +681,35 @@ __global__ __launch_bounds__(WV *kWave) void k_sweep_direct(const DevItem *__res
     }
 }
 
+// Grouped sweep whose items may carry a fused RMSNorm and/or be SwiGLU
+// pairs: the same tile loop, with the item's kind chosen per tile.
+template <int R, int WV, int U>
+__global__ __launch_bounds__(WV *kWave) void k_sweep_fused(const DevItem *__restrict__ items,
+                                                            const DevTile *__restrict__ tiles,
+                                                            int ntiles)
+{
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const DevTile tl = tiles[t];
+        const DevItem it = items[tl.item];
+        if (it.dtype == 1)
+            tile_any<_Float16, R, WV, U>(it, tl.row0);
+        else
+            tile_any<float, R, WV, U>(it, tl.row0);
+        __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
+    }
+}
+
+// One item passed by value: workgroup b computes its row tile b.
+template <int R, int WV, int U>
+__global__ __launch_bounds__(WV *kWave) void k_item(const DevItem it)
+{
+    const int row0 = (int)blockIdx.x * tile_rows<R, WV>(it.op);
+    if (it.dtype == 1)
+        tile_any<_Float16, R, WV, U>(it, row0);
+    else
+        tile_any<float, R, WV, U>(it, row0);
+}
+
 template <typename E>
 __global__ __launch_bounds__(256) void k_pack(E *__restrict__ dst, int64_t ldw,
                                               const E *__restrict__ src, int64_t M, int64_t K)
@@ -603,6 +776,28 @@ __global__ __launch_bounds__(256) void k_copy(f4 *__restrict__ dst, const f4 *__
     X(1, 1, 4) X(1, 1, 8) X(2, 1, 2) X(2, 1, 3) X(2, 1, 4) X(2, 1, 8) X(4, 1, 1) X(4, 1, 2)       \
     X(4, 1, 3) X(4, 1, 4) X(8, 1, 1) X(8, 1, 2) X(1, 4, 4) X(1, 4, 8) X(2, 4, 2) X(2, 4, 3)       \
     X(2, 4, 4) X(2, 4, 8) X(4, 4, 1) X(4, 4, 2) X(4, 4, 3) X(4, 4, 4) X(8, 4, 1) X(8, 4, 2)
+
+// (R, waves per block, U) triples with fused RMSNorm / SwiGLU support.
+#define TVL_FUSED_SHAPES(X)                                                                       \
+    X(2, 4, 2) X(2, 4, 3) X(2, 4, 4) X(2, 1, 4) X(4, 1, 2) X(4, 1, 4) X(4, 4, 2) X(2, 1, 8)
+
+template <int R, int WV, int U>
+struct InstFused {
+    static hipError_t sweep(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
+                            hipStream_t st)
+    {
+        hipLaunchKernelGGL((k_sweep_fused<R, WV, U>), dim3(grid), dim3(WV * kWave), 0, st, items,
+                           tiles, ntiles);
+        return hipGetLastError();
+    }
+    static hipError_t item(const DevItem &it, hipStream_t st)
+    {
+        const int rows = tile_rows<R, WV>(it.op);
+        const dim3 grid((it.M + rows - 1) / rows), block(WV * kWave);
+        hipLaunchKernelGGL((k_item<R, WV, U>), grid, block, 0, st, it);
+        return hipGetLastError();
+    }
+};
 
 template <int R, int WV, int U, int XM>
 hipError_t launch_ksplit(int dtype, const void *W, int64_t ldw, const float *x, float *y, int M,
@@ -755,6 +950,35 @@ hipError_t launch_sweep(const Shape &s, const DevItem *items, const DevTile *til
     }
 #undef X
 #undef Y
+    return hipErrorInvalidValue;
+}
+
+bool fused_shape_supported(const Shape &s)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return s.xmode == kXDirect;
+    TVL_FUSED_SHAPES(X)
+#undef X
+    return false;
+}
+
+hipError_t launch_sweep_fused(const Shape &s, const DevItem *items, const DevTile *tiles,
+                              int ntiles, int grid, hipStream_t st)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return InstFused<R_, W_, U_>::sweep(items, tiles, ntiles, grid, st);
+    TVL_FUSED_SHAPES(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_item(const Shape &s, const DevItem &item, hipStream_t st)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return InstFused<R_, W_, U_>::item(item, st);
+    TVL_FUSED_SHAPES(X)
+#undef X
     return hipErrorInvalidValue;
 }
 

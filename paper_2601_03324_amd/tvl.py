@@ -32,6 +32,7 @@ DIRECT_SHAPES = tuple((r, w, u) for w in (1, 4)
 
 # every symbol include/tvl.h declares
 EXPORTS = ("tvl_version", "tvl_row_stride", "tvl_pack_rows", "tvl_gemv", "tvl_gemv_ex",
+           "tvl_gemv_item",
            "tvl_gemv_batch_sweep", "tvl_sweep_plan_create", "tvl_sweep_plan_run",
            "tvl_sweep_plan_info", "tvl_sweep_plan_destroy", "tvl_release_workspaces",
            "tvl_util_read_stream", "tvl_util_copy", "tvl_status_str", "tvl_last_error")
@@ -43,10 +44,14 @@ class TvlError(RuntimeError):
         super().__init__(f"{fn}: {STATUS.get(status, status)}: {detail}")
 
 
+TVL_OP_GEMV, TVL_OP_SWIGLU = 0, 1
+
+
 class tvl_item(ctypes.Structure):
     _fields_ = [("W", ctypes.c_void_p), ("ldw", ctypes.c_int64), ("x", ctypes.c_void_p),
                 ("y", ctypes.c_void_p), ("M", ctypes.c_int64), ("K", ctypes.c_int64),
-                ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("dtype", ctypes.c_int32), ("op", ctypes.c_int32), ("W3", ctypes.c_void_p),
+                ("g", ctypes.c_void_p), ("eps", ctypes.c_float), ("reserved", ctypes.c_int32)]
 
 
 class tvl_tuning(ctypes.Structure):
@@ -55,7 +60,7 @@ class tvl_tuning(ctypes.Structure):
                 ("grid", ctypes.c_int32), ("flags", ctypes.c_int32)]
 
 
-assert ctypes.sizeof(tvl_item) == 56
+assert ctypes.sizeof(tvl_item) == 80
 
 
 def _bind_hip_runtime() -> None:
@@ -86,6 +91,7 @@ def _load() -> ctypes.CDLL:
         "tvl_pack_rows": ([P, I64, P, I64, I64, I32, P], I32),
         "tvl_gemv": ([P, I64, I32, P, P, I64, I64, P], I32),
         "tvl_gemv_ex": ([P, I64, I32, P, P, I64, I64, P, P], I32),
+        "tvl_gemv_item": ([P, P, P], I32),
         "tvl_gemv_batch_sweep": ([P, I32, P], I32),
         "tvl_sweep_plan_create": ([P, I32, P, P], I32),
         "tvl_sweep_plan_run": ([P, P], I32),
@@ -163,17 +169,37 @@ def tvl_gemv_ex(W, ldw: int, dtype: int, x, y, M: int, K: int, tuning=None, stre
          "tvl_gemv_ex")
 
 
+def item(W, ldw: int, x, y, M: int, K: int, dtype: int, op: int = TVL_OP_GEMV, W3=None,
+         g=None, eps: float = 0.0) -> tvl_item:
+    """One tvl_item; pointers as ints or tensors."""
+    return tvl_item(_p(W), ldw, _p(x), _p(y), M, K, dtype, op, _p(W3) or None, _p(g) or None,
+                    eps, 0)
+
+
 def make_items(items) -> ctypes.Array:
-    """items: iterable of tvl_item or (W, ldw, x, y, M, K, dtype) tuples."""
+    """items: iterable of tvl_item, (W, ldw, x, y, M, K, dtype) tuples, or
+    dicts of item() keywords."""
     lst = list(items)
     arr = (tvl_item * max(len(lst), 1))()
     for i, it in enumerate(lst):
         if isinstance(it, tvl_item):
             arr[i] = it
+        elif isinstance(it, dict):
+            arr[i] = item(**it)
         else:
-            W, ldw, x, y, M, K, dt = it
-            arr[i] = tvl_item(_p(W), ldw, _p(x), _p(y), M, K, dt, 0)
+            arr[i] = item(*it)
     return arr, len(lst)
+
+
+def tvl_gemv_item(it, tuning=None, stream=None) -> None:
+    """Run one item (GEMV or SwiGLU, with or without RMSNorm) in one launch."""
+    if isinstance(it, dict):
+        it = item(**it)
+    elif not isinstance(it, tvl_item):
+        it = item(*it)
+    t = _tuning(tuning)
+    _chk(lib.tvl_gemv_item(ctypes.byref(it), ctypes.byref(t) if t is not None else None,
+                           _stream(stream)), "tvl_gemv_item")
 
 
 def tvl_gemv_batch_sweep(items, stream=None) -> None:

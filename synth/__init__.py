@@ -207,3 +207,104 @@ WORKLOADS = {
     # 8 layers of a Llama-2 70B-shaped stack, fp16 weights (GQA: wk, wv are 1024 x 8192)
     "stack70b8": Workload("stack70b8", 5, _llama(5, 8, 8192, 28672, None, "f16", kv=1024)),
 }
+
+
+# ------------------------------------------------------- fused decode items
+KIND_G = 2  # RMSNorm weight vectors
+
+
+@dataclass(frozen=True)
+class VecSpec:
+    """A seeded fp32 vector (an activation x or an RMSNorm weight g)."""
+    K: int
+    cfg: int
+    layer: int
+    group: int
+    kind: int  # KIND_X or KIND_G
+
+    def values(self) -> np.ndarray:
+        k = key(self.cfg, self.layer, 100 + self.group, self.kind, 0)
+        if self.kind == KIND_G:  # RMSNorm weights: positive, around 1
+            return uniform_f32(self.K, k, 0.5, 1.5)
+        return normal_f32(self.K, k, 1.0)
+
+
+@dataclass(frozen=True)
+class FusedSpec:
+    """One item of a fused decode sweep: a GEMV or a SwiGLU pair (W = w1,
+    W3 = w3), with x optionally RMS-normalised by g first (eps 1e-5)."""
+    name: str
+    W: MatSpec
+    x: VecSpec
+    W3: MatSpec | None = None
+    g: VecSpec | None = None
+    eps: float = 1e-5
+
+    @property
+    def M(self) -> int:
+        return self.W.M
+
+    @property
+    def K(self) -> int:
+        return self.W.K
+
+    def algo_bytes(self) -> int:
+        """|W| (+|W3|) + |x| (+|g|) + |y|: every input read once, y written once."""
+        b = self.W.wbytes + 4 * self.K + 4 * self.M
+        if self.W3 is not None:
+            b += self.W3.wbytes
+        if self.g is not None:
+            b += 4 * self.K
+        return b
+
+
+@dataclass(frozen=True)
+class FusedWorkload:
+    name: str
+    cfg: int
+    items: tuple
+
+    def algo_bytes(self) -> int:
+        return sum(i.algo_bytes() for i in self.items)
+
+    def weight_bytes(self) -> int:
+        return sum(i.W.wbytes + (i.W3.wbytes if i.W3 is not None else 0) for i in self.items)
+
+
+# groups of activation / norm vectors within a layer
+G_ATT, G_WO, G_FFN, G_W2, G_FINAL = 0, 1, 2, 3, 4
+
+
+def _llama_fused(cfg: int, layers: int, dim: int, hidden: int, vocab: int | None,
+                 dtype: str, kv: int | None = None, sigma: float = 0.02) -> tuple:
+    """A Llama-2 decode token as fused items: RMSNorm -> wq, wk, wv (one shared
+    normalised input); wo; RMSNorm -> SwiGLU(w1, w3); w2; final RMSNorm -> cls."""
+    kv = dim if kv is None else kv
+    items = []
+    for l in range(layers):
+        def mat(nm, M, K):
+            return MatSpec(f"L{l}.{nm}", M, K, dtype, ("normal", sigma), cfg, l, MATRIX_IDS[nm])
+        xa, ga = VecSpec(dim, cfg, l, G_ATT, KIND_X), VecSpec(dim, cfg, l, G_ATT, KIND_G)
+        for nm, M in (("wq", dim), ("wk", kv), ("wv", kv)):
+            items.append(FusedSpec(f"L{l}.{nm}", mat(nm, M, dim), xa, g=ga))
+        items.append(FusedSpec(f"L{l}.wo", mat("wo", dim, dim), VecSpec(dim, cfg, l, G_WO, KIND_X)))
+        xf, gf = VecSpec(dim, cfg, l, G_FFN, KIND_X), VecSpec(dim, cfg, l, G_FFN, KIND_G)
+        items.append(FusedSpec(f"L{l}.w1w3", mat("w1", hidden, dim), xf, W3=mat("w3", hidden, dim),
+                               g=gf))
+        items.append(FusedSpec(f"L{l}.w2", mat("w2", dim, hidden),
+                               VecSpec(hidden, cfg, l, G_W2, KIND_X)))
+    if vocab:
+        items.append(FusedSpec("cls", MatSpec("cls", vocab, dim, dtype, ("normal", sigma), cfg, 0,
+                                              MATRIX_IDS["cls"]),
+                               VecSpec(dim, cfg, 0, G_FINAL, KIND_X),
+                               g=VecSpec(dim, cfg, 0, G_FINAL, KIND_G)))
+    return tuple(items)
+
+
+FUSED_WORKLOADS = {
+    # the 110M decode token with its RMSNorms and SwiGLU gates fused (73 items)
+    "fused110m": FusedWorkload("fused110m", 2, _llama_fused(2, 12, 768, 2048, 32000, "f32")),
+    # 8 fused layers of the 70B-shaped stack, fp16 weights (40 items)
+    "fused70b8": FusedWorkload("fused70b8", 5, _llama_fused(5, 8, 8192, 28672, None, "f16",
+                                                            kv=1024)),
+}

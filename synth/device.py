@@ -70,3 +70,46 @@ def sample_rows(M: int, n: int, seed: int) -> np.ndarray:
     rows = {0, M - 1}
     rows.update(int(r) for r in rng.integers(0, M, max(n - 2, 0)))
     return np.array(sorted(rows), dtype=np.int64)
+
+
+@dataclass
+class DevFused:
+    spec: object  # FusedSpec
+    W: object     # TvlMatrix
+    W3: object    # TvlMatrix or None
+    x: object     # torch fp32 [K]
+    g: object     # torch fp32 [K] or None
+    y: object     # torch fp32 [M]
+
+    def item(self) -> dict:
+        from paper_2601_03324_amd import tvl
+        return dict(W=self.W.ptr, ldw=self.W.ldw, x=self.x, y=self.y, M=self.spec.M,
+                    K=self.spec.K, dtype=self.W.dtype,
+                    op=tvl.TVL_OP_SWIGLU if self.W3 is not None else tvl.TVL_OP_GEMV,
+                    W3=self.W3.ptr if self.W3 is not None else None, g=self.g,
+                    eps=self.spec.eps if self.g is not None else 0.0)
+
+
+def load_fused(wl, device="cuda", progress: bool = False) -> list:
+    """Upload every item of a fused workload; x and g vectors shared by a
+    group (e.g. wq, wk, wv) are uploaded once and shared."""
+    import torch
+    from paper_2601_03324_amd import tvl
+    vecs = {}
+
+    def vec(v):
+        if v is None:
+            return None
+        if v not in vecs:
+            vecs[v] = torch.from_numpy(v.values()).to(device)
+        return vecs[v]
+
+    out = []
+    for i, it in enumerate(wl.items):
+        Wd = tvl.upload_matrix(it.W.weights(), dtype_code(it.W), device)
+        W3 = tvl.upload_matrix(it.W3.weights(), dtype_code(it.W3), device) if it.W3 else None
+        y = torch.full((it.M,), float("nan"), dtype=torch.float32, device=device)
+        out.append(DevFused(it, Wd, W3, vec(it.x), vec(it.g), y))
+        if progress and (i % 8 == 0 or i == len(wl.items) - 1):
+            print(f"  loaded {wl.name} {i + 1}/{len(wl.items)}", flush=True, file=sys.stderr)
+    return out

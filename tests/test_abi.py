@@ -46,9 +46,44 @@ def test_missing_library_fails_loudly(tmp_path, monkeypatch):
 
 
 def test_item_layout_matches_header():
-    assert ctypes.sizeof(tvl.tvl_item) == 56
+    assert ctypes.sizeof(tvl.tvl_item) == 80
     assert tvl.tvl_item.dtype.offset == 48
+    assert tvl.tvl_item.op.offset == 52
+    assert tvl.tvl_item.W3.offset == 56
+    assert tvl.tvl_item.g.offset == 64
+    assert tvl.tvl_item.eps.offset == 72
     assert ctypes.sizeof(tvl.tvl_tuning) == 24
+
+
+D = 4 << 40  # another fake, far-away device address (g, W3)
+
+
+@pytest.mark.parametrize("kw,st", [
+    (dict(op=2), ARG), (dict(op=1), NULL), (dict(op=1, W3=D + 64), ALIGN),
+    (dict(W3=D), ARG), (dict(g=D + 4), ALIGN), (dict(g=D, eps=-1.0), ARG),
+    (dict(g=D, eps=float("nan")), ARG), (dict(g=D, eps=float("inf")), ARG),
+    (dict(op=1, W3=D, y=D + 128), ALIAS), (dict(g=D, eps=1e-5, y=D + 1024), ALIAS),
+    (dict(reserved=1), ARG),
+])
+def test_fused_item_rejects(kw, st):
+    base = dict(W=A, ldw=768, x=B, y=C, M=768, K=768, dtype=0)
+    reserved = kw.pop("reserved", 0)
+    it = tvl.item(**{**base, **kw})
+    it.reserved = reserved
+    assert L.tvl_gemv_item(ctypes.byref(it), None, None) == st
+    arr, n = tvl.make_items([it])
+    assert L.tvl_gemv_batch_sweep(arr, n, None) == st
+
+
+def test_fused_item_needs_direct_shape():
+    it = tvl.item(A, 768, B, C, 768, 768, 0, g=D, eps=1e-5)
+    t = tvl.tvl_tuning(flags=1)  # LDS-x
+    assert L.tvl_gemv_item(ctypes.byref(it), ctypes.byref(t), None) == ARG
+    t = tvl.tvl_tuning(ksplit=2)
+    assert L.tvl_gemv_item(ctypes.byref(it), ctypes.byref(t), None) == ARG
+    t = tvl.tvl_tuning(rows_per_wave=1, waves_per_block=4, unroll=8, flags=2)  # no fused form
+    assert L.tvl_gemv_item(ctypes.byref(it), ctypes.byref(t), None) == ARG
+    assert L.tvl_gemv_item(None, None, None) == NULL
 
 
 @pytest.mark.parametrize("K,dt,ldw", [(1, 0, 32), (32, 0, 32), (33, 0, 64), (768, 0, 768),
