@@ -15,7 +15,9 @@ figure is HBM streaming.  ``--warm`` times a single copy instead.
 ``--workload`` measures the other workloads the same way (not the headline):
 sweep7b (Llama-2 7B token, fp32), stack70b8 (8 layers of a 70B-shaped stack,
 fp16 weights), cls32000 (the 110M classifier alone, 100 fresh x, 6 weight
-copies rotated) and gemv768 (one 768x768 fp32 GEMV, cache-resident).
+copies rotated), gemv768 (one 768x768 fp32 GEMV, cache-resident), and the
+decode tokens with RMSNorm and SwiGLU fused into the GEMVs: fused110m (fp32,
+2 weight copies alternated) and fused70b8 (fp16 weights).
 
 Prints ONE JSON line with the metric, a roofline object for the dominant
 kernel and the CPU oracle's throughput on a bounded sample of the workload.
@@ -47,6 +49,11 @@ DESCRIBE = {
     "cls32000": "cls32000: the 110M classifier 32000x768 fp32, one GEMV per step, "
                 "100 seeded x and 6 weight copies rotated",
     "gemv768": "gemv768: one 768x768 fp32 GEMV per step (cache-resident, launch-bound)",
+    "fused110m": "fused110m: one decode token of Llama-2 110M as 73 fused items (RMSNorm -> "
+                 "wq/wk/wv, wo, RMSNorm -> SwiGLU(w1, w3), w2, RMSNorm -> classifier), fp32, "
+                 "one launch",
+    "fused70b8": "fused70b8: 8 layers of the 70B-shaped stack as 48 fused items (RMSNorm -> "
+                 "wq/wk/wv, wo, RMSNorm -> SwiGLU(w1, w3), w2), fp16 weights, one launch",
 }
 
 
@@ -131,6 +138,8 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     torch.cuda.set_device(0)
+    if args.workload in synth.FUSED_WORKLOADS:
+        return run_fused(args, tvl, torch, np, oracle, synth, sdev)
     wl = synth.WORKLOADS[args.workload]
     single = args.workload in ("cls32000", "gemv768")
     algo = wl.mats[0].algo_bytes() if single else wl.algo_bytes()
@@ -311,6 +320,136 @@ def main() -> int:
     if not single:
         for p in plans:
             p.destroy()
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def time_steps(step, steps, warmup, torch, np, stream):
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for i in range(steps):
+        step(i)
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    n_lat = min(steps, 200)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(n_lat + 1)]
+    evs[0].record(stream)
+    for i in range(n_lat):
+        step(i)
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    lat = np.array([evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(n_lat)])
+    return ms, lat
+
+
+def run_fused(args, tvl, torch, np, oracle, synth, sdev) -> int:
+    """A decode token as fused items (RMSNorm / SwiGLU folded into the GEMVs)."""
+    wl = synth.FUSED_WORKLOADS[args.workload]
+    algo = wl.algo_bytes()
+    big = wl.weight_bytes() > 4e9
+    log(f"generating {wl.name}: {len(wl.items)} items, {wl.weight_bytes() / 1e6:.1f} MB of weights")
+    items_a = sdev.load_fused(wl, "cuda", progress=big)
+    copies = [items_a]
+    if not (args.warm or big):
+        clone = []
+        for d in items_a:
+            W = tvl.TvlMatrix(d.W.buf.clone(), d.W.M, d.W.K, d.W.ldw, d.W.dtype)
+            W3 = (tvl.TvlMatrix(d.W3.buf.clone(), d.W3.M, d.W3.K, d.W3.ldw, d.W3.dtype)
+                  if d.W3 is not None else None)
+            clone.append(sdev.DevFused(d.spec, W, W3, d.x, d.g, torch.empty_like(d.y)))
+        copies.append(clone)
+    tuning = dict(rows_per_wave=args.rows_per_wave, waves_per_block=args.waves_per_block,
+                  unroll=args.unroll, grid=args.grid,
+                  flags={"auto": 0, "lds": 1, "direct": 2}[args.x_mode])
+    use_tuning = any(tuning.values())
+    plans = [tvl.tvl_sweep_plan_create([d.item() for d in c], tuning if use_tuning else None)
+             for c in copies]
+    info = plans[0].info()
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        plans[i % len(plans)].run()
+
+    ms, lat = time_steps(step, args.steps, args.warmup, torch, np, stream)
+    # spot parity: three items of copy 0 (a normalised GEMV, a SwiGLU pair, a plain GEMV)
+    plans[0].run()
+    torch.cuda.synchronize()
+    worst = 0.0
+    picks = [d for d in items_a if d.W3 is None and d.g is not None][:1] + \
+            [d for d in items_a if d.W3 is not None][:1] + \
+            [d for d in items_a if d.W3 is None and d.g is None][:1]
+    samples = []
+    for d in picks:
+        it = d.spec
+        rows = sdev.sample_rows(it.M, 64, 11)
+        W = np.stack([it.W.weights(int(r), 1)[0] for r in rows])
+        x = it.x.values()
+        g = it.g.values() if it.g is not None else None
+        y = d.y.cpu().numpy()[rows]
+        tol = 1e-5 if it.W.dtype == "f32" else 2e-3
+        if it.W3 is None:
+            xd = oracle.rmsnorm(x, g, it.eps) if g is not None else x.astype(np.float64)
+            yref, S = oracle.gemv_dx(W, xd)
+            r = oracle.check(y, yref, S, tol)
+        else:
+            W3 = np.stack([it.W3.weights(int(rr), 1)[0] for rr in rows])
+            href, a, b, Sa, Sb = oracle.swiglu_ffn_in(W, W3, x, g, it.eps)
+            r = oracle.check(y, href, oracle.swiglu_bound(a, b, Sa, Sb, href), tol)
+        worst = max(worst, r["max_err"])
+        if r["bad"]:
+            log(f"PARITY FAILURE in {it.name}: {r}")
+            return 1
+        samples.append((it, W, x, g))
+    us = ms * 1e3
+    gbs = algo / (ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC, "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 6),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16 weights, f32 x/accumulation" if wl.items[0].W.dtype == "f16" else "f32",
+        "data": "synthetic (seeded SplitMix64; W ~ N(0, 0.02^2), x ~ N(0, 1), g ~ U(0.5, 1.5))",
+        "config": {"workload": DESCRIBE[args.workload], "algorithmic_bytes_per_step": algo,
+                   "weight_copies_rotated": len(copies), "tiles": info["ntiles"],
+                   "rows_per_tile": info["rows_per_tile"], "grid": info["grid"]},
+        "pct_of_peak": round(100.0 * gbs / PEAK_GBS, 2),
+        "us_per_sweep": round(us, 3),
+        "tok_s_equiv": round(1e6 / us, 1),
+        "latency_us": {"p5": round(float(np.percentile(lat, 5)), 3),
+                       "p50": round(float(np.percentile(lat, 50)), 3),
+                       "p95": round(float(np.percentile(lat, 95)), 3),
+                       "p99": round(float(np.percentile(lat, 99)), 3)},
+        "parity_spot_max_err": worst,
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / PEAK_GBS, 4),
+                     "traffic": measured_traffic(args.workload)},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle baseline")
+        full = [(it, it.W.weights(), it.W3.weights() if it.W3 is not None else None, x, g)
+                for it, _, x, g in samples]
+        t0 = time.perf_counter()
+        nbytes, n = 0, 0
+        while time.perf_counter() - t0 < args.cpu_seconds:
+            for it, W, W3, x, g in full:
+                if W3 is None:
+                    xd = oracle.rmsnorm(x, g, it.eps) if g is not None else x.astype(np.float64)
+                    oracle.gemv_dx(W, xd)
+                else:
+                    oracle.swiglu_ffn_in(W, W3, x, g, it.eps)
+                nbytes += it.algo_bytes()
+                n += 1
+        el = time.perf_counter() - t0
+        out["cpu_baseline"] = {
+            "value": round(nbytes / el / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} fused items of {wl.name} (a normalised GEMV, a SwiGLU pair, a plain "
+                      f"GEMV in turn; {nbytes / 1e9:.2f} GB algorithmic) in {el:.1f} s on one "
+                      f"host thread"}
+    for p in plans:
+        p.destroy()
     print(json.dumps(out), flush=True)
     return 0
 
