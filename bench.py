@@ -54,7 +54,12 @@ DESCRIBE = {
                  "one launch",
     "fused70b8": "fused70b8: 8 layers of the 70B-shaped stack as 48 fused items (RMSNorm -> "
                  "wq/wk/wv, wo, RMSNorm -> SwiGLU(w1, w3), w2), fp16 weights, one launch",
+    "beam4_110m": "beam4_110m: one decode token of Llama-2 110M for 4 beam hypotheses: 85 fp32 "
+                  "GEMVs x 4 x vectors, weights read once, one launch",
+    "beam8_110m": "beam8_110m: one decode token of Llama-2 110M for 8 beam hypotheses: 85 fp32 "
+                  "GEMVs x 8 x vectors, weights read once, one launch",
 }
+BEAMS = {"beam4_110m": 4, "beam8_110m": 8}
 
 
 def log(msg: str) -> None:
@@ -140,6 +145,8 @@ def main() -> int:
     torch.cuda.set_device(0)
     if args.workload in synth.FUSED_WORKLOADS:
         return run_fused(args, tvl, torch, np, oracle, synth, sdev)
+    if args.workload in BEAMS:
+        return run_beam(args, tvl, torch, np, oracle, synth, sdev)
     wl = synth.WORKLOADS[args.workload]
     single = args.workload in ("cls32000", "gemv768")
     algo = wl.mats[0].algo_bytes() if single else wl.algo_bytes()
@@ -344,6 +351,78 @@ def time_steps(step, steps, warmup, torch, np, stream):
     torch.cuda.synchronize()
     lat = np.array([evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(n_lat)])
     return ms, lat
+
+
+def run_beam(args, tvl, torch, np, oracle, synth, sdev) -> int:
+    """The 110M decode token for B beam hypotheses (several x vectors per GEMV)."""
+    B = BEAMS[args.workload]
+    wl = synth.WORKLOADS["sweep110m"]
+    algo = sum(m.wbytes + B * (4 * m.K + 4 * m.M) for m in wl.mats)
+    log(f"generating {args.workload}: {len(wl.mats)} GEMVs x {B} vectors")
+    a = sdev.load_multi(wl, B, "cuda")
+    copies = [a]
+    if not args.warm:
+        copies.append(sdev.load_multi(wl, B, "cuda", share_from=[
+            sdev.DevGemv(d.spec, tvl.TvlMatrix(d.W.buf.clone(), d.W.M, d.W.K, d.W.ldw, d.W.dtype),
+                         None, None) for d in a]))
+    tuning = dict(rows_per_wave=args.rows_per_wave, waves_per_block=args.waves_per_block,
+                  unroll=args.unroll, grid=args.grid,
+                  flags={"auto": 0, "lds": 1, "direct": 2}[args.x_mode])
+    use_tuning = any(tuning.values())
+    plans = [tvl.tvl_sweep_plan_create([d.item() for d in c], tuning if use_tuning else None)
+             for c in copies]
+    info = plans[0].info()
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        plans[i % len(plans)].run()
+
+    ms, lat = time_steps(step, args.steps, args.warmup, torch, np, stream)
+    plans[0].run()
+    torch.cuda.synchronize()
+    worst = 0.0
+    for j in (0, 6, 84):
+        d = a[j]
+        m = d.spec
+        rows = sdev.sample_rows(m.M, 64, 13)
+        Wr = np.stack([m.weights(int(r), 1)[0] for r in rows])
+        Y = d.Y.cpu().numpy()
+        for b in range(B):
+            ref, S = oracle.gemv_f32(Wr, m.x(b))
+            r = oracle.check(Y[b][rows], ref, S, 1e-5)
+            worst = max(worst, r["max_err"])
+            if r["bad"]:
+                log(f"PARITY FAILURE in {m.name} vector {b}: {r}")
+                return 1
+    us = ms * 1e3
+    gbs = algo / (ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC, "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 6),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded SplitMix64; W ~ N(0, 0.02^2), x ~ N(0, 1) per vector)",
+        "config": {"workload": DESCRIBE[args.workload], "algorithmic_bytes_per_step": algo,
+                   "vectors": B, "weight_copies_rotated": len(copies), "tiles": info["ntiles"],
+                   "rows_per_tile": info["rows_per_tile"], "grid": info["grid"]},
+        "pct_of_peak": round(100.0 * gbs / PEAK_GBS, 2),
+        "us_per_sweep": round(us, 3),
+        "tok_s_equiv": round(B * 1e6 / us, 1),
+        "latency_us": {"p5": round(float(np.percentile(lat, 5)), 3),
+                       "p50": round(float(np.percentile(lat, 50)), 3),
+                       "p95": round(float(np.percentile(lat, 95)), 3),
+                       "p99": round(float(np.percentile(lat, 99)), 3)},
+        "parity_spot_max_err": worst,
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / PEAK_GBS, 4),
+                     "traffic": measured_traffic(args.workload)},
+    }
+    if not args.no_cpu_baseline:
+        samples = [(m, m.weights(), m.x(0)) for m in wl.mats[:7]]
+        out["cpu_baseline"] = cpu_baseline(samples, args.cpu_seconds, "sweep110m (per vector)")
+    for p in plans:
+        p.destroy()
+    print(json.dumps(out), flush=True)
+    return 0
 
 
 def run_fused(args, tvl, torch, np, oracle, synth, sdev) -> int:

@@ -91,8 +91,8 @@ typedef enum tvl_status {
                            gated FFN input of Sec. 2.1 (W = w1, W3 = w3)          */
 
 /* One GEMV of a batch: y = W x with the same meaning as tvl_gemv's
- * arguments, optionally with its input normalised and/or as a SwiGLU pair.
- * 80 bytes, no implicit padding.
+ * arguments, optionally with its input normalised and/or as a SwiGLU pair,
+ * or with several x vectors.  96 bytes, no implicit padding.
  *
  *   RMSNorm (g != NULL; Sec. 2.1 pre-normalisation, Sec. 11.2 listing):
  *     x is replaced by x_j * g_j / sqrt(mean_j(x_j^2) + eps) before the
@@ -100,8 +100,13 @@ typedef enum tvl_status {
  *     listing; the root is exact (no reciprocal-root estimate).
  *   SwiGLU (op == TVL_OP_SWIGLU): y_i = silu(a_i) * b_i with a = W x and
  *     b = W3 x over the (normalised) x; W3 has W's M, K, ldw and dtype.
- * Items with g != NULL or op != TVL_OP_GEMV run in direct-x mode and cannot
- * be K-split. */
+ *   Several vectors (nrhs > 1; beam search with nrhs hypotheses, Sec. 9.1):
+ *     y[b*ldy + i] = sum_j W[i*ldw + j] * x[b*ldx + j] for b < nrhs <= 8; the
+ *     weights are read once for all vectors.  Only for plain GEMV items
+ *     (op == TVL_OP_GEMV, g == NULL); a plan may not mix several-vector items
+ *     with RMSNorm or SwiGLU items.
+ * Items with g != NULL, op != TVL_OP_GEMV or nrhs > 1 run in direct-x mode
+ * and cannot be K-split. */
 typedef struct tvl_item {
     const void *W;      /* device, M whole rows of ldw elements of `dtype`   */
     int64_t ldw;        /* row stride in elements                             */
@@ -114,7 +119,9 @@ typedef struct tvl_item {
     const void *W3;     /* TVL_OP_SWIGLU: second matrix (same layout), else NULL */
     const float *g;     /* RMSNorm weight, K floats, 16-byte aligned; NULL = none */
     float eps;          /* RMSNorm epsilon (finite, >= 0; ignored when g == NULL) */
-    int32_t reserved;   /* must be 0                                          */
+    int32_t nrhs;       /* x vectors: 0 or 1 = one; 2..8 = several            */
+    int64_t ldx;        /* nrhs > 1: x row stride in floats (>= K, % 4 == 0)  */
+    int64_t ldy;        /* nrhs > 1: y row stride in floats (>= M)            */
 } tvl_item;
 
 /* Launch shape override.  A zero field means "choose by shape".

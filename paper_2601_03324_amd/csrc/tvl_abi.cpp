@@ -28,6 +28,7 @@ using tvl::Shape;
 struct tvl_plan {
     int device = -1;
     bool fused = false;
+    int multiB = 0; // > 0: several-vector plan holding B x vectors
     Shape shape{4, 4, 2, tvl::kXLds};
     int ks_cap = 0;
     int ntiles = 0;
@@ -108,11 +109,22 @@ Range f_range(const float *p, int64_t n)
 bool overlap(const Range &a, const Range &b) { return a.b < b.e && b.b < a.e; }
 
 // Outputs must not overlap each other or any input of the batch.
+int64_t nvec(const tvl_item &t) { return t.nrhs > 1 ? t.nrhs : 1; }
+// x and y spans: one vector, or nrhs rows at strides ldx / ldy
+Range x_range(const tvl_item &t)
+{
+    return f_range(t.x, nvec(t) > 1 ? (nvec(t) - 1) * t.ldx + t.K : t.K);
+}
+Range y_range(const tvl_item &t)
+{
+    return f_range(t.y, nvec(t) > 1 ? (nvec(t) - 1) * t.ldy + t.M : t.M);
+}
+
 tvl_status check_alias(const tvl_item *items, int32_t n)
 {
     std::vector<Range> wr(n);
     for (int32_t i = 0; i < n; ++i)
-        wr[i] = f_range(items[i].y, items[i].M);
+        wr[i] = y_range(items[i]);
     std::vector<int32_t> ord(n);
     for (int32_t i = 0; i < n; ++i)
         ord[i] = i;
@@ -137,7 +149,7 @@ tvl_status check_alias(const tvl_item *items, int32_t n)
         int32_t h = hits(w_range(t.W, t.ldw, t.dtype, t.M));
         if (h >= 0)
             return fail(TVL_ERR_ALIAS, "output of item %d overlaps W of item %d", (int)h, (int)i);
-        h = hits(f_range(t.x, t.K));
+        h = hits(x_range(t));
         if (h >= 0)
             return fail(TVL_ERR_ALIAS, "output of item %d overlaps x of item %d", (int)h, (int)i);
         if (t.op == TVL_OP_SWIGLU) {
@@ -156,12 +168,25 @@ tvl_status check_alias(const tvl_item *items, int32_t n)
     return TVL_OK;
 }
 
+bool is_fused(const tvl_item &t) { return t.op != TVL_OP_GEMV || t.g != nullptr; }
+bool is_multi(const tvl_item &t) { return t.nrhs > 1; }
+
 // The item's GEMV arguments plus its RMSNorm / SwiGLU fields.
 tvl_status check_fused(const tvl_item &t, const char *who)
 {
     tvl_status st = check_one(t.W, t.ldw, t.dtype, t.x, t.y, t.M, t.K, who);
     if (st != TVL_OK) return st;
-    if (t.reserved != 0) return fail(TVL_ERR_ARG, "%s: reserved must be 0", who);
+    if (t.nrhs < 0 || t.nrhs > 8) return fail(TVL_ERR_ARG, "%s: nrhs must be 0..8", who);
+    if (t.nrhs > 1) {
+        if (t.op != TVL_OP_GEMV || t.g)
+            return fail(TVL_ERR_ARG, "%s: several x vectors only for plain GEMV items", who);
+        if (t.ldx < t.K || t.ldy < t.M)
+            return fail(TVL_ERR_SHAPE, "%s: need ldx >= K and ldy >= M", who);
+        if (t.ldx % 4 != 0)
+            return fail(TVL_ERR_ALIGN, "%s: ldx must be a multiple of 4 (16-byte rows)", who);
+        if (t.ldx > (int64_t(1) << 40) || t.ldy > (int64_t(1) << 40))
+            return fail(TVL_ERR_SHAPE, "%s: ldx or ldy too large", who);
+    }
     if (t.op != TVL_OP_GEMV && t.op != TVL_OP_SWIGLU)
         return fail(TVL_ERR_ARG, "%s: unknown op %d", who, (int)t.op);
     if (t.op == TVL_OP_SWIGLU) {
@@ -191,10 +216,36 @@ tvl_status check_items(const tvl_item *items, int32_t n)
         const tvl_status st = check_fused(t, who);
         if (st != TVL_OK) return st;
     }
+    bool any_fused = false, any_multi = false;
+    for (int32_t i = 0; i < n; ++i) {
+        any_fused = any_fused || is_fused(items[i]);
+        any_multi = any_multi || is_multi(items[i]);
+    }
+    if (any_fused && any_multi)
+        return fail(TVL_ERR_ARG, "sweep: several-vector items cannot share a launch with RMSNorm "
+                                 "or SwiGLU items");
     return check_alias(items, n);
 }
 
-bool is_fused(const tvl_item &t) { return t.op != TVL_OP_GEMV || t.g != nullptr; }
+
+// x vectors a several-vector kernel must hold: the next power of two >= n
+int multi_B(int n) { return n <= 2 ? 2 : n <= 4 ? 4 : 8; }
+
+// Default several-vector shape (direct-x), by B, measured on MI355X on the
+// 110M decode token: more rows per wavefront amortise each x read over more
+// weights (R = 4), and fewer loads in flight keep the R x B accumulators in
+// registers as B grows.
+Shape default_multi_shape(int B)
+{
+    return B == 2 ? Shape{4, 4, 2, tvl::kXDirect} : Shape{4, 4, 1, tvl::kXDirect};
+}
+
+tvl::DevItem dev_item(const tvl_item &t)
+{
+    return tvl::DevItem{t.W,    t.ldw, t.x,   t.y,        (int32_t)t.M, (int32_t)t.K,
+                        t.dtype, t.op, t.W3, t.g,        t.eps,        (int32_t)nvec(t),
+                        t.ldx,  t.ldy};
+}
 
 tvl_status check_tuning(const tvl_tuning *t, bool allow_ksplit)
 {
@@ -277,8 +328,12 @@ Shape default_shape_items(const tvl_item *items, int32_t n)
         }
     }
     bool fused = false;
-    for (int32_t i = 0; i < n; ++i)
+    int nmax = 1;
+    for (int32_t i = 0; i < n; ++i) {
         fused = fused || is_fused(items[i]);
+        nmax = std::max<int>(nmax, (int)nvec(items[i]));
+    }
+    if (nmax > 1) return default_multi_shape(multi_B(nmax));
     if (fused) return default_fused_shape(b16, b32);
     return default_shape(b16, b32, b32 > 0 ? row32 / b32 : 0.0);
 }
@@ -286,7 +341,9 @@ Shape default_shape_items(const tvl_item *items, int32_t n)
 int64_t item_bytes_factor(const tvl_item &t) { return t.op == TVL_OP_SWIGLU ? 2 : 1; }
 
 // Shape from a tuning override, else the default.
-tvl_status pick_shape(const tvl_tuning *t, Shape def, Shape *out)
+// `plain`: check against the plain GEMV kernels (callers that launch the
+// fused or several-vector kernels check their own lists).
+tvl_status pick_shape(const tvl_tuning *t, Shape def, Shape *out, bool plain = true)
 {
     Shape s = def;
     if (t) {
@@ -306,7 +363,7 @@ tvl_status pick_shape(const tvl_tuning *t, Shape def, Shape *out)
             s.U = s.R >= 4 ? 2 : s.R == 2 ? 4 : 8;
         }
     }
-    if (!tvl::shape_supported(s))
+    if (plain && !tvl::shape_supported(s))
         return fail(TVL_ERR_ARG, "tuning: (rows_per_wave %d, waves_per_block %d, unroll %d) is "
                                  "not an instantiated %s shape",
                     s.R, s.W, s.U, s.xmode == tvl::kXLds ? "LDS-x" : "direct-x");
@@ -365,8 +422,11 @@ tvl_status get_workspace(int dev, hipStream_t st, int64_t nfloat, int64_t ncnt, 
 // -------------------------------------------------------------- plans
 tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning, tvl_plan **out)
 {
+    bool special = false;
+    for (int32_t i = 0; i < n; ++i)
+        special = special || is_fused(items[i]) || is_multi(items[i]);
     Shape shape;
-    tvl_status st = pick_shape(tuning, default_shape_items(items, n), &shape);
+    tvl_status st = pick_shape(tuning, default_shape_items(items, n), &shape, !special);
     if (st != TVL_OK) return st;
     int dev = 0;
     DevInfo info;
@@ -378,8 +438,25 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
     p->device = dev;
     p->shape = shape;
     p->items.assign(items, items + n);
-    for (int32_t i = 0; i < n; ++i)
+    int nmax = 1;
+    for (int32_t i = 0; i < n; ++i) {
         p->fused = p->fused || is_fused(items[i]);
+        nmax = std::max<int>(nmax, (int)nvec(items[i]));
+    }
+    if (nmax > 1) {
+        p->multiB = multi_B(nmax);
+        if (p->fused) {
+            delete p;
+            return fail(TVL_ERR_ARG, "plan: several-vector items cannot share a plan with "
+                                     "RMSNorm or SwiGLU items");
+        }
+        if (!tvl::multi_shape_supported(shape, p->multiB)) {
+            delete p;
+            return fail(TVL_ERR_ARG, "plan: no several-vector kernel for (%d, %d, %d) with %d "
+                                     "vectors",
+                        shape.R, shape.W, shape.U, p->multiB);
+        }
+    }
     if (p->fused && !tvl::fused_shape_supported(shape)) {
         delete p;
         return fail(TVL_ERR_ARG, "plan: items with RMSNorm or SwiGLU need a direct-x shape with "
@@ -405,8 +482,7 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
     int64_t kmax = 1;
     for (int32_t i = 0; i < n; ++i) {
         const tvl_item &t = items[i];
-        hitems[i] = DevItem{t.W,     t.ldw, t.x, t.y, (int32_t)t.M, (int32_t)t.K, t.dtype,
-                            t.op,    t.W3,  t.g, t.eps, 0};
+        hitems[i] = dev_item(t);
         ntiles += (t.M + rows_of(t) - 1) / rows_of(t);
         kmax = std::max<int64_t>(kmax, t.K);
     }
@@ -448,9 +524,12 @@ tvl_status plan_launch(const tvl_plan *p, hipStream_t st)
 {
     if (p->ntiles == 0) return TVL_OK;
     const hipError_t e =
-        p->fused ? tvl::launch_sweep_fused(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid, st)
-                 : tvl::launch_sweep(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid,
-                                     p->ks_cap, st);
+        p->multiB ? tvl::launch_sweep_multi(p->shape, p->multiB, p->d_items, p->d_tiles,
+                                            p->ntiles, p->grid, st)
+        : p->fused ? tvl::launch_sweep_fused(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid,
+                                             st)
+                   : tvl::launch_sweep(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid,
+                                       p->ks_cap, st);
     if (e != hipSuccess) return fail_hip(e, "sweep launch");
     return TVL_OK;
 }
@@ -515,7 +594,7 @@ tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype, const float *x
     g_err[0] = 0;
     tvl_status st = check_one(W, ldw, dtype, x, y, M, K, "tvl_gemv");
     if (st != TVL_OK) return st;
-    tvl_item it{W, ldw, x, y, M, K, dtype, TVL_OP_GEMV, nullptr, nullptr, 0.f, 0};
+    tvl_item it{W, ldw, x, y, M, K, dtype, TVL_OP_GEMV, nullptr, nullptr, 0.f, 1, 0, 0};
     st = check_alias(&it, 1);
     if (st != TVL_OK) return st;
     st = check_tuning(tuning, true);
@@ -585,7 +664,7 @@ tvl_status tvl_gemv_item(const tvl_item *item, const tvl_tuning *tuning, hipStre
     if (!item) return fail(TVL_ERR_NULL, "tvl_gemv_item: item is NULL");
     tvl_status st = check_fused(*item, "tvl_gemv_item");
     if (st != TVL_OK) return st;
-    if (!is_fused(*item))
+    if (!is_fused(*item) && !is_multi(*item))
         return tvl_gemv_ex(item->W, item->ldw, item->dtype, item->x, item->y, item->M, item->K,
                            tuning, stream);
     st = check_alias(item, 1);
@@ -593,22 +672,25 @@ tvl_status tvl_gemv_item(const tvl_item *item, const tvl_tuning *tuning, hipStre
     st = check_tuning(tuning, false);
     if (st != TVL_OK) return st;
     const bool f16 = item->dtype == TVL_F16;
+    const int B = is_multi(*item) ? multi_B((int)item->nrhs) : 0;
     Shape shape;
-    st = pick_shape(tuning, default_fused_shape(f16 ? 1.0 : 0.0, f16 ? 0.0 : 1.0), &shape);
+    st = pick_shape(tuning,
+                    B ? default_multi_shape(B)
+                      : default_fused_shape(f16 ? 1.0 : 0.0, f16 ? 0.0 : 1.0),
+                    &shape, false);
     if (st != TVL_OK) return st;
-    if (!tvl::fused_shape_supported(shape))
-        return fail(TVL_ERR_ARG, "tvl_gemv_item: RMSNorm/SwiGLU items need a direct-x shape with "
-                                 "fused support");
+    if (B ? !tvl::multi_shape_supported(shape, B) : !tvl::fused_shape_supported(shape))
+        return fail(TVL_ERR_ARG, "tvl_gemv_item: no %s kernel for (%d, %d, %d)",
+                    B ? "several-vector" : "RMSNorm/SwiGLU", shape.R, shape.W, shape.U);
     if (tuning && tuning->grid)
         return fail(TVL_ERR_ARG, "tvl_gemv_item: grid applies to sweeps");
     int dev = 0;
     DevInfo info;
     st = current_device(&dev, &info);
     if (st != TVL_OK) return st;
-    const tvl_item &t = *item;
-    const DevItem d{t.W,  t.ldw, t.x, t.y,   (int32_t)t.M, (int32_t)t.K, t.dtype,
-                    t.op, t.W3,  t.g, t.eps, 0};
-    const hipError_t e = tvl::launch_item(shape, d, stream);
+    const DevItem d = dev_item(*item);
+    const hipError_t e =
+        B ? tvl::launch_item_multi(shape, B, d, stream) : tvl::launch_item(shape, d, stream);
     if (e != hipSuccess) return fail_hip(e, "item launch");
     return TVL_OK;
 }

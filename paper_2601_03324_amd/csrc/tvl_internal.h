@@ -16,9 +16,10 @@ constexpr int kSliceCap = 8192;    // x elements staged per pass: 32 KB of LDS
 constexpr int kOpGemv = 0;
 constexpr int kOpSwiglu = 1;
 
-// One GEMV as the kernels read it (72 bytes).  M and K fit in int32 (the
+// One GEMV as the kernels read it (88 bytes).  M and K fit in int32 (the
 // ABI rejects larger), ldw stays 64-bit.  W3 is the second matrix of a
-// SwiGLU item; g (or NULL) the RMSNorm weight applied to x first.
+// SwiGLU item; g (or NULL) the RMSNorm weight applied to x first; nrhs x
+// vectors at a stride of ldx floats give nrhs outputs at a stride of ldy.
 struct DevItem {
     const void *W;
     int64_t ldw;
@@ -31,9 +32,11 @@ struct DevItem {
     const void *W3;
     const float *g;
     float eps;
-    int32_t pad;
+    int32_t nrhs;
+    int64_t ldx;
+    int64_t ldy;
 };
-static_assert(sizeof(DevItem) == 72, "DevItem layout");
+static_assert(sizeof(DevItem) == 88, "DevItem layout");
 
 // One row tile of a sweep: item index and first row.
 struct DevTile {
@@ -81,6 +84,12 @@ hipError_t launch_sweep_fused(const Shape &s, const DevItem *items, const DevTil
                               int ntiles, int grid, hipStream_t st);
 // One item (any op) as one launch: grid = its row tiles, item by value.
 hipError_t launch_item(const Shape &s, const DevItem &item, hipStream_t st);
+
+// Several x vectors per item (B = 2, 4 or 8 >= every item's nrhs; direct-x).
+bool multi_shape_supported(const Shape &s, int B);
+hipError_t launch_sweep_multi(const Shape &s, int B, const DevItem *items, const DevTile *tiles,
+                              int ntiles, int grid, hipStream_t st);
+hipError_t launch_item_multi(const Shape &s, int B, const DevItem &item, hipStream_t st);
 
 hipError_t launch_pack(int dtype, void *dst, int64_t ldw, const void *src, int64_t M,
                        int64_t K, hipStream_t st);

@@ -29,6 +29,7 @@
 namespace tvl {
 namespace {
 
+typedef float f2 __attribute__((ext_vector_type(2)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef float f8 __attribute__((ext_vector_type(8)));
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
@@ -105,6 +106,28 @@ __device__ __forceinline__ void mac_x(f4 &a, const h8 w, const f4 xa, const f4 x
     const f4 hi = {wf[4], wf[5], wf[6], wf[7]};
     fma4(a, lo, xa);
     fma4(a, hi, xb);
+}
+
+// Two accumulators per (row, vector) for the several-vector kernel: half
+// the registers of four, and each still sums only K/128 products.
+__device__ __forceinline__ void mac2(f2 &a, const f4 w, const f4 xa, const f4)
+{
+    a.x = __builtin_fmaf(w.x, xa.x, a.x);
+    a.y = __builtin_fmaf(w.y, xa.y, a.y);
+    a.x = __builtin_fmaf(w.z, xa.z, a.x);
+    a.y = __builtin_fmaf(w.w, xa.w, a.y);
+}
+__device__ __forceinline__ void mac2(f2 &a, const h8 w, const f4 xa, const f4 xb)
+{
+    const f8 wf = __builtin_convertvector(w, f8);
+    a.x = __builtin_fmaf(wf[0], xa.x, a.x);
+    a.y = __builtin_fmaf(wf[1], xa.y, a.y);
+    a.x = __builtin_fmaf(wf[2], xa.z, a.x);
+    a.y = __builtin_fmaf(wf[3], xa.w, a.y);
+    a.x = __builtin_fmaf(wf[4], xb.x, a.x);
+    a.y = __builtin_fmaf(wf[5], xb.y, a.y);
+    a.x = __builtin_fmaf(wf[6], xb.z, a.x);
+    a.y = __builtin_fmaf(wf[7], xb.w, a.y);
 }
 
 template <typename V, int N>
@@ -252,6 +275,29 @@ __device__ __forceinline__ void halve(float *v, int lane)
     }
 }
 
+// Apply the exchange steps for N values: offsets 32, 16, ... (log2 N steps).
+template <int N, int O>
+__device__ __forceinline__ void halve_all(float *v, int lane)
+{
+    if constexpr (N > 1) {
+        halve<N / 2, O>(v, lane);
+        halve_all<N / 2, O / 2>(v, lane);
+    }
+}
+
+// Reduce N values per lane over the wavefront (N a power of two <= 64).  On
+// return every lane holds the total of value lane / (64 / N).
+template <int N>
+__device__ __forceinline__ float reduce_vals(float *v, int lane)
+{
+    static_assert(N >= 1 && N <= 64 && (N & (N - 1)) == 0, "N must be a power of two <= 64");
+    halve_all<N, 32>(v, lane);
+#pragma unroll
+    for (int o = 32 / N; o >= 1; o >>= 1)
+        v[0] += __shfl_xor(v[0], o);
+    return v[0];
+}
+
 // Reduce R rows of per-lane float4 partials over the wavefront.  On return
 // every lane holds the total of row lane / (64 / R).
 template <int R>
@@ -261,20 +307,7 @@ __device__ __forceinline__ float reduce_rows(const f4 (&acc)[R], int lane)
 #pragma unroll
     for (int r = 0; r < R; ++r)
         v[r] = (acc[r].x + acc[r].y) + (acc[r].z + acc[r].w);
-    if constexpr (R == 8) {
-        halve<4, 32>(v, lane);
-        halve<2, 16>(v, lane);
-        halve<1, 8>(v, lane);
-    } else if constexpr (R == 4) {
-        halve<2, 32>(v, lane);
-        halve<1, 16>(v, lane);
-    } else if constexpr (R == 2) {
-        halve<1, 32>(v, lane);
-    }
-#pragma unroll
-    for (int o = 32 / R; o >= 1; o >>= 1)
-        v[0] += __shfl_xor(v[0], o);
-    return v[0];
+    return reduce_vals<R>(v, lane);
 }
 
 // One row tile, x staged in LDS: WV wavefronts x R rows, columns
@@ -681,6 +714,165 @@ __global__ __launch_bounds__(WV *kWave) void k_sweep_direct(const DevItem *__res
     }
 }
 
+// Several x vectors against the same weights (beam search with B
+// hypotheses, Sec. 9.1: each extra hypothesis would otherwise stream every
+// weight again).  Y[b][i] = sum_j W_ij X[b][j] for b < nb <= B: the weights
+// are loaded once per wavefront and multiplied into R x B accumulators; the
+// x vectors come straight from global memory (L1/L2-cached).  Vectors
+// b >= nb re-read vector 0 and their results are dropped.
+template <typename T, int R, int U, int B>
+struct MultiRows {
+    using V = typename Vec<T>::type;
+    static constexpr int N = Vec<T>::N;
+    static constexpr int CH = kWave * N;
+    const T *rows[R];
+    const float *xl[B]; // vector b at this lane's first column
+    int kn, nv, nfull;
+
+    __device__ __forceinline__ MultiRows(const T *w0, int64_t ldw, int nrows, const float *x,
+                                         int64_t ldx, int nb, int kn_, int lane)
+        : kn(kn_), nv((kn_ + N - 1) / N), nfull(kn_ / CH)
+    {
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            rows[r] = w0 + (int64_t)(r < nrows ? r : nrows - 1) * ldw + lane * N;
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+            xl[b] = x + (int64_t)(b < nb ? b : 0) * ldx + lane * N;
+    }
+
+    __device__ __forceinline__ void run(f2 (&acc)[R][B], int lane) const
+    {
+        int c = 0;
+        for (; c + U <= nfull; c += U) {
+            V w[U][R];
+            f4 xa[U][B], xb[U][B];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    w[u][r] = load_w<T>(rows[r] + (c + u) * CH);
+#pragma unroll
+                for (int b = 0; b < B; ++b) {
+                    xa[u][b] = load_x4(xl[b] + (c + u) * CH);
+                    xb[u][b] = (N == 8) ? load_x4(xl[b] + (c + u) * CH + 4) : xa[u][b];
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0); // all loads of the batch first
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+#pragma unroll
+                    for (int b = 0; b < B; ++b)
+                        mac2(acc[r][b], w[u][r], xa[u][b], xb[u][b]);
+        }
+        for (; c < nfull; ++c) {
+            V w[R];
+            f4 xa[B], xb[B];
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                w[r] = load_w<T>(rows[r] + c * CH);
+#pragma unroll
+            for (int b = 0; b < B; ++b) {
+                xa[b] = load_x4(xl[b] + c * CH);
+                xb[b] = (N == 8) ? load_x4(xl[b] + c * CH + 4) : xa[b];
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int b = 0; b < B; ++b)
+                    mac2(acc[r][b], w[r], xa[b], xb[b]);
+        }
+        if (c * kWave < nv) { // ragged last chunk: mask W and x past kn
+            const int v = c * kWave + lane;
+            if (v < nv) {
+                const int valid = kn - v * N;
+                V w[R];
+                f4 xa[B], xb[B];
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    w[r] = mask_from<V, N>(load_w<T>(rows[r] + c * CH), valid);
+#pragma unroll
+                for (int b = 0; b < B; ++b) {
+                    xa[b] = mask_from<f4, 4>(load_x4(xl[b] + c * CH), valid);
+                    xb[b] = xa[b];
+                    if constexpr (N == 8) {
+                        xb[b] = f4{0.f, 0.f, 0.f, 0.f};
+                        if (valid > 4)
+                            xb[b] = mask_from<f4, 4>(load_x4(xl[b] + c * CH + 4), valid - 4);
+                    }
+                }
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+#pragma unroll
+                    for (int b = 0; b < B; ++b)
+                        mac2(acc[r][b], w[r], xa[b], xb[b]);
+            }
+        }
+    }
+};
+
+template <typename T, int R, int WV, int U, int B>
+__device__ __forceinline__ void tile_multi(const DevItem &it, int row0)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wrow0 = row0 + wave * R;
+    const int nrows = it.M - wrow0;
+    if (nrows <= 0) return;
+    const int nb = it.nrhs < 1 ? 1 : it.nrhs;
+    f2 acc[R][B];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+            acc[r][b] = f2{0.f, 0.f};
+    const MultiRows<T, R, U, B> mr(static_cast<const T *>(it.W) + (int64_t)wrow0 * it.ldw, it.ldw,
+                                   min(nrows, R), it.x, it.ldx, nb, it.K, lane);
+    mr.run(acc, lane);
+    float v[R * B];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+            v[r * B + b] = acc[r][b].x + acc[r][b].y;
+    const float t = reduce_vals<R * B>(v, lane);
+    constexpr int G = kWave / (R * B);
+    if ((lane % G) == 0) {
+        const int q = lane / G;
+        const int r = q / B, b = q % B;
+        const int row = wrow0 + r;
+        if (b < nb && r < nrows) it.y[(int64_t)b * it.ldy + row] = t;
+    }
+}
+
+template <int R, int WV, int U, int B>
+__global__ __launch_bounds__(WV *kWave) void k_sweep_multi(const DevItem *__restrict__ items,
+                                                            const DevTile *__restrict__ tiles,
+                                                            int ntiles)
+{
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const DevTile tl = tiles[t];
+        const DevItem it = items[tl.item];
+        if (it.dtype == 1)
+            tile_multi<_Float16, R, WV, U, B>(it, tl.row0);
+        else
+            tile_multi<float, R, WV, U, B>(it, tl.row0);
+        __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
+    }
+}
+
+template <int R, int WV, int U, int B>
+__global__ __launch_bounds__(WV *kWave) void k_item_multi(const DevItem it)
+{
+    const int row0 = (int)blockIdx.x * (R * WV);
+    if (it.dtype == 1)
+        tile_multi<_Float16, R, WV, U, B>(it, row0);
+    else
+        tile_multi<float, R, WV, U, B>(it, row0);
+}
+
 // Grouped sweep whose items may carry a fused RMSNorm and/or be SwiGLU
 // pairs: the same tile loop, with the item's kind chosen per tile.
 template <int R, int WV, int U>
@@ -795,6 +987,28 @@ struct InstFused {
         const int rows = tile_rows<R, WV>(it.op);
         const dim3 grid((it.M + rows - 1) / rows), block(WV * kWave);
         hipLaunchKernelGGL((k_item<R, WV, U>), grid, block, 0, st, it);
+        return hipGetLastError();
+    }
+};
+
+// (R, waves per block, U, B) with B x vectors per launch (B >= nrhs).
+#define TVL_MULTI_SHAPES(X)                                                                       \
+    X(2, 4, 2, 2) X(2, 4, 4, 2) X(4, 4, 2, 2) X(2, 4, 1, 4) X(2, 4, 2, 4) X(4, 4, 1, 4)          \
+        X(4, 4, 2, 4) X(2, 4, 1, 8) X(2, 4, 2, 8) X(4, 4, 1, 8)
+
+template <int R, int WV, int U, int B>
+struct InstMulti {
+    static hipError_t sweep(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
+                            hipStream_t st)
+    {
+        hipLaunchKernelGGL((k_sweep_multi<R, WV, U, B>), dim3(grid), dim3(WV * kWave), 0, st,
+                           items, tiles, ntiles);
+        return hipGetLastError();
+    }
+    static hipError_t item(const DevItem &it, hipStream_t st)
+    {
+        const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
+        hipLaunchKernelGGL((k_item_multi<R, WV, U, B>), grid, block, 0, st, it);
         return hipGetLastError();
     }
 };
@@ -978,6 +1192,36 @@ hipError_t launch_item(const Shape &s, const DevItem &item, hipStream_t st)
 #define X(R_, W_, U_)                                                                             \
     if (s.R == R_ && s.W == W_ && s.U == U_) return InstFused<R_, W_, U_>::item(item, st);
     TVL_FUSED_SHAPES(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+bool multi_shape_supported(const Shape &s, int B)
+{
+#define X(R_, W_, U_, B_)                                                                         \
+    if (s.R == R_ && s.W == W_ && s.U == U_ && B == B_) return s.xmode == kXDirect;
+    TVL_MULTI_SHAPES(X)
+#undef X
+    return false;
+}
+
+hipError_t launch_sweep_multi(const Shape &s, int B, const DevItem *items, const DevTile *tiles,
+                              int ntiles, int grid, hipStream_t st)
+{
+#define X(R_, W_, U_, B_)                                                                         \
+    if (s.R == R_ && s.W == W_ && s.U == U_ && B == B_)                                          \
+        return InstMulti<R_, W_, U_, B_>::sweep(items, tiles, ntiles, grid, st);
+    TVL_MULTI_SHAPES(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_item_multi(const Shape &s, int B, const DevItem &item, hipStream_t st)
+{
+#define X(R_, W_, U_, B_)                                                                         \
+    if (s.R == R_ && s.W == W_ && s.U == U_ && B == B_)                                          \
+        return InstMulti<R_, W_, U_, B_>::item(item, st);
+    TVL_MULTI_SHAPES(X)
 #undef X
     return hipErrorInvalidValue;
 }

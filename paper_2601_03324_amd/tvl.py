@@ -51,7 +51,8 @@ class tvl_item(ctypes.Structure):
     _fields_ = [("W", ctypes.c_void_p), ("ldw", ctypes.c_int64), ("x", ctypes.c_void_p),
                 ("y", ctypes.c_void_p), ("M", ctypes.c_int64), ("K", ctypes.c_int64),
                 ("dtype", ctypes.c_int32), ("op", ctypes.c_int32), ("W3", ctypes.c_void_p),
-                ("g", ctypes.c_void_p), ("eps", ctypes.c_float), ("reserved", ctypes.c_int32)]
+                ("g", ctypes.c_void_p), ("eps", ctypes.c_float), ("nrhs", ctypes.c_int32),
+                ("ldx", ctypes.c_int64), ("ldy", ctypes.c_int64)]
 
 
 class tvl_tuning(ctypes.Structure):
@@ -60,7 +61,7 @@ class tvl_tuning(ctypes.Structure):
                 ("grid", ctypes.c_int32), ("flags", ctypes.c_int32)]
 
 
-assert ctypes.sizeof(tvl_item) == 80
+assert ctypes.sizeof(tvl_item) == 96
 
 
 def _bind_hip_runtime() -> None:
@@ -170,10 +171,10 @@ def tvl_gemv_ex(W, ldw: int, dtype: int, x, y, M: int, K: int, tuning=None, stre
 
 
 def item(W, ldw: int, x, y, M: int, K: int, dtype: int, op: int = TVL_OP_GEMV, W3=None,
-         g=None, eps: float = 0.0) -> tvl_item:
+         g=None, eps: float = 0.0, nrhs: int = 1, ldx: int = 0, ldy: int = 0) -> tvl_item:
     """One tvl_item; pointers as ints or tensors."""
     return tvl_item(_p(W), ldw, _p(x), _p(y), M, K, dtype, op, _p(W3) or None, _p(g) or None,
-                    eps, 0)
+                    eps, nrhs, ldx, ldy)
 
 
 def make_items(items) -> ctypes.Array:

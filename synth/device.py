@@ -113,3 +113,35 @@ def load_fused(wl, device="cuda", progress: bool = False) -> list:
         if progress and (i % 8 == 0 or i == len(wl.items) - 1):
             print(f"  loaded {wl.name} {i + 1}/{len(wl.items)}", flush=True, file=sys.stderr)
     return out
+
+
+@dataclass
+class DevMulti:
+    spec: MatSpec
+    W: object   # TvlMatrix
+    X: object   # torch fp32 [B, ldx]
+    Y: object   # torch fp32 [B, ldy]
+    B: int
+
+    def item(self) -> dict:
+        return dict(W=self.W.ptr, ldw=self.W.ldw, x=self.X, y=self.Y, M=self.spec.M,
+                    K=self.spec.K, dtype=self.W.dtype, nrhs=self.B, ldx=self.X.shape[1],
+                    ldy=self.Y.shape[1])
+
+
+def load_multi(wl: Workload, B: int, device="cuda", share_from: list | None = None) -> list:
+    """Every matrix of ``wl`` with B x vectors (reps 0..B-1 of its x stream),
+    stored as B rows padded to a multiple of 4 floats; y as B rows of M."""
+    import torch
+    from paper_2601_03324_amd import tvl
+    out = []
+    for i, m in enumerate(wl.mats):
+        Wd = share_from[i].W if share_from is not None else tvl.upload_matrix(
+            m.weights(), dtype_code(m), device)
+        ldx = (m.K + 3) // 4 * 4
+        X = torch.zeros((B, ldx), dtype=torch.float32)
+        for b in range(B):
+            X[b, :m.K] = torch.from_numpy(m.x(b))
+        Y = torch.full((B, m.M), float("nan"), dtype=torch.float32, device=device)
+        out.append(DevMulti(m, Wd, X.to(device), Y, B))
+    return out

@@ -46,7 +46,10 @@ def test_missing_library_fails_loudly(tmp_path, monkeypatch):
 
 
 def test_item_layout_matches_header():
-    assert ctypes.sizeof(tvl.tvl_item) == 80
+    assert ctypes.sizeof(tvl.tvl_item) == 96
+    assert tvl.tvl_item.nrhs.offset == 76
+    assert tvl.tvl_item.ldx.offset == 80
+    assert tvl.tvl_item.ldy.offset == 88
     assert tvl.tvl_item.dtype.offset == 48
     assert tvl.tvl_item.op.offset == 52
     assert tvl.tvl_item.W3.offset == 56
@@ -63,13 +66,16 @@ D = 4 << 40  # another fake, far-away device address (g, W3)
     (dict(W3=D), ARG), (dict(g=D + 4), ALIGN), (dict(g=D, eps=-1.0), ARG),
     (dict(g=D, eps=float("nan")), ARG), (dict(g=D, eps=float("inf")), ARG),
     (dict(op=1, W3=D, y=D + 128), ALIAS), (dict(g=D, eps=1e-5, y=D + 1024), ALIAS),
-    (dict(reserved=1), ARG),
+    (dict(nrhs=9, ldx=768, ldy=768), ARG), (dict(nrhs=-1), ARG),
+    (dict(nrhs=2, ldx=767, ldy=768), SHAPE), (dict(nrhs=2, ldx=768, ldy=700), SHAPE),
+    (dict(nrhs=2, ldx=770, ldy=768), ALIGN), (dict(nrhs=2, ldx=768, ldy=768, g=D), ARG),
+    (dict(nrhs=2, ldx=768, ldy=768, op=1, W3=D), ARG),
+    # the second y row runs into the second x row's neighbour: y rows span (n-1)*ldy + M
+    (dict(nrhs=4, ldx=1024, ldy=1024, y=B + 4 * 3 * 1024), ALIAS),
 ])
 def test_fused_item_rejects(kw, st):
     base = dict(W=A, ldw=768, x=B, y=C, M=768, K=768, dtype=0)
-    reserved = kw.pop("reserved", 0)
     it = tvl.item(**{**base, **kw})
-    it.reserved = reserved
     assert L.tvl_gemv_item(ctypes.byref(it), None, None) == st
     arr, n = tvl.make_items([it])
     assert L.tvl_gemv_batch_sweep(arr, n, None) == st
@@ -153,9 +159,13 @@ def test_sweep_rejects_and_enqueues_nothing():
     # output of one item over the x of another
     arr, n = items(good, (A + (1 << 30), 768, C + 16, C + (1 << 24), 768, 768, 0))
     assert L.tvl_gemv_batch_sweep(arr, n, None) == ALIAS
-    # reserved field must be zero
-    arr, n = items(good)
-    arr[0].reserved = 1
+    # several-vector items cannot share a plan with fused items
+    arr, n = tvl.make_items([dict(W=A, ldw=768, x=B, y=C, M=768, K=768, dtype=0, nrhs=2,
+                                  ldx=768, ldy=768),
+                             dict(W=A, ldw=768, x=B, y=C + (1 << 20), M=768, K=768, dtype=0,
+                                  g=D, eps=1e-5)])
+    h = ctypes.c_void_p()
+    assert L.tvl_sweep_plan_create(arr, n, None, ctypes.byref(h)) == ARG
     assert L.tvl_gemv_batch_sweep(arr, n, None) == ARG
     assert L.tvl_gemv_batch_sweep(None, 3, None) == NULL
     assert L.tvl_gemv_batch_sweep(None, -1, None) == SHAPE

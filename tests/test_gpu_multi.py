@@ -1,0 +1,126 @@
+"""GPU parity of the several-vector GEMV (beam search with B hypotheses,
+Sec. 9.1: one pass over the weights serves every hypothesis).  Each output
+vector is checked against the oracle's GEMV of its own x (the plain
+definition, applied per vector), with the GEMV parity norm.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2601_03324_amd import tvl  # noqa: E402
+import synth.device as sdev  # noqa: E402
+
+TOL = {0: 1e-5, 1: 2e-3}
+DEV = "cuda"
+MULTI = [(2, 4, 2, 2), (2, 4, 4, 2), (4, 4, 2, 2), (2, 4, 1, 4), (2, 4, 2, 4), (4, 4, 1, 4),
+         (4, 4, 2, 4), (2, 4, 1, 8), (2, 4, 2, 8), (4, 4, 1, 8)]
+
+
+def tunings(nrhs):
+    out = [None]
+    for r, w, u, b in MULTI:
+        if b >= nrhs and (b == 2 or b // 2 < nrhs):  # the kernels the library would pick from
+            out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
+    return out
+
+
+def dev_matrix(host, dt):
+    M, K = host.shape
+    ldw = tvl.tvl_row_stride(K, dt)
+    if dt == 0:
+        buf = torch.full((M, ldw), float("nan"), dtype=torch.float32, device=DEV)
+        buf[:, :K] = torch.from_numpy(np.ascontiguousarray(host, np.float32)).to(DEV)
+    else:
+        buf = torch.full((M, ldw), 0x7E00, dtype=torch.int16, device=DEV)
+        buf[:, :K] = torch.from_numpy(np.ascontiguousarray(host, np.uint16).view(np.int16)).to(DEV)
+    return buf, ldw
+
+
+def run(buf, ldw, dt, X, M, K, nrhs, ldy, t):
+    """X: host [nrhs, K]; x rows padded to ldx with NaN (never read); y rows
+    of ldy floats, the gap after each row holds a sentinel that must stay."""
+    ldx = (K + 3) // 4 * 4 + 4
+    Xd = torch.full((nrhs, ldx), float("nan"), device=DEV)
+    Xd[:, :K] = torch.from_numpy(X).to(DEV)
+    Yd = torch.full((nrhs, ldy), -12345.0, device=DEV)
+    tvl.tvl_gemv_item(dict(W=buf, ldw=ldw, x=Xd, y=Yd, M=M, K=K, dtype=dt, nrhs=nrhs, ldx=ldx,
+                           ldy=ldy), t)
+    torch.cuda.synchronize()
+    Y = Yd.cpu().numpy()
+    assert np.all(Y[:, M:] == -12345.0), "wrote past M in a y row"
+    return Y[:, :M]
+
+
+SHAPES = [(1, 1), (3, 17), (64, 63), (65, 65), (257, 255), (1000, 1000), (33, 4095),
+          (130, 11008), (5, 28672), (2048, 768)]
+
+
+@pytest.mark.parametrize("nrhs", [2, 3, 4, 5, 8])
+@pytest.mark.parametrize("dt", [0, 1], ids=["f32", "f16"])
+@pytest.mark.parametrize("M,K", SHAPES, ids=[f"{m}x{k}" for m, k in SHAPES])
+def test_multi_vectors(M, K, dt, nrhs):
+    rng = np.random.default_rng(M * 31 + K * 7 + dt * 3 + nrhs)
+    Wf = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    W = Wf if dt == 0 else synth.f32_to_f16_bits(Wf)
+    X = rng.standard_normal((nrhs, K)).astype(np.float32)
+    refs = [(oracle.gemv_f32 if dt == 0 else oracle.gemv_f16)(W, X[b]) for b in range(nrhs)]
+    buf, ldw = dev_matrix(W, dt)
+    for t in tunings(nrhs):
+        Y = run(buf, ldw, dt, X, M, K, nrhs, M + 3, t)
+        for b in range(nrhs):
+            r = oracle.check(Y[b], refs[b][0], refs[b][1], TOL[dt])
+            assert r["bad"] == 0, (M, K, nrhs, b, t, r)
+
+
+def test_multi_matches_single_bitwise_on_integers():
+    """Integer data: every vector's result is exact, so it equals the
+    single-vector result bit for bit."""
+    M, K = 300, 2000
+    W = synth.int_f32(M * K, synth.key(77, 1), -3, 3).reshape(M, K)
+    X = synth.int_f32(8 * K, synth.key(77, 2), -8, 8).reshape(8, K)
+    buf, ldw = dev_matrix(W, 0)
+    for t in tunings(8):
+        Y = run(buf, ldw, 0, X, M, K, 8, M, t)
+        for b in range(8):
+            ref, _ = oracle.gemv_f32(W, X[b])
+            assert np.array_equal(Y[b].astype(np.float64), ref), (b, t)
+
+
+def test_beam4_sweep110m():
+    """The 110M decode token for 4 hypotheses (85 items x 4 vectors), one
+    launch; every output of every vector against the oracle."""
+    wl = synth.WORKLOADS["sweep110m"]
+    ms = sdev.load_multi(wl, 4, DEV)
+    for t in (None, dict(rows_per_wave=2, waves_per_block=4, unroll=2, flags=2),
+              dict(rows_per_wave=4, waves_per_block=4, unroll=1, flags=2, grid=500)):
+        for d in ms:
+            d.Y.fill_(float("nan"))
+        plan = tvl.tvl_sweep_plan_create([d.item() for d in ms], t)
+        plan.run()
+        torch.cuda.synchronize()
+        for d in ms:
+            m = d.spec
+            Wh = m.weights() if m.M < 32000 else None
+            Y = d.Y.cpu().numpy()
+            for b in range(4):
+                if Wh is None:  # the classifier: sampled rows
+                    rows = sdev.sample_rows(m.M, 256, 5)
+                    ref, S = oracle.gemv_f32(np.stack([m.weights(int(r), 1)[0] for r in rows]),
+                                             m.x(b))
+                    yb = Y[b][rows]
+                else:
+                    ref, S = oracle.gemv_f32(Wh, m.x(b))
+                    yb = Y[b]
+                r = oracle.check(yb, ref, S, 1e-5)
+                assert r["bad"] == 0, (m.name, b, t, r)
+        plan.destroy()
