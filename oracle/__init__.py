@@ -56,6 +56,10 @@ def load(path: str) -> ctypes.CDLL:
     L.oracle_gemv_dx.restype = None
     L.oracle_swiglu.argtypes = [P, P, I64, P]
     L.oracle_swiglu.restype = None
+    L.oracle_gemv_q.argtypes = [P, ctypes.c_int32, I64, P, I64, I64, P, P]
+    L.oracle_gemv_q.restype = None
+    L.oracle_q_weight.argtypes = [P, ctypes.c_int32, I64, I64, I64, I64]
+    L.oracle_q_weight.restype = D
     return L
 
 
@@ -215,3 +219,22 @@ def swiglu_bound(a: np.ndarray, b: np.ndarray, Sa: np.ndarray, Sb: np.ndarray,
     sig = 1.0 / (1.0 + np.exp(-a))
     dsilu = sig * (1.0 + a * (1.0 - sig))
     return np.abs(dsilu) * np.abs(b) * Sa + np.abs(a * sig) * Sb + np.abs(h) * 2.0 ** -20
+
+
+def gemv_q(Wq: np.ndarray, bits: int, x: np.ndarray, K: int):
+    """(y, S) for block-quantised rows (uint8 [M, ldw] bytes, codes then fp32
+    group scales, see oracle.c), 8- or 4-bit codes."""
+    Wq = np.ascontiguousarray(Wq, dtype=np.uint8)
+    if Wq.ndim != 2 or bits not in (4, 8):
+        raise ValueError("Wq must be [M, ldw] uint8 and bits 4 or 8")
+    M, ldw = Wq.shape
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    y = np.empty(M, dtype=np.float64)
+    S = np.empty(M, dtype=np.float64)
+    lib().oracle_gemv_q(_ptr(Wq), bits, ldw, _ptr(x), M, K, _ptr(y), _ptr(S))
+    return y, S
+
+
+def q_weight(Wq: np.ndarray, bits: int, K: int, i: int, j: int) -> float:
+    Wq = np.ascontiguousarray(Wq, dtype=np.uint8)
+    return lib().oracle_q_weight(_ptr(Wq), bits, Wq.shape[1], K, i, j)

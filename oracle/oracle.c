@@ -182,3 +182,59 @@ void oracle_swiglu(const double *a, const double *b, int64_t M, double *h)
     for (int64_t i = 0; i < M; ++i)
         h[i] = a[i] / (1.0 + exp(-a[i])) * b[i];
 }
+
+/* ------------------------------------------------------------------------ */
+/* Block-quantised weights (Sec. 8.2 proposes 4-bit weights unpacked on the  */
+/* fly; Sec. 2.2 names 4/8-bit quantisation; the paper fixes no format).     */
+/* Format of this library, one row per ldw bytes:                            */
+/*   bytes [0, cb): codes, column j at byte j (8-bit) or nibble j of byte    */
+/*                  j/2, low nibble first (4-bit);                           */
+/*   bytes [cb, cb + 4 ceil(K/64)): one fp32 scale per group of 64 columns;  */
+/*   cb = roundup(ceil(K * bits / 8), 128).                                  */
+/*   8-bit: w_ij = s_{i, j/64} * q_ij, q two's complement in [-128, 127];    */
+/*   4-bit: w_ij = s_{i, j/64} * (u_ij - 8), u the unsigned nibble.          */
+/* The products and sums are done exactly as in oracle_gemv_f32, in double.  */
+/* ------------------------------------------------------------------------ */
+static int64_t q_code_bytes(int64_t K, int bits)
+{
+    const int64_t b = (K * bits + 7) / 8;
+    return (b + 127) / 128 * 128;
+}
+
+static double q_weight(const uint8_t *row, int64_t j, int64_t K, int bits)
+{
+    const float *scales = (const float *)(row + q_code_bytes(K, bits));
+    const double s = (double)scales[j / 64];
+    double q;
+    if (bits == 8) {
+        q = (double)(int8_t)row[j];
+    } else {
+        const uint8_t byte = row[j / 2];
+        const int u = (j % 2 == 0) ? (byte & 0x0f) : (byte >> 4);
+        q = (double)(u - 8);
+    }
+    return s * q; /* exact: 24-bit scale times a code of at most 8 bits */
+}
+
+void oracle_gemv_q(const uint8_t *W, int32_t bits, int64_t ldw, const float *x,
+                   int64_t M, int64_t K, double *y, double *S)
+{
+    for (int64_t i = 0; i < M; ++i) {
+        const uint8_t *row = W + i * ldw;
+        double acc = 0.0, s = 0.0;
+        for (int64_t j = 0; j < K; ++j) {
+            const double p = q_weight(row, j, K, bits) * (double)x[j];
+            acc += p;
+            s += fabs(p);
+        }
+        y[i] = acc;
+        if (S) S[i] = s;
+    }
+}
+
+/* Decoded fp64 weight of row i, column j (for tests). */
+double oracle_q_weight(const uint8_t *W, int32_t bits, int64_t ldw, int64_t K, int64_t i,
+                       int64_t j)
+{
+    return q_weight(W + i * ldw, j, K, bits);
+}

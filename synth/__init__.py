@@ -55,8 +55,11 @@ def lib() -> ctypes.CDLL:
         L.synth_normal_f16.argtypes = [P, I64, U64, U64, D]
         L.synth_int_f32.argtypes = [P, I64, U64, U64, I64, I64]
         L.synth_int_f16.argtypes = [P, I64, U64, U64, I64, I64]
+        L.synth_q_row_bytes.argtypes = [I64, ctypes.c_int]
+        L.synth_q_row_bytes.restype = I64
+        L.synth_quantize_rows.argtypes = [P, I64, I64, ctypes.c_int, P, I64]
         for n in ("synth_f32_to_f16", "synth_uniform_f32", "synth_normal_f32",
-                  "synth_normal_f16", "synth_int_f32", "synth_int_f16"):
+                  "synth_normal_f16", "synth_int_f32", "synth_int_f16", "synth_quantize_rows"):
             getattr(L, n).restype = None
         _lib = L
     return _lib
@@ -107,6 +110,21 @@ def f32_to_f16_bits(a: np.ndarray) -> np.ndarray:
     a = np.ascontiguousarray(a, dtype=np.float32)
     out = np.empty(a.shape, np.uint16)
     lib().synth_f32_to_f16(a.ctypes.data, out.ctypes.data, a.size)
+    return out
+
+
+def q_row_bytes(K: int, bits: int) -> int:
+    return int(lib().synth_q_row_bytes(K, bits))
+
+
+def quantize_rows(w: np.ndarray, bits: int, ldw: int | None = None, pad: int = 0) -> np.ndarray:
+    """fp32 [M, K] -> block-quantised rows [M, ldw] uint8 (codes, then fp32
+    scales per 64 columns); padding bytes = `pad`."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    M, K = w.shape
+    ldw = q_row_bytes(K, bits) if ldw is None else ldw
+    out = np.full((M, ldw), pad, np.uint8)
+    lib().synth_quantize_rows(w.ctypes.data, M, K, bits, out.ctypes.data, ldw)
     return out
 
 

@@ -3,7 +3,7 @@
  *
  * Serves both the oracle side and the HIP side with identical inputs.  It
  * holds none of the GEMV arithmetic: it only draws numbers and rounds them to
- * the storage types (fp32, binary16).
+ * the storage types (fp32, binary16, block-quantised 8/4-bit codes).
  *
  * Generator: SplitMix64 (G. L. Steele, D. Lea, C. H. Flood, "Fast splittable
  * pseudorandom number generators", OOPSLA 2014).  The k-th output (k >= 0) of
@@ -150,4 +150,62 @@ void synth_int_f16(uint16_t *out, int64_t n, uint64_t key, uint64_t offset,
     for (int64_t i = 0; i < n; ++i)
         out[i] = synth_f32_to_f16_bits(
             (float)(lo + (int64_t)(synth_u64(key, offset + (uint64_t)i) % span)));
+}
+
+/* ------------------------------------------------------------------------ */
+/* Block quantisation of fp32 rows into the quantised row format (codes,    */
+/* then one fp32 scale per 64 columns; see the library header).  Symmetric: */
+/* 8-bit s = max|w| / 127, q = round(w / s) in [-127, 127]; 4-bit            */
+/* s = max|w| / 7, q = round(w / s) in [-7, 7] stored as nibble q + 8.       */
+/* An all-zero group gets s = 0 and q = 0.  Padding bytes are left as they  */
+/* are in `out` (the caller fills them).                                     */
+/* ------------------------------------------------------------------------ */
+static int64_t q_code_bytes(int64_t K, int bits)
+{
+    const int64_t b = (K * bits + 7) / 8;
+    return (b + 127) / 128 * 128;
+}
+
+int64_t synth_q_row_bytes(int64_t K, int bits)
+{
+    const int64_t r = q_code_bytes(K, bits) + 4 * ((K + 63) / 64);
+    return (r + 127) / 128 * 128;
+}
+
+void synth_quantize_rows(const float *w, int64_t M, int64_t K, int bits, uint8_t *out,
+                         int64_t ldw)
+{
+    const int64_t cb = q_code_bytes(K, bits);
+    const int64_t ng = (K + 63) / 64;
+    const int qmax = bits == 8 ? 127 : 7;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < M; ++i) {
+        const float *src = w + i * K;
+        uint8_t *row = out + i * ldw;
+        float *scales = (float *)(row + cb);
+        for (int64_t g = 0; g < ng; ++g) {
+            const int64_t j0 = g * 64, j1 = (j0 + 64 < K) ? j0 + 64 : K;
+            float amax = 0.f;
+            for (int64_t j = j0; j < j1; ++j)
+                amax = fabsf(src[j]) > amax ? fabsf(src[j]) : amax;
+            const float s = amax / (float)qmax;
+            scales[g] = s;
+            for (int64_t j = j0; j < j1; ++j) {
+                int q = 0;
+                if (s > 0.f) {
+                    q = (int)lrintf(src[j] / s);
+                    q = q > qmax ? qmax : (q < -qmax ? -qmax : q);
+                }
+                if (bits == 8) {
+                    row[j] = (uint8_t)(int8_t)q;
+                } else {
+                    const uint8_t u = (uint8_t)(q + 8);
+                    if (j % 2 == 0)
+                        row[j / 2] = (uint8_t)((row[j / 2] & 0xf0) | u);
+                    else
+                        row[j / 2] = (uint8_t)((row[j / 2] & 0x0f) | (u << 4));
+                }
+            }
+        }
+    }
 }
