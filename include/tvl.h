@@ -66,10 +66,28 @@ extern "C" {
 
 #define TVL_VERSION 100 /* 1.0.0 */
 
-/* Weight element type.  x and y are always fp32. */
+/* Weight element type.  x and y are always fp32.
+ *
+ * Block-quantised weights (TVL_Q8, TVL_Q4): the paper proposes 4-bit weights
+ * unpacked on the fly (Sec. 8.2) and names 4/8-bit quantisation (Sec. 2.2)
+ * but fixes no format.  This library's format for an M x K matrix is one
+ * 128-byte-aligned buffer:
+ *   code plane    M rows of ldw BYTES (ldw a multiple of 128, at least
+ *                 roundup(ceil(K*bits/8), 128) = tvl_row_stride);
+ *                 8-bit: column j at byte j, two's complement q in [-128, 127];
+ *                 4-bit: column j in byte j/2, low nibble first, unsigned u,
+ *                 q = u - 8 in [-8, 7];
+ *   scale plane   at byte M*ldw: fp32 s[i][g], row-major, ceil(K/64) per
+ *                 row, s[i][g] scaling columns 64g .. 64g+63 of row i;
+ *   w_ij = s[i][j/64] * q_ij        (converted exactly; fp32 accumulation).
+ * Keeping the scales out of the code rows keeps every fetched 128-byte line
+ * full.  Code bytes past column K are padding and never change the result;
+ * the whole buffer spans M*ldw + 4*M*ceil(K/64) bytes. */
 typedef enum tvl_dtype {
     TVL_F32 = 0, /* IEEE binary32 weights */
-    TVL_F16 = 1  /* IEEE binary16 weights, converted exactly to fp32 */
+    TVL_F16 = 1, /* IEEE binary16 weights, converted exactly to fp32 */
+    TVL_Q8 = 2,  /* 8-bit block-quantised weights (ldw in bytes) */
+    TVL_Q4 = 3   /* 4-bit block-quantised weights (ldw in bytes) */
 } tvl_dtype;
 
 typedef enum tvl_status {
@@ -163,14 +181,16 @@ typedef struct tvl_plan tvl_plan;
 TVL_API int32_t tvl_version(void);
 
 /* Row stride, in elements, of the TVL layout for K columns of `dtype`:
- * roundup(K * size, 128) / size.  Returns -1 for K < 1 or an unknown dtype.
- * Pure host function. */
+ * roundup(K * size, 128) / size; for TVL_Q8 / TVL_Q4 the code row size in
+ * bytes, roundup(ceil(K * bits / 8), 128) (see tvl_dtype for the scale
+ * plane).  Returns -1 for K < 1 or an unknown dtype.  Pure host function. */
 TVL_API int64_t tvl_row_stride(int64_t K, int32_t dtype);
 
 /* TVL pack (Sec. 3.2 alignment): copy a dense row-major [M x K] matrix
  * `src` (device) into `dst` (device, M rows of stride ldw, 128-byte aligned)
  * and zero elements K..ldw-1 of every row.  One kernel launch on `stream`.
- * `src` is only required to be element aligned; `dst` must not overlap `src`. */
+ * `src` is only required to be element aligned; `dst` must not overlap `src`.
+ * fp32 and fp16 only (quantised rows are written by the quantiser). */
 TVL_API tvl_status tvl_pack_rows(void *dst, int64_t ldw, const void *src,
                                  int64_t M, int64_t K, int32_t dtype,
                                  hipStream_t stream);

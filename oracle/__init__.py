@@ -58,7 +58,7 @@ def load(path: str) -> ctypes.CDLL:
     L.oracle_swiglu.restype = None
     L.oracle_gemv_q.argtypes = [P, ctypes.c_int32, I64, P, I64, I64, P, P]
     L.oracle_gemv_q.restype = None
-    L.oracle_q_weight.argtypes = [P, ctypes.c_int32, I64, I64, I64, I64]
+    L.oracle_q_weight.argtypes = [P, ctypes.c_int32, I64, I64, I64, I64, I64]
     L.oracle_q_weight.restype = D
     return L
 
@@ -221,13 +221,16 @@ def swiglu_bound(a: np.ndarray, b: np.ndarray, Sa: np.ndarray, Sb: np.ndarray,
     return np.abs(dsilu) * np.abs(b) * Sa + np.abs(a * sig) * Sb + np.abs(h) * 2.0 ** -20
 
 
-def gemv_q(Wq: np.ndarray, bits: int, x: np.ndarray, K: int):
-    """(y, S) for block-quantised rows (uint8 [M, ldw] bytes, codes then fp32
-    group scales, see oracle.c), 8- or 4-bit codes."""
-    Wq = np.ascontiguousarray(Wq, dtype=np.uint8)
-    if Wq.ndim != 2 or bits not in (4, 8):
-        raise ValueError("Wq must be [M, ldw] uint8 and bits 4 or 8")
-    M, ldw = Wq.shape
+def gemv_q(Wq: np.ndarray, bits: int, ldw: int, M: int, K: int, x: np.ndarray):
+    """(y, S) for a block-quantised matrix given as one uint8 buffer: the code
+    plane (M rows of ldw bytes) followed by the fp32 scale plane (M rows of
+    ceil(K/64)); 8- or 4-bit codes (format in oracle.c)."""
+    Wq = np.ascontiguousarray(Wq, dtype=np.uint8).reshape(-1)
+    if bits not in (4, 8):
+        raise ValueError("bits must be 4 or 8")
+    need = M * ldw + 4 * M * ((K + 63) // 64)
+    if Wq.size < need:
+        raise ValueError(f"buffer of {Wq.size} bytes, need {need}")
     x = np.ascontiguousarray(x, dtype=np.float32)
     y = np.empty(M, dtype=np.float64)
     S = np.empty(M, dtype=np.float64)
@@ -235,6 +238,6 @@ def gemv_q(Wq: np.ndarray, bits: int, x: np.ndarray, K: int):
     return y, S
 
 
-def q_weight(Wq: np.ndarray, bits: int, K: int, i: int, j: int) -> float:
-    Wq = np.ascontiguousarray(Wq, dtype=np.uint8)
-    return lib().oracle_q_weight(_ptr(Wq), bits, Wq.shape[1], K, i, j)
+def q_weight(Wq: np.ndarray, bits: int, ldw: int, M: int, K: int, i: int, j: int) -> float:
+    Wq = np.ascontiguousarray(Wq, dtype=np.uint8).reshape(-1)
+    return lib().oracle_q_weight(_ptr(Wq), bits, ldw, M, K, i, j)

@@ -186,25 +186,23 @@ void oracle_swiglu(const double *a, const double *b, int64_t M, double *h)
 /* ------------------------------------------------------------------------ */
 /* Block-quantised weights (Sec. 8.2 proposes 4-bit weights unpacked on the  */
 /* fly; Sec. 2.2 names 4/8-bit quantisation; the paper fixes no format).     */
-/* Format of this library, one row per ldw bytes:                            */
-/*   bytes [0, cb): codes, column j at byte j (8-bit) or nibble j of byte    */
-/*                  j/2, low nibble first (4-bit);                           */
-/*   bytes [cb, cb + 4 ceil(K/64)): one fp32 scale per group of 64 columns;  */
-/*   cb = roundup(ceil(K * bits / 8), 128).                                  */
+/* Format of this library for an M x K matrix:                               */
+/*   code plane: M rows of ldw bytes; column j of a row at byte j (8-bit) or */
+/*               in nibble j of byte j/2, low nibble first (4-bit);          */
+/*   scale plane: right after the code plane (byte M*ldw), fp32, row-major,  */
+/*               ng = ceil(K/64) scales per row, s_{i,g} for columns         */
+/*               64g .. 64g+63;                                              */
 /*   8-bit: w_ij = s_{i, j/64} * q_ij, q two's complement in [-128, 127];    */
 /*   4-bit: w_ij = s_{i, j/64} * (u_ij - 8), u the unsigned nibble.          */
 /* The products and sums are done exactly as in oracle_gemv_f32, in double.  */
 /* ------------------------------------------------------------------------ */
-static int64_t q_code_bytes(int64_t K, int bits)
+static double q_weight(const uint8_t *W, int64_t ldw, int64_t M, int64_t K, int bits,
+                       int64_t i, int64_t j)
 {
-    const int64_t b = (K * bits + 7) / 8;
-    return (b + 127) / 128 * 128;
-}
-
-static double q_weight(const uint8_t *row, int64_t j, int64_t K, int bits)
-{
-    const float *scales = (const float *)(row + q_code_bytes(K, bits));
-    const double s = (double)scales[j / 64];
+    const float *scales = (const float *)(W + M * ldw);
+    const int64_t ng = (K + 63) / 64;
+    const double s = (double)scales[i * ng + j / 64];
+    const uint8_t *row = W + i * ldw;
     double q;
     if (bits == 8) {
         q = (double)(int8_t)row[j];
@@ -220,10 +218,9 @@ void oracle_gemv_q(const uint8_t *W, int32_t bits, int64_t ldw, const float *x,
                    int64_t M, int64_t K, double *y, double *S)
 {
     for (int64_t i = 0; i < M; ++i) {
-        const uint8_t *row = W + i * ldw;
         double acc = 0.0, s = 0.0;
         for (int64_t j = 0; j < K; ++j) {
-            const double p = q_weight(row, j, K, bits) * (double)x[j];
+            const double p = q_weight(W, ldw, M, K, bits, i, j) * (double)x[j];
             acc += p;
             s += fabs(p);
         }
@@ -233,8 +230,8 @@ void oracle_gemv_q(const uint8_t *W, int32_t bits, int64_t ldw, const float *x,
 }
 
 /* Decoded fp64 weight of row i, column j (for tests). */
-double oracle_q_weight(const uint8_t *W, int32_t bits, int64_t ldw, int64_t K, int64_t i,
-                       int64_t j)
+double oracle_q_weight(const uint8_t *W, int32_t bits, int64_t ldw, int64_t M, int64_t K,
+                       int64_t i, int64_t j)
 {
-    return q_weight(W + i * ldw, j, K, bits);
+    return q_weight(W, ldw, M, K, bits, i, j);
 }

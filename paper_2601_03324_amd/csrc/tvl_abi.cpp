@@ -29,6 +29,7 @@ struct tvl_plan {
     int device = -1;
     bool fused = false;
     int multiB = 0; // > 0: several-vector plan holding B x vectors
+    bool quant = false; // some item has block-quantised weights
     Shape shape{4, 4, 2, tvl::kXLds};
     int ks_cap = 0;
     int ntiles = 0;
@@ -59,9 +60,20 @@ tvl_status fail_hip(hipError_t e, const char *what)
 constexpr int64_t kMaxDim = 2147483647LL; // M and tile counts fit in int32
 constexpr int64_t kMaxK = 1LL << 30;       // K plus one LDS slice still fits in int32
 
-int elem_size(int32_t dt) { return dt == TVL_F16 ? 2 : 4; }
+// Bytes per ldw unit: quantised rows are measured in bytes.
+int elem_size(int32_t dt) { return dt == TVL_F16 ? 2 : (dt == TVL_F32 ? 4 : 1); }
 
-bool dtype_ok(int32_t dt) { return dt == TVL_F32 || dt == TVL_F16; }
+bool dtype_ok(int32_t dt) { return dt >= TVL_F32 && dt <= TVL_Q4; }
+bool is_quant(int32_t dt) { return dt == TVL_Q8 || dt == TVL_Q4; }
+
+// Bytes of one quantised code row (128-byte aligned); the fp32 scales, one
+// per 64 columns, sit in a plane of their own after the M code rows.
+int64_t q_row_bytes(int64_t K, int32_t dt)
+{
+    const int bits = dt == TVL_Q4 ? 4 : 8;
+    return ((K * bits + 7) / 8 + 127) / 128 * 128;
+}
+int64_t q_scale_bytes(int64_t M, int64_t K) { return 4 * M * ((K + 63) / 64); }
 
 struct Range {
     uintptr_t b, e; // [b, e)
@@ -76,11 +88,16 @@ tvl_status check_one(const void *W, int64_t ldw, int32_t dt, const float *x, con
     if (M < 1 || K < 1 || M > kMaxDim || K > kMaxK)
         return fail(TVL_ERR_SHAPE, "%s: need 1 <= M <= 2^31-1 and 1 <= K <= 2^30 (M=%lld K=%lld)",
                     who, (long long)M, (long long)K);
-    if (ldw < K) return fail(TVL_ERR_SHAPE, "%s: ldw (%lld) < K (%lld)", who, (long long)ldw,
-                             (long long)K);
+    if (!is_quant(dt) && ldw < K)
+        return fail(TVL_ERR_SHAPE, "%s: ldw (%lld) < K (%lld)", who, (long long)ldw,
+                    (long long)K);
+    if (is_quant(dt) && ldw < q_row_bytes(K, dt))
+        return fail(TVL_ERR_SHAPE, "%s: a quantised row of K=%lld needs ldw >= %lld bytes", who,
+                    (long long)K, (long long)q_row_bytes(K, dt));
     const int s = elem_size(dt);
-    // the weight span must be addressable: ((M-1)*ldw + K) * s < 2^62
-    if (ldw > (int64_t(1) << 62) / s / M)
+    // the weight span (with a quantised matrix's scale plane) must be
+    // addressable: M * (ldw * s + scale bytes per row) < 2^62
+    if (ldw > (int64_t(1) << 62) / M / s - (is_quant(dt) ? 4 * ((K + 63) / 64) : 0))
         return fail(TVL_ERR_SHAPE, "%s: M * ldw overflows", who);
     if (reinterpret_cast<uintptr_t>(W) % tvl::kLineBytes != 0)
         return fail(TVL_ERR_ALIGN, "%s: W must be 128-byte aligned", who);
@@ -95,11 +112,13 @@ tvl_status check_one(const void *W, int64_t ldw, int32_t dt, const float *x, con
 }
 
 // A TVL matrix spans M whole rows of ldw elements: the kernels' 16-byte loads
-// may touch the padding of the last row (its values are never used).
-Range w_range(const void *W, int64_t ldw, int32_t dt, int64_t M)
+// may touch the padding of the last row (its values are never used).  A
+// quantised matrix also spans its scale plane.
+Range w_range(const void *W, int64_t ldw, int32_t dt, int64_t M, int64_t K)
 {
     const uintptr_t b = reinterpret_cast<uintptr_t>(W);
-    return {b, b + (uintptr_t)(M * ldw * elem_size(dt))};
+    const int64_t n = M * ldw * elem_size(dt) + (is_quant(dt) ? q_scale_bytes(M, K) : 0);
+    return {b, b + (uintptr_t)n};
 }
 Range f_range(const float *p, int64_t n)
 {
@@ -146,14 +165,14 @@ tvl_status check_alias(const tvl_item *items, int32_t n)
     };
     for (int32_t i = 0; i < n; ++i) {
         const tvl_item &t = items[i];
-        int32_t h = hits(w_range(t.W, t.ldw, t.dtype, t.M));
+        int32_t h = hits(w_range(t.W, t.ldw, t.dtype, t.M, t.K));
         if (h >= 0)
             return fail(TVL_ERR_ALIAS, "output of item %d overlaps W of item %d", (int)h, (int)i);
         h = hits(x_range(t));
         if (h >= 0)
             return fail(TVL_ERR_ALIAS, "output of item %d overlaps x of item %d", (int)h, (int)i);
         if (t.op == TVL_OP_SWIGLU) {
-            h = hits(w_range(t.W3, t.ldw, t.dtype, t.M));
+            h = hits(w_range(t.W3, t.ldw, t.dtype, t.M, t.K));
             if (h >= 0)
                 return fail(TVL_ERR_ALIAS, "output of item %d overlaps W3 of item %d", (int)h,
                             (int)i);
@@ -189,6 +208,9 @@ tvl_status check_fused(const tvl_item &t, const char *who)
     }
     if (t.op != TVL_OP_GEMV && t.op != TVL_OP_SWIGLU)
         return fail(TVL_ERR_ARG, "%s: unknown op %d", who, (int)t.op);
+    if (is_quant(t.dtype) && (t.op != TVL_OP_GEMV || t.g || t.nrhs > 1))
+        return fail(TVL_ERR_ARG, "%s: quantised weights only for plain one-vector GEMV items",
+                    who);
     if (t.op == TVL_OP_SWIGLU) {
         if (!t.W3) return fail(TVL_ERR_NULL, "%s: a SwiGLU item needs W3", who);
         if (reinterpret_cast<uintptr_t>(t.W3) % tvl::kLineBytes != 0)
@@ -216,14 +238,15 @@ tvl_status check_items(const tvl_item *items, int32_t n)
         const tvl_status st = check_fused(t, who);
         if (st != TVL_OK) return st;
     }
-    bool any_fused = false, any_multi = false;
+    bool any_fused = false, any_multi = false, any_quant = false;
     for (int32_t i = 0; i < n; ++i) {
         any_fused = any_fused || is_fused(items[i]);
         any_multi = any_multi || is_multi(items[i]);
+        any_quant = any_quant || is_quant(items[i].dtype);
     }
-    if (any_fused && any_multi)
-        return fail(TVL_ERR_ARG, "sweep: several-vector items cannot share a launch with RMSNorm "
-                                 "or SwiGLU items");
+    if ((any_fused ? 1 : 0) + (any_multi ? 1 : 0) + (any_quant ? 1 : 0) > 1)
+        return fail(TVL_ERR_ARG, "sweep: several-vector, RMSNorm/SwiGLU and quantised items "
+                                 "need separate launches");
     return check_alias(items, n);
 }
 
@@ -315,6 +338,9 @@ Shape default_fused_shape(double bytes_f16, double bytes_f32)
     return bytes_f16 > bytes_f32 ? Shape{4, 4, 2, tvl::kXDirect} : Shape{2, 4, 3, tvl::kXDirect};
 }
 
+// Default shape for plans or items with block-quantised weights.
+Shape default_quant_shape() { return Shape{4, 4, 1, tvl::kXDirect}; }
+
 Shape default_shape_items(const tvl_item *items, int32_t n)
 {
     double b16 = 0, b32 = 0, row32 = 0;
@@ -333,6 +359,10 @@ Shape default_shape_items(const tvl_item *items, int32_t n)
         fused = fused || is_fused(items[i]);
         nmax = std::max<int>(nmax, (int)nvec(items[i]));
     }
+    bool quant = false;
+    for (int32_t i = 0; i < n; ++i)
+        quant = quant || is_quant(items[i].dtype);
+    if (quant) return default_quant_shape();
     if (nmax > 1) return default_multi_shape(multi_B(nmax));
     if (fused) return default_fused_shape(b16, b32);
     return default_shape(b16, b32, b32 > 0 ? row32 / b32 : 0.0);
@@ -424,7 +454,7 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
 {
     bool special = false;
     for (int32_t i = 0; i < n; ++i)
-        special = special || is_fused(items[i]) || is_multi(items[i]);
+        special = special || is_fused(items[i]) || is_multi(items[i]) || is_quant(items[i].dtype);
     Shape shape;
     tvl_status st = pick_shape(tuning, default_shape_items(items, n), &shape, !special);
     if (st != TVL_OK) return st;
@@ -456,6 +486,13 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
                                      "vectors",
                         shape.R, shape.W, shape.U, p->multiB);
         }
+    }
+    for (int32_t i = 0; i < n; ++i)
+        p->quant = p->quant || is_quant(items[i].dtype);
+    if (p->quant && !tvl::quant_shape_supported(shape)) {
+        delete p;
+        return fail(TVL_ERR_ARG, "plan: no quantised-weight kernel for (%d, %d, %d)", shape.R,
+                    shape.W, shape.U);
     }
     if (p->fused && !tvl::fused_shape_supported(shape)) {
         delete p;
@@ -524,8 +561,10 @@ tvl_status plan_launch(const tvl_plan *p, hipStream_t st)
 {
     if (p->ntiles == 0) return TVL_OK;
     const hipError_t e =
-        p->multiB ? tvl::launch_sweep_multi(p->shape, p->multiB, p->d_items, p->d_tiles,
-                                            p->ntiles, p->grid, st)
+        p->quant    ? tvl::launch_sweep_quant(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid,
+                                              st)
+        : p->multiB ? tvl::launch_sweep_multi(p->shape, p->multiB, p->d_items, p->d_tiles,
+                                              p->ntiles, p->grid, st)
         : p->fused ? tvl::launch_sweep_fused(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid,
                                              st)
                    : tvl::launch_sweep(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid,
@@ -560,6 +599,7 @@ int32_t tvl_version(void) { return TVL_VERSION; }
 int64_t tvl_row_stride(int64_t K, int32_t dtype)
 {
     if (K < 1 || !dtype_ok(dtype)) return -1;
+    if (is_quant(dtype)) return K > kMaxK ? -1 : q_row_bytes(K, dtype);
     const int s = elem_size(dtype);
     if (K > (INT64_MAX - tvl::kLineBytes) / s) return -1;
     return (K * s + tvl::kLineBytes - 1) / tvl::kLineBytes * tvl::kLineBytes / s;
@@ -570,7 +610,8 @@ tvl_status tvl_pack_rows(void *dst, int64_t ldw, const void *src, int64_t M, int
 {
     g_err[0] = 0;
     if (!dst || !src) return fail(TVL_ERR_NULL, "tvl_pack_rows: dst and src must be non-NULL");
-    if (!dtype_ok(dtype)) return fail(TVL_ERR_DTYPE, "tvl_pack_rows: unknown dtype %d", (int)dtype);
+    if (!dtype_ok(dtype) || is_quant(dtype))
+        return fail(TVL_ERR_DTYPE, "tvl_pack_rows: dtype %d (fp32 and fp16 only)", (int)dtype);
     if (M < 1 || K < 1 || M > kMaxDim || K > kMaxK || ldw < K)
         return fail(TVL_ERR_SHAPE, "tvl_pack_rows: need 1 <= M <= 2^31-1, 1 <= K <= 2^30, "
                                    "ldw >= K");
@@ -580,8 +621,8 @@ tvl_status tvl_pack_rows(void *dst, int64_t ldw, const void *src, int64_t M, int
         return fail(TVL_ERR_ALIGN, "tvl_pack_rows: dst rows must start on 128-byte boundaries");
     if (reinterpret_cast<uintptr_t>(src) % s != 0)
         return fail(TVL_ERR_ALIGN, "tvl_pack_rows: src must be element aligned");
-    const Range d = w_range(dst, ldw, dtype, M);
-    const Range r = w_range(src, K, dtype, M);
+    const Range d = w_range(dst, ldw, dtype, M, K);
+    const Range r = w_range(src, K, dtype, M, K);
     if (overlap(d, r)) return fail(TVL_ERR_ALIAS, "tvl_pack_rows: dst overlaps src");
     const hipError_t e = tvl::launch_pack(dtype, dst, ldw, src, M, K, stream);
     if (e != hipSuccess) return fail_hip(e, "pack launch");
@@ -607,6 +648,25 @@ tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype, const float *x
     int S = 1;
     const bool user_shape =
         tuning && (tuning->rows_per_wave || tuning->waves_per_block || tuning->unroll);
+    if (is_quant(dtype)) {
+        if (tuning && tuning->ksplit > 1)
+            return fail(TVL_ERR_ARG, "tvl_gemv: quantised weights have no K split");
+        if (tuning && (tuning->flags & TVL_FLAG_X_LDS))
+            return fail(TVL_ERR_ARG, "tvl_gemv: quantised weights read x directly (direct-x)");
+        Shape qs;
+        st = pick_shape(tuning, default_quant_shape(), &qs, false);
+        if (st != TVL_OK) return st;
+        if (!tvl::quant_shape_supported(qs))
+            return fail(TVL_ERR_ARG, "tvl_gemv: no quantised-weight kernel for (%d, %d, %d)", qs.R,
+                        qs.W, qs.U);
+        int qdev = 0;
+        DevInfo qinfo;
+        st = current_device(&qdev, &qinfo);
+        if (st != TVL_OK) return st;
+        const hipError_t qe = tvl::launch_item_quant(qs, dev_item(it), stream);
+        if (qe != hipSuccess) return fail_hip(qe, "quantised gemv launch");
+        return TVL_OK;
+    }
     const Shape def = default_shape(dtype == TVL_F16 ? 1.0 : 0.0, dtype == TVL_F16 ? 0.0 : 1.0,
                                     (double)K * 4.0);
     shape = def;

@@ -85,6 +85,12 @@ hipError_t launch_sweep_fused(const Shape &s, const DevItem *items, const DevTil
 // One item (any op) as one launch: grid = its row tiles, item by value.
 hipError_t launch_item(const Shape &s, const DevItem &item, hipStream_t st);
 
+// Plans or items with block-quantised weights (any plain item, direct-x).
+bool quant_shape_supported(const Shape &s);
+hipError_t launch_sweep_quant(const Shape &s, const DevItem *items, const DevTile *tiles,
+                              int ntiles, int grid, hipStream_t st);
+hipError_t launch_item_quant(const Shape &s, const DevItem &item, hipStream_t st);
+
 // Several x vectors per item (B = 2, 4 or 8 >= every item's nrhs; direct-x).
 bool multi_shape_supported(const Shape &s, int B);
 hipError_t launch_sweep_multi(const Shape &s, int B, const DevItem *items, const DevTile *tiles,

@@ -29,6 +29,7 @@
 namespace tvl {
 namespace {
 
+typedef unsigned int u4 __attribute__((ext_vector_type(4)));
 typedef float f2 __attribute__((ext_vector_type(2)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef float f8 __attribute__((ext_vector_type(8)));
@@ -873,6 +874,193 @@ __global__ __launch_bounds__(WV *kWave) void k_item_multi(const DevItem it)
         tile_multi<float, R, WV, U, B>(it, row0);
 }
 
+// Block-quantised weights (8- or 4-bit codes in M rows of ldw bytes; fp32
+// scale per 64 columns in a row-major plane after the code rows).  A 16-byte load
+// brings N = 16 (8-bit) or 32 (4-bit) codes of one row; each code is
+// sign-extended and converted exactly to fp32, the codes are dotted with x
+// into a float4, and the row's accumulators take scale * that float4.  All
+// of a lane's N columns lie in one 64-column group, so one scale per load.
+// t += codes(w) . x over the N columns of one 16-byte weight vector
+template <int BITS>
+__device__ __forceinline__ void qdot(f4 &t, const u4 w, const f4 (&xv)[128 / BITS / 4])
+{
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        if constexpr (BITS == 8) {
+            const unsigned v = w[d];
+            const f4 q = {(float)((int)(v << 24) >> 24), (float)((int)(v << 16) >> 24),
+                          (float)((int)(v << 8) >> 24), (float)((int)v >> 24)};
+            fma4(t, q, xv[d]);
+        } else {
+            // nibble u -> code u - 8: flip the top bit of every nibble, then
+            // sign-extend the 4-bit field
+            const unsigned v = w[d] ^ 0x88888888u;
+            const f4 qa = {(float)((int)(v << 28) >> 28), (float)((int)(v << 24) >> 28),
+                           (float)((int)(v << 20) >> 28), (float)((int)(v << 16) >> 28)};
+            const f4 qb = {(float)((int)(v << 12) >> 28), (float)((int)(v << 8) >> 28),
+                           (float)((int)(v << 4) >> 28), (float)((int)v >> 28)};
+            fma4(t, qa, xv[2 * d]);
+            fma4(t, qb, xv[2 * d + 1]);
+        }
+    }
+}
+
+template <int BITS, int R, int U>
+struct QuantRows {
+    static constexpr int N = 128 / BITS; // columns per 16-byte load
+    static constexpr int NX = N / 4;     // float4 of x per load
+    static constexpr int CH = kWave * N; // columns per wavefront load
+    const unsigned char *rows[R];        // this lane's first code byte
+    const float *scl[R];                 // this lane's first scale
+    const float *xl;
+    int kn, nv, nfull;
+
+    // w0 / s0: code row and scale row of the wave's first row; ng scales per row
+    __device__ __forceinline__ QuantRows(const unsigned char *w0, int64_t ldw, const float *s0,
+                                         int ng, int nrows, const float *x, int K, int lane)
+        : xl(x + lane * N), kn(K), nv((K + N - 1) / N), nfull(K / CH)
+    {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int rr = r < nrows ? r : nrows - 1;
+            rows[r] = w0 + (int64_t)rr * ldw + lane * 16;
+            scl[r] = s0 + (int64_t)rr * ng + lane * N / 64;
+        }
+    }
+
+    __device__ __forceinline__ u4 wload(int r, int c) const
+    {
+        return __builtin_nontemporal_load((const TVL_GLOBAL u4 *)(rows[r] + (int64_t)c * CH * BITS / 8));
+    }
+    __device__ __forceinline__ float sload(int r, int c) const
+    {
+        return *(const TVL_GLOBAL float *)(scl[r] + c * (CH / 64));
+    }
+
+    __device__ __forceinline__ void run(f4 (&acc)[R], int lane) const
+    {
+        int c = 0;
+        for (; c + U <= nfull; c += U) {
+            u4 w[U][R];
+            float sc[U][R];
+            f4 xv[U][NX];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    w[u][r] = wload(r, c + u);
+                    sc[u][r] = sload(r, c + u);
+                }
+#pragma unroll
+                for (int k = 0; k < NX; ++k)
+                    xv[u][k] = load_x4(xl + (c + u) * CH + 4 * k);
+            }
+            __builtin_amdgcn_sched_barrier(0); // all loads of the batch first
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    f4 t = {0.f, 0.f, 0.f, 0.f};
+                    qdot<BITS>(t, w[u][r], xv[u]);
+                    fma4(acc[r], f4{sc[u][r], sc[u][r], sc[u][r], sc[u][r]}, t);
+                }
+        }
+        for (; c < nfull; ++c) {
+            f4 xv[NX];
+#pragma unroll
+            for (int k = 0; k < NX; ++k)
+                xv[k] = load_x4(xl + c * CH + 4 * k);
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const u4 w = wload(r, c);
+                const float sc = sload(r, c);
+                f4 t = {0.f, 0.f, 0.f, 0.f};
+                qdot<BITS>(t, w, xv);
+                fma4(acc[r], f4{sc, sc, sc, sc}, t);
+            }
+        }
+        if (c * kWave < nv) { // ragged last chunk: x past kn is zero (codes are finite)
+            const int v = c * kWave + lane;
+            if (v < nv) {
+                const int valid = kn - v * N;
+                f4 xv[NX];
+#pragma unroll
+                for (int k = 0; k < NX; ++k) {
+                    xv[k] = f4{0.f, 0.f, 0.f, 0.f};
+                    if (4 * k < valid)
+                        xv[k] = mask_from<f4, 4>(load_x4(xl + c * CH + 4 * k), valid - 4 * k);
+                }
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const u4 w = wload(r, c);
+                    const float sc = sload(r, c);
+                    f4 t = {0.f, 0.f, 0.f, 0.f};
+                    qdot<BITS>(t, w, xv);
+                    fma4(acc[r], f4{sc, sc, sc, sc}, t);
+                }
+            }
+        }
+    }
+};
+
+template <int BITS, int R, int WV, int U>
+__device__ __forceinline__ void tile_quant(const DevItem &it, int row0)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wrow0 = row0 + wave * R;
+    const int nrows = it.M - wrow0;
+    if (nrows <= 0) return;
+    f4 acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        acc[r] = f4{0.f, 0.f, 0.f, 0.f};
+    const unsigned char *codes = static_cast<const unsigned char *>(it.W);
+    const int ng = (it.K + 63) / 64;
+    const float *scales = reinterpret_cast<const float *>(codes + (int64_t)it.M * it.ldw);
+    const QuantRows<BITS, R, U> qr(codes + (int64_t)wrow0 * it.ldw, it.ldw,
+                                   scales + (int64_t)wrow0 * ng, ng, min(nrows, R), it.x, it.K,
+                                   lane);
+    qr.run(acc, lane);
+    const float v = reduce_rows<R>(acc, lane);
+    constexpr int G = kWave / R;
+    if ((lane % G) == 0) {
+        const int row = wrow0 + lane / G;
+        if (row < it.M) it.y[row] = v;
+    }
+}
+
+// Any plain item (fp32, fp16, 8-bit or 4-bit weights), direct-x.
+template <int R, int WV, int U>
+__device__ __forceinline__ void tile_plain_any(const DevItem &it, int row0)
+{
+    switch (it.dtype) {
+    case 3: tile_quant<4, R, WV, U>(it, row0); break;
+    case 2: tile_quant<8, R, WV, U>(it, row0); break;
+    case 1: tile_fused<_Float16, R, WV, U, false, false>(it, row0); break;
+    default: tile_fused<float, R, WV, U, false, false>(it, row0); break;
+    }
+}
+
+template <int R, int WV, int U>
+__global__ __launch_bounds__(WV *kWave) void k_sweep_quant(const DevItem *__restrict__ items,
+                                                            const DevTile *__restrict__ tiles,
+                                                            int ntiles)
+{
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const DevTile tl = tiles[t];
+        const DevItem it = items[tl.item];
+        tile_plain_any<R, WV, U>(it, tl.row0);
+        __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
+    }
+}
+
+template <int R, int WV, int U>
+__global__ __launch_bounds__(WV *kWave) void k_item_quant(const DevItem it)
+{
+    tile_plain_any<R, WV, U>(it, (int)blockIdx.x * (R * WV));
+}
+
 // Grouped sweep whose items may carry a fused RMSNorm and/or be SwiGLU
 // pairs: the same tile loop, with the item's kind chosen per tile.
 template <int R, int WV, int U>
@@ -1009,6 +1197,27 @@ struct InstMulti {
     {
         const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
         hipLaunchKernelGGL((k_item_multi<R, WV, U, B>), grid, block, 0, st, it);
+        return hipGetLastError();
+    }
+};
+
+// (R, waves per block, U) for plans holding block-quantised weights.
+#define TVL_QUANT_SHAPES(X)                                                                       \
+    X(2, 4, 2) X(2, 4, 4) X(4, 4, 1) X(4, 4, 2) X(4, 1, 2) X(8, 4, 1) X(1, 4, 4) X(2, 1, 4)
+
+template <int R, int WV, int U>
+struct InstQuant {
+    static hipError_t sweep(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
+                            hipStream_t st)
+    {
+        hipLaunchKernelGGL((k_sweep_quant<R, WV, U>), dim3(grid), dim3(WV * kWave), 0, st, items,
+                           tiles, ntiles);
+        return hipGetLastError();
+    }
+    static hipError_t item(const DevItem &it, hipStream_t st)
+    {
+        const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
+        hipLaunchKernelGGL((k_item_quant<R, WV, U>), grid, block, 0, st, it);
         return hipGetLastError();
     }
 };
@@ -1222,6 +1431,35 @@ hipError_t launch_item_multi(const Shape &s, int B, const DevItem &item, hipStre
     if (s.R == R_ && s.W == W_ && s.U == U_ && B == B_)                                          \
         return InstMulti<R_, W_, U_, B_>::item(item, st);
     TVL_MULTI_SHAPES(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+bool quant_shape_supported(const Shape &s)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return s.xmode == kXDirect;
+    TVL_QUANT_SHAPES(X)
+#undef X
+    return false;
+}
+
+hipError_t launch_sweep_quant(const Shape &s, const DevItem *items, const DevTile *tiles,
+                              int ntiles, int grid, hipStream_t st)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return InstQuant<R_, W_, U_>::sweep(items, tiles, ntiles, grid, st);
+    TVL_QUANT_SHAPES(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_item_quant(const Shape &s, const DevItem &item, hipStream_t st)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return InstQuant<R_, W_, U_>::item(item, st);
+    TVL_QUANT_SHAPES(X)
 #undef X
     return hipErrorInvalidValue;
 }

@@ -15,7 +15,7 @@ from dataclasses import dataclass
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtvl.so")
 
-TVL_F32, TVL_F16 = 0, 1
+TVL_F32, TVL_F16, TVL_Q8, TVL_Q4 = 0, 1, 2, 3
 TVL_FLAG_X_LDS = 1
 TVL_FLAG_X_DIRECT = 2
 STATUS = {0: "TVL_OK", -1: "TVL_ERR_NULL", -2: "TVL_ERR_SHAPE", -3: "TVL_ERR_ALIGN",
@@ -300,6 +300,32 @@ def upload_matrix(host, dtype: int, device="cuda", stream=None) -> TvlMatrix:
         tvl_pack_rows(buf, ldw, dense, M, K, dtype, stream)
         torch.cuda.current_stream().synchronize()
         del dense
+    if buf.data_ptr() % 128:
+        raise RuntimeError("device allocation is not 128-byte aligned")
+    return TvlMatrix(buf, M, K, ldw, dtype)
+
+
+def quant_matrix_bytes(M: int, K: int, dtype: int, ldw: int | None = None) -> int:
+    """Bytes of a block-quantised matrix: M code rows of ldw bytes, then the
+    fp32 scale plane (M x ceil(K/64))."""
+    ldw = tvl_row_stride(K, dtype) if ldw is None else ldw
+    return M * ldw + 4 * M * ((K + 63) // 64)
+
+
+def upload_quant(host, M: int, K: int, dtype: int, ldw: int | None = None,
+                 device="cuda") -> TvlMatrix:
+    """Copy an already-quantised matrix (one uint8 buffer: code plane, then
+    scale plane) to the GPU as is."""
+    import numpy as np
+    import torch
+    if dtype not in (TVL_Q8, TVL_Q4):
+        raise ValueError("upload_quant: dtype must be TVL_Q8 or TVL_Q4")
+    ldw = tvl_row_stride(K, dtype) if ldw is None else ldw
+    host = np.ascontiguousarray(host, dtype=np.uint8).reshape(-1)
+    if host.size != quant_matrix_bytes(M, K, dtype, ldw):
+        raise ValueError(f"upload_quant: {host.size} bytes, expected "
+                         f"{quant_matrix_bytes(M, K, dtype, ldw)}")
+    buf = torch.from_numpy(host).to(device)
     if buf.data_ptr() % 128:
         raise RuntimeError("device allocation is not 128-byte aligned")
     return TvlMatrix(buf, M, K, ldw, dtype)

@@ -114,16 +114,22 @@ def f32_to_f16_bits(a: np.ndarray) -> np.ndarray:
 
 
 def q_row_bytes(K: int, bits: int) -> int:
+    """Bytes of one code row: ceil(K * bits / 8) rounded up to 128."""
     return int(lib().synth_q_row_bytes(K, bits))
 
 
+def q_matrix_bytes(M: int, K: int, bits: int, ldw: int | None = None) -> int:
+    ldw = q_row_bytes(K, bits) if ldw is None else ldw
+    return M * ldw + 4 * M * ((K + 63) // 64)
+
+
 def quantize_rows(w: np.ndarray, bits: int, ldw: int | None = None, pad: int = 0) -> np.ndarray:
-    """fp32 [M, K] -> block-quantised rows [M, ldw] uint8 (codes, then fp32
-    scales per 64 columns); padding bytes = `pad`."""
+    """fp32 [M, K] -> one uint8 buffer: the code plane (M rows of ldw bytes)
+    then the fp32 scale plane (M x ceil(K/64)); code padding = `pad`."""
     w = np.ascontiguousarray(w, dtype=np.float32)
     M, K = w.shape
     ldw = q_row_bytes(K, bits) if ldw is None else ldw
-    out = np.full((M, ldw), pad, np.uint8)
+    out = np.full(q_matrix_bytes(M, K, bits, ldw), pad, np.uint8)
     lib().synth_quantize_rows(w.ctypes.data, M, K, bits, out.ctypes.data, ldw)
     return out
 

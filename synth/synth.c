@@ -153,36 +153,30 @@ void synth_int_f16(uint16_t *out, int64_t n, uint64_t key, uint64_t offset,
 }
 
 /* ------------------------------------------------------------------------ */
-/* Block quantisation of fp32 rows into the quantised row format (codes,    */
-/* then one fp32 scale per 64 columns; see the library header).  Symmetric: */
-/* 8-bit s = max|w| / 127, q = round(w / s) in [-127, 127]; 4-bit            */
-/* s = max|w| / 7, q = round(w / s) in [-7, 7] stored as nibble q + 8.       */
-/* An all-zero group gets s = 0 and q = 0.  Padding bytes are left as they  */
-/* are in `out` (the caller fills them).                                     */
+/* Block quantisation of an fp32 matrix into the quantised format (a code   */
+/* plane of M rows x ldw bytes, then an fp32 scale plane of M x ceil(K/64); */
+/* see the library header).  Symmetric: 8-bit s = max|w| / 127,             */
+/* q = round(w / s) in [-127, 127]; 4-bit s = max|w| / 7, q in [-7, 7]      */
+/* stored as nibble q + 8.  An all-zero group gets s = 0 and q = 0.         */
+/* Padding bytes of the code rows keep what the caller put in `out`.        */
 /* ------------------------------------------------------------------------ */
-static int64_t q_code_bytes(int64_t K, int bits)
+int64_t synth_q_row_bytes(int64_t K, int bits)
 {
     const int64_t b = (K * bits + 7) / 8;
     return (b + 127) / 128 * 128;
 }
 
-int64_t synth_q_row_bytes(int64_t K, int bits)
-{
-    const int64_t r = q_code_bytes(K, bits) + 4 * ((K + 63) / 64);
-    return (r + 127) / 128 * 128;
-}
-
 void synth_quantize_rows(const float *w, int64_t M, int64_t K, int bits, uint8_t *out,
                          int64_t ldw)
 {
-    const int64_t cb = q_code_bytes(K, bits);
     const int64_t ng = (K + 63) / 64;
     const int qmax = bits == 8 ? 127 : 7;
+    float *plane = (float *)(out + M * ldw);
 #pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < M; ++i) {
         const float *src = w + i * K;
         uint8_t *row = out + i * ldw;
-        float *scales = (float *)(row + cb);
+        float *scales = plane + i * ng;
         for (int64_t g = 0; g < ng; ++g) {
             const int64_t j0 = g * 64, j1 = (j0 + 64 < K) ? j0 + 64 : K;
             float amax = 0.f;

@@ -12,6 +12,8 @@ import re
 
 import pytest
 
+import synth
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "tvl.h")
 
@@ -99,6 +101,35 @@ def test_row_stride(K, dt, ldw):
     assert tvl.tvl_row_stride(K, dt) == ldw
 
 
+@pytest.mark.parametrize("K,dt,ldw", [(1, 2, 128), (128, 2, 128), (129, 2, 256), (768, 2, 768),
+                                      (100, 3, 128), (256, 3, 128), (257, 3, 256), (768, 3, 384),
+                                      (4096, 3, 2048), (11008, 2, 11008), (11008, 3, 5504)])
+def test_row_stride_quantised(K, dt, ldw):
+    # code bytes ceil(K * bits / 8) rounded up to 128; the scales live apart
+    assert tvl.tvl_row_stride(K, dt) == ldw
+    assert synth.q_row_bytes(K, 8 if dt == 2 else 4) == ldw
+
+
+def test_quantised_item_rejects():
+    base = dict(W=A, ldw=768, x=B, y=C, M=768, K=768, dtype=2)
+    for kw in (dict(g=D, eps=1e-5), dict(op=1, W3=D), dict(nrhs=2, ldx=768, ldy=768)):
+        it = tvl.item(**{**base, **kw})
+        assert L.tvl_gemv_item(ctypes.byref(it), None, None) == ARG
+    assert L.tvl_pack_rows(A, 896, B, 4, 768, 2, None) == DTYPE
+    # quantised and fused items may not share one launch
+    arr, n = tvl.make_items([base, dict(W=A + (1 << 30), ldw=768, x=B, y=C + (1 << 20), M=768,
+                                        K=768, dtype=0, g=D, eps=1e-5)])
+    assert L.tvl_gemv_batch_sweep(arr, n, None) == ARG
+
+
+def test_quantised_alias_covers_scale_plane():
+    # 768 x 768 8-bit: code plane 768*768 bytes, then 768*12 fp32 scales
+    end_codes = A + 768 * 768
+    for y in (end_codes, end_codes + 4 * 768 * 12 - 4):
+        it = tvl.item(W=A, ldw=768, x=B, y=y, M=768, K=768, dtype=2)
+        assert L.tvl_gemv_item(ctypes.byref(it), None, None) == ALIAS
+
+
 def test_row_stride_rejects():
     assert tvl.tvl_row_stride(0, 0) == -1
     assert tvl.tvl_row_stride(5, 7) == -1
@@ -112,7 +143,9 @@ def gemv(W=A, ldw=768, dt=0, x=B, y=C, M=768, K=768, tuning=None):
 
 @pytest.mark.parametrize("kw,st", [
     (dict(W=0), NULL), (dict(x=0), NULL), (dict(y=0), NULL),
-    (dict(dt=2), DTYPE), (dict(dt=-1), DTYPE),
+    (dict(dt=4), DTYPE), (dict(dt=-1), DTYPE),
+    (dict(dt=2, ldw=640), SHAPE), (dict(dt=3, ldw=256), SHAPE), (dict(dt=2, ldw=896, tuning=dict(ksplit=2)), ARG),
+    (dict(dt=3, ldw=512, tuning=dict(flags=1)), ARG),
     (dict(M=0), SHAPE), (dict(K=0), SHAPE), (dict(M=-5), SHAPE), (dict(M=1 << 31), SHAPE),
     (dict(K=(1 << 30) + 1, ldw=(1 << 30) + 32), SHAPE), (dict(ldw=767), SHAPE),
     (dict(W=A + 64), ALIGN), (dict(ldw=770), ALIGN), (dict(dt=1, ldw=800), ALIGN),

@@ -1,0 +1,178 @@
+"""GPU parity of block-quantised weights (8-bit and 4-bit codes, one fp32
+scale per 64 columns; Sec. 8.2 proposes 4-bit weights unpacked on the fly,
+Sec. 2.2 names 4/8-bit quantisation) against the CPU oracle, which decodes
+every weight exactly and sums in double.
+
+Parity norm: |y - ref| / sum_j |w_ij x_j| with the decoded weights, 1e-5
+(the kernel converts codes exactly and accumulates in fp32, as for fp32
+weights).  With integer x and power-of-two scales every partial sum is
+exact, so those cases must match bit for bit.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2601_03324_amd import tvl  # noqa: E402
+
+TOL = 1e-5
+DEV = "cuda"
+BITS = {tvl.TVL_Q8: 8, tvl.TVL_Q4: 4}
+QUANT_SHAPES = [(2, 4, 2), (2, 4, 4), (4, 4, 1), (4, 4, 2), (4, 1, 2), (8, 4, 1), (1, 4, 4),
+                (2, 1, 4)]
+RAGGED = [(1, 1), (3, 17), (17, 3), (64, 63), (65, 65), (257, 255), (1000, 1000), (33, 4095),
+          (130, 11008), (5, 28672), (2048, 768), (768, 2048), (9, 2049), (31, 1023)]
+
+
+def log(msg):
+    print(msg, flush=True, file=sys.stderr)
+
+
+def quant_case(seed, M, K, dt, extra=0, pad=0xCD):
+    """Seeded fp32 weights quantised by the generator, x ~ N(0, 1); code rows
+    of ldw = stride + extra bytes whose padding holds `pad`."""
+    rng = np.random.default_rng(seed)
+    w = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    x = rng.standard_normal(K).astype(np.float32)
+    ldw = tvl.tvl_row_stride(K, dt) + extra
+    Wq = synth.quantize_rows(w, BITS[dt], ldw=ldw, pad=pad)
+    return Wq, ldw, x
+
+
+def run_item(Wq, ldw, dt, x, M, K, tuning=None):
+    Wd = tvl.upload_quant(Wq, M, K, dt, ldw, DEV)
+    xd = torch.from_numpy(x).to(DEV)
+    y = torch.full((M,), float("nan"), dtype=torch.float32, device=DEV)
+    if tuning is None:
+        tvl.tvl_gemv(Wd.buf, ldw, dt, xd, y, M, K)
+    else:
+        tvl.tvl_gemv_ex(Wd.buf, ldw, dt, xd, y, M, K, tuning)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+def check(y, yref, S, what):
+    r = oracle.check(y, yref, S, TOL)
+    assert r["bad"] == 0, f"{what}: {r}"
+    return r["max_err"]
+
+
+@pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
+@pytest.mark.parametrize("M,K", RAGGED, ids=[f"{m}x{k}" for m, k in RAGGED])
+def test_quant_gemv(M, K, dt):
+    log(f"quant gemv {M}x{K} dtype={dt}")
+    Wq, ldw, x = quant_case(M * 7919 + K * 13 + dt, M, K, dt)
+    yref, S = oracle.gemv_q(Wq, BITS[dt], ldw, M, K, x)
+    check(run_item(Wq, ldw, dt, x, M, K), yref, S, f"{M}x{K} dt={dt}")
+
+
+@pytest.mark.parametrize("shape", QUANT_SHAPES, ids=[f"R{r}W{w}U{u}" for r, w, u in QUANT_SHAPES])
+@pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
+def test_quant_shapes(shape, dt):
+    r, w, u = shape
+    log(f"quant shape {shape} dtype={dt}")
+    for M, K in ((37, 5000), (130, 768), (7, 4097)):
+        Wq, ldw, x = quant_case(M + K + r * 100 + u, M, K, dt)
+        yref, S = oracle.gemv_q(Wq, BITS[dt], ldw, M, K, x)
+        t = dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
+        check(run_item(Wq, ldw, dt, x, M, K, t), yref, S, f"{shape} {M}x{K}")
+
+
+@pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
+def test_quant_wide_rows_and_junk_padding(dt):
+    """ldw beyond the minimum, padding full of junk codes: never read into y."""
+    for M, K, extra in ((65, 1000, 128), (3, 130, 1024), (100, 4095, 384)):
+        for pad in (0x00, 0x77, 0xFF):
+            Wq, ldw, x = quant_case(K + extra + pad, M, K, dt, extra, pad)
+            yref, S = oracle.gemv_q(Wq, BITS[dt], ldw, M, K, x)
+            check(run_item(Wq, ldw, dt, x, M, K), yref, S, f"{M}x{K}+{extra} pad={pad:#x}")
+
+
+@pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
+def test_quant_exact_on_integers(dt):
+    """Codes over the full range, power-of-two scales, integer x: the result
+    is exact, so it must equal the oracle bit for bit."""
+    bits = BITS[dt]
+    for M, K in ((77, 4096), (5, 3000), (300, 129)):
+        rng = np.random.default_rng(M * K + bits)
+        ldw = tvl.tvl_row_stride(K, dt)
+        ng = (K + 63) // 64
+        codes = rng.integers(0, 256 if bits == 8 else 16, (M, ldw * 8 // bits)).astype(np.uint8)
+        if bits == 8:
+            plane = codes
+        else:
+            plane = codes[:, 0::2] | (codes[:, 1::2] << 4)
+        scales = np.exp2(rng.integers(-2, 1, (M, ng))).astype(np.float32)
+        Wq = np.concatenate([plane.reshape(-1), scales.reshape(-1).view(np.uint8)])
+        x = rng.integers(-4, 5, K).astype(np.float32)
+        yref, _ = oracle.gemv_q(Wq, bits, ldw, M, K, x)
+        y = run_item(Wq, ldw, dt, x, M, K)
+        assert np.array_equal(y.astype(np.float64), yref), f"{M}x{K}"
+
+
+def test_quant_plan_mixed_with_float_items():
+    """One plan over 8-bit, 4-bit, fp32 and fp16 items, run twice."""
+    rng = np.random.default_rng(99)
+    cases, items, keep = [], [], []
+    for i, (M, K, dt) in enumerate([(768, 768, tvl.TVL_Q8), (2048, 768, tvl.TVL_Q4),
+                                    (768, 2048, tvl.TVL_Q4), (33, 4095, tvl.TVL_Q8),
+                                    (500, 300, tvl.TVL_F32), (257, 255, tvl.TVL_F16),
+                                    (1, 1, tvl.TVL_Q4)]):
+        x = rng.standard_normal(K).astype(np.float32)
+        if dt in BITS:
+            Wq, ldw, _ = quant_case(1000 + i, M, K, dt)
+            Wd = tvl.upload_quant(Wq, M, K, dt, ldw, DEV)
+            yref, S = oracle.gemv_q(Wq, BITS[dt], ldw, M, K, x)
+        else:
+            Wf = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+            if dt == tvl.TVL_F32:
+                Wd = tvl.upload_matrix(Wf, dt, DEV)
+                yref, S = oracle.gemv_f32(Wf, x)
+            else:
+                Wh = synth.f32_to_f16_bits(Wf)
+                Wd = tvl.upload_matrix(Wh, dt, DEV)
+                yref, S = oracle.gemv_f16(Wh, x)
+        xd = torch.from_numpy(x).to(DEV)
+        y = torch.full((M,), float("nan"), dtype=torch.float32, device=DEV)
+        keep.append((Wd, xd))
+        items.append((Wd.ptr, Wd.ldw, xd, y, M, K, dt))
+        cases.append((y, yref, S, f"item {i} {M}x{K} dt={dt}"))
+    plan = tvl.tvl_sweep_plan_create(items)
+    try:
+        for rep in range(2):
+            for y, *_ in cases:
+                y.fill_(float("nan"))
+            plan.run()
+            torch.cuda.synchronize()
+            for y, yref, S, what in cases:
+                check(y.cpu().numpy(), yref, S, f"rep {rep} {what}")
+    finally:
+        plan.destroy()
+    for y, *_ in cases:
+        y.fill_(float("nan"))
+    tvl.tvl_gemv_batch_sweep(items)
+    torch.cuda.synchronize()
+    for y, yref, S, what in cases:
+        check(y.cpu().numpy(), yref, S, f"batch sweep {what}")
+
+
+@pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
+def test_quant_7b_layer_shapes(dt):
+    """Full-size Llama-2-7B projections (4096 x 4096, 11008 x 4096,
+    4096 x 11008) and the 32000-row classifier, every row checked."""
+    for M, K in ((4096, 4096), (11008, 4096), (4096, 11008), (32000, 4096)):
+        log(f"quant 7B shape {M}x{K} dtype={dt}")
+        Wq, ldw, x = quant_case(M ^ K ^ dt, M, K, dt)
+        yref, S = oracle.gemv_q(Wq, BITS[dt], ldw, M, K, x)
+        check(run_item(Wq, ldw, dt, x, M, K), yref, S, f"{M}x{K}")

@@ -342,58 +342,61 @@ def pin_swiglu():
 
 
 # --------------------------------------------------- quantised-weight pins
-def _q_rows(codes: np.ndarray, scales: np.ndarray, bits: int) -> np.ndarray:
-    """Build quantised rows by hand (not with the generator's quantiser):
-    codes [M, K] in the signed range, scales [M, ceil(K/64)] fp32."""
+def _q_rows(codes: np.ndarray, scales: np.ndarray, bits: int, extra: int = 0):
+    """Build a quantised matrix by hand (not with the generator's quantiser):
+    codes [M, K] in the signed range, scales [M, ceil(K/64)] fp32.  Returns
+    (buffer, ldw); code rows padded to 128 bytes (+ extra) with junk."""
     M, K = codes.shape
-    cb = ((K * bits + 7) // 8 + 127) // 128 * 128
-    ldw = ((cb + 4 * ((K + 63) // 64)) + 127) // 128 * 128
-    out = np.full((M, ldw), 0xAB, np.uint8)  # junk padding
+    ldw = ((K * bits + 7) // 8 + 127) // 128 * 128 + extra
+    out = np.full(M * ldw + 4 * scales.size, 0xAB, np.uint8)
+    rows = out[:M * ldw].reshape(M, ldw)
     if bits == 8:
-        out[:, :K] = codes.astype(np.int8).view(np.uint8)
+        rows[:, :K] = codes.astype(np.int8).view(np.uint8)
     else:
         u = (codes + 8).astype(np.uint8)
         for j in range(K):
             if j % 2 == 0:
-                out[:, j // 2] = (out[:, j // 2] & 0xF0) | u[:, j]
+                rows[:, j // 2] = (rows[:, j // 2] & 0xF0) | u[:, j]
             else:
-                out[:, j // 2] = (out[:, j // 2] & 0x0F) | (u[:, j] << 4)
-    sc = np.ascontiguousarray(scales, np.float32).view(np.uint8)
-    out[:, cb:cb + sc.shape[1]] = sc
-    return out
+                rows[:, j // 2] = (rows[:, j // 2] & 0x0F) | (u[:, j] << 4)
+    out[M * ldw:] = np.ascontiguousarray(scales, np.float32).reshape(-1).view(np.uint8)
+    return out, ldw
 
 
 def pin_quant_golden():
     """Hand-worked 4-bit row: codes (1, -2, 7), scale 1/2, x = (2, 1, -1):
     w = (0.5, -1, 3.5), y = 1 - 1 - 3.5 = -3.5, S = 5.5."""
-    Wq = _q_rows(np.array([[1, -2, 7]]), np.array([[0.5]], np.float32), 4)
-    assert Wq[0, 0] == 0x69 and Wq[0, 1] & 0x0F == 0x0F
-    y, S = oracle.gemv_q(Wq, 4, np.array([2, 1, -1], np.float32), 3)
+    Wq, ldw = _q_rows(np.array([[1, -2, 7]]), np.array([[0.5]], np.float32), 4)
+    assert Wq[0] == 0x69 and Wq[1] & 0x0F == 0x0F and ldw == 128
+    y, S = oracle.gemv_q(Wq, 4, ldw, 1, 3, np.array([2, 1, -1], np.float32))
     assert y[0] == -3.5 and S[0] == 5.5
-    # 8-bit: codes (-128, 127, 3), scale 2^-3
-    Wq = _q_rows(np.array([[-128, 127, 3]]), np.array([[0.125]], np.float32), 8)
-    y, S = oracle.gemv_q(Wq, 8, np.array([1, 1, -4], np.float32), 3)
+    # 8-bit, two rows: codes (-128, 127, 3) with scale 2^-3, (1, 1, 1) with scale 2
+    Wq, ldw = _q_rows(np.array([[-128, 127, 3], [1, 1, 1]]),
+                      np.array([[0.125], [2.0]], np.float32), 8)
+    y, S = oracle.gemv_q(Wq, 8, ldw, 2, 3, np.array([1, 1, -4], np.float32))
     assert y[0] == (-128 + 127 - 12) * 0.125 and S[0] == (128 + 127 + 12) * 0.125
+    assert y[1] == 2.0 * (1 + 1 - 4) and S[1] == 2.0 * 6
 
 
 def pin_quant_matches_dequantized():
     """Power-of-two scales make every dequantised weight exact in fp32: the
     quantised oracle must then equal the fp32 oracle on numpy's dequantised
-    matrix bit for bit, across group boundaries and ragged K."""
+    matrix bit for bit, across group boundaries, ragged K and wide rows."""
     rng = np.random.default_rng(23)
     for bits, lo, hi in ((8, -128, 127), (4, -8, 7)):
-        for M, K in ((5, 1), (7, 63), (3, 64), (9, 130), (4, 1000)):
+        for M, K, extra in ((5, 1, 0), (7, 63, 128), (3, 64, 0), (9, 130, 0), (4, 1000, 256)):
             codes = rng.integers(lo, hi + 1, (M, K))
             scales = np.exp2(rng.integers(-12, 3, (M, (K + 63) // 64))).astype(np.float32)
-            Wq = _q_rows(codes, scales, bits)
+            Wq, ldw = _q_rows(codes, scales, bits, extra)
             deq = (codes * np.repeat(scales, 64, axis=1)[:, :K]).astype(np.float32)
             x = rng.standard_normal(K).astype(np.float32)
-            yq, Sq = oracle.gemv_q(Wq, bits, x, K)
+            yq, Sq = oracle.gemv_q(Wq, bits, ldw, M, K, x)
             yf, Sf = oracle.gemv_f32(deq, x)
             assert np.array_equal(yq, yf) and np.array_equal(Sq, Sf), (bits, M, K)
-            # one weight at a time, at the group edges
-            for j in {0, min(63, K - 1), min(64, K - 1), K - 1}:
-                assert oracle.q_weight(Wq, bits, K, M - 1, j) == float(deq[M - 1, j])
+            # single weights at the group edges of every row
+            for i in range(M):
+                for j in {0, min(63, K - 1), min(64, K - 1), K - 1}:
+                    assert oracle.q_weight(Wq, bits, ldw, M, K, i, j) == float(deq[i, j])
 
 
 PINS = [pin_golden, pin_products_exact, pin_brute_force_exact, pin_brute_force_exact_f16,
@@ -442,11 +445,15 @@ MUTANTS = {
     "swiglu_sign": ("a[i] / (1.0 + exp(-a[i])) * b[i]", "a[i] / (1.0 + exp(a[i])) * b[i]"),
     "swiglu_sigmoid_only": ("a[i] / (1.0 + exp(-a[i])) * b[i]", "1.0 / (1.0 + exp(-a[i])) * b[i]"),
     "swiglu_no_b": ("a[i] / (1.0 + exp(-a[i])) * b[i]", "a[i] / (1.0 + exp(-a[i]))"),
-    "q_group_32": ("const double s = (double)scales[j / 64];", "const double s = (double)scales[j / 32];"),
+    "q_group_32": ("const double s = (double)scales[i * ng + j / 64];",
+                   "const double s = (double)scales[i * ng + j / 32];"),
+    "q_scale_row_stride": ("const double s = (double)scales[i * ng + j / 64];",
+                           "const double s = (double)scales[j / 64];"),
     "q4_nibble_order": ("(j % 2 == 0) ? (byte & 0x0f) : (byte >> 4)", "(j % 2 == 0) ? (byte >> 4) : (byte & 0x0f)"),
     "q4_offset": ("q = (double)(u - 8);", "q = (double)(u - 7);"),
     "q8_unsigned": ("q = (double)(int8_t)row[j];", "q = (double)row[j];"),
-    "q_scales_unaligned": ("return (b + 127) / 128 * 128;", "return b;"),
+    "q_code_row_stride": ("const uint8_t *row = W + i * ldw;\n    double q;",
+                          "const uint8_t *row = W + i * K * bits / 8;\n    double q;"),
 }
 
 

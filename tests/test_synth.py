@@ -121,22 +121,23 @@ def test_workload_tables():
 
 
 def test_quantize_rows_format_and_error():
-    """The generator's block quantiser writes the row format the oracle
-    decodes: codes within range, scale = max|w| / qmax per 64 columns, every
-    weight within half a step of the fp32 value."""
+    """The generator's block quantiser writes the format the oracle decodes:
+    scale = max|w| / qmax per 64 columns, every weight within half a step of
+    its fp32 value, zero groups exactly zero."""
     import oracle
     rng = np.random.default_rng(5)
     for bits, qmax in ((8, 127), (4, 7)):
         for M, K in ((3, 1), (4, 63), (5, 130), (2, 1000)):
             w = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
             w[0, :min(K, 64)] = 0.0  # an all-zero group
+            ldw = synth.q_row_bytes(K, bits)
             Wq = synth.quantize_rows(w, bits, pad=0xCD)
-            assert Wq.shape == (M, synth.q_row_bytes(K, bits))
+            assert Wq.size == synth.q_matrix_bytes(M, K, bits)
             for i in range(M):
                 for j in range(K):
                     g = j // 64
                     s = float(np.abs(w[i, g * 64:min(K, g * 64 + 64)]).max()) / qmax
-                    d = oracle.q_weight(Wq, bits, K, i, j)
+                    d = oracle.q_weight(Wq, bits, ldw, M, K, i, j)
                     assert abs(d - float(w[i, j])) <= 0.5 * s * (1 + 1e-6) + 1e-12
                     if s == 0.0:
                         assert d == 0.0
