@@ -8,16 +8,20 @@ every weight matrix of a Llama-2 110M decode step (12 layers x wq, wk, wv, wo
 grouped sweep kernel (a plan run).  The weights, the 85 x vectors and the 85
 y buffers are resident in HBM before timing starts.
 
-Two copies of the weights (877 MB together) are alternated step by step, so
-the 256 MB last-level cache cannot hand one sweep's weights to the next: the
-figure is HBM streaming.  ``--warm`` times a single copy instead.
+Copies of the weights are rotated step by step (three for this workload,
+1.3 GB together; as many as it takes to span 1 GB for smaller weight sets),
+so the 256 MB last-level cache cannot hand one sweep's weights to the next:
+the figure is HBM streaming.  ``--warm`` times a single copy instead.
 
 ``--workload`` measures the other workloads the same way (not the headline):
 sweep7b (Llama-2 7B token, fp32), stack70b8 (8 layers of a 70B-shaped stack,
 fp16 weights), cls32000 (the 110M classifier alone, 100 fresh x, 6 weight
 copies rotated), gemv768 (one 768x768 fp32 GEMV, cache-resident), and the
 decode tokens with RMSNorm and SwiGLU fused into the GEMVs: fused110m (fp32,
-2 weight copies alternated) and fused70b8 (fp16 weights).
+2 weight copies alternated) and fused70b8 (fp16 weights); the 110M and 7B
+tokens with block-quantised 8-bit / 4-bit weights (sweep110m_q8, sweep110m_q4,
+sweep7b_q8, sweep7b_q4; small weight sets are rotated over enough copies to
+span 1 GB); and beam4_110m / beam8_110m (several x vectors per weight read).
 
 Prints ONE JSON line with the metric, a roofline object for the dominant
 kernel and the CPU oracle's throughput on a bounded sample of the workload.
@@ -59,7 +63,40 @@ DESCRIBE = {
     "beam8_110m": "beam8_110m: one decode token of Llama-2 110M for 8 beam hypotheses: 85 fp32 "
                   "GEMVs x 8 x vectors, weights read once, one launch",
 }
+for _nm, _tok, _n in (("110m", "Llama-2 110M", 85), ("7b", "Llama-2 7B", 225)):
+    for _b in (8, 4):
+        DESCRIBE[f"sweep{_nm}_q{_b}"] = (
+            f"sweep{_nm}_q{_b}: one decode token of {_tok}, {_n} GEMVs with {_b}-bit "
+            f"block-quantised weights (one fp32 scale per 64 columns), one launch")
 BEAMS = {"beam4_110m": 4, "beam8_110m": 8}
+
+
+def oracle_rows(oracle, synth, m, rows, x):
+    """Oracle (y, S) of the sampled rows of matrix ``m``, each row regenerated
+    on its own from the counter-based generator."""
+    import numpy as np
+    if m.quantised:
+        ys, Ss = [], []
+        for r in rows:
+            y, S = oracle.gemv_q(m.weights(int(r), 1), m.bits, synth.q_row_bytes(m.K, m.bits),
+                                 1, m.K, x)
+            ys.append(y[0])
+            Ss.append(S[0])
+        return np.array(ys), np.array(Ss)
+    Wr = np.stack([m.weights(int(r), 1)[0] for r in rows])
+    return (oracle.gemv_f32 if m.dtype == "f32" else oracle.gemv_f16)(Wr, x)
+
+
+def oracle_gemv(oracle, synth, m, W, x):
+    if m.quantised:
+        return oracle.gemv_q(W, m.bits, synth.q_row_bytes(m.K, m.bits), m.M, m.K, x)
+    return (oracle.gemv_f32 if m.dtype == "f32" else oracle.gemv_f16)(W, x)
+
+
+def dtype_label(m) -> str:
+    if m.quantised:
+        return f"{m.dtype} weights (fp32 scale per 64 columns), f32 x/accumulation"
+    return "f16 weights, f32 x/accumulation" if m.dtype == "f16" else "f32"
 
 
 def log(msg: str) -> None:
@@ -87,14 +124,12 @@ def cpu_baseline(samples, seconds: float, what: str) -> dict:
     """The oracle as it stands (single-threaded naive double GEMV), cycling over
     (spec, W, x) samples of the workload for about ``seconds`` of CPU time."""
     import oracle
+    import synth
     t0 = time.perf_counter()
     nbytes, ngemv = 0, 0
     while True:
         for m, W, x in samples:
-            if m.dtype == "f32":
-                oracle.gemv_f32(W, x)
-            else:
-                oracle.gemv_f16(W, x)
+            oracle_gemv(oracle, synth, m, W, x)
             nbytes += m.algo_bytes()
             ngemv += 1
         el = time.perf_counter() - t0
@@ -164,8 +199,7 @@ def main() -> int:
     gemvs = []
     for i, m in enumerate(wl.mats):
         W = m.weights()
-        dt = sdev.dtype_code(m)
-        Wd = tvl.upload_matrix(W, dt, "cuda")
+        Wd = sdev.upload(m, W, "cuda")
         x = m.x()
         gemvs.append(sdev.DevGemv(m, Wd, torch.from_numpy(x).cuda(),
                                   torch.empty(m.M, dtype=torch.float32, device="cuda")))
@@ -193,7 +227,8 @@ def main() -> int:
         copies_used = ncopy
         plan_info = {}
     else:
-        ncopy = 1 if (args.warm or big) else 2
+        # enough copies that the rotation spans >= 1 GB (4x the last-level cache)
+        ncopy = 1 if (args.warm or big) else max(2, -(-1_000_000_000 // wl.weight_bytes()))
         copies = [gemvs] + [sdev.clone_weights(gemvs) for _ in range(ncopy - 1)]
         plans = [tvl.tvl_sweep_plan_create([g.item() for g in c], tuning if use_tuning else None)
                  for c in copies]
@@ -267,10 +302,8 @@ def main() -> int:
         g = next(gg for gg in gemvs if gg.spec is m)
         ydev = (y if single else g.y).cpu().numpy()
         rows = sdev.sample_rows(m.M, 64, 7)
-        Wr = np.stack([m.weights(int(r), 1)[0] for r in rows]) if W is None else W[rows]
-        xr = m.x(0)
-        yref, S = (oracle.gemv_f32 if m.dtype == "f32" else oracle.gemv_f16)(Wr, xr)
-        r = oracle.check(ydev[rows], yref, S, 1e-5 if m.dtype == "f32" else 2e-3)
+        yref, S = oracle_rows(oracle, synth, m, rows, m.x(0))
+        r = oracle.check(ydev[rows], yref, S, 2e-3 if m.dtype == "f16" else 1e-5)
         worst = max(worst, r["max_err"])
         if r["bad"]:
             log(f"PARITY FAILURE in {m.name}: {r}")
@@ -278,7 +311,7 @@ def main() -> int:
 
     us = ms * 1e3
     gbs = algo / (ms * 1e-3) / 1e9
-    dtype = "f16 weights, f32 x/accumulation" if wl.mats[0].dtype == "f16" else "f32"
+    dtype = dtype_label(wl.mats[0])
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),

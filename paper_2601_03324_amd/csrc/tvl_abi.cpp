@@ -263,11 +263,20 @@ Shape default_multi_shape(int B)
     return B == 2 ? Shape{4, 4, 2, tvl::kXDirect} : Shape{4, 4, 1, tvl::kXDirect};
 }
 
+int quant_bits(int32_t dt) { return dt == TVL_Q4 ? 4 : 8; }
+
+// Lanes per row of an item (block-quantised weights may share a wavefront
+// between several short rows; every other item uses all 64 lanes).
+int item_lanes(const tvl_item &t)
+{
+    return is_quant(t.dtype) ? tvl::quant_lanes(t.K, quant_bits(t.dtype)) : 64;
+}
+
 tvl::DevItem dev_item(const tvl_item &t)
 {
     return tvl::DevItem{t.W,    t.ldw, t.x,   t.y,        (int32_t)t.M, (int32_t)t.K,
                         t.dtype, t.op, t.W3, t.g,        t.eps,        (int32_t)nvec(t),
-                        t.ldx,  t.ldy};
+                        t.ldx,  t.ldy, item_lanes(t), 0};
 }
 
 tvl_status check_tuning(const tvl_tuning *t, bool allow_ksplit)
@@ -339,7 +348,12 @@ Shape default_fused_shape(double bytes_f16, double bytes_f32)
 }
 
 // Default shape for plans or items with block-quantised weights.
-Shape default_quant_shape() { return Shape{4, 4, 1, tvl::kXDirect}; }
+// (from sweeps of the 110M and 7B tokens on MI355X: 8 rows per wavefront
+// suit 4-bit rows, which carry half the bytes per column; 4 suit 8-bit)
+Shape default_quant_shape(bool all_q4)
+{
+    return all_q4 ? Shape{8, 4, 1, tvl::kXDirect} : Shape{4, 4, 1, tvl::kXDirect};
+}
 
 Shape default_shape_items(const tvl_item *items, int32_t n)
 {
@@ -359,10 +373,12 @@ Shape default_shape_items(const tvl_item *items, int32_t n)
         fused = fused || is_fused(items[i]);
         nmax = std::max<int>(nmax, (int)nvec(items[i]));
     }
-    bool quant = false;
-    for (int32_t i = 0; i < n; ++i)
+    bool quant = false, all_q4 = true;
+    for (int32_t i = 0; i < n; ++i) {
         quant = quant || is_quant(items[i].dtype);
-    if (quant) return default_quant_shape();
+        all_q4 = all_q4 && items[i].dtype == TVL_Q4;
+    }
+    if (quant) return default_quant_shape(all_q4);
     if (nmax > 1) return default_multi_shape(multi_B(nmax));
     if (fused) return default_fused_shape(b16, b32);
     return default_shape(b16, b32, b32 > 0 ? row32 / b32 : 0.0);
@@ -501,9 +517,10 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
                     shape.R, shape.W, shape.U, shape.xmode == tvl::kXLds ? "LDS-x" : "direct-x");
     }
     // output rows per tile: a SwiGLU tile streams R rows of W and of W3 per
-    // wavefront, i.e. R/2 output rows
+    // wavefront, i.e. R/2 output rows; a quantised item whose rows share a
+    // wavefront in groups of G lanes covers 64 / G times R rows per wavefront
     auto rows_of = [&](const tvl_item &t) {
-        return (t.op == TVL_OP_SWIGLU ? shape.R / 2 : shape.R) * shape.W;
+        return (t.op == TVL_OP_SWIGLU ? shape.R / 2 : shape.R) * shape.W * (64 / item_lanes(t));
     };
     // bytes per tile, largest first, so the longest tiles start first
     std::vector<int32_t> ord(n);
@@ -654,7 +671,7 @@ tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype, const float *x
         if (tuning && (tuning->flags & TVL_FLAG_X_LDS))
             return fail(TVL_ERR_ARG, "tvl_gemv: quantised weights read x directly (direct-x)");
         Shape qs;
-        st = pick_shape(tuning, default_quant_shape(), &qs, false);
+        st = pick_shape(tuning, default_quant_shape(dtype == TVL_Q4), &qs, false);
         if (st != TVL_OK) return st;
         if (!tvl::quant_shape_supported(qs))
             return fail(TVL_ERR_ARG, "tvl_gemv: no quantised-weight kernel for (%d, %d, %d)", qs.R,

@@ -16,10 +16,12 @@ constexpr int kSliceCap = 8192;    // x elements staged per pass: 32 KB of LDS
 constexpr int kOpGemv = 0;
 constexpr int kOpSwiglu = 1;
 
-// One GEMV as the kernels read it (88 bytes).  M and K fit in int32 (the
+// One GEMV as the kernels read it (96 bytes).  M and K fit in int32 (the
 // ABI rejects larger), ldw stays 64-bit.  W3 is the second matrix of a
 // SwiGLU item; g (or NULL) the RMSNorm weight applied to x first; nrhs x
 // vectors at a stride of ldx floats give nrhs outputs at a stride of ldy.
+// lanes: for block-quantised weights, the lanes of a wavefront that share
+// one row (8, 16, 32 or 64; see quant_lanes); unused otherwise.
 struct DevItem {
     const void *W;
     int64_t ldw;
@@ -35,8 +37,31 @@ struct DevItem {
     int32_t nrhs;
     int64_t ldx;
     int64_t ldy;
+    int32_t lanes;
+    int32_t reserved;
 };
-static_assert(sizeof(DevItem) == 88, "DevItem layout");
+static_assert(sizeof(DevItem) == 96, "DevItem layout");
+
+// Lanes per row for a block-quantised row of K columns at `bits` per code.
+// A lane loads 16 bytes (128 / bits columns) at a time, so a row is
+// nv = ceil(K * bits / 128) loads.  Short rows would leave most of a
+// 64-lane wavefront idle (a 4-bit row of 768 columns is 24 loads), so a
+// wavefront splits into 64 / G groups of G lanes, one row per group: G is
+// the group size in {64, 32, 16, 8} that pads nv the least (ties: larger G).
+inline int quant_lanes(int64_t K, int bits)
+{
+    const int64_t nv = (K * bits + 127) / 128;
+    int best = 64;
+    int64_t best_pad = (nv + 63) / 64 * 64;
+    for (int g = 32; g >= 8; g /= 2) {
+        const int64_t pad = (nv + g - 1) / g * g;
+        if (pad < best_pad) {
+            best = g;
+            best_pad = pad;
+        }
+    }
+    return best;
+}
 
 // One row tile of a sweep: item index and first row.
 struct DevTile {

@@ -875,56 +875,89 @@ __global__ __launch_bounds__(WV *kWave) void k_item_multi(const DevItem it)
 }
 
 // Block-quantised weights (8- or 4-bit codes in M rows of ldw bytes; fp32
-// scale per 64 columns in a row-major plane after the code rows).  A 16-byte load
-// brings N = 16 (8-bit) or 32 (4-bit) codes of one row; each code is
-// sign-extended and converted exactly to fp32, the codes are dotted with x
-// into a float4, and the row's accumulators take scale * that float4.  All
-// of a lane's N columns lie in one 64-column group, so one scale per load.
-// t += codes(w) . x over the N columns of one 16-byte weight vector
-template <int BITS>
-__device__ __forceinline__ void qdot(f4 &t, const u4 w, const f4 (&xv)[128 / BITS / 4])
+// scale per 64 columns in a row-major plane after the code rows).  A 16-byte
+// load brings N = 16 (8-bit) or 32 (4-bit) codes of one row, all in one
+// 64-column scale group, so each load is dotted with x first and scaled once.
+//
+// Decoding costs VALU work per code, and a 4-bit row streams two codes per
+// byte, so the decode is kept to about two VALU operations per code:
+//   8-bit: each byte converts with one sign-extending SDWA conversion, then
+//          one FMA;
+//   4-bit: masking a dword with 0x000F000F (0x00F000F0) leaves two nibbles
+//          (two nibbles times 16) in the mantissas of the two binary16
+//          halves, i.e. the exact values u * 2^-24 (16u * 2^-24) as fp16
+//          subnormals; v_fma_mix_f32 multiplies such a half with fp32 x and
+//          accumulates in fp32, so a code costs one FMA plus a shared mask.
+//          The codes are unsigned u = q + 8, so the load adds
+//          s * (sum_j u_j x_j - 8 sum_j x_j), with sum_j x_j formed once per
+//          load of x and shared by the R rows of the lane.
+// Products of the 4-bit path are formed at 2^-24 scale: x entries below about
+// 2^-100 in magnitude fall into fp32 subnormals there and lose precision.
+//
+// Short rows: a wavefront splits into 64 / G groups of G lanes, one row per
+// group (G from quant_lanes), so a 384-byte row still fills its lanes.
+typedef _Float16 h2v __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ h2v as_h2(unsigned v) { return __builtin_bit_cast(h2v, v); }
+
+// 8-bit: t += q . x over the 16 columns of one 16-byte weight vector
+__device__ __forceinline__ float qdot8(const u4 w, const f4 (&xv)[4])
 {
+    float ta = 0.f, tb = 0.f;
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
-        if constexpr (BITS == 8) {
-            const unsigned v = w[d];
-            const f4 q = {(float)((int)(v << 24) >> 24), (float)((int)(v << 16) >> 24),
-                          (float)((int)(v << 8) >> 24), (float)((int)v >> 24)};
-            fma4(t, q, xv[d]);
-        } else {
-            // nibble u -> code u - 8: flip the top bit of every nibble, then
-            // sign-extend the 4-bit field
-            const unsigned v = w[d] ^ 0x88888888u;
-            const f4 qa = {(float)((int)(v << 28) >> 28), (float)((int)(v << 24) >> 28),
-                           (float)((int)(v << 20) >> 28), (float)((int)(v << 16) >> 28)};
-            const f4 qb = {(float)((int)(v << 12) >> 28), (float)((int)(v << 8) >> 28),
-                           (float)((int)(v << 4) >> 28), (float)((int)v >> 28)};
-            fma4(t, qa, xv[2 * d]);
-            fma4(t, qb, xv[2 * d + 1]);
-        }
+        const unsigned v = w[d];
+        ta = fmaf((float)(int)(signed char)(v & 0xffu), xv[d].x, ta);
+        tb = fmaf((float)(int)(signed char)((v >> 8) & 0xffu), xv[d].y, tb);
+        ta = fmaf((float)(int)(signed char)((v >> 16) & 0xffu), xv[d].z, ta);
+        tb = fmaf((float)(int)(signed char)(v >> 24), xv[d].w, tb);
     }
+    return ta + tb;
 }
 
-template <int BITS, int R, int U>
+// 4-bit: 2^-24 * sum_j u_j x_j over the 32 columns of one 16-byte vector
+__device__ __forceinline__ float qdot4(const u4 w, const f4 (&xv)[8])
+{
+    float ta = 0.f, tb = 0.f; // nibbles 0, 2, 4, 6 of a dword; 16 x nibbles 1, 3, 5, 7
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        const unsigned v = w[d], v8 = v >> 8;
+        const h2v a = as_h2(v & 0x000F000Fu), b = as_h2(v & 0x00F000F0u);
+        const h2v c = as_h2(v8 & 0x000F000Fu), e = as_h2(v8 & 0x00F000F0u);
+        const f4 x0 = xv[2 * d], x1 = xv[2 * d + 1];
+        ta = fmaf((float)a.x, x0.x, ta);
+        tb = fmaf((float)b.x, x0.y, tb);
+        ta = fmaf((float)c.x, x0.z, ta);
+        tb = fmaf((float)e.x, x0.w, tb);
+        ta = fmaf((float)a.y, x1.x, ta);
+        tb = fmaf((float)b.y, x1.y, tb);
+        ta = fmaf((float)c.y, x1.z, ta);
+        tb = fmaf((float)e.y, x1.w, tb);
+    }
+    return fmaf(tb, 0.0625f, ta);
+}
+
+template <int BITS, int G, int R, int U>
 struct QuantRows {
     static constexpr int N = 128 / BITS; // columns per 16-byte load
     static constexpr int NX = N / 4;     // float4 of x per load
-    static constexpr int CH = kWave * N; // columns per wavefront load
-    const unsigned char *rows[R];        // this lane's first code byte
-    const float *scl[R];                 // this lane's first scale
+    static constexpr int CH = G * N;     // columns per row per wavefront load
+    static_assert(CH % 64 == 0, "a chunk spans whole scale groups");
+    const unsigned char *rows[R]; // this lane's first code byte of each row
+    const float *scl[R];          // this lane's first scale of each row
     const float *xl;
-    int kn, nv, nfull;
+    int kn, nv, nfull, seg;
 
-    // w0 / s0: code row and scale row of the wave's first row; ng scales per row
-    __device__ __forceinline__ QuantRows(const unsigned char *w0, int64_t ldw, const float *s0,
-                                         int ng, int nrows, const float *x, int K, int lane)
-        : xl(x + lane * N), kn(K), nv((K + N - 1) / N), nfull(K / CH)
+    // rowp[r]: code row and scale row of the lane's r-th row
+    __device__ __forceinline__ QuantRows(const unsigned char *const (&rowp)[R],
+                                         const float *const (&sclp)[R], const float *x, int K,
+                                         int seg_)
+        : xl(x + seg_ * N), kn(K), nv((K + N - 1) / N), nfull(K / CH), seg(seg_)
     {
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-            const int rr = r < nrows ? r : nrows - 1;
-            rows[r] = w0 + (int64_t)rr * ldw + lane * 16;
-            scl[r] = s0 + (int64_t)rr * ng + lane * N / 64;
+            rows[r] = rowp[r] + seg_ * 16;
+            scl[r] = sclp[r] + seg_ * N / 64;
         }
     }
 
@@ -937,7 +970,30 @@ struct QuantRows {
         return *(const TVL_GLOBAL float *)(scl[r] + c * (CH / 64));
     }
 
-    __device__ __forceinline__ void run(f4 (&acc)[R], int lane) const
+    // -8 * sum of the lane's N x values (the 4-bit code offset), 0 for 8-bit
+    __device__ __forceinline__ float offset_term(const f4 (&xv)[NX]) const
+    {
+        if constexpr (BITS == 4) {
+            f4 s = xv[0];
+#pragma unroll
+            for (int k = 1; k < NX; ++k)
+                s += xv[k];
+            return -8.f * ((s.x + s.y) + (s.z + s.w));
+        } else {
+            return 0.f;
+        }
+    }
+
+    __device__ __forceinline__ void accumulate(float &acc, const u4 w, float sc, const f4 (&xv)[NX],
+                                               float off) const
+    {
+        if constexpr (BITS == 4)
+            acc = fmaf(sc, fmaf(qdot4(w, xv), 16777216.f, off), acc);
+        else
+            acc = fmaf(sc, qdot8(w, xv), acc);
+    }
+
+    __device__ __forceinline__ void run(float (&acc)[R]) const
     {
         int c = 0;
         for (; c + U <= nfull; c += U) {
@@ -957,30 +1013,32 @@ struct QuantRows {
             }
             __builtin_amdgcn_sched_barrier(0); // all loads of the batch first
 #pragma unroll
-            for (int u = 0; u < U; ++u)
+            for (int u = 0; u < U; ++u) {
+                const float off = offset_term(xv[u]);
 #pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    f4 t = {0.f, 0.f, 0.f, 0.f};
-                    qdot<BITS>(t, w[u][r], xv[u]);
-                    fma4(acc[r], f4{sc[u][r], sc[u][r], sc[u][r], sc[u][r]}, t);
-                }
+                for (int r = 0; r < R; ++r)
+                    accumulate(acc[r], w[u][r], sc[u][r], xv[u], off);
+            }
         }
         for (; c < nfull; ++c) {
             f4 xv[NX];
 #pragma unroll
             for (int k = 0; k < NX; ++k)
                 xv[k] = load_x4(xl + c * CH + 4 * k);
+            u4 w[R];
+            float sc[R];
 #pragma unroll
             for (int r = 0; r < R; ++r) {
-                const u4 w = wload(r, c);
-                const float sc = sload(r, c);
-                f4 t = {0.f, 0.f, 0.f, 0.f};
-                qdot<BITS>(t, w, xv);
-                fma4(acc[r], f4{sc, sc, sc, sc}, t);
+                w[r] = wload(r, c);
+                sc[r] = sload(r, c);
             }
+            const float off = offset_term(xv);
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                accumulate(acc[r], w[r], sc[r], xv, off);
         }
-        if (c * kWave < nv) { // ragged last chunk: x past kn is zero (codes are finite)
-            const int v = c * kWave + lane;
+        if (c * G < nv) { // ragged last chunk: x past kn is zero (codes are finite)
+            const int v = c * G + seg;
             if (v < nv) {
                 const int valid = kn - v * N;
                 f4 xv[NX];
@@ -990,43 +1048,78 @@ struct QuantRows {
                     if (4 * k < valid)
                         xv[k] = mask_from<f4, 4>(load_x4(xl + c * CH + 4 * k), valid - 4 * k);
                 }
+                const float off = offset_term(xv);
 #pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    const u4 w = wload(r, c);
-                    const float sc = sload(r, c);
-                    f4 t = {0.f, 0.f, 0.f, 0.f};
-                    qdot<BITS>(t, w, xv);
-                    fma4(acc[r], f4{sc, sc, sc, sc}, t);
-                }
+                for (int r = 0; r < R; ++r)
+                    accumulate(acc[r], wload(r, c), sload(r, c), xv, off);
             }
         }
     }
 };
 
-template <int BITS, int R, int WV, int U>
-__device__ __forceinline__ void tile_quant(const DevItem &it, int row0)
+// Reduce R values per lane over each group of G consecutive lanes (R <= G,
+// both powers of two).  On return lane l holds the group total of value
+// (l % G) / (G / R).
+template <int R, int G>
+__device__ __forceinline__ float reduce_group(float (&v)[R], int lane)
 {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int wrow0 = row0 + wave * R;
-    const int nrows = it.M - wrow0;
-    if (nrows <= 0) return;
-    f4 acc[R];
+    static_assert(R <= G && G <= kWave, "R <= G <= 64");
+    halve_all<R, G / 2>(v, lane);
 #pragma unroll
-    for (int r = 0; r < R; ++r)
-        acc[r] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int o = G / (2 * R); o >= 1; o >>= 1)
+        v[0] += __shfl_xor(v[0], o);
+    return v[0];
+}
+
+// One quantised row tile: WV wavefronts, each 64 / G row groups x R rows.
+// Group p of a wavefront takes rows wrow0 + r * P + p (P = 64 / G groups).
+template <int BITS, int G, int R, int WV, int U>
+__device__ __forceinline__ void tile_quant_g(const DevItem &it, int row0)
+{
+    constexpr int P = kWave / G;
+    int lane = threadIdx.x & (kWave - 1);
+    // lane-derived values (group, masks of the reduction) are cheap to form
+    // per tile; hiding the lane index from the optimiser keeps it from
+    // hoisting them for every (bits, G) branch out of a sweep's tile loop,
+    // where they would stay live and cost occupancy
+    asm volatile("" : "+v"(lane));
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wrow0 = row0 + wave * (P * R);
+    if (wrow0 >= it.M) return;
+    const int sub = lane / G, seg = lane % G;
     const unsigned char *codes = static_cast<const unsigned char *>(it.W);
     const int ng = (it.K + 63) / 64;
     const float *scales = reinterpret_cast<const float *>(codes + (int64_t)it.M * it.ldw);
-    const QuantRows<BITS, R, U> qr(codes + (int64_t)wrow0 * it.ldw, it.ldw,
-                                   scales + (int64_t)wrow0 * ng, ng, min(nrows, R), it.x, it.K,
-                                   lane);
-    qr.run(acc, lane);
-    const float v = reduce_rows<R>(acc, lane);
-    constexpr int G = kWave / R;
-    if ((lane % G) == 0) {
-        const int row = wrow0 + lane / G;
+    const unsigned char *rowp[R];
+    const float *sclp[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int row = min(wrow0 + r * P + sub, it.M - 1); // rows past M: computed, not stored
+        rowp[r] = codes + (int64_t)row * it.ldw;
+        sclp[r] = scales + (int64_t)row * ng;
+    }
+    float acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        acc[r] = 0.f;
+    const QuantRows<BITS, G, R, U> qr(rowp, sclp, it.x, it.K, seg);
+    qr.run(acc);
+    const float v = reduce_group<R, G>(acc, lane);
+    constexpr int S = G / R; // lanes holding each row's total
+    if (seg % S == 0) {
+        const int row = wrow0 + (seg / S) * P + sub;
         if (row < it.M) it.y[row] = v;
+    }
+}
+
+template <int BITS, int R, int WV, int U>
+__device__ __forceinline__ void tile_quant(const DevItem &it, int row0)
+{
+    switch (it.lanes) {
+    case 8: tile_quant_g<BITS, 8, R, WV, U>(it, row0); break;
+    case 16: tile_quant_g<BITS, 16, R, WV, U>(it, row0); break;
+    case 32: tile_quant_g<BITS, 32, R, WV, U>(it, row0); break;
+    default: tile_quant_g<BITS, 64, R, WV, U>(it, row0); break;
     }
 }
 
@@ -1058,7 +1151,7 @@ __global__ __launch_bounds__(WV *kWave) void k_sweep_quant(const DevItem *__rest
 template <int R, int WV, int U>
 __global__ __launch_bounds__(WV *kWave) void k_item_quant(const DevItem it)
 {
-    tile_plain_any<R, WV, U>(it, (int)blockIdx.x * (R * WV));
+    tile_plain_any<R, WV, U>(it, (int)blockIdx.x * (R * WV * (kWave / it.lanes)));
 }
 
 // Grouped sweep whose items may carry a fused RMSNorm and/or be SwiGLU
@@ -1203,7 +1296,7 @@ struct InstMulti {
 
 // (R, waves per block, U) for plans holding block-quantised weights.
 #define TVL_QUANT_SHAPES(X)                                                                       \
-    X(2, 4, 2) X(2, 4, 4) X(4, 4, 1) X(4, 4, 2) X(4, 1, 2) X(8, 4, 1) X(1, 4, 4) X(2, 1, 4)
+    X(2, 4, 2) X(4, 4, 1) X(4, 4, 2) X(4, 1, 2) X(8, 4, 1) X(8, 2, 1)
 
 template <int R, int WV, int U>
 struct InstQuant {
@@ -1216,7 +1309,8 @@ struct InstQuant {
     }
     static hipError_t item(const DevItem &it, hipStream_t st)
     {
-        const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
+        const int rows = R * WV * (kWave / it.lanes);
+        const dim3 grid((it.M + rows - 1) / rows), block(WV * kWave);
         hipLaunchKernelGGL((k_item_quant<R, WV, U>), grid, block, 0, st, it);
         return hipGetLastError();
     }

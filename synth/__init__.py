@@ -145,7 +145,7 @@ class MatSpec:
     name: str
     M: int
     K: int
-    dtype: str  # "f32" or "f16" (weights); x and y are fp32
+    dtype: str  # "f32", "f16", or block-quantised "q8" / "q4" (weights); x and y are fp32
     dist: tuple  # ("normal", sigma) or ("uniform", a, b)
     cfg: int
     layer: int
@@ -159,17 +159,34 @@ class MatSpec:
         return key(self.cfg, self.layer, self.mat, KIND_X, rep)
 
     @property
+    def bits(self) -> int:
+        return {"f32": 32, "f16": 16, "q8": 8, "q4": 4}[self.dtype]
+
+    @property
+    def quantised(self) -> bool:
+        return self.dtype in ("q8", "q4")
+
+    @property
     def wbytes(self) -> int:
-        return self.M * self.K * (4 if self.dtype == "f32" else 2)
+        """Weight bytes a GEMV must read: the values, and for block-quantised
+        weights the codes plus one fp32 scale per 64 columns (no padding)."""
+        if self.quantised:
+            return self.M * ((self.K * self.bits + 7) // 8) + 4 * self.M * ((self.K + 63) // 64)
+        return self.M * self.K * self.bits // 8
 
     def algo_bytes(self) -> int:
         """Algorithmic bytes of one GEMV: |W| + |x| + |y| (paper Sec. 3.1)."""
         return self.wbytes + 4 * self.K + 4 * self.M
 
     def weights(self, row0: int = 0, nrows: int | None = None) -> np.ndarray:
-        """Rows [row0, row0+nrows) as a dense [nrows, K] array (fp32, or uint16 bits)."""
+        """Rows [row0, row0+nrows) as a dense [nrows, K] array (fp32, or uint16
+        bits); for "q8" / "q4" the fp32 draw quantised row by row into one
+        uint8 buffer (code plane of nrows rows, then their scale plane)."""
         nrows = self.M - row0 if nrows is None else nrows
         n, off = nrows * self.K, row0 * self.K
+        if self.quantised:
+            w = normal_f32(n, self.w_key, self.dist[1], off).reshape(nrows, self.K)
+            return quantize_rows(w, self.bits)
         if self.dist[0] == "uniform":
             w = uniform_f32(n, self.w_key, self.dist[1], self.dist[2], off)
             if self.dtype == "f16":
@@ -230,6 +247,12 @@ WORKLOADS = {
     "sweep7b": Workload("sweep7b", 4, _llama(4, 32, 4096, 11008, 32000, "f32")),
     # 8 layers of a Llama-2 70B-shaped stack, fp16 weights (GQA: wk, wv are 1024 x 8192)
     "stack70b8": Workload("stack70b8", 5, _llama(5, 8, 8192, 28672, None, "f16", kv=1024)),
+    # the same 110M and 7B tokens with block-quantised weights: the fp32 draws
+    # above, quantised per 64 columns to 8-bit or 4-bit codes
+    "sweep110m_q8": Workload("sweep110m_q8", 2, _llama(2, 12, 768, 2048, 32000, "q8")),
+    "sweep110m_q4": Workload("sweep110m_q4", 2, _llama(2, 12, 768, 2048, 32000, "q4")),
+    "sweep7b_q8": Workload("sweep7b_q8", 4, _llama(4, 32, 4096, 11008, 32000, "q8")),
+    "sweep7b_q4": Workload("sweep7b_q4", 4, _llama(4, 32, 4096, 11008, 32000, "q4")),
 }
 
 

@@ -27,7 +27,15 @@ class DevGemv:
 
 
 def dtype_code(spec: MatSpec) -> int:
-    return 0 if spec.dtype == "f32" else 1
+    return {"f32": 0, "f16": 1, "q8": 2, "q4": 3}[spec.dtype]
+
+
+def upload(spec: MatSpec, host, device="cuda"):
+    """A TvlMatrix of ``spec``'s weights (``host`` = spec.weights())."""
+    from paper_2601_03324_amd import tvl
+    if spec.quantised:
+        return tvl.upload_quant(host, spec.M, spec.K, dtype_code(spec), device=device)
+    return tvl.upload_matrix(host, dtype_code(spec), device)
 
 
 def load(wl: Workload, device="cuda", rep: int = 0, progress: bool = False,
@@ -41,7 +49,7 @@ def load(wl: Workload, device="cuda", rep: int = 0, progress: bool = False,
         if share_from is not None:
             Wd = share_from[i].W
         else:
-            Wd = tvl.upload_matrix(m.weights(), dtype_code(m), device)
+            Wd = upload(m, m.weights(), device)
         x = torch.from_numpy(m.x(rep)).to(device)
         y = torch.full((m.M,), float("nan"), dtype=torch.float32, device=device)
         out.append(DevGemv(m, Wd, x, y))

@@ -112,8 +112,18 @@ def test_workload_tables():
     assert len(W["stack70b8"].mats) == 56
     assert W["gemv768"].algo_bytes() == 2_365_440
     assert W["cls32000"].algo_bytes() == 98_435_072
-    keys = {m.w_key for wl in W.values() for m in wl.mats}
-    assert len(keys) == sum(len(wl.mats) for wl in W.values())
+    plain = [wl for wl in W.values() if not wl.mats[0].quantised]
+    keys = {m.w_key for wl in plain for m in wl.mats}
+    assert len(keys) == sum(len(wl.mats) for wl in plain)
+    # the quantised workloads quantise the fp32 draws of their source token:
+    # 110M: 109,510,656 code bytes + 6,844,416 scale bytes (8-bit)
+    for src, q in (("sweep110m", "sweep110m_q8"), ("sweep110m", "sweep110m_q4"),
+                   ("sweep7b", "sweep7b_q8"), ("sweep7b", "sweep7b_q4")):
+        assert [m.w_key for m in W[q].mats] == [m.w_key for m in W[src].mats]
+        assert [(m.M, m.K) for m in W[q].mats] == [(m.M, m.K) for m in W[src].mats]
+    assert W["sweep110m_q8"].weight_bytes() == 109_510_656 + 6_844_416
+    assert W["sweep110m_q4"].weight_bytes() == 109_510_656 // 2 + 6_844_416
+    assert W["sweep110m_q8"].algo_bytes() == 117_186_560
     # row regeneration equals the full draw
     m = W["sweep110m"].mats[4]
     full = m.weights()
