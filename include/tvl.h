@@ -82,7 +82,10 @@ extern "C" {
  *   w_ij = s[i][j/64] * q_ij        (converted exactly; fp32 accumulation).
  * Keeping the scales out of the code rows keeps every fetched 128-byte line
  * full.  Code bytes past column K are padding and never change the result;
- * the whole buffer spans M*ldw + 4*M*ceil(K/64) bytes. */
+ * the whole buffer spans M*ldw + 4*M*ceil(K/64) bytes.  Quantised items take
+ * K <= 2^24 and ldw <= 2^24 bytes (else TVL_ERR_SHAPE).  The 4-bit kernels
+ * form products at 2^-24 scale: x entries below about 2^-100 in magnitude
+ * fall into fp32 subnormals there and lose relative precision. */
 typedef enum tvl_dtype {
     TVL_F32 = 0, /* IEEE binary32 weights */
     TVL_F16 = 1, /* IEEE binary16 weights, converted exactly to fp32 */

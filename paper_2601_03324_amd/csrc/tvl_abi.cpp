@@ -59,6 +59,7 @@ tvl_status fail_hip(hipError_t e, const char *what)
 
 constexpr int64_t kMaxDim = 2147483647LL; // M and tile counts fit in int32
 constexpr int64_t kMaxK = 1LL << 30;       // K plus one LDS slice still fits in int32
+constexpr int64_t kMaxQuantK = 1LL << 24;  // quantised K and ldw (bytes)
 
 // Bytes per ldw unit: quantised rows are measured in bytes.
 int elem_size(int32_t dt) { return dt == TVL_F16 ? 2 : (dt == TVL_F32 ? 4 : 1); }
@@ -94,6 +95,10 @@ tvl_status check_one(const void *W, int64_t ldw, int32_t dt, const float *x, con
     if (is_quant(dt) && ldw < q_row_bytes(K, dt))
         return fail(TVL_ERR_SHAPE, "%s: a quantised row of K=%lld needs ldw >= %lld bytes", who,
                     (long long)K, (long long)q_row_bytes(K, dt));
+    // quantised kernels address a row tile with 32-bit buffer offsets
+    if (is_quant(dt) && (K > kMaxQuantK || ldw > kMaxQuantK))
+        return fail(TVL_ERR_SHAPE, "%s: quantised weights need K and ldw <= 2^24 (K=%lld ldw=%lld)",
+                    who, (long long)K, (long long)ldw);
     const int s = elem_size(dt);
     // the weight span (with a quantised matrix's scale plane) must be
     // addressable: M * (ldw * s + scale bytes per row) < 2^62
@@ -347,13 +352,9 @@ Shape default_fused_shape(double bytes_f16, double bytes_f32)
     return bytes_f16 > bytes_f32 ? Shape{4, 4, 2, tvl::kXDirect} : Shape{2, 4, 3, tvl::kXDirect};
 }
 
-// Default shape for plans or items with block-quantised weights.
-// (from sweeps of the 110M and 7B tokens on MI355X: 8 rows per wavefront
-// suit 4-bit rows, which carry half the bytes per column; 4 suit 8-bit)
-Shape default_quant_shape(bool all_q4)
-{
-    return all_q4 ? Shape{8, 4, 1, tvl::kXDirect} : Shape{4, 4, 1, tvl::kXDirect};
-}
+// Default shape for plans or items with block-quantised weights (from
+// sweeps of the 110M and 7B tokens, 8- and 4-bit, on MI355X).
+Shape default_quant_shape() { return Shape{8, 4, 1, tvl::kXDirect}; }
 
 Shape default_shape_items(const tvl_item *items, int32_t n)
 {
@@ -373,12 +374,10 @@ Shape default_shape_items(const tvl_item *items, int32_t n)
         fused = fused || is_fused(items[i]);
         nmax = std::max<int>(nmax, (int)nvec(items[i]));
     }
-    bool quant = false, all_q4 = true;
-    for (int32_t i = 0; i < n; ++i) {
+    bool quant = false;
+    for (int32_t i = 0; i < n; ++i)
         quant = quant || is_quant(items[i].dtype);
-        all_q4 = all_q4 && items[i].dtype == TVL_Q4;
-    }
-    if (quant) return default_quant_shape(all_q4);
+    if (quant) return default_quant_shape();
     if (nmax > 1) return default_multi_shape(multi_B(nmax));
     if (fused) return default_fused_shape(b16, b32);
     return default_shape(b16, b32, b32 > 0 ? row32 / b32 : 0.0);
@@ -671,7 +670,7 @@ tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype, const float *x
         if (tuning && (tuning->flags & TVL_FLAG_X_LDS))
             return fail(TVL_ERR_ARG, "tvl_gemv: quantised weights read x directly (direct-x)");
         Shape qs;
-        st = pick_shape(tuning, default_quant_shape(dtype == TVL_Q4), &qs, false);
+        st = pick_shape(tuning, default_quant_shape(), &qs, false);
         if (st != TVL_OK) return st;
         if (!tvl::quant_shape_supported(qs))
             return fail(TVL_ERR_ARG, "tvl_gemv: no quantised-weight kernel for (%d, %d, %d)", qs.R,

@@ -937,37 +937,65 @@ __device__ __forceinline__ float qdot4(const u4 w, const f4 (&xv)[8])
     return fmaf(tb, 0.0625f, ta);
 }
 
+// Buffer descriptor (CDNA V#) over [base, base + bytes): raw addressing, the
+// gfx9-family default format word.  Loads through it take a 32-bit per-lane
+// offset and a scalar offset, so R rows cost R offset registers instead of
+// R 64-bit pointers, and the chunk advance is one scalar add.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, int64_t bytes)
+{
+    const int n = bytes > 0x7fffffff ? 0x7fffffff : (int)bytes;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, n, 0x00020000);
+}
+constexpr int kBufNT = 2; // cache policy: non-temporal (streamed once)
+
 template <int BITS, int G, int R, int U>
 struct QuantRows {
-    static constexpr int N = 128 / BITS; // columns per 16-byte load
-    static constexpr int NX = N / 4;     // float4 of x per load
-    static constexpr int CH = G * N;     // columns per row per wavefront load
+    static constexpr int N = 128 / BITS;       // columns per 16-byte load
+    static constexpr int NX = N / 4;           // float4 of x per load
+    static constexpr int CH = G * N;           // columns per row per wavefront load
+    static constexpr int CB = CH * BITS / 8;   // code bytes per row per chunk
+    static constexpr int SB = CH / 64 * 4;     // scale bytes per row per chunk
+    static constexpr int XB = CH * 4;          // x bytes per chunk
     static_assert(CH % 64 == 0, "a chunk spans whole scale groups");
-    const unsigned char *rows[R]; // this lane's first code byte of each row
-    const float *scl[R];          // this lane's first scale of each row
-    const float *xl;
+    __amdgpu_buffer_rsrc_t wr, sr, xr; // codes and scales from the wave's first row; x
+    int vw[R], vs[R];                  // this lane's byte offsets of each row
+    int vx;
     int kn, nv, nfull, seg;
 
-    // rowp[r]: code row and scale row of the lane's r-th row
-    __device__ __forceinline__ QuantRows(const unsigned char *const (&rowp)[R],
-                                         const float *const (&sclp)[R], const float *x, int K,
+    // lrow[r]: the lane's r-th row, relative to the wave's first row (in
+    // range: rows past M are clamped by the caller)
+    __device__ __forceinline__ QuantRows(const unsigned char *codes0, int64_t code_bytes,
+                                         const float *scales0, int64_t scale_bytes, int64_t ldw,
+                                         int ng, const int (&lrow)[R], const float *x, int K,
                                          int seg_)
-        : xl(x + seg_ * N), kn(K), nv((K + N - 1) / N), nfull(K / CH), seg(seg_)
+        : wr(make_rsrc(codes0, code_bytes)), sr(make_rsrc(scales0, scale_bytes)),
+          xr(make_rsrc(x, ((int64_t)K * 4 + 15) & ~(int64_t)15)), vx(seg_ * N * 4), kn(K),
+          nv((K + N - 1) / N), nfull(K / CH), seg(seg_)
     {
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-            rows[r] = rowp[r] + seg_ * 16;
-            scl[r] = sclp[r] + seg_ * N / 64;
+            vw[r] = (int)(lrow[r] * ldw) + seg_ * 16;
+            vs[r] = (lrow[r] * ng + seg_ * N / 64) * 4;
         }
     }
 
     __device__ __forceinline__ u4 wload(int r, int c) const
     {
-        return __builtin_nontemporal_load((const TVL_GLOBAL u4 *)(rows[r] + (int64_t)c * CH * BITS / 8));
+        return __builtin_amdgcn_raw_buffer_load_b128(wr, vw[r], c * CB, kBufNT);
     }
     __device__ __forceinline__ float sload(int r, int c) const
     {
-        return *(const TVL_GLOBAL float *)(scl[r] + c * (CH / 64));
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(sr, vs[r], c * SB, 0));
+    }
+    __device__ __forceinline__ f4 xload(int c, int k) const
+    {
+        return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(xr, vx + 16 * k, c * XB, 0));
+    }
+    // The same load with the whole offset in the range-checked VGPR part:
+    // past the end of x (rounded to 16 bytes) it returns zeros, no branch.
+    __device__ __forceinline__ f4 xload_checked(int c, int k) const
+    {
+        return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(xr, vx + 16 * k + c * XB, 0, 0));
     }
 
     // -8 * sum of the lane's N x values (the 4-bit code offset), 0 for 8-bit
@@ -993,7 +1021,31 @@ struct QuantRows {
             acc = fmaf(sc, qdot8(w, xv), acc);
     }
 
-    __device__ __forceinline__ void run(float (&acc)[R]) const
+    __device__ __forceinline__ void load_codes(int c, u4 (&w)[R], float (&sc)[R]) const
+    {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            w[r] = wload(r, c);
+            sc[r] = sload(r, c);
+        }
+    }
+    __device__ __forceinline__ void load_x(int c, f4 (&xv)[NX]) const
+    {
+#pragma unroll
+        for (int k = 0; k < NX; ++k)
+            xv[k] = xload(c, k);
+    }
+    __device__ __forceinline__ void compute(float (&acc)[R], const u4 (&w)[R], const float (&sc)[R],
+                                            const f4 (&xv)[NX]) const
+    {
+        const float off = offset_term(xv);
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            accumulate(acc[r], w[r], sc[r], xv, off);
+    }
+
+    // Full chunks in batches of U (all loads of a batch issued first).
+    __device__ __forceinline__ void run_batched(float (&acc)[R]) const
     {
         int c = 0;
         for (; c + U <= nfull; c += U) {
@@ -1002,56 +1054,40 @@ struct QuantRows {
             f4 xv[U][NX];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    w[u][r] = wload(r, c + u);
-                    sc[u][r] = sload(r, c + u);
-                }
-#pragma unroll
-                for (int k = 0; k < NX; ++k)
-                    xv[u][k] = load_x4(xl + (c + u) * CH + 4 * k);
+                load_codes(c + u, w[u], sc[u]);
+                load_x(c + u, xv[u]);
             }
-            __builtin_amdgcn_sched_barrier(0); // all loads of the batch first
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const float off = offset_term(xv[u]);
-#pragma unroll
-                for (int r = 0; r < R; ++r)
-                    accumulate(acc[r], w[u][r], sc[u][r], xv[u], off);
-            }
+            for (int u = 0; u < U; ++u)
+                compute(acc, w[u], sc[u], xv[u]);
         }
         for (; c < nfull; ++c) {
-            f4 xv[NX];
-#pragma unroll
-            for (int k = 0; k < NX; ++k)
-                xv[k] = load_x4(xl + c * CH + 4 * k);
             u4 w[R];
             float sc[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                w[r] = wload(r, c);
-                sc[r] = sload(r, c);
-            }
-            const float off = offset_term(xv);
-#pragma unroll
-            for (int r = 0; r < R; ++r)
-                accumulate(acc[r], w[r], sc[r], xv, off);
+            f4 xv[NX];
+            load_codes(c, w, sc);
+            load_x(c, xv);
+            compute(acc, w, sc, xv);
         }
+    }
+
+    __device__ __forceinline__ void run(float (&acc)[R]) const
+    {
+        run_batched(acc);
+        const int c = nfull;
         if (c * G < nv) { // ragged last chunk: x past kn is zero (codes are finite)
             const int v = c * G + seg;
             if (v < nv) {
                 const int valid = kn - v * N;
                 f4 xv[NX];
 #pragma unroll
-                for (int k = 0; k < NX; ++k) {
-                    xv[k] = f4{0.f, 0.f, 0.f, 0.f};
-                    if (4 * k < valid)
-                        xv[k] = mask_from<f4, 4>(load_x4(xl + c * CH + 4 * k), valid - 4 * k);
-                }
-                const float off = offset_term(xv);
-#pragma unroll
-                for (int r = 0; r < R; ++r)
-                    accumulate(acc[r], wload(r, c), sload(r, c), xv, off);
+                for (int k = 0; k < NX; ++k)
+                    xv[k] = mask_from<f4, 4>(xload_checked(c, k), valid - 4 * k);
+                u4 w[R];
+                float sc[R];
+                load_codes(c, w, sc);
+                compute(acc, w, sc, xv);
             }
         }
     }
@@ -1090,19 +1126,18 @@ __device__ __forceinline__ void tile_quant_g(const DevItem &it, int row0)
     const unsigned char *codes = static_cast<const unsigned char *>(it.W);
     const int ng = (it.K + 63) / 64;
     const float *scales = reinterpret_cast<const float *>(codes + (int64_t)it.M * it.ldw);
-    const unsigned char *rowp[R];
-    const float *sclp[R];
+    const int rows_left = it.M - wrow0; // >= 1
+    int lrow[R];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int row = min(wrow0 + r * P + sub, it.M - 1); // rows past M: computed, not stored
-        rowp[r] = codes + (int64_t)row * it.ldw;
-        sclp[r] = scales + (int64_t)row * ng;
-    }
+    for (int r = 0; r < R; ++r) // rows past M: computed from row M - 1, not stored
+        lrow[r] = min(r * P + sub, rows_left - 1);
     float acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r)
         acc[r] = 0.f;
-    const QuantRows<BITS, G, R, U> qr(rowp, sclp, it.x, it.K, seg);
+    const QuantRows<BITS, G, R, U> qr(codes + (int64_t)wrow0 * it.ldw, (int64_t)rows_left * it.ldw,
+                                      scales + (int64_t)wrow0 * ng, (int64_t)rows_left * ng * 4,
+                                      it.ldw, ng, lrow, it.x, it.K, seg);
     qr.run(acc);
     const float v = reduce_group<R, G>(acc, lane);
     constexpr int S = G / R; // lanes holding each row's total

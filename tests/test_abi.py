@@ -146,6 +146,8 @@ def gemv(W=A, ldw=768, dt=0, x=B, y=C, M=768, K=768, tuning=None):
     (dict(dt=4), DTYPE), (dict(dt=-1), DTYPE),
     (dict(dt=2, ldw=640), SHAPE), (dict(dt=3, ldw=256), SHAPE), (dict(dt=2, ldw=896, tuning=dict(ksplit=2)), ARG),
     (dict(dt=3, ldw=512, tuning=dict(flags=1)), ARG),
+    (dict(dt=2, K=(1 << 24) + 128, ldw=(1 << 24) + 128), SHAPE),
+    (dict(dt=3, ldw=(1 << 24) + 128), SHAPE),
     (dict(M=0), SHAPE), (dict(K=0), SHAPE), (dict(M=-5), SHAPE), (dict(M=1 << 31), SHAPE),
     (dict(K=(1 << 30) + 1, ldw=(1 << 30) + 32), SHAPE), (dict(ldw=767), SHAPE),
     (dict(W=A + 64), ALIGN), (dict(ldw=770), ALIGN), (dict(dt=1, ldw=800), ALIGN),
