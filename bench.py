@@ -178,6 +178,15 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     torch.cuda.set_device(0)
+    if args.calib_copy_mib:
+        # one plain copy of known size: its FETCH_SIZE / WRITE_SIZE counters
+        # calibrate what those counters read for the kernels of this run
+        nb = args.calib_copy_mib << 20
+        a = torch.empty(nb // 4, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        tvl.tvl_util_copy(b, a, nb)
+        torch.cuda.synchronize()
+        del a, b
     if args.workload in synth.FUSED_WORKLOADS:
         return run_fused(args, tvl, torch, np, oracle, synth, sdev)
     if args.workload in BEAMS:
@@ -239,14 +248,6 @@ def main() -> int:
 
         copies_used = ncopy
     torch.cuda.synchronize()
-
-    if args.calib_copy_mib:
-        nb = args.calib_copy_mib << 20
-        a = torch.empty(nb // 4, dtype=torch.float32, device="cuda")
-        b = torch.empty_like(a)
-        tvl.tvl_util_copy(b, a, nb)
-        torch.cuda.synchronize()
-        del a, b
 
     # read-only streaming ceiling with the same load kind (context)
     ceil_gbs = None
