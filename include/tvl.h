@@ -75,17 +75,15 @@ extern "C" {
  *   code plane    M rows of ldw BYTES (ldw a multiple of 128, at least
  *                 roundup(ceil(K*bits/8), 128) = tvl_row_stride);
  *                 8-bit: column j at byte j, two's complement q in [-128, 127];
- *                 4-bit: column j in byte j/2, low nibble first, unsigned u,
- *                 q = u - 8 in [-8, 7];
+ *                 4-bit: column j in byte j/2, low nibble first, two's
+ *                 complement q in [-8, 7];
  *   scale plane   at byte M*ldw: fp32 s[i][g], row-major, ceil(K/64) per
  *                 row, s[i][g] scaling columns 64g .. 64g+63 of row i;
  *   w_ij = s[i][j/64] * q_ij        (converted exactly; fp32 accumulation).
  * Keeping the scales out of the code rows keeps every fetched 128-byte line
  * full.  Code bytes past column K are padding and never change the result;
  * the whole buffer spans M*ldw + 4*M*ceil(K/64) bytes.  Quantised items take
- * K <= 2^24 and ldw <= 2^24 bytes (else TVL_ERR_SHAPE).  The 4-bit kernels
- * form products at 2^-24 scale: x entries below about 2^-100 in magnitude
- * fall into fp32 subnormals there and lose relative precision. */
+ * K <= 2^24 and ldw <= 2^24 bytes (else TVL_ERR_SHAPE). */
 typedef enum tvl_dtype {
     TVL_F32 = 0, /* IEEE binary32 weights */
     TVL_F16 = 1, /* IEEE binary16 weights, converted exactly to fp32 */
@@ -124,10 +122,13 @@ typedef enum tvl_status {
  *   Several vectors (nrhs > 1; beam search with nrhs hypotheses, Sec. 9.1):
  *     y[b*ldy + i] = sum_j W[i*ldw + j] * x[b*ldx + j] for b < nrhs <= 8; the
  *     weights are read once for all vectors.  Only for plain GEMV items
- *     (op == TVL_OP_GEMV, g == NULL); a plan may not mix several-vector items
- *     with RMSNorm or SwiGLU items.
- * Items with g != NULL, op != TVL_OP_GEMV or nrhs > 1 run in direct-x mode
- * and cannot be K-split. */
+ *     (op == TVL_OP_GEMV, g == NULL).
+ *   Block-quantised weights (dtype TVL_Q8 / TVL_Q4): plain one-vector GEMV
+ *     items only (op == TVL_OP_GEMV, g == NULL, nrhs <= 1).
+ * One launch (plan or batch) may hold plain fp32/fp16 items together with
+ * ONE of: RMSNorm/SwiGLU items, several-vector items, quantised items.
+ * Items with g != NULL, op != TVL_OP_GEMV, nrhs > 1 or quantised weights run
+ * in direct-x mode and cannot be K-split. */
 typedef struct tvl_item {
     const void *W;      /* device, M whole rows of ldw elements of `dtype`   */
     int64_t ldw;        /* row stride in elements                             */
@@ -164,7 +165,15 @@ typedef struct tvl_item {
  *                  (8,1) (8,2);  W=8: (2,4) (2,8) (4,2);
  *             W=2: (1,8) (2,8) (4,4) (8,2)
  *   direct-x: W=1 and W=4: (1,4) (1,8) (2,2) (2,3) (2,4) (2,8) (4,1) (4,2)
- *                  (4,3) (4,4) (8,1) (8,2) */
+ *                  (4,3) (4,4) (8,1) (8,2)
+ * Launches holding RMSNorm or SwiGLU items (direct-x only):
+ *   (2,4,2) (2,4,3) (2,4,4) (2,1,4) (4,1,2) (4,1,4) (4,4,2) (2,1,8)
+ * Launches holding several-vector items (direct-x only), per vector class
+ * (nrhs <= 2, <= 4, <= 8):
+ *   2: (2,4,2) (2,4,4) (4,4,2);  4: (2,4,1) (2,4,2) (4,4,1) (4,4,2);
+ *   8: (2,4,1) (2,4,2) (4,4,1)
+ * Launches holding block-quantised items (direct-x only; R rows per group of
+ * lanes, see tvl_dtype): (2,4,2) (4,4,1) (4,4,2) (4,1,2) (8,4,1) (8,2,1) */
 typedef struct tvl_tuning {
     int32_t rows_per_wave;
     int32_t waves_per_block;
@@ -234,8 +243,9 @@ TVL_API tvl_status tvl_gemv_item(const tvl_item *item, const tvl_tuning *tuning,
 TVL_API tvl_status tvl_gemv_batch_sweep(const tvl_item *items, int32_t n,
                                         hipStream_t stream);
 
-/* Sweep plan: validate `items`, build the tile table (tiles of R*W rows,
- * ordered by bytes per tile, largest first) and upload it once.  The item
+/* Sweep plan: validate `items`, build the tile table (tiles of R*W output
+ * rows; R/2*W for SwiGLU items; R*W*64/G for quantised items whose rows use
+ * G lanes each; ordered by bytes per tile, largest first) and upload it once.  The item
  * list is copied; the W, x, y buffers it names must stay valid for every
  * run.  `tuning` may be NULL.  The plan belongs to the device current at
  * creation. */

@@ -189,11 +189,11 @@ void oracle_swiglu(const double *a, const double *b, int64_t M, double *h)
 /* Format of this library for an M x K matrix:                               */
 /*   code plane: M rows of ldw bytes; column j of a row at byte j (8-bit) or */
 /*               in nibble j of byte j/2, low nibble first (4-bit);          */
+/*   codes are two's complement: q in [-128, 127] (8-bit), [-8, 7] (4-bit);  */
 /*   scale plane: right after the code plane (byte M*ldw), fp32, row-major,  */
 /*               ng = ceil(K/64) scales per row, s_{i,g} for columns         */
 /*               64g .. 64g+63;                                              */
-/*   8-bit: w_ij = s_{i, j/64} * q_ij, q two's complement in [-128, 127];    */
-/*   4-bit: w_ij = s_{i, j/64} * (u_ij - 8), u the unsigned nibble.          */
+/*   w_ij = s_{i, j/64} * q_ij.                                              */
 /* The products and sums are done exactly as in oracle_gemv_f32, in double.  */
 /* ------------------------------------------------------------------------ */
 static double q_weight(const uint8_t *W, int64_t ldw, int64_t M, int64_t K, int bits,
@@ -209,7 +209,7 @@ static double q_weight(const uint8_t *W, int64_t ldw, int64_t M, int64_t K, int 
     } else {
         const uint8_t byte = row[j / 2];
         const int u = (j % 2 == 0) ? (byte & 0x0f) : (byte >> 4);
-        q = (double)(u - 8);
+        q = (double)(u >= 8 ? u - 16 : u); /* 4-bit two's complement */
     }
     return s * q; /* exact: 24-bit scale times a code of at most 8 bits */
 }

@@ -874,67 +874,68 @@ __global__ __launch_bounds__(WV *kWave) void k_item_multi(const DevItem it)
         tile_multi<float, R, WV, U, B>(it, row0);
 }
 
-// Block-quantised weights (8- or 4-bit codes in M rows of ldw bytes; fp32
-// scale per 64 columns in a row-major plane after the code rows).  A 16-byte
-// load brings N = 16 (8-bit) or 32 (4-bit) codes of one row, all in one
-// 64-column scale group, so each load is dotted with x first and scaled once.
+// Block-quantised weights (8- or 4-bit two's-complement codes in M rows of
+// ldw bytes; fp32 scale per 64 columns in a row-major plane after the code
+// rows).  A 16-byte load brings N = 16 (8-bit) or 32 (4-bit) codes of one
+// row, all in one 64-column scale group, so each load is dotted with x first
+// and scaled once.
 //
-// Decoding costs VALU work per code, and a 4-bit row streams two codes per
-// byte, so the decode is kept to about two VALU operations per code:
-//   8-bit: each byte converts with one sign-extending SDWA conversion, then
-//          one FMA;
-//   4-bit: masking a dword with 0x000F000F (0x00F000F0) leaves two nibbles
-//          (two nibbles times 16) in the mantissas of the two binary16
-//          halves, i.e. the exact values u * 2^-24 (16u * 2^-24) as fp16
-//          subnormals; v_fma_mix_f32 multiplies such a half with fp32 x and
-//          accumulates in fp32, so a code costs one FMA plus a shared mask.
-//          The codes are unsigned u = q + 8, so the load adds
-//          s * (sum_j u_j x_j - 8 sum_j x_j), with sum_j x_j formed once per
-//          load of x and shared by the R rows of the lane.
-// Products of the 4-bit path are formed at 2^-24 scale: x entries below about
-// 2^-100 in magnitude fall into fp32 subnormals there and lose precision.
+// Decoding costs VALU work per code (a 4-bit row streams two codes per byte),
+// so every code converts with ONE sign-extending SDWA conversion of a byte
+// (v_cvt_f32_i32 with a byte select) and one FMA, exactly:
+//   8-bit: the bytes are the codes;
+//   4-bit: (v << 4) & 0xF0F0F0F0 and v & 0xF0F0F0F0 put 16 * q of the low
+//          and of the high nibbles in the top of each byte; the factor 16
+//          is folded into the scale (a power of two, exact).
 //
 // Short rows: a wavefront splits into 64 / G groups of G lanes, one row per
 // group (G from quant_lanes), so a 384-byte row still fills its lanes.
-typedef _Float16 h2v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float sbyte(unsigned v, int b) { return (float)(int)(signed char)(v >> (8 * b)); }
 
-__device__ __forceinline__ h2v as_h2(unsigned v) { return __builtin_bit_cast(h2v, v); }
-
-// 8-bit: t += q . x over the 16 columns of one 16-byte weight vector
+// 8-bit: sum_j q_j x_j over the 16 columns of one 16-byte weight vector
 __device__ __forceinline__ float qdot8(const u4 w, const f4 (&xv)[4])
 {
     float ta = 0.f, tb = 0.f;
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
         const unsigned v = w[d];
-        ta = fmaf((float)(int)(signed char)(v & 0xffu), xv[d].x, ta);
-        tb = fmaf((float)(int)(signed char)((v >> 8) & 0xffu), xv[d].y, tb);
-        ta = fmaf((float)(int)(signed char)((v >> 16) & 0xffu), xv[d].z, ta);
-        tb = fmaf((float)(int)(signed char)(v >> 24), xv[d].w, tb);
+        ta = fmaf(sbyte(v, 0), xv[d].x, ta);
+        tb = fmaf(sbyte(v, 1), xv[d].y, tb);
+        ta = fmaf(sbyte(v, 2), xv[d].z, ta);
+        tb = fmaf(sbyte(v, 3), xv[d].w, tb);
     }
     return ta + tb;
 }
 
-// 4-bit: 2^-24 * sum_j u_j x_j over the 32 columns of one 16-byte vector
+// 4-bit: 16 * sum_j q_j x_j over the 32 columns of one 16-byte vector.  Dword
+// d holds columns 8d .. 8d+7, column 8d + 2b in the low nibble of byte b and
+// 8d + 2b + 1 in its high nibble.
 __device__ __forceinline__ float qdot4(const u4 w, const f4 (&xv)[8])
 {
-    float ta = 0.f, tb = 0.f; // nibbles 0, 2, 4, 6 of a dword; 16 x nibbles 1, 3, 5, 7
+    float ta = 0.f, tb = 0.f; // even columns; odd columns
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
-        const unsigned v = w[d], v8 = v >> 8;
-        const h2v a = as_h2(v & 0x000F000Fu), b = as_h2(v & 0x00F000F0u);
-        const h2v c = as_h2(v8 & 0x000F000Fu), e = as_h2(v8 & 0x00F000F0u);
+        // lo = (w << 4) & 0xF0F0F0F0, hi = w & 0xF0F0F0F0, formed here and
+        // only here: written plainly, the optimiser moves each mask past the
+        // byte sign extension (an AND per code instead of per dword) and
+        // hoists every row's masks together (registers)
+        unsigned lo, hi;
+        asm volatile("v_lshlrev_b32 %0, 4, %2\n\t"
+                     "v_and_b32 %0, 0xf0f0f0f0, %0\n\t"
+                     "v_and_b32 %1, 0xf0f0f0f0, %2"
+                     : "=&v"(lo), "=v"(hi)
+                     : "v"(w[d]));
         const f4 x0 = xv[2 * d], x1 = xv[2 * d + 1];
-        ta = fmaf((float)a.x, x0.x, ta);
-        tb = fmaf((float)b.x, x0.y, tb);
-        ta = fmaf((float)c.x, x0.z, ta);
-        tb = fmaf((float)e.x, x0.w, tb);
-        ta = fmaf((float)a.y, x1.x, ta);
-        tb = fmaf((float)b.y, x1.y, tb);
-        ta = fmaf((float)c.y, x1.z, ta);
-        tb = fmaf((float)e.y, x1.w, tb);
+        ta = fmaf(sbyte(lo, 0), x0.x, ta);
+        tb = fmaf(sbyte(hi, 0), x0.y, tb);
+        ta = fmaf(sbyte(lo, 1), x0.z, ta);
+        tb = fmaf(sbyte(hi, 1), x0.w, tb);
+        ta = fmaf(sbyte(lo, 2), x1.x, ta);
+        tb = fmaf(sbyte(hi, 2), x1.y, tb);
+        ta = fmaf(sbyte(lo, 3), x1.z, ta);
+        tb = fmaf(sbyte(hi, 3), x1.w, tb);
     }
-    return fmaf(tb, 0.0625f, ta);
+    return ta + tb;
 }
 
 // Buffer descriptor (CDNA V#) over [base, base + bytes): raw addressing, the
@@ -998,25 +999,10 @@ struct QuantRows {
         return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(xr, vx + 16 * k + c * XB, 0, 0));
     }
 
-    // -8 * sum of the lane's N x values (the 4-bit code offset), 0 for 8-bit
-    __device__ __forceinline__ float offset_term(const f4 (&xv)[NX]) const
-    {
-        if constexpr (BITS == 4) {
-            f4 s = xv[0];
-#pragma unroll
-            for (int k = 1; k < NX; ++k)
-                s += xv[k];
-            return -8.f * ((s.x + s.y) + (s.z + s.w));
-        } else {
-            return 0.f;
-        }
-    }
-
-    __device__ __forceinline__ void accumulate(float &acc, const u4 w, float sc, const f4 (&xv)[NX],
-                                               float off) const
+    __device__ __forceinline__ void accumulate(float &acc, const u4 w, float sc, const f4 (&xv)[NX]) const
     {
         if constexpr (BITS == 4)
-            acc = fmaf(sc, fmaf(qdot4(w, xv), 16777216.f, off), acc);
+            acc = fmaf(sc * 0.0625f, qdot4(w, xv), acc);
         else
             acc = fmaf(sc, qdot8(w, xv), acc);
     }
@@ -1038,10 +1024,12 @@ struct QuantRows {
     __device__ __forceinline__ void compute(float (&acc)[R], const u4 (&w)[R], const float (&sc)[R],
                                             const f4 (&xv)[NX]) const
     {
-        const float off = offset_term(xv);
 #pragma unroll
-        for (int r = 0; r < R; ++r)
-            accumulate(acc[r], w[r], sc[r], xv, off);
+        for (int r = 0; r < R; ++r) {
+            accumulate(acc[r], w[r], sc[r], xv);
+            // decode one row at a time: only its masked dwords stay live
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
 
     // Full chunks in batches of U (all loads of a batch issued first).

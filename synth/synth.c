@@ -156,8 +156,8 @@ void synth_int_f16(uint16_t *out, int64_t n, uint64_t key, uint64_t offset,
 /* Block quantisation of an fp32 matrix into the quantised format (a code   */
 /* plane of M rows x ldw bytes, then an fp32 scale plane of M x ceil(K/64); */
 /* see the library header).  Symmetric: 8-bit s = max|w| / 127,             */
-/* q = round(w / s) in [-127, 127]; 4-bit s = max|w| / 7, q in [-7, 7]      */
-/* stored as nibble q + 8.  An all-zero group gets s = 0 and q = 0.         */
+/* q = round(w / s) in [-127, 127]; 4-bit s = max|w| / 7, q in [-7, 7];     */
+/* codes stored in two's complement.  An all-zero group gets s = 0, q = 0.  */
 /* Padding bytes of the code rows keep what the caller put in `out`.        */
 /* ------------------------------------------------------------------------ */
 int64_t synth_q_row_bytes(int64_t K, int bits)
@@ -193,7 +193,7 @@ void synth_quantize_rows(const float *w, int64_t M, int64_t K, int bits, uint8_t
                 if (bits == 8) {
                     row[j] = (uint8_t)(int8_t)q;
                 } else {
-                    const uint8_t u = (uint8_t)(q + 8);
+                    const uint8_t u = (uint8_t)(q & 0x0f);
                     if (j % 2 == 0)
                         row[j / 2] = (uint8_t)((row[j / 2] & 0xf0) | u);
                     else

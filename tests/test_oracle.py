@@ -353,7 +353,7 @@ def _q_rows(codes: np.ndarray, scales: np.ndarray, bits: int, extra: int = 0):
     if bits == 8:
         rows[:, :K] = codes.astype(np.int8).view(np.uint8)
     else:
-        u = (codes + 8).astype(np.uint8)
+        u = (codes & 0x0F).astype(np.uint8)  # two's complement nibbles
         for j in range(K):
             if j % 2 == 0:
                 rows[:, j // 2] = (rows[:, j // 2] & 0xF0) | u[:, j]
@@ -367,9 +367,16 @@ def pin_quant_golden():
     """Hand-worked 4-bit row: codes (1, -2, 7), scale 1/2, x = (2, 1, -1):
     w = (0.5, -1, 3.5), y = 1 - 1 - 3.5 = -3.5, S = 5.5."""
     Wq, ldw = _q_rows(np.array([[1, -2, 7]]), np.array([[0.5]], np.float32), 4)
-    assert Wq[0] == 0x69 and Wq[1] & 0x0F == 0x0F and ldw == 128
+    assert Wq[0] == 0xE1 and Wq[1] & 0x0F == 0x07 and ldw == 128
     y, S = oracle.gemv_q(Wq, 4, ldw, 1, 3, np.array([2, 1, -1], np.float32))
     assert y[0] == -3.5 and S[0] == 5.5
+    # the extreme 4-bit codes, low nibble first: byte 0x78 holds column 0 =
+    # nibble 0x8 = -8 and column 1 = nibble 0x7 = 7
+    Wq = np.zeros(128 + 4, np.uint8)
+    Wq[0] = 0x78
+    Wq[128:] = np.array([0.25], np.float32).view(np.uint8)
+    y, S = oracle.gemv_q(Wq, 4, 128, 1, 2, np.array([1, 2], np.float32))
+    assert y[0] == 0.25 * (-8 + 14) and S[0] == 0.25 * (8 + 14)
     # 8-bit, two rows: codes (-128, 127, 3) with scale 2^-3, (1, 1, 1) with scale 2
     Wq, ldw = _q_rows(np.array([[-128, 127, 3], [1, 1, 1]]),
                       np.array([[0.125], [2.0]], np.float32), 8)
@@ -450,7 +457,8 @@ MUTANTS = {
     "q_scale_row_stride": ("const double s = (double)scales[i * ng + j / 64];",
                            "const double s = (double)scales[j / 64];"),
     "q4_nibble_order": ("(j % 2 == 0) ? (byte & 0x0f) : (byte >> 4)", "(j % 2 == 0) ? (byte >> 4) : (byte & 0x0f)"),
-    "q4_offset": ("q = (double)(u - 8);", "q = (double)(u - 7);"),
+    "q4_offset_not_twos_complement": ("q = (double)(u >= 8 ? u - 16 : u);", "q = (double)(u - 8);"),
+    "q4_sign_threshold": ("q = (double)(u >= 8 ? u - 16 : u);", "q = (double)(u > 8 ? u - 16 : u);"),
     "q8_unsigned": ("q = (double)(int8_t)row[j];", "q = (double)row[j];"),
     "q_code_row_stride": ("const uint8_t *row = W + i * ldw;\n    double q;",
                           "const uint8_t *row = W + i * K * bits / 8;\n    double q;"),
