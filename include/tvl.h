@@ -77,13 +77,18 @@ extern "C" {
  *                 8-bit: column j at byte j, two's complement q in [-128, 127];
  *                 4-bit: column j in byte j/2, low nibble first, two's
  *                 complement q in [-8, 7];
- *   scale plane   at byte M*ldw: fp32 s[i][g], row-major, ceil(K/64) per
- *                 row, s[i][g] scaling columns 64g .. 64g+63 of row i;
- *   w_ij = s[i][j/64] * q_ij        (converted exactly; fp32 accumulation).
+ *   scale plane   at byte M*ldw: fp32 in blocks of 4 rows: the scale s_ig
+ *                 of columns 64g .. 64g+63 of row i at float index
+ *                 (i/4)*4*ng + 4*g + i%4, ng = ceil(K/64), rows padded to
+ *                 Mp = M rounded up to a multiple of 4 (entries of rows
+ *                 i >= M are padding, never used);
+ *   w_ij = s_{i,j/64} * q_ij        (converted exactly; fp32 accumulation).
  * Keeping the scales out of the code rows keeps every fetched 128-byte line
- * full.  Code bytes past column K are padding and never change the result;
- * the whole buffer spans M*ldw + 4*M*ceil(K/64) bytes.  Quantised items take
- * K <= 2^24 and ldw <= 2^24 bytes (else TVL_ERR_SHAPE). */
+ * full; the 4-row blocks put the scales of 4 neighbouring rows side by side
+ * (one 16-byte load) and the groups of a block in consecutive 16 bytes.  Code bytes past column K are
+ * padding and never change the result; the whole buffer spans
+ * M*ldw + 4*Mp*ceil(K/64) bytes.  Quantised items take K <= 2^24,
+ * ldw <= 2^24 bytes and a scale plane below 2^31 bytes (else TVL_ERR_SHAPE). */
 typedef enum tvl_dtype {
     TVL_F32 = 0, /* IEEE binary32 weights */
     TVL_F16 = 1, /* IEEE binary16 weights, converted exactly to fp32 */

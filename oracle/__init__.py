@@ -223,12 +223,13 @@ def swiglu_bound(a: np.ndarray, b: np.ndarray, Sa: np.ndarray, Sb: np.ndarray,
 
 def gemv_q(Wq: np.ndarray, bits: int, ldw: int, M: int, K: int, x: np.ndarray):
     """(y, S) for a block-quantised matrix given as one uint8 buffer: the code
-    plane (M rows of ldw bytes) followed by the fp32 scale plane (M rows of
-    ceil(K/64)); 8- or 4-bit codes (format in oracle.c)."""
+    plane (M rows of ldw bytes) followed by the fp32 scale plane in blocks of
+    4 rows (M rounded up to 4, ceil(K/64) groups); 8- or 4-bit codes (format
+    in oracle.c)."""
     Wq = np.ascontiguousarray(Wq, dtype=np.uint8).reshape(-1)
     if bits not in (4, 8):
         raise ValueError("bits must be 4 or 8")
-    need = M * ldw + 4 * M * ((K + 63) // 64)
+    need = M * ldw + 4 * ((M + 3) // 4 * 4) * ((K + 63) // 64)
     if Wq.size < need:
         raise ValueError(f"buffer of {Wq.size} bytes, need {need}")
     x = np.ascontiguousarray(x, dtype=np.float32)

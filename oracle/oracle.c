@@ -190,9 +190,11 @@ void oracle_swiglu(const double *a, const double *b, int64_t M, double *h)
 /*   code plane: M rows of ldw bytes; column j of a row at byte j (8-bit) or */
 /*               in nibble j of byte j/2, low nibble first (4-bit);          */
 /*   codes are two's complement: q in [-128, 127] (8-bit), [-8, 7] (4-bit);  */
-/*   scale plane: right after the code plane (byte M*ldw), fp32, row-major,  */
-/*               ng = ceil(K/64) scales per row, s_{i,g} for columns         */
-/*               64g .. 64g+63;                                              */
+/*   scale plane: right after the code plane (byte M*ldw), fp32, in blocks   */
+/*               of 4 rows: s_{i,g} (columns 64g .. 64g+63 of row i) at      */
+/*               index (i/4)*4*ng + 4*g + i%4, ng = ceil(K/64) groups, rows  */
+/*               padded to Mp = M rounded up to 4 (entries of rows i >= M    */
+/*               are padding);                                               */
 /*   w_ij = s_{i, j/64} * q_ij.                                              */
 /* The products and sums are done exactly as in oracle_gemv_f32, in double.  */
 /* ------------------------------------------------------------------------ */
@@ -201,7 +203,7 @@ static double q_weight(const uint8_t *W, int64_t ldw, int64_t M, int64_t K, int 
 {
     const float *scales = (const float *)(W + M * ldw);
     const int64_t ng = (K + 63) / 64;
-    const double s = (double)scales[i * ng + j / 64];
+    const double s = (double)scales[(i / 4) * 4 * ng + 4 * (j / 64) + i % 4];
     const uint8_t *row = W + i * ldw;
     double q;
     if (bits == 8) {

@@ -74,7 +74,8 @@ int64_t q_row_bytes(int64_t K, int32_t dt)
     const int bits = dt == TVL_Q4 ? 4 : 8;
     return ((K * bits + 7) / 8 + 127) / 128 * 128;
 }
-int64_t q_scale_bytes(int64_t M, int64_t K) { return 4 * M * ((K + 63) / 64); }
+// Scale plane: ceil(K/64) groups of M rounded up to 4 floats (group-major).
+int64_t q_scale_bytes(int64_t M, int64_t K) { return 4 * ((M + 3) / 4 * 4) * ((K + 63) / 64); }
 
 struct Range {
     uintptr_t b, e; // [b, e)
@@ -95,14 +96,18 @@ tvl_status check_one(const void *W, int64_t ldw, int32_t dt, const float *x, con
     if (is_quant(dt) && ldw < q_row_bytes(K, dt))
         return fail(TVL_ERR_SHAPE, "%s: a quantised row of K=%lld needs ldw >= %lld bytes", who,
                     (long long)K, (long long)q_row_bytes(K, dt));
-    // quantised kernels address a row tile with 32-bit buffer offsets
+    // quantised kernels address a row tile and the scale plane with 32-bit
+    // buffer offsets
     if (is_quant(dt) && (K > kMaxQuantK || ldw > kMaxQuantK))
         return fail(TVL_ERR_SHAPE, "%s: quantised weights need K and ldw <= 2^24 (K=%lld ldw=%lld)",
                     who, (long long)K, (long long)ldw);
+    if (is_quant(dt) && q_scale_bytes(M, K) > 0x7fffffffLL)
+        return fail(TVL_ERR_SHAPE, "%s: quantised scale plane of %lld bytes exceeds 2^31 - 1", who,
+                    (long long)q_scale_bytes(M, K));
     const int s = elem_size(dt);
-    // the weight span (with a quantised matrix's scale plane) must be
-    // addressable: M * (ldw * s + scale bytes per row) < 2^62
-    if (ldw > (int64_t(1) << 62) / M / s - (is_quant(dt) ? 4 * ((K + 63) / 64) : 0))
+    // the weight span (with a quantised matrix's scale plane, < 2^31 bytes,
+    // checked below) must be addressable: M * ldw * s < 2^61
+    if (ldw > (int64_t(1) << 61) / M / s)
         return fail(TVL_ERR_SHAPE, "%s: M * ldw overflows", who);
     if (reinterpret_cast<uintptr_t>(W) % tvl::kLineBytes != 0)
         return fail(TVL_ERR_ALIGN, "%s: W must be 128-byte aligned", who);

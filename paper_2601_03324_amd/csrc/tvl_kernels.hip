@@ -955,38 +955,60 @@ struct QuantRows {
     static constexpr int NX = N / 4;           // float4 of x per load
     static constexpr int CH = G * N;           // columns per row per wavefront load
     static constexpr int CB = CH * BITS / 8;   // code bytes per row per chunk
-    static constexpr int SB = CH / 64 * 4;     // scale bytes per row per chunk
     static constexpr int XB = CH * 4;          // x bytes per chunk
     static_assert(CH % 64 == 0, "a chunk spans whole scale groups");
-    __amdgpu_buffer_rsrc_t wr, sr, xr; // codes and scales from the wave's first row; x
-    int vw[R], vs[R];                  // this lane's byte offsets of each row
+    static_assert(R == 1 || R == 2 || R % 4 == 0, "scale loads of 1, 2 or 4k rows");
+    static constexpr int SSTEP = CH / 64 * 16; // scale-plane bytes between chunks
+    __amdgpu_buffer_rsrc_t wr, sr, xr; // codes from the wave's first row; scale plane; x
+    int vw[R];                         // this lane's byte offset of each code row
+    int vs;                            // byte offset of the lane's first scale in chunk 0
+    int sblk;                          // bytes between 4-row blocks of the scale plane
     int vx;
     int kn, nv, nfull, seg;
 
-    // lrow[r]: the lane's r-th row, relative to the wave's first row (in
-    // range: rows past M are clamped by the caller)
+    // lrow[r]: the lane's r-th row relative to the wave's first row (in range:
+    // rows past M are clamped by the caller); srow0: the lane's first row in
+    // the scale plane (rows past M read padding or, past the plane, zeros).
+    // Scale of row i, group g: float (i/4)*4*ng + 4*g + i%4.
     __device__ __forceinline__ QuantRows(const unsigned char *codes0, int64_t code_bytes,
-                                         const float *scales0, int64_t scale_bytes, int64_t ldw,
-                                         int ng, const int (&lrow)[R], const float *x, int K,
-                                         int seg_)
-        : wr(make_rsrc(codes0, code_bytes)), sr(make_rsrc(scales0, scale_bytes)),
-          xr(make_rsrc(x, ((int64_t)K * 4 + 15) & ~(int64_t)15)), vx(seg_ * N * 4), kn(K),
-          nv((K + N - 1) / N), nfull(K / CH), seg(seg_)
+                                         const float *plane, int64_t plane_bytes, int64_t ldw,
+                                         int ng, const int (&lrow)[R], int srow0, const float *x,
+                                         int K, int seg_)
+        : wr(make_rsrc(codes0, code_bytes)), sr(make_rsrc(plane, plane_bytes)),
+          xr(make_rsrc(x, ((int64_t)K * 4 + 15) & ~(int64_t)15)),
+          vs(16 * ((srow0 / 4) * ng + seg_ * N / 64) + 4 * (srow0 % 4)), sblk(16 * ng),
+          vx(seg_ * N * 4), kn(K), nv((K + N - 1) / N), nfull(K / CH), seg(seg_)
     {
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
+        for (int r = 0; r < R; ++r)
             vw[r] = (int)(lrow[r] * ldw) + seg_ * 16;
-            vs[r] = (lrow[r] * ng + seg_ * N / 64) * 4;
-        }
     }
 
     __device__ __forceinline__ u4 wload(int r, int c) const
     {
         return __builtin_amdgcn_raw_buffer_load_b128(wr, vw[r], c * CB, kBufNT);
     }
-    __device__ __forceinline__ float sload(int r, int c) const
+    // the scales of the lane's R consecutive rows for chunk c: one 16-byte
+    // load per 4-row block when R >= 4, the whole offset range-checked
+    __device__ __forceinline__ void sload(int c, float (&sc)[R]) const
     {
-        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(sr, vs[r], c * SB, 0));
+        const int off = vs + c * SSTEP;
+        if constexpr (R < 4) {
+            // (the 64-bit raw buffer load builtin is lowered to a single
+            // dword load by this compiler, so R = 2 takes two dword loads)
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                sc[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(sr, off + 4 * r, 0, 0));
+        } else {
+#pragma unroll
+            for (int q = 0; q < R / 4; ++q) {
+                const f4 v = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(sr, off + sblk * q, 0, 0));
+                sc[4 * q] = v.x;
+                sc[4 * q + 1] = v.y;
+                sc[4 * q + 2] = v.z;
+                sc[4 * q + 3] = v.w;
+            }
+        }
     }
     __device__ __forceinline__ f4 xload(int c, int k) const
     {
@@ -1010,10 +1032,9 @@ struct QuantRows {
     __device__ __forceinline__ void load_codes(int c, u4 (&w)[R], float (&sc)[R]) const
     {
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
+        for (int r = 0; r < R; ++r)
             w[r] = wload(r, c);
-            sc[r] = sload(r, c);
-        }
+        sload(c, sc);
     }
     __device__ __forceinline__ void load_x(int c, f4 (&xv)[NX]) const
     {
@@ -1096,7 +1117,8 @@ __device__ __forceinline__ float reduce_group(float (&v)[R], int lane)
 }
 
 // One quantised row tile: WV wavefronts, each 64 / G row groups x R rows.
-// Group p of a wavefront takes rows wrow0 + r * P + p (P = 64 / G groups).
+// Group p of a wavefront takes the R consecutive rows wrow0 + p * R + r, so
+// its R scales of a group sit side by side in the scale plane's 4-row blocks.
 template <int BITS, int G, int R, int WV, int U>
 __device__ __forceinline__ void tile_quant_g(const DevItem &it, int row0)
 {
@@ -1112,25 +1134,26 @@ __device__ __forceinline__ void tile_quant_g(const DevItem &it, int row0)
     if (wrow0 >= it.M) return;
     const int sub = lane / G, seg = lane % G;
     const unsigned char *codes = static_cast<const unsigned char *>(it.W);
-    const int ng = (it.K + 63) / 64;
-    const float *scales = reinterpret_cast<const float *>(codes + (int64_t)it.M * it.ldw);
+    const int Mp = (it.M + 3) / 4 * 4;
+    const float *plane = reinterpret_cast<const float *>(codes + (int64_t)it.M * it.ldw);
     const int rows_left = it.M - wrow0; // >= 1
     int lrow[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) // rows past M: computed from row M - 1, not stored
-        lrow[r] = min(r * P + sub, rows_left - 1);
+        lrow[r] = min(sub * R + r, rows_left - 1);
     float acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r)
         acc[r] = 0.f;
+    const int ng = (it.K + 63) / 64;
     const QuantRows<BITS, G, R, U> qr(codes + (int64_t)wrow0 * it.ldw, (int64_t)rows_left * it.ldw,
-                                      scales + (int64_t)wrow0 * ng, (int64_t)rows_left * ng * 4,
-                                      it.ldw, ng, lrow, it.x, it.K, seg);
+                                      plane, (int64_t)4 * Mp * ng, it.ldw, ng, lrow,
+                                      wrow0 + sub * R, it.x, it.K, seg);
     qr.run(acc);
     const float v = reduce_group<R, G>(acc, lane);
     constexpr int S = G / R; // lanes holding each row's total
     if (seg % S == 0) {
-        const int row = wrow0 + (seg / S) * P + sub;
+        const int row = wrow0 + sub * R + seg / S;
         if (row < it.M) it.y[row] = v;
     }
 }

@@ -307,9 +307,9 @@ def upload_matrix(host, dtype: int, device="cuda", stream=None) -> TvlMatrix:
 
 def quant_matrix_bytes(M: int, K: int, dtype: int, ldw: int | None = None) -> int:
     """Bytes of a block-quantised matrix: M code rows of ldw bytes, then the
-    fp32 scale plane (M x ceil(K/64))."""
+    group-major fp32 scale plane (ceil(K/64) groups of M rounded up to 4)."""
     ldw = tvl_row_stride(K, dtype) if ldw is None else ldw
-    return M * ldw + 4 * M * ((K + 63) // 64)
+    return M * ldw + 4 * ((M + 3) // 4 * 4) * ((K + 63) // 64)
 
 
 def upload_quant(host, M: int, K: int, dtype: int, ldw: int | None = None,

@@ -119,13 +119,15 @@ def q_row_bytes(K: int, bits: int) -> int:
 
 
 def q_matrix_bytes(M: int, K: int, bits: int, ldw: int | None = None) -> int:
+    """Code plane (M rows of ldw bytes) + scale plane (M rounded up to 4
+    rows x ceil(K/64) groups, fp32, in blocks of 4 rows)."""
     ldw = q_row_bytes(K, bits) if ldw is None else ldw
-    return M * ldw + 4 * M * ((K + 63) // 64)
+    return M * ldw + 4 * ((M + 3) // 4 * 4) * ((K + 63) // 64)
 
 
 def quantize_rows(w: np.ndarray, bits: int, ldw: int | None = None, pad: int = 0) -> np.ndarray:
     """fp32 [M, K] -> one uint8 buffer: the code plane (M rows of ldw bytes)
-    then the fp32 scale plane (M x ceil(K/64)); code padding = `pad`."""
+    then the fp32 scale plane; code padding = `pad`."""
     w = np.ascontiguousarray(w, dtype=np.float32)
     M, K = w.shape
     ldw = q_row_bytes(K, bits) if ldw is None else ldw

@@ -154,9 +154,11 @@ void synth_int_f16(uint16_t *out, int64_t n, uint64_t key, uint64_t offset,
 
 /* ------------------------------------------------------------------------ */
 /* Block quantisation of an fp32 matrix into the quantised format (a code   */
-/* plane of M rows x ldw bytes, then an fp32 scale plane of M x ceil(K/64); */
-/* see the library header).  Symmetric: 8-bit s = max|w| / 127,             */
-/* q = round(w / s) in [-127, 127]; 4-bit s = max|w| / 7, q in [-7, 7];     */
+/* plane of M rows x ldw bytes, then the fp32 scale plane in blocks of 4   */
+/* rows: group g of row i at (i/4)*4*ng + 4*g + i%4; see the library        */
+/* header).                                                                 */
+/* Symmetric: 8-bit s = max|w| / 127, q = round(w / s) in [-127, 127];      */
+/* 4-bit s = max|w| / 7, q in [-7, 7].                                      */
 /* codes stored in two's complement.  An all-zero group gets s = 0, q = 0.  */
 /* Padding bytes of the code rows keep what the caller put in `out`.        */
 /* ------------------------------------------------------------------------ */
@@ -169,21 +171,23 @@ int64_t synth_q_row_bytes(int64_t K, int bits)
 void synth_quantize_rows(const float *w, int64_t M, int64_t K, int bits, uint8_t *out,
                          int64_t ldw)
 {
-    const int64_t ng = (K + 63) / 64;
+    const int64_t ng = (K + 63) / 64, Mp = (M + 3) / 4 * 4;
     const int qmax = bits == 8 ? 127 : 7;
     float *plane = (float *)(out + M * ldw);
+    for (int64_t g = 0; g < ng; ++g) /* scale padding rows M .. Mp-1 */
+        for (int64_t i = M; i < Mp; ++i)
+            plane[(i / 4) * 4 * ng + 4 * g + i % 4] = 0.f;
 #pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < M; ++i) {
         const float *src = w + i * K;
         uint8_t *row = out + i * ldw;
-        float *scales = plane + i * ng;
         for (int64_t g = 0; g < ng; ++g) {
             const int64_t j0 = g * 64, j1 = (j0 + 64 < K) ? j0 + 64 : K;
             float amax = 0.f;
             for (int64_t j = j0; j < j1; ++j)
                 amax = fabsf(src[j]) > amax ? fabsf(src[j]) : amax;
             const float s = amax / (float)qmax;
-            scales[g] = s;
+            plane[(i / 4) * 4 * ng + 4 * g + i % 4] = s;
             for (int64_t j = j0; j < j1; ++j) {
                 int q = 0;
                 if (s > 0.f) {

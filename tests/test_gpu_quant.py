@@ -113,7 +113,11 @@ def test_quant_exact_on_integers(dt):
         else:
             plane = codes[:, 0::2] | (codes[:, 1::2] << 4)
         scales = np.exp2(rng.integers(-2, 1, (M, ng))).astype(np.float32)
-        Wq = np.concatenate([plane.reshape(-1), scales.reshape(-1).view(np.uint8)])
+        Mp = (M + 3) // 4 * 4
+        full = np.full((Mp, ng), np.float32(1e30))  # junk in the padding rows
+        full[:M] = scales
+        sp = np.ascontiguousarray(full.reshape(Mp // 4, 4, ng).transpose(0, 2, 1))  # 4-row blocks
+        Wq = np.concatenate([plane.reshape(-1), sp.reshape(-1).view(np.uint8)])
         x = rng.integers(-4, 5, K).astype(np.float32)
         yref, _ = oracle.gemv_q(Wq, bits, ldw, M, K, x)
         y = run_item(Wq, ldw, dt, x, M, K)

@@ -344,11 +344,13 @@ def pin_swiglu():
 # --------------------------------------------------- quantised-weight pins
 def _q_rows(codes: np.ndarray, scales: np.ndarray, bits: int, extra: int = 0):
     """Build a quantised matrix by hand (not with the generator's quantiser):
-    codes [M, K] in the signed range, scales [M, ceil(K/64)] fp32.  Returns
+    codes [M, K] in the signed range, scales [M, ceil(K/64)] fp32, stored
+    in blocks of 4 rows with M padded to 4 (pad entries NaN: never read).  Returns
     (buffer, ldw); code rows padded to 128 bytes (+ extra) with junk."""
     M, K = codes.shape
     ldw = ((K * bits + 7) // 8 + 127) // 128 * 128 + extra
-    out = np.full(M * ldw + 4 * scales.size, 0xAB, np.uint8)
+    Mp = (M + 3) // 4 * 4
+    out = np.full(M * ldw + 4 * Mp * scales.shape[1], 0xAB, np.uint8)
     rows = out[:M * ldw].reshape(M, ldw)
     if bits == 8:
         rows[:, :K] = codes.astype(np.int8).view(np.uint8)
@@ -359,7 +361,12 @@ def _q_rows(codes: np.ndarray, scales: np.ndarray, bits: int, extra: int = 0):
                 rows[:, j // 2] = (rows[:, j // 2] & 0xF0) | u[:, j]
             else:
                 rows[:, j // 2] = (rows[:, j // 2] & 0x0F) | (u[:, j] << 4)
-    out[M * ldw:] = np.ascontiguousarray(scales, np.float32).reshape(-1).view(np.uint8)
+    ng = scales.shape[1]
+    full = np.full((Mp, ng), np.nan, np.float32)  # pad rows NaN (never read)
+    full[:M] = scales
+    # blocks of 4 rows: [block][group][row in block]
+    plane = full.reshape(Mp // 4, 4, ng).transpose(0, 2, 1)
+    out[M * ldw:] = np.ascontiguousarray(plane).reshape(-1).view(np.uint8)
     return out, ldw
 
 
@@ -372,9 +379,9 @@ def pin_quant_golden():
     assert y[0] == -3.5 and S[0] == 5.5
     # the extreme 4-bit codes, low nibble first: byte 0x78 holds column 0 =
     # nibble 0x8 = -8 and column 1 = nibble 0x7 = 7
-    Wq = np.zeros(128 + 4, np.uint8)
+    Wq = np.zeros(128 + 16, np.uint8)  # one code row, scale plane of 1 group x 4 rows
     Wq[0] = 0x78
-    Wq[128:] = np.array([0.25], np.float32).view(np.uint8)
+    Wq[128:] = np.array([0.25, np.nan, np.nan, np.nan], np.float32).view(np.uint8)
     y, S = oracle.gemv_q(Wq, 4, 128, 1, 2, np.array([1, 2], np.float32))
     assert y[0] == 0.25 * (-8 + 14) and S[0] == 0.25 * (8 + 14)
     # 8-bit, two rows: codes (-128, 127, 3) with scale 2^-3, (1, 1, 1) with scale 2
@@ -452,10 +459,12 @@ MUTANTS = {
     "swiglu_sign": ("a[i] / (1.0 + exp(-a[i])) * b[i]", "a[i] / (1.0 + exp(a[i])) * b[i]"),
     "swiglu_sigmoid_only": ("a[i] / (1.0 + exp(-a[i])) * b[i]", "1.0 / (1.0 + exp(-a[i])) * b[i]"),
     "swiglu_no_b": ("a[i] / (1.0 + exp(-a[i])) * b[i]", "a[i] / (1.0 + exp(-a[i]))"),
-    "q_group_32": ("const double s = (double)scales[i * ng + j / 64];",
-                   "const double s = (double)scales[i * ng + j / 32];"),
-    "q_scale_row_stride": ("const double s = (double)scales[i * ng + j / 64];",
-                           "const double s = (double)scales[j / 64];"),
+    "q_group_32": ("scales[(i / 4) * 4 * ng + 4 * (j / 64) + i % 4]",
+                   "scales[(i / 4) * 4 * ng + 4 * (j / 32) + i % 4]"),
+    "q_scale_row_major": ("scales[(i / 4) * 4 * ng + 4 * (j / 64) + i % 4]",
+                          "scales[i * ng + j / 64]"),
+    "q_scale_group_major": ("scales[(i / 4) * 4 * ng + 4 * (j / 64) + i % 4]",
+                            "scales[(j / 64) * ((M + 3) / 4 * 4) + i]"),
     "q4_nibble_order": ("(j % 2 == 0) ? (byte & 0x0f) : (byte >> 4)", "(j % 2 == 0) ? (byte >> 4) : (byte & 0x0f)"),
     "q4_offset_not_twos_complement": ("q = (double)(u >= 8 ? u - 16 : u);", "q = (double)(u - 8);"),
     "q4_sign_threshold": ("q = (double)(u >= 8 ? u - 16 : u);", "q = (double)(u > 8 ? u - 16 : u);"),
