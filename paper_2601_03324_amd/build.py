@@ -4,6 +4,7 @@ Usage: ``python -m paper_2601_03324_amd.build`` (or call ``build()``).
 """
 from __future__ import annotations
 
+import concurrent.futures
 import os
 import shutil
 import subprocess
@@ -16,13 +17,15 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libtvl.so")
 
 ARCH = "gfx950"
-SOURCES = ["tvl_kernels.hip", "tvl_abi.cpp"]
+# one translation unit per kernel family, plus the C-ABI layer
+SOURCES = ["tvl_gemv.hip", "tvl_fused.hip", "tvl_multi.hip", "tvl_quant.hip", "tvl_util.hip",
+           "tvl_abi.cpp"]
+OBJDIR = os.path.join(PKG, "_build")
 FLAGS = [
     f"--offload-arch={ARCH}",
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     "-fvisibility=hidden",
     "-Wall",
     # no packed-fp32 instructions (v_pk_{add,mul,fma}_f32) in device code
@@ -37,11 +40,7 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libtvl.so)")
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source into ``libtvl.so`` next to this file (always rebuilds)."""
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), *FLAGS, "-I", INCLUDE, "-I", CSRC, "-o", tmp,
-           *[os.path.join(CSRC, s) for s in SOURCES]]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -50,10 +49,31 @@ def build(verbose: bool = False) -> str:
              if l.strip() and "packed-fp32-ops" not in l and "warnings generated" not in l]
     if r.returncode != 0:
         sys.stderr.write(r.stderr)
-        raise RuntimeError(f"hipcc failed with exit code {r.returncode}")
+        raise RuntimeError(f"hipcc failed with exit code {r.returncode}: {' '.join(cmd)}")
     if verbose and noise:
         sys.stderr.write("\n".join(noise) + "\n")
-    os.replace(tmp, LIB)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source (in parallel, one object each) and link them into
+    ``libtvl.so`` next to this file.  Always rebuilds."""
+    os.makedirs(OBJDIR, exist_ok=True)
+    tag = "%d" % os.getpid()
+    objs = [os.path.join(OBJDIR, os.path.splitext(s)[0] + f".{tag}.o") for s in SOURCES]
+    cmds = [[hipcc(), *FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", "-o", o, os.path.join(CSRC, s)]
+            for s, o in zip(SOURCES, objs)]
+    jobs = min(len(cmds), max(1, min(16, os.cpu_count() or 1)))
+    try:
+        with concurrent.futures.ThreadPoolExecutor(jobs) as ex:
+            for f in [ex.submit(_run, c, verbose) for c in cmds]:
+                f.result()
+        tmp = LIB + ".tmp" + tag
+        _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
+        os.replace(tmp, LIB)
+    finally:
+        for o in objs:
+            if os.path.exists(o):
+                os.remove(o)
     return LIB
 
 

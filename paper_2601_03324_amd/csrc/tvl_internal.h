@@ -1,5 +1,6 @@
 // tvl_internal.h -- declarations shared by the C-ABI layer (tvl_abi.cpp) and
-// the gfx950 kernels (tvl_kernels.hip).  Not installed, not part of the ABI.
+// the gfx950 kernels (tvl_*.hip, tvl_device.h).  Not installed, not part of
+// the ABI.
 #pragma once
 
 #include <hip/hip_runtime_api.h>

@@ -1,0 +1,392 @@
+// tvl_quant.hip -- GEMV over block-quantised weights (8- and 4-bit codes,
+// one fp32 scale per 64 columns; the format is defined in tvl.h), the
+// on-the-fly unpacking the paper proposes for low-bit weights (Sec. 8.2).
+// A plan holding quantised items may also hold plain fp32 / fp16 items.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tvl_device.h"
+
+namespace tvl {
+namespace {
+
+// Block-quantised weights (8- or 4-bit two's-complement codes in M rows of
+// ldw bytes; fp32 scale per 64 columns in a row-major plane after the code
+// rows).  A 16-byte load brings N = 16 (8-bit) or 32 (4-bit) codes of one
+// row, all in one 64-column scale group, so each load is dotted with x first
+// and scaled once.
+//
+// Decoding costs VALU work per code (a 4-bit row streams two codes per byte),
+// so every code converts with ONE sign-extending SDWA conversion of a byte
+// (v_cvt_f32_i32 with a byte select) and one FMA, exactly:
+//   8-bit: the bytes are the codes;
+//   4-bit: (v << 4) & 0xF0F0F0F0 and v & 0xF0F0F0F0 put 16 * q of the low
+//          and of the high nibbles in the top of each byte; the factor 16
+//          is folded into the scale (a power of two, exact).
+//
+// Short rows: a wavefront splits into 64 / G groups of G lanes, one row per
+// group (G from quant_lanes), so a 384-byte row still fills its lanes.
+__device__ __forceinline__ float sbyte(unsigned v, int b) { return (float)(int)(signed char)(v >> (8 * b)); }
+
+// 8-bit: sum_j q_j x_j over the 16 columns of one 16-byte weight vector
+__device__ __forceinline__ float qdot8(const u4 w, const f4 (&xv)[4])
+{
+    float ta = 0.f, tb = 0.f;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        const unsigned v = w[d];
+        ta = fmaf(sbyte(v, 0), xv[d].x, ta);
+        tb = fmaf(sbyte(v, 1), xv[d].y, tb);
+        ta = fmaf(sbyte(v, 2), xv[d].z, ta);
+        tb = fmaf(sbyte(v, 3), xv[d].w, tb);
+    }
+    return ta + tb;
+}
+
+// 4-bit: 16 * sum_j q_j x_j over the 32 columns of one 16-byte vector.  Dword
+// d holds columns 8d .. 8d+7, column 8d + 2b in the low nibble of byte b and
+// 8d + 2b + 1 in its high nibble.
+__device__ __forceinline__ float qdot4(const u4 w, const f4 (&xv)[8])
+{
+    float ta = 0.f, tb = 0.f; // even columns; odd columns
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        // lo = (w << 4) & 0xF0F0F0F0, hi = w & 0xF0F0F0F0, formed here and
+        // only here: written plainly, the optimiser moves each mask past the
+        // byte sign extension (an AND per code instead of per dword) and
+        // hoists every row's masks together (registers)
+        unsigned lo, hi;
+        asm volatile("v_lshlrev_b32 %0, 4, %2\n\t"
+                     "v_and_b32 %0, 0xf0f0f0f0, %0\n\t"
+                     "v_and_b32 %1, 0xf0f0f0f0, %2"
+                     : "=&v"(lo), "=v"(hi)
+                     : "v"(w[d]));
+        const f4 x0 = xv[2 * d], x1 = xv[2 * d + 1];
+        ta = fmaf(sbyte(lo, 0), x0.x, ta);
+        tb = fmaf(sbyte(hi, 0), x0.y, tb);
+        ta = fmaf(sbyte(lo, 1), x0.z, ta);
+        tb = fmaf(sbyte(hi, 1), x0.w, tb);
+        ta = fmaf(sbyte(lo, 2), x1.x, ta);
+        tb = fmaf(sbyte(hi, 2), x1.y, tb);
+        ta = fmaf(sbyte(lo, 3), x1.z, ta);
+        tb = fmaf(sbyte(hi, 3), x1.w, tb);
+    }
+    return ta + tb;
+}
+
+// Buffer descriptor (CDNA V#) over [base, base + bytes): raw addressing, the
+// gfx9-family default format word.  Loads through it take a 32-bit per-lane
+// offset and a scalar offset, so R rows cost R offset registers instead of
+// R 64-bit pointers, and the chunk advance is one scalar add.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, int64_t bytes)
+{
+    const int n = bytes > 0x7fffffff ? 0x7fffffff : (int)bytes;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, n, 0x00020000);
+}
+constexpr int kBufNT = 2; // cache policy: non-temporal (streamed once)
+
+template <int BITS, int G, int R, int U>
+struct QuantRows {
+    static constexpr int N = 128 / BITS;       // columns per 16-byte load
+    static constexpr int NX = N / 4;           // float4 of x per load
+    static constexpr int CH = G * N;           // columns per row per wavefront load
+    static constexpr int CB = CH * BITS / 8;   // code bytes per row per chunk
+    static constexpr int XB = CH * 4;          // x bytes per chunk
+    static_assert(CH % 64 == 0, "a chunk spans whole scale groups");
+    static_assert(R == 1 || R == 2 || R % 4 == 0, "scale loads of 1, 2 or 4k rows");
+    static constexpr int SSTEP = CH / 64 * 16; // scale-plane bytes between chunks
+    __amdgpu_buffer_rsrc_t wr, sr, xr; // codes from the wave's first row; scale plane; x
+    int vw[R];                         // this lane's byte offset of each code row
+    int vs;                            // byte offset of the lane's first scale in chunk 0
+    int sblk;                          // bytes between 4-row blocks of the scale plane
+    int vx;
+    int kn, nv, nfull, seg;
+
+    // lrow[r]: the lane's r-th row relative to the wave's first row (in range:
+    // rows past M are clamped by the caller); srow0: the lane's first row in
+    // the scale plane (rows past M read padding or, past the plane, zeros).
+    // Scale of row i, group g: float (i/4)*4*ng + 4*g + i%4.
+    __device__ __forceinline__ QuantRows(const unsigned char *codes0, int64_t code_bytes,
+                                         const float *plane, int64_t plane_bytes, int64_t ldw,
+                                         int ng, const int (&lrow)[R], int srow0, const float *x,
+                                         int K, int seg_)
+        : wr(make_rsrc(codes0, code_bytes)), sr(make_rsrc(plane, plane_bytes)),
+          xr(make_rsrc(x, ((int64_t)K * 4 + 15) & ~(int64_t)15)),
+          vs(16 * ((srow0 / 4) * ng + seg_ * N / 64) + 4 * (srow0 % 4)), sblk(16 * ng),
+          vx(seg_ * N * 4), kn(K), nv((K + N - 1) / N), nfull(K / CH), seg(seg_)
+    {
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            vw[r] = (int)(lrow[r] * ldw) + seg_ * 16;
+    }
+
+    __device__ __forceinline__ u4 wload(int r, int c) const
+    {
+        return __builtin_amdgcn_raw_buffer_load_b128(wr, vw[r], c * CB, kBufNT);
+    }
+    // the scales of the lane's R consecutive rows for chunk c: one 16-byte
+    // load per 4-row block when R >= 4, the whole offset range-checked
+    __device__ __forceinline__ void sload(int c, float (&sc)[R]) const
+    {
+        const int off = vs + c * SSTEP;
+        if constexpr (R < 4) {
+            // (the 64-bit raw buffer load builtin is lowered to a single
+            // dword load by this compiler, so R = 2 takes two dword loads)
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                sc[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(sr, off + 4 * r, 0, 0));
+        } else {
+#pragma unroll
+            for (int q = 0; q < R / 4; ++q) {
+                const f4 v = __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(sr, off + sblk * q, 0, 0));
+                sc[4 * q] = v.x;
+                sc[4 * q + 1] = v.y;
+                sc[4 * q + 2] = v.z;
+                sc[4 * q + 3] = v.w;
+            }
+        }
+    }
+    __device__ __forceinline__ f4 xload(int c, int k) const
+    {
+        return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(xr, vx + 16 * k, c * XB, 0));
+    }
+    // The same load with the whole offset in the range-checked VGPR part:
+    // past the end of x (rounded to 16 bytes) it returns zeros, no branch.
+    __device__ __forceinline__ f4 xload_checked(int c, int k) const
+    {
+        return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(xr, vx + 16 * k + c * XB, 0, 0));
+    }
+
+    __device__ __forceinline__ void accumulate(float &acc, const u4 w, float sc, const f4 (&xv)[NX]) const
+    {
+        if constexpr (BITS == 4)
+            acc = fmaf(sc * 0.0625f, qdot4(w, xv), acc);
+        else
+            acc = fmaf(sc, qdot8(w, xv), acc);
+    }
+
+    __device__ __forceinline__ void load_codes(int c, u4 (&w)[R], float (&sc)[R]) const
+    {
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            w[r] = wload(r, c);
+        sload(c, sc);
+    }
+    __device__ __forceinline__ void load_x(int c, f4 (&xv)[NX]) const
+    {
+#pragma unroll
+        for (int k = 0; k < NX; ++k)
+            xv[k] = xload(c, k);
+    }
+    __device__ __forceinline__ void compute(float (&acc)[R], const u4 (&w)[R], const float (&sc)[R],
+                                            const f4 (&xv)[NX]) const
+    {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            accumulate(acc[r], w[r], sc[r], xv);
+            // decode one row at a time: only its masked dwords stay live
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+
+    // Full chunks in batches of U (all loads of a batch issued first).
+    __device__ __forceinline__ void run_batched(float (&acc)[R]) const
+    {
+        int c = 0;
+        for (; c + U <= nfull; c += U) {
+            u4 w[U][R];
+            float sc[U][R];
+            f4 xv[U][NX];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                load_codes(c + u, w[u], sc[u]);
+                load_x(c + u, xv[u]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                compute(acc, w[u], sc[u], xv[u]);
+        }
+        for (; c < nfull; ++c) {
+            u4 w[R];
+            float sc[R];
+            f4 xv[NX];
+            load_codes(c, w, sc);
+            load_x(c, xv);
+            compute(acc, w, sc, xv);
+        }
+    }
+
+    __device__ __forceinline__ void run(float (&acc)[R]) const
+    {
+        run_batched(acc);
+        const int c = nfull;
+        if (c * G < nv) { // ragged last chunk: x past kn is zero (codes are finite)
+            const int v = c * G + seg;
+            if (v < nv) {
+                const int valid = kn - v * N;
+                f4 xv[NX];
+#pragma unroll
+                for (int k = 0; k < NX; ++k)
+                    xv[k] = mask_from<f4, 4>(xload_checked(c, k), valid - 4 * k);
+                u4 w[R];
+                float sc[R];
+                load_codes(c, w, sc);
+                compute(acc, w, sc, xv);
+            }
+        }
+    }
+};
+
+// Reduce R values per lane over each group of G consecutive lanes (R <= G,
+// both powers of two).  On return lane l holds the group total of value
+// (l % G) / (G / R).
+template <int R, int G>
+__device__ __forceinline__ float reduce_group(float (&v)[R], int lane)
+{
+    static_assert(R <= G && G <= kWave, "R <= G <= 64");
+    halve_all<R, G / 2>(v, lane);
+#pragma unroll
+    for (int o = G / (2 * R); o >= 1; o >>= 1)
+        v[0] += __shfl_xor(v[0], o);
+    return v[0];
+}
+
+// One quantised row tile: WV wavefronts, each 64 / G row groups x R rows.
+// Group p of a wavefront takes the R consecutive rows wrow0 + p * R + r, so
+// its R scales of a group sit side by side in the scale plane's 4-row blocks.
+template <int BITS, int G, int R, int WV, int U>
+__device__ __forceinline__ void tile_quant_g(const DevItem &it, int row0)
+{
+    constexpr int P = kWave / G;
+    int lane = threadIdx.x & (kWave - 1);
+    // lane-derived values (group, masks of the reduction) are cheap to form
+    // per tile; hiding the lane index from the optimiser keeps it from
+    // hoisting them for every (bits, G) branch out of a sweep's tile loop,
+    // where they would stay live and cost occupancy
+    asm volatile("" : "+v"(lane));
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wrow0 = row0 + wave * (P * R);
+    if (wrow0 >= it.M) return;
+    const int sub = lane / G, seg = lane % G;
+    const unsigned char *codes = static_cast<const unsigned char *>(it.W);
+    const int Mp = (it.M + 3) / 4 * 4;
+    const float *plane = reinterpret_cast<const float *>(codes + (int64_t)it.M * it.ldw);
+    const int rows_left = it.M - wrow0; // >= 1
+    int lrow[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) // rows past M: computed from row M - 1, not stored
+        lrow[r] = min(sub * R + r, rows_left - 1);
+    float acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+        acc[r] = 0.f;
+    const int ng = (it.K + 63) / 64;
+    const QuantRows<BITS, G, R, U> qr(codes + (int64_t)wrow0 * it.ldw, (int64_t)rows_left * it.ldw,
+                                      plane, (int64_t)4 * Mp * ng, it.ldw, ng, lrow,
+                                      wrow0 + sub * R, it.x, it.K, seg);
+    qr.run(acc);
+    const float v = reduce_group<R, G>(acc, lane);
+    constexpr int S = G / R; // lanes holding each row's total
+    if (seg % S == 0) {
+        const int row = wrow0 + sub * R + seg / S;
+        if (row < it.M) it.y[row] = v;
+    }
+}
+
+template <int BITS, int R, int WV, int U>
+__device__ __forceinline__ void tile_quant(const DevItem &it, int row0)
+{
+    switch (it.lanes) {
+    case 8: tile_quant_g<BITS, 8, R, WV, U>(it, row0); break;
+    case 16: tile_quant_g<BITS, 16, R, WV, U>(it, row0); break;
+    case 32: tile_quant_g<BITS, 32, R, WV, U>(it, row0); break;
+    default: tile_quant_g<BITS, 64, R, WV, U>(it, row0); break;
+    }
+}
+
+// Any plain item (fp32, fp16, 8-bit or 4-bit weights), direct-x.
+template <int R, int WV, int U>
+__device__ __forceinline__ void tile_plain_any(const DevItem &it, int row0)
+{
+    switch (it.dtype) {
+    case 3: tile_quant<4, R, WV, U>(it, row0); break;
+    case 2: tile_quant<8, R, WV, U>(it, row0); break;
+    case 1: tile_fused<_Float16, R, WV, U, false, false>(it, row0); break;
+    default: tile_fused<float, R, WV, U, false, false>(it, row0); break;
+    }
+}
+
+template <int R, int WV, int U>
+__global__ __launch_bounds__(WV *kWave) void k_sweep_quant(const DevItem *__restrict__ items,
+                                                            const DevTile *__restrict__ tiles,
+                                                            int ntiles)
+{
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const DevTile tl = tiles[t];
+        const DevItem it = items[tl.item];
+        tile_plain_any<R, WV, U>(it, tl.row0);
+        __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
+    }
+}
+
+template <int R, int WV, int U>
+__global__ __launch_bounds__(WV *kWave) void k_item_quant(const DevItem it)
+{
+    tile_plain_any<R, WV, U>(it, (int)blockIdx.x * (R * WV * (kWave / it.lanes)));
+}
+
+// (R, waves per block, U) for plans holding block-quantised weights.
+#define TVL_QUANT_SHAPES(X)                                                                       \
+    X(2, 4, 2) X(4, 4, 1) X(4, 4, 2) X(4, 1, 2) X(8, 4, 1) X(8, 2, 1)
+
+template <int R, int WV, int U>
+struct InstQuant {
+    static hipError_t sweep(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
+                            hipStream_t st)
+    {
+        hipLaunchKernelGGL((k_sweep_quant<R, WV, U>), dim3(grid), dim3(WV * kWave), 0, st, items,
+                           tiles, ntiles);
+        return hipGetLastError();
+    }
+    static hipError_t item(const DevItem &it, hipStream_t st)
+    {
+        const int rows = R * WV * (kWave / it.lanes);
+        const dim3 grid((it.M + rows - 1) / rows), block(WV * kWave);
+        hipLaunchKernelGGL((k_item_quant<R, WV, U>), grid, block, 0, st, it);
+        return hipGetLastError();
+    }
+};
+
+}  // namespace
+
+bool quant_shape_supported(const Shape &s)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return s.xmode == kXDirect;
+    TVL_QUANT_SHAPES(X)
+#undef X
+    return false;
+}
+
+hipError_t launch_sweep_quant(const Shape &s, const DevItem *items, const DevTile *tiles,
+                              int ntiles, int grid, hipStream_t st)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return InstQuant<R_, W_, U_>::sweep(items, tiles, ntiles, grid, st);
+    TVL_QUANT_SHAPES(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_item_quant(const Shape &s, const DevItem &item, hipStream_t st)
+{
+#define X(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return InstQuant<R_, W_, U_>::item(item, st);
+    TVL_QUANT_SHAPES(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+}  // namespace tvl
