@@ -21,7 +21,8 @@ decode tokens with RMSNorm and SwiGLU fused into the GEMVs: fused110m (fp32,
 2 weight copies alternated) and fused70b8 (fp16 weights); the 110M and 7B
 tokens with block-quantised 8-bit / 4-bit weights (sweep110m_q8, sweep110m_q4,
 sweep7b_q8, sweep7b_q4; small weight sets are rotated over enough copies to
-span 1 GB); and beam4_110m / beam8_110m (several x vectors per weight read).
+span 1 GB); and beam4_110m / beam8_110m / beam16_110m (several x vectors per
+weight read).
 
 Prints ONE JSON line with the metric, a roofline object for the dominant
 kernel and the CPU oracle's throughput on a bounded sample of the workload.
@@ -46,7 +47,8 @@ CSRC = os.path.join(ROOT, "paper_2601_03324_amd", "csrc")
 # declarations and device code, plus its family's translation unit.
 KERNEL_COMMON = ("tvl_internal.h", "tvl_device.h")
 KERNEL_FAMILY = {"fused110m": "tvl_fused.hip", "fused70b8": "tvl_fused.hip",
-                 "beam4_110m": "tvl_multi.hip", "beam8_110m": "tvl_multi.hip"}
+                 "beam4_110m": "tvl_multi.hip", "beam8_110m": "tvl_multi.hip",
+                 "beam16_110m": "tvl_multi.hip"}
 
 DESCRIBE = {
     "sweep110m": "sweep110m: one decode token of Llama-2 110M, 85 fp32 GEMVs "
@@ -67,13 +69,15 @@ DESCRIBE = {
                   "GEMVs x 4 x vectors, weights read once, one launch",
     "beam8_110m": "beam8_110m: one decode token of Llama-2 110M for 8 beam hypotheses: 85 fp32 "
                   "GEMVs x 8 x vectors, weights read once, one launch",
+    "beam16_110m": "beam16_110m: one decode token of Llama-2 110M for 16 beam hypotheses: 85 "
+                   "fp32 GEMVs x 16 x vectors, weights read once, one launch",
 }
 for _nm, _tok, _n in (("110m", "Llama-2 110M", 85), ("7b", "Llama-2 7B", 225)):
     for _b in (8, 4):
         DESCRIBE[f"sweep{_nm}_q{_b}"] = (
             f"sweep{_nm}_q{_b}: one decode token of {_tok}, {_n} GEMVs with {_b}-bit "
             f"block-quantised weights (one fp32 scale per 64 columns), one launch")
-BEAMS = {"beam4_110m": 4, "beam8_110m": 8}
+BEAMS = {"beam4_110m": 4, "beam8_110m": 8, "beam16_110m": 16}
 
 
 def oracle_rows(oracle, synth, m, rows, x):

@@ -125,9 +125,11 @@ typedef enum tvl_status {
  *   SwiGLU (op == TVL_OP_SWIGLU): y_i = silu(a_i) * b_i with a = W x and
  *     b = W3 x over the (normalised) x; W3 has W's M, K, ldw and dtype.
  *   Several vectors (nrhs > 1; beam search with nrhs hypotheses, Sec. 9.1):
- *     y[b*ldy + i] = sum_j W[i*ldw + j] * x[b*ldx + j] for b < nrhs <= 8; the
- *     weights are read once for all vectors.  Only for plain GEMV items
- *     (op == TVL_OP_GEMV, g == NULL).
+ *     y[b*ldy + i] = sum_j W[i*ldw + j] * x[b*ldx + j] for b < nrhs <= 16;
+ *     the weights are read once for all vectors.  Only for plain GEMV items
+ *     (op == TVL_OP_GEMV, g == NULL).  Up to 4 vectors the products run on
+ *     the vector ALUs, from 5 on (by default) on the matrix cores, in fp32
+ *     with fp32 accumulation either way.
  *   Block-quantised weights (dtype TVL_Q8 / TVL_Q4): plain one-vector GEMV
  *     items only (op == TVL_OP_GEMV, g == NULL, nrhs <= 1).
  * One launch (plan or batch) may hold plain fp32/fp16 items together with
@@ -146,13 +148,13 @@ typedef struct tvl_item {
     const void *W3;     /* TVL_OP_SWIGLU: second matrix (same layout), else NULL */
     const float *g;     /* RMSNorm weight, K floats, 16-byte aligned; NULL = none */
     float eps;          /* RMSNorm epsilon (finite, >= 0; ignored when g == NULL) */
-    int32_t nrhs;       /* x vectors: 0 or 1 = one; 2..8 = several            */
+    int32_t nrhs;       /* x vectors: 0 or 1 = one; 2..16 = several           */
     int64_t ldx;        /* nrhs > 1: x row stride in floats (>= K, % 4 == 0)  */
     int64_t ldy;        /* nrhs > 1: y row stride in floats (>= M)            */
 } tvl_item;
 
 /* Launch shape override.  A zero field means "choose by shape".
- *   rows_per_wave   R in {1, 2, 4, 8}: rows one wavefront computes at once
+ *   rows_per_wave   R in {1, 2, 4, 8, 16}: rows one wavefront computes at once
  *   waves_per_block W in {1, 2, 4, 8}: wavefronts per workgroup
  *   unroll          U in {1, 2, 3, 4, 8}: 16-byte weight loads per row kept in
  *                   flight per lane
@@ -174,9 +176,11 @@ typedef struct tvl_item {
  * Launches holding RMSNorm or SwiGLU items (direct-x only):
  *   (2,4,2) (2,4,3) (2,4,4) (2,1,4) (4,1,2) (4,1,4) (4,4,2) (2,1,8)
  * Launches holding several-vector items (direct-x only), per vector class
- * (nrhs <= 2, <= 4, <= 8):
+ * (nrhs <= 2, <= 4, <= 8) on the vector ALUs:
  *   2: (2,4,2) (2,4,4) (4,4,2);  4: (2,4,1) (2,4,2) (4,4,1) (4,4,2);
  *   8: (2,4,1) (2,4,2) (4,4,1)
+ * and, for any nrhs <= 16, on the matrix cores (R = 8 or 16 rows per
+ * wavefront in groups of 4): (8,1,1) (8,4,1) (16,1,1) (16,2,1) (16,4,1)
  * Launches holding block-quantised items (direct-x only; R rows per group of
  * lanes, see tvl_dtype): (2,4,2) (4,4,1) (4,4,2) (4,1,2) (8,4,1) (8,2,1) */
 typedef struct tvl_tuning {

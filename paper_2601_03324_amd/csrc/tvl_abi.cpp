@@ -29,6 +29,7 @@ struct tvl_plan {
     int device = -1;
     bool fused = false;
     int multiB = 0; // > 0: several-vector plan holding B x vectors
+    int wmode = 0;  // weight dtypes: 0 fp32 only, 1 fp16 only, 2 both
     bool quant = false; // some item has block-quantised weights
     Shape shape{4, 4, 2, tvl::kXLds};
     int ks_cap = 0;
@@ -205,7 +206,7 @@ tvl_status check_fused(const tvl_item &t, const char *who)
 {
     tvl_status st = check_one(t.W, t.ldw, t.dtype, t.x, t.y, t.M, t.K, who);
     if (st != TVL_OK) return st;
-    if (t.nrhs < 0 || t.nrhs > 8) return fail(TVL_ERR_ARG, "%s: nrhs must be 0..8", who);
+    if (t.nrhs < 0 || t.nrhs > 16) return fail(TVL_ERR_ARG, "%s: nrhs must be 0..16", who);
     if (t.nrhs > 1) {
         if (t.op != TVL_OP_GEMV || t.g)
             return fail(TVL_ERR_ARG, "%s: several x vectors only for plain GEMV items", who);
@@ -262,14 +263,20 @@ tvl_status check_items(const tvl_item *items, int32_t n)
 
 
 // x vectors a several-vector kernel must hold: the next power of two >= n
-int multi_B(int n) { return n <= 2 ? 2 : n <= 4 ? 4 : 8; }
+// (the matrix-core form holds any number up to 16)
+int multi_B(int n) { return n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16; }
 
 // Default several-vector shape (direct-x), by B, measured on MI355X on the
-// 110M decode token: more rows per wavefront amortise each x read over more
-// weights (R = 4), and fewer loads in flight keep the R x B accumulators in
-// registers as B grows.
+// 110M decode token.  Up to 4 vectors the VALU form wins: more rows per
+// wavefront amortise each x read over more weights (R = 4), and fewer loads
+// in flight keep the R x B accumulators in registers.  From 5 vectors on,
+// the FMAs would take ~half the VALU issue slots and the matrix-core form
+// wins (8 vectors: 4.58 TB/s vs 4.07 TB/s; 16 vectors: 8 rows and one
+// wavefront per block, 2.93 TB/s, against 2.51-2.79 TB/s for the others).
 Shape default_multi_shape(int B)
 {
+    if (B > 8) return Shape{8, 1, 1, tvl::kXDirect};
+    if (B > 4) return Shape{16, 2, 1, tvl::kXDirect};
     return B == 2 ? Shape{4, 4, 2, tvl::kXDirect} : Shape{4, 4, 1, tvl::kXDirect};
 }
 
@@ -493,6 +500,12 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
         p->fused = p->fused || is_fused(items[i]);
         nmax = std::max<int>(nmax, (int)nvec(items[i]));
     }
+    {
+        bool f32 = false, f16 = false;
+        for (int32_t i = 0; i < n; ++i)
+            (items[i].dtype == TVL_F16 ? f16 : f32) = true;
+        p->wmode = f32 && f16 ? 2 : f16 ? 1 : 0;
+    }
     if (nmax > 1) {
         p->multiB = multi_B(nmax);
         if (p->fused) {
@@ -584,8 +597,8 @@ tvl_status plan_launch(const tvl_plan *p, hipStream_t st)
     const hipError_t e =
         p->quant    ? tvl::launch_sweep_quant(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid,
                                               st)
-        : p->multiB ? tvl::launch_sweep_multi(p->shape, p->multiB, p->d_items, p->d_tiles,
-                                              p->ntiles, p->grid, st)
+        : p->multiB ? tvl::launch_sweep_multi(p->shape, p->multiB, p->wmode, p->d_items,
+                                              p->d_tiles, p->ntiles, p->grid, st)
         : p->fused ? tvl::launch_sweep_fused(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid,
                                              st)
                    : tvl::launch_sweep(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid,

@@ -117,10 +117,12 @@ hipError_t launch_sweep_quant(const Shape &s, const DevItem *items, const DevTil
                               int ntiles, int grid, hipStream_t st);
 hipError_t launch_item_quant(const Shape &s, const DevItem &item, hipStream_t st);
 
-// Several x vectors per item (B = 2, 4 or 8 >= every item's nrhs; direct-x).
+// Several x vectors per item (B = 2, 4, 8 or 16 >= every item's nrhs;
+// direct-x).  Shapes with R >= 8 run on the matrix cores (any B); wmode tells
+// them which weight dtypes the launch holds: 0 fp32 only, 1 fp16 only, 2 both.
 bool multi_shape_supported(const Shape &s, int B);
-hipError_t launch_sweep_multi(const Shape &s, int B, const DevItem *items, const DevTile *tiles,
-                              int ntiles, int grid, hipStream_t st);
+hipError_t launch_sweep_multi(const Shape &s, int B, int wmode, const DevItem *items,
+                              const DevTile *tiles, int ntiles, int grid, hipStream_t st);
 hipError_t launch_item_multi(const Shape &s, int B, const DevItem &item, hipStream_t st);
 
 hipError_t launch_pack(int dtype, void *dst, int64_t ldw, const void *src, int64_t M,

@@ -1,5 +1,6 @@
-// tvl_multi.hip -- several-vector GEMV (beam search with up to 8
-// hypotheses, Sec. 9.1): the weights are read once for all x vectors.
+// tvl_multi.hip -- several-vector GEMV (beam search with up to 16
+// hypotheses, Sec. 9.1): the weights are read once for all x vectors, on the
+// vector ALUs (up to 8 vectors) or on the matrix cores (up to 16).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -167,6 +168,364 @@ __global__ __launch_bounds__(WV *kWave) void k_item_multi(const DevItem it)
         tile_multi<float, R, WV, U, B>(it, row0);
 }
 
+// ------------------------------------------------------------ matrix cores
+// With several vectors the GEMV is a skinny dense contraction,
+// Y^T[M x nb] = W[M x K] X^T[K x nb], and the VALU form above spends its
+// issue slots on nb FMAs per weight.  The matrix cores take the products:
+// v_mfma_f32_4x4x1f32 (16 blocks) computes 16 independent 4 x 4 outer
+// products per instruction, in fp32 with fp32 accumulation.
+//
+// Operand layout of the 16-block 4x4x1 form (CDNA3/4 ISA): lane l = 4 b + q
+// supplies A_b[q][0] and B_b[0][q] and holds D_b[v][q] in element v of its
+// 4-float accumulator, for block b = l / 4.
+//
+// So the four lanes of a quad must hold four rows (and four vectors) at one
+// column.  Loading that layout directly has every quad touch four cache
+// lines, and the texture unit then spends four times the cycles per load;
+// instead every load here is the fully coalesced one of the VALU kernels
+// (lane l reads 16 bytes at column N l of ONE row: 1 KB per wavefront load),
+// four rows (or four vectors) are loaded, and a 4 x 4 transpose across each
+// quad (two DPP exchange steps) moves row q's 16 bytes at column N (4 b + s)
+// into register s of lane 4 b + q.  MFMA (s, e) then multiplies, in block b,
+// column N (4 b + s) + e of the rows by the same column of the vectors.  A
+// chunk is 64 N columns; per chunk and group of 4 rows that is 4 N MFMAs per
+// group of 4 vectors, and the 16 blocks are added across lanes at the end
+// (a fixed tree).
+//
+// Accumulation: every kFlush chunks the block accumulators are added into a
+// per-wavefront fp32 total in LDS and cleared (the totals stay out of the
+// register file, which bounds the loads a wavefront keeps in flight), so each
+// output sums at most 4 N kFlush products per block and window, then
+// K / (64 N kFlush) window totals, then a 16-way tree:
+// |error| <= (4 N kFlush + K / (64 N kFlush) + 6) * 2^-24 * sum_j |W_ij x_j|
+// to first order (2.9e-6 at K = 11008, fp32).
+constexpr int kFlush = 2;
+
+__device__ __forceinline__ f4 mfma4x4(float a, float b, f4 c)
+{
+    return __builtin_amdgcn_mfma_f32_4x4x1f32(a, b, c, 0, 0, 0);
+}
+
+// value of v in lane (lane ^ 1) / (lane ^ 2) of the same quad (DPP quad_perm)
+__device__ __forceinline__ float quad_xor1(float v)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1,
+                                                              0xF, 0xF, false));
+}
+__device__ __forceinline__ float quad_xor2(float v)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E,
+                                                              0xF, 0xF, false));
+}
+
+// 4 x 4 transpose across a quad, element by element: on return register s of
+// lane q holds what register q of lane s held (q = lane % 4).  Each step
+// swaps one bit of the register index with the same bit of the lane index:
+// the lane whose bit is set sends its lower register, the other its upper.
+__device__ __forceinline__ void quad_transpose(f4 (&v)[4], int lane)
+{
+    const bool q0 = (lane & 1) != 0, q1 = (lane & 2) != 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        // plain values (selecting between array elements would make the
+        // compiler address the array, i.e. put it in scratch memory)
+        float m0 = v[0][e], m1 = v[1][e], m2 = v[2][e], m3 = v[3][e];
+        // pairs (0, 1), (2, 3): lane bit 0
+        const float r01 = quad_xor1(q0 ? m0 : m1);
+        const float r23 = quad_xor1(q0 ? m2 : m3);
+        m0 = q0 ? r01 : m0;
+        m1 = q0 ? m1 : r01;
+        m2 = q0 ? r23 : m2;
+        m3 = q0 ? m3 : r23;
+        // pairs (0, 2), (1, 3): lane bit 1
+        const float r02 = quad_xor2(q1 ? m0 : m2);
+        const float r13 = quad_xor2(q1 ? m1 : m3);
+        v[0][e] = q1 ? r02 : m0;
+        v[2][e] = q1 ? m2 : r02;
+        v[1][e] = q1 ? r13 : m1;
+        v[3][e] = q1 ? m3 : r13;
+    }
+}
+
+// TT groups of 4 rows, P groups of 4 vectors.  A wavefront issues a whole
+// chunk (4 TT weight loads of 1 KB and 4 P NX x loads) before it transposes
+// and multiplies it.
+template <typename T, int TT, int P>
+struct MfmaRows {
+    using V = typename Vec<T>::type;
+    static constexpr int N = Vec<T>::N;  // columns per 16-byte weight load
+    static constexpr int CH = kWave * N; // columns per chunk
+    static constexpr int NX = N / 4;     // x float4 per lane per vector per chunk
+    const T *w0;     // the wavefront's first row, at this lane's column N l
+    const float *x0; // vector 0, at column N l
+    int64_t ldw, ldx;
+    int rmax, nb, kn, nfull, lane; // rmax: last row offset in range (rows past M re-read it)
+
+    __device__ __forceinline__ MfmaRows(const T *W, int64_t ldw_, int wrow0, int M,
+                                        const float *x, int64_t ldx_, int nb_, int K, int lane_)
+        : w0(W + (int64_t)wrow0 * ldw_ + N * lane_), x0(x + N * lane_), ldw(ldw_), ldx(ldx_),
+          rmax(M - 1 - wrow0), nb(nb_), kn(K), nfull(K / CH), lane(lane_)
+    {
+    }
+
+    // rows 4t .. 4t+3 (row r in register r) and vectors 4p .. 4p+3 (vector r
+    // in register r) of chunk c, columns past K masked to zero when RAGGED.
+    // An x float4 is read only when it starts before K, so it lies in a
+    // 16-byte block holding a valid element.
+    template <bool RAGGED>
+    __device__ __forceinline__ void load(int c, V (&w)[TT][4], f4 (&xv)[P][NX][4]) const
+    {
+        const int valid = kn - (c * CH + N * lane);
+#pragma unroll
+        for (int t = 0; t < TT; ++t)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const T *src = w0 + (int64_t)min(4 * t + r, rmax) * ldw + c * CH;
+                if constexpr (RAGGED)
+                    w[t][r] = valid > 0 ? mask_from<V, N>(load_w<T>(src), valid) : V{};
+                else
+                    w[t][r] = load_w<T>(src);
+            }
+        const f4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const bool on = 4 * p + r < nb; // wave-uniform
+                const float *src = x0 + (int64_t)(on ? 4 * p + r : 0) * ldx + c * CH;
+#pragma unroll
+                for (int h = 0; h < NX; ++h) {
+                    if constexpr (RAGGED)
+                        xv[p][h][r] = (on && valid > 4 * h)
+                                          ? mask_from<f4, 4>(load_x4(src + 4 * h), valid - 4 * h)
+                                          : z;
+                    else
+                        xv[p][h][r] = on ? load_x4(src + 4 * h) : z;
+                }
+            }
+    }
+
+    __device__ __forceinline__ void compute(V (&w)[TT][4], f4 (&xv)[P][NX][4],
+                                            f4 (&acc)[TT][P]) const
+    {
+#pragma unroll
+        for (int p = 0; p < P; ++p)
+#pragma unroll
+            for (int h = 0; h < NX; ++h)
+                quad_transpose(xv[p][h], lane);
+#pragma unroll
+        for (int t = 0; t < TT; ++t) {
+            // transpose the raw 16-byte weight pieces (fp16: two halves per
+            // dword move together; converted to fp32 per piece below)
+            f4 raw[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                raw[r] = __builtin_bit_cast(f4, w[t][r]);
+            quad_transpose(raw, lane);
+            f4 wf[NX][4];
+#pragma unroll
+            for (int sidx = 0; sidx < 4; ++sidx) {
+                if constexpr (N == 4) {
+                    wf[0][sidx] = raw[sidx];
+                } else {
+                    const f8 c8 = __builtin_convertvector(__builtin_bit_cast(V, raw[sidx]), f8);
+                    wf[0][sidx] = f4{c8[0], c8[1], c8[2], c8[3]}; // exact
+                    wf[1][sidx] = f4{c8[4], c8[5], c8[6], c8[7]};
+                }
+            }
+#pragma unroll
+            for (int p = 0; p < P; ++p)
+#pragma unroll
+                for (int sidx = 0; sidx < 4; ++sidx)
+#pragma unroll
+                    for (int h = 0; h < NX; ++h)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            acc[t][p] = mfma4x4(wf[h][sidx][e], xv[p][h][sidx][e], acc[t][p]);
+        }
+    }
+
+    template <bool RAGGED>
+    __device__ __forceinline__ void chunk(int c, f4 (&acc)[TT][P]) const
+    {
+        V w[TT][4];
+        f4 xv[P][NX][4];
+        load<RAGGED>(c, w, xv);
+        __builtin_amdgcn_sched_barrier(0); // the chunk's loads first
+        compute(w, xv, acc);
+        __builtin_amdgcn_sched_barrier(0); // the next chunk's loads stay below
+    }
+
+    // slot[(t * P + p) * 64]: this lane's LDS total of group (t, p)
+    __device__ __forceinline__ static void flush(f4 (&acc)[TT][P], f4 *slot)
+    {
+#pragma unroll
+        for (int t = 0; t < TT; ++t)
+#pragma unroll
+            for (int p = 0; p < P; ++p) {
+                slot[(t * P + p) * kWave] += acc[t][p];
+                acc[t][p] = f4{0.f, 0.f, 0.f, 0.f};
+            }
+    }
+
+    // on return tot[t][p] holds the group's block sums
+    __device__ __forceinline__ void run(f4 (&tot)[TT][P], f4 *slot) const
+    {
+        f4 acc[TT][P];
+#pragma unroll
+        for (int t = 0; t < TT; ++t)
+#pragma unroll
+            for (int p = 0; p < P; ++p) {
+                acc[t][p] = f4{0.f, 0.f, 0.f, 0.f};
+                slot[(t * P + p) * kWave] = acc[t][p];
+            }
+        int c = 0;
+        for (; c + kFlush <= nfull; c += kFlush) {
+#pragma unroll
+            for (int h = 0; h < kFlush; ++h)
+                chunk<false>(c + h, acc);
+            flush(acc, slot);
+        }
+        for (; c < nfull; ++c)
+            chunk<false>(c, acc);
+        if (c * CH < kn) // every lane reaches the DPP steps and the MFMAs
+            chunk<true>(c, acc);
+        // LDS totals + the last window, still in registers
+#pragma unroll
+        for (int t = 0; t < TT; ++t)
+#pragma unroll
+            for (int p = 0; p < P; ++p)
+                tot[t][p] = slot[(t * P + p) * kWave] + acc[t][p];
+    }
+};
+
+// One row tile of a several-vector item on the matrix cores: WV wavefronts
+// x TT groups of 4 rows, all nb <= 4 P vectors.  `slots`: this wavefront's
+// TT * P * 64 float4 of LDS.
+template <typename T, int TT, int P, int WV, int U>
+__device__ __forceinline__ void tile_mfma_p(const DevItem &it, int row0, f4 *slots)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wrow0 = row0 + wave * (4 * TT);
+    if (wrow0 >= it.M) return; // no barrier follows
+    const int nb = it.nrhs < 1 ? 1 : it.nrhs;
+    f4 tot[TT][P];
+    const MfmaRows<T, TT, P> mr(static_cast<const T *>(it.W), it.ldw, wrow0, it.M, it.x, it.ldx,
+                                   nb, it.K, lane);
+    mr.run(tot, slots + lane);
+    // add the 16 blocks: lane l = 4 b + j holds D_b[v][j] in element v; two
+    // exchange steps leave row v = (l >> 4) & 3 in each lane, two more sum
+    // the remaining 4 blocks, and lanes with b % 4 == 0 store
+    const int i = (lane >> 4) & 3, j = lane & 3;
+#pragma unroll
+    for (int t = 0; t < TT; ++t) {
+        const int row = wrow0 + 4 * t + i;
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+            float v[4] = {tot[t][p].x, tot[t][p].y, tot[t][p].z, tot[t][p].w};
+            halve<2, 32>(v, lane);
+            halve<1, 16>(v, lane);
+            v[0] += __shfl_xor(v[0], 8);
+            v[0] += __shfl_xor(v[0], 4);
+            if ((lane & 12) == 0 && row < it.M && 4 * p + j < nb)
+                it.y[(int64_t)(4 * p + j) * it.ldy + row] = v[0];
+        }
+    }
+}
+
+// Weight dtypes a matrix-core launch holds: fp32 only, fp16 only, or both
+// (a mixed launch pays the registers of both paths).
+constexpr int kWF32 = 0, kWF16 = 1, kWMixed = 2;
+
+template <int WM, int TT, int P, int WV, int U>
+__device__ __forceinline__ void tile_mfma(const DevItem &it, int row0, f4 *slots)
+{
+    if constexpr (WM == kWF32)
+        tile_mfma_p<float, TT, P, WV, U>(it, row0, slots);
+    else if constexpr (WM == kWF16)
+        tile_mfma_p<_Float16, TT, P, WV, U>(it, row0, slots);
+    else if (it.dtype == 1)
+        tile_mfma_p<_Float16, TT, P, WV, U>(it, row0, slots);
+    else
+        tile_mfma_p<float, TT, P, WV, U>(it, row0, slots);
+}
+
+// P groups of 4 vectors: chosen per launch from the largest nrhs (registers
+// grow with P, so a launch holds only the groups it needs)
+template <int WM, int TT, int P, int WV, int U>
+__global__ __launch_bounds__(WV *kWave) void k_sweep_mfma(const DevItem *__restrict__ items,
+                                                           const DevTile *__restrict__ tiles,
+                                                           int ntiles)
+{
+    __shared__ f4 lds[WV * TT * P * kWave];
+    f4 *slots = lds + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave) * (TT * P * kWave);
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const DevTile tl = tiles[t];
+        const DevItem it = items[tl.item];
+        tile_mfma<WM, TT, P, WV, U>(it, tl.row0, slots);
+        __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
+    }
+}
+
+template <int WM, int TT, int P, int WV, int U>
+__global__ __launch_bounds__(WV *kWave) void k_item_mfma(const DevItem it)
+{
+    __shared__ f4 lds[WV * TT * P * kWave];
+    f4 *slots = lds + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave) * (TT * P * kWave);
+    tile_mfma<WM, TT, P, WV, U>(it, (int)blockIdx.x * (4 * TT * WV), slots);
+}
+
+// (rows per wavefront = 4 TT in {8, 16}, waves per block, U = 1: one chunk
+// of 64 N columns in flight) of the matrix-core form; any number of vectors
+// up to 16.
+#define TVL_MFMA_SHAPES(X) X(8, 1, 1) X(8, 4, 1) X(16, 1, 1) X(16, 2, 1) X(16, 4, 1)
+
+template <int R, int WV, int U>
+struct InstMfma {
+    template <int WM, int P>
+    static hipError_t sweep_p(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
+                              hipStream_t st)
+    {
+        hipLaunchKernelGGL((k_sweep_mfma<WM, R / 4, P, WV, U>), dim3(grid), dim3(WV * kWave), 0,
+                           st, items, tiles, ntiles);
+        return hipGetLastError();
+    }
+    template <int WM>
+    static hipError_t sweep_w(int B, const DevItem *items, const DevTile *tiles, int ntiles,
+                              int grid, hipStream_t st)
+    {
+        return B <= 4   ? sweep_p<WM, 1>(items, tiles, ntiles, grid, st)
+               : B <= 8 ? sweep_p<WM, 2>(items, tiles, ntiles, grid, st)
+                        : sweep_p<WM, 4>(items, tiles, ntiles, grid, st);
+    }
+    // B: the launch's vector bound (2, 4, 8 or 16) -> P = ceil(B / 4);
+    // wm: the weight dtypes the launch holds
+    static hipError_t sweep(int B, int wm, const DevItem *items, const DevTile *tiles, int ntiles,
+                            int grid, hipStream_t st)
+    {
+        return wm == kWF32   ? sweep_w<kWF32>(B, items, tiles, ntiles, grid, st)
+               : wm == kWF16 ? sweep_w<kWF16>(B, items, tiles, ntiles, grid, st)
+                             : sweep_w<kWMixed>(B, items, tiles, ntiles, grid, st);
+    }
+    template <int WM, int P>
+    static hipError_t item_p(const DevItem &it, hipStream_t st)
+    {
+        const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
+        hipLaunchKernelGGL((k_item_mfma<WM, R / 4, P, WV, U>), grid, block, 0, st, it);
+        return hipGetLastError();
+    }
+    template <int WM>
+    static hipError_t item_w(int B, const DevItem &it, hipStream_t st)
+    {
+        return B <= 4 ? item_p<WM, 1>(it, st) : B <= 8 ? item_p<WM, 2>(it, st) : item_p<WM, 4>(it, st);
+    }
+    static hipError_t item(int B, const DevItem &it, hipStream_t st)
+    {
+        return it.dtype == 1 ? item_w<kWF16>(B, it, st) : item_w<kWF32>(B, it, st);
+    }
+};
+
 // (R, waves per block, U, B) with B x vectors per launch (B >= nrhs).
 #define TVL_MULTI_SHAPES(X)                                                                       \
     X(2, 4, 2, 2) X(2, 4, 4, 2) X(4, 4, 2, 2) X(2, 4, 1, 4) X(2, 4, 2, 4) X(4, 4, 1, 4)          \
@@ -195,19 +554,28 @@ bool multi_shape_supported(const Shape &s, int B)
 {
 #define X(R_, W_, U_, B_)                                                                         \
     if (s.R == R_ && s.W == W_ && s.U == U_ && B == B_) return s.xmode == kXDirect;
+#define Y(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return s.xmode == kXDirect && B <= 16;
     TVL_MULTI_SHAPES(X)
+    TVL_MFMA_SHAPES(Y)
 #undef X
+#undef Y
     return false;
 }
 
-hipError_t launch_sweep_multi(const Shape &s, int B, const DevItem *items, const DevTile *tiles,
-                              int ntiles, int grid, hipStream_t st)
+hipError_t launch_sweep_multi(const Shape &s, int B, int wmode, const DevItem *items,
+                              const DevTile *tiles, int ntiles, int grid, hipStream_t st)
 {
 #define X(R_, W_, U_, B_)                                                                         \
     if (s.R == R_ && s.W == W_ && s.U == U_ && B == B_)                                          \
         return InstMulti<R_, W_, U_, B_>::sweep(items, tiles, ntiles, grid, st);
+#define Y(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return InstMfma<R_, W_, U_>::sweep(B, wmode, items, tiles, ntiles, grid, st);
     TVL_MULTI_SHAPES(X)
+    TVL_MFMA_SHAPES(Y)
 #undef X
+#undef Y
     return hipErrorInvalidValue;
 }
 
@@ -216,8 +584,12 @@ hipError_t launch_item_multi(const Shape &s, int B, const DevItem &item, hipStre
 #define X(R_, W_, U_, B_)                                                                         \
     if (s.R == R_ && s.W == W_ && s.U == U_ && B == B_)                                          \
         return InstMulti<R_, W_, U_, B_>::item(item, st);
+#define Y(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfma<R_, W_, U_>::item(B, item, st);
     TVL_MULTI_SHAPES(X)
+    TVL_MFMA_SHAPES(Y)
 #undef X
+#undef Y
     return hipErrorInvalidValue;
 }
 

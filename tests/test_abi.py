@@ -68,7 +68,7 @@ D = 4 << 40  # another fake, far-away device address (g, W3)
     (dict(W3=D), ARG), (dict(g=D + 4), ALIGN), (dict(g=D, eps=-1.0), ARG),
     (dict(g=D, eps=float("nan")), ARG), (dict(g=D, eps=float("inf")), ARG),
     (dict(op=1, W3=D, y=D + 128), ALIAS), (dict(g=D, eps=1e-5, y=D + 1024), ALIAS),
-    (dict(nrhs=9, ldx=768, ldy=768), ARG), (dict(nrhs=-1), ARG),
+    (dict(nrhs=17, ldx=768, ldy=768), ARG), (dict(nrhs=-1), ARG),
     (dict(nrhs=2, ldx=767, ldy=768), SHAPE), (dict(nrhs=2, ldx=768, ldy=700), SHAPE),
     (dict(nrhs=2, ldx=770, ldy=768), ALIGN), (dict(nrhs=2, ldx=768, ldy=768, g=D), ARG),
     (dict(nrhs=2, ldx=768, ldy=768, op=1, W3=D), ARG),
@@ -81,6 +81,16 @@ def test_fused_item_rejects(kw, st):
     assert L.tvl_gemv_item(ctypes.byref(it), None, None) == st
     arr, n = tvl.make_items([it])
     assert L.tvl_gemv_batch_sweep(arr, n, None) == st
+
+
+@pytest.mark.parametrize("nrhs", list(range(2, 17)))
+def test_multi_item_default_shape_exists(nrhs):
+    """Every vector count has a default several-vector kernel: validation
+    passes and the call only fails at the device query of a GPU-less host."""
+    it = tvl.item(A, 768, B, C, 768, 768, 0, nrhs=nrhs, ldx=768, ldy=768)
+    assert L.tvl_gemv_item(ctypes.byref(it), None, None) == HIP
+    arr, n = tvl.make_items([it])
+    assert L.tvl_gemv_batch_sweep(arr, n, None) == HIP
 
 
 def test_fused_item_needs_direct_shape():

@@ -24,6 +24,8 @@ TOL = {0: 1e-5, 1: 2e-3}
 DEV = "cuda"
 MULTI = [(2, 4, 2, 2), (2, 4, 4, 2), (4, 4, 2, 2), (2, 4, 1, 4), (2, 4, 2, 4), (4, 4, 1, 4),
          (4, 4, 2, 4), (2, 4, 1, 8), (2, 4, 2, 8), (4, 4, 1, 8)]
+# matrix-core form: (rows per wavefront = 8 or 16, waves per block, unroll), any nrhs <= 16
+MFMA = [(8, 1, 1), (8, 4, 1), (16, 1, 1), (16, 2, 1), (16, 4, 1)]
 
 
 def tunings(nrhs):
@@ -31,6 +33,8 @@ def tunings(nrhs):
     for r, w, u, b in MULTI:
         if b >= nrhs and (b == 2 or b // 2 < nrhs):  # the kernels the library would pick from
             out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
+    for r, w, u in MFMA:
+        out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
     return out
 
 
@@ -65,7 +69,7 @@ SHAPES = [(1, 1), (3, 17), (64, 63), (65, 65), (257, 255), (1000, 1000), (33, 40
           (130, 11008), (5, 28672), (2048, 768)]
 
 
-@pytest.mark.parametrize("nrhs", [2, 3, 4, 5, 8])
+@pytest.mark.parametrize("nrhs", [2, 3, 4, 5, 8, 11, 16])
 @pytest.mark.parametrize("dt", [0, 1], ids=["f32", "f16"])
 @pytest.mark.parametrize("M,K", SHAPES, ids=[f"{m}x{k}" for m, k in SHAPES])
 def test_multi_vectors(M, K, dt, nrhs):
@@ -102,7 +106,9 @@ def test_beam4_sweep110m():
     wl = synth.WORKLOADS["sweep110m"]
     ms = sdev.load_multi(wl, 4, DEV)
     for t in (None, dict(rows_per_wave=2, waves_per_block=4, unroll=2, flags=2),
-              dict(rows_per_wave=4, waves_per_block=4, unroll=1, flags=2, grid=500)):
+              dict(rows_per_wave=4, waves_per_block=4, unroll=1, flags=2, grid=500),
+              dict(rows_per_wave=8, waves_per_block=4, unroll=1, flags=2),
+              dict(rows_per_wave=16, waves_per_block=1, unroll=1, flags=2, grid=700)):
         for d in ms:
             d.Y.fill_(float("nan"))
         plan = tvl.tvl_sweep_plan_create([d.item() for d in ms], t)
