@@ -143,9 +143,10 @@ def measured_traffic(workload: str):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(samples, seconds: float, what: str) -> dict:
+def cpu_baseline(samples, seconds: float, what: str, threads: int = 1) -> dict:
     """The oracle as it stands (single-threaded naive double GEMV), cycling over
-    (spec, W, x) samples of the workload for about ``seconds`` of CPU time."""
+    (spec, W, x) samples of the workload for about ``seconds`` of CPU time; with
+    ``threads`` > 1 also the same calls on that many host threads at once."""
     import oracle
     import synth
     t0 = time.perf_counter()
@@ -159,10 +160,61 @@ def cpu_baseline(samples, seconds: float, what: str) -> dict:
         if el >= seconds:
             break
     gbs = nbytes / el / 1e9
-    return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{ngemv} GEMVs of {what} ({nbytes / 1e9:.2f} GB algorithmic) in "
-                      f"{el:.1f} s on one host thread "
-                      f"({platform.processor() or platform.machine()})"}
+    out = {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+           "sample": f"{ngemv} GEMVs of {what} ({nbytes / 1e9:.2f} GB algorithmic) in "
+                     f"{el:.1f} s on one host thread "
+                     f"({platform.processor() or platform.machine()})"}
+    if threads > 1:
+        out["all_cores"] = cpu_baseline_threads(samples, seconds / 2, what, threads)
+    return out
+
+
+def host_threads() -> int:
+    """Host threads for the all-cores leg: the CPUs this process may run on,
+    capped by OMP_NUM_THREADS when set (a GPU machine's share of its host)."""
+    n = len(os.sched_getaffinity(0))
+    omp = os.environ.get("OMP_NUM_THREADS", "")
+    return min(n, int(omp)) if omp.isdigit() and int(omp) > 0 else n
+
+
+def cpu_baseline_threads(samples, seconds: float, what: str, threads: int) -> dict:
+    """The same oracle calls on `threads` host threads at once, each taking
+    whole GEMVs of the sample in turn (ctypes releases the GIL during a call,
+    so the GEMVs run in parallel; the per-row arithmetic is unchanged)."""
+    import itertools
+    import threading
+    import oracle
+    import synth
+    nxt = itertools.count()
+    done = [0] * threads
+    t0 = time.perf_counter()
+
+    def worker(t):
+        while time.perf_counter() - t0 < seconds:
+            m, W, x = samples[next(nxt) % len(samples)]
+            oracle_gemv(oracle, synth, m, W, x)
+            done[t] += m.algo_bytes()
+
+    ts = [threading.Thread(target=worker, args=(t,)) for t in range(threads)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    el = time.perf_counter() - t0
+    return {"value": round(sum(done) / el / 1e9, 4), "unit": "GB/s", "cores": threads,
+            "sample": f"GEMVs of {what} on {threads} host threads, whole GEMVs per thread, "
+                      f"{sum(done) / 1e9:.2f} GB algorithmic in {el:.1f} s"}
+
+
+def emit(out: dict) -> None:
+    """Print the JSON line, with the device it was measured on."""
+    import torch
+    p = torch.cuda.get_device_properties(0)
+    out["device"] = {"name": p.name, "arch": getattr(p, "gcnArchName", ""),
+                     "compute_units": p.multi_processor_count,
+                     "hbm_GiB": round(p.total_memory / 2**30, 1),
+                     "hip_runtime": torch.version.hip}
+    print(json.dumps(out), flush=True)
 
 
 def main() -> int:
@@ -390,11 +442,12 @@ def main() -> int:
                                 "(whole decode step, not this GEMV sweep alone)")
     if not args.no_cpu_baseline:
         log("timing the CPU oracle baseline")
-        out["cpu_baseline"] = cpu_baseline(cpu_samples, args.cpu_seconds, wl.name)
+        out["cpu_baseline"] = cpu_baseline(cpu_samples, args.cpu_seconds, wl.name,
+                                           host_threads())
     if not single:
         for p in plans:
             p.destroy()
-    print(json.dumps(out), flush=True)
+    emit(out)
     return 0
 
 
@@ -489,7 +542,7 @@ def run_beam(args, tvl, torch, np, oracle, synth, sdev) -> int:
         out["cpu_baseline"] = cpu_baseline(samples, args.cpu_seconds, "sweep110m (per vector)")
     for p in plans:
         p.destroy()
-    print(json.dumps(out), flush=True)
+    emit(out)
     return 0
 
 
@@ -598,7 +651,7 @@ def run_fused(args, tvl, torch, np, oracle, synth, sdev) -> int:
                       f"host thread"}
     for p in plans:
         p.destroy()
-    print(json.dumps(out), flush=True)
+    emit(out)
     return 0
 
 

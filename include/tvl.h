@@ -154,7 +154,8 @@ typedef struct tvl_item {
 } tvl_item;
 
 /* Launch shape override.  A zero field means "choose by shape".
- *   rows_per_wave   R in {1, 2, 4, 8, 16}: rows one wavefront computes at once
+ *   rows_per_wave   R in {1, 2, 4, 8, 16, 32, 64}: rows one wavefront computes
+ *                   at once (32 and 64: several-vector launches only)
  *   waves_per_block W in {1, 2, 4, 8}: wavefronts per workgroup
  *   unroll          U in {1, 2, 3, 4, 8}: 16-byte weight loads per row kept in
  *                   flight per lane
@@ -179,8 +180,10 @@ typedef struct tvl_item {
  * (nrhs <= 2, <= 4, <= 8) on the vector ALUs:
  *   2: (2,4,2) (2,4,4) (4,4,2);  4: (2,4,1) (2,4,2) (4,4,1) (4,4,2);
  *   8: (2,4,1) (2,4,2) (4,4,1)
- * and, for any nrhs <= 16, on the matrix cores (R = 8 or 16 rows per
- * wavefront in groups of 4): (8,1,1) (8,4,1) (16,1,1) (16,2,1) (16,4,1)
+ * and, for any nrhs <= 16, on the matrix cores: the 4x4x1 form (rows in
+ * groups of 4, U = 1) (8,4,1) (16,1,1) (16,2,1), and the 16x16x4 form (rows
+ * in groups of 16, U = loads per group in flight) (16,4,8) (32,1,4) (32,2,4)
+ * (64,1,4)
  * Launches holding block-quantised items (direct-x only; R rows per group of
  * lanes, see tvl_dtype): (2,4,2) (4,4,1) (4,4,2) (4,1,2) (8,4,1) (8,2,1) */
 typedef struct tvl_tuning {

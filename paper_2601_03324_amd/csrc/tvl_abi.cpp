@@ -270,12 +270,14 @@ int multi_B(int n) { return n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16; }
 // 110M decode token.  Up to 4 vectors the VALU form wins: more rows per
 // wavefront amortise each x read over more weights (R = 4), and fewer loads
 // in flight keep the R x B accumulators in registers.  From 5 vectors on,
-// the FMAs would take ~half the VALU issue slots and the matrix-core form
-// wins (8 vectors: 4.58 TB/s vs 4.07 TB/s; 16 vectors: 8 rows and one
-// wavefront per block, 2.93 TB/s, against 2.51-2.79 TB/s for the others).
+// the FMAs would take ~half the VALU issue slots and the matrix cores win:
+// at 8 vectors the 4 x 4 x 1 form with 16 rows per wavefront (4.70 TB/s
+// against 4.07 on the VALU and 3.84 for the 16 x 16 x 4 form), at 16
+// vectors the 16 x 16 x 4 form with 32 rows and one wavefront per block
+// (3.61 TB/s against 3.14 for the 4 x 4 x 1 form).
 Shape default_multi_shape(int B)
 {
-    if (B > 8) return Shape{8, 1, 1, tvl::kXDirect};
+    if (B > 8) return Shape{32, 1, 4, tvl::kXDirect};
     if (B > 4) return Shape{16, 2, 1, tvl::kXDirect};
     return B == 2 ? Shape{4, 4, 2, tvl::kXDirect} : Shape{4, 4, 1, tvl::kXDirect};
 }
@@ -417,7 +419,8 @@ tvl_status pick_shape(const tvl_tuning *t, Shape def, Shape *out, bool plain = t
         }
         if (t->rows_per_wave && !t->unroll) {
             // keep about 16 KB of weights in flight per wavefront by default
-            s.U = s.R >= 4 ? 2 : s.R == 2 ? 4 : 8;
+            // (R >= 32: the 16 x 16 x 4 several-vector form, 4 loads per group)
+            s.U = s.R >= 32 ? 4 : s.R >= 4 ? 2 : s.R == 2 ? 4 : 8;
         }
     }
     if (plain && !tvl::shape_supported(s))

@@ -479,7 +479,7 @@ __global__ __launch_bounds__(WV *kWave) void k_item_mfma(const DevItem it)
 // (rows per wavefront = 4 TT in {8, 16}, waves per block, U = 1: one chunk
 // of 64 N columns in flight) of the matrix-core form; any number of vectors
 // up to 16.
-#define TVL_MFMA_SHAPES(X) X(8, 1, 1) X(8, 4, 1) X(16, 1, 1) X(16, 2, 1) X(16, 4, 1)
+#define TVL_MFMA_SHAPES(X) X(8, 4, 1) X(16, 1, 1) X(16, 2, 1)
 
 template <int R, int WV, int U>
 struct InstMfma {
@@ -526,6 +526,245 @@ struct InstMfma {
     }
 };
 
+// ------------------------------------------------ matrix cores, 16 x 16 x 4
+// v_mfma_f32_16x16x4f32: D[16 x 16] += A[16 x 4] B[4 x 16], fp32 inputs and
+// accumulation.  Lane l = 16 g + i supplies A[i][g] and B[g][i] and holds
+// D[4 g + v][i] in element v of its accumulator (checked on gfx950).
+//
+// A is 16 rows of W and B holds up to 16 x vectors (vector j in column j),
+// so each lane loads 16 bytes of row i: 16-byte block g of a 64-byte row
+// segment.  One wavefront load then covers 16 rows x 64 bytes (N columns
+// per lane: 4 fp32 or 8 fp16), and its e-th MFMA multiplies column
+// 4 N q + N g + e of the 16 rows by the same column of the 16 vectors.
+// The loads feed the matrix cores as they arrive: no lane exchange, and
+// only the loaded registers in flight (62-144 VGPRs against 146-256 for the
+// 4 x 4 x 1 form).  The price: such a load touches 16 half lines rather than
+// 8 whole ones (the other half comes with the next load of the same batch).
+// HBM bytes stay within 4 % of the whole-line form, but the L1 receives 1.7x
+// the requests and the address unit stalls on it (rocprofv3 on MI355X), so
+// this form tops out near 3.8 TB/s whatever the vector count.  It is the
+// faster form from 9 to 16 vectors, where the 4 x 4 x 1 form runs out of
+// registers; up to 8 vectors the 4 x 4 x 1 form is faster.
+//
+// The x loads (vector i, columns as for the weights) hit the cache: every
+// wavefront of a matrix reads the same vectors; RG groups of 16 rows share
+// each x load.  Vectors past nb re-read vector nb - 1, rows past M the last
+// row; those results are dropped.
+//
+// Accumulation: the MFMAs of one batch (Q loads per row group) chain into
+// one accumulator, which is then added into a first-level total and cleared;
+// every kMfmaLevel batches the first-level total is added into a second.
+// Each output therefore sums at most Q N MFMA steps of 4 products, then
+// kMfmaLevel batch sums, then K / (kMfmaLevel 4 N Q) totals:
+// |error| <= (Q N + 4 + kMfmaLevel + K / (kMfmaLevel 4 N Q) + 1) 2^-24
+// sum_j |W_ij x_j| to first order (3.5e-6 at K = 11008, fp32, Q = 8).
+constexpr int kMfmaLevel = 16;
+
+__device__ __forceinline__ f4 mfma16(float a, float b, f4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+template <typename T, int RG, int Q>
+struct Mfma16Rows {
+    using V = typename Vec<T>::type;
+    static constexpr int N = Vec<T>::N; // columns per lane per load
+    static constexpr int CL = 4 * N;    // columns per wavefront load
+    static constexpr int CB = Q * CL;   // columns per batch
+    const T *w[RG];  // row 16 rg + i of the wavefront, at column N g
+    const float *xv; // vector i (clamped), at column N g
+    int kn, g;
+
+    __device__ __forceinline__ Mfma16Rows(const T *W, int64_t ldw, int wrow0, int M,
+                                          const float *x, int64_t ldx, int nb, int K, int lane)
+        : kn(K), g(lane >> 4)
+    {
+        const int i = lane & 15;
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+            w[rg] = W + (int64_t)min(wrow0 + 16 * rg + i, M - 1) * ldw + N * g;
+        xv = x + (int64_t)min(i, nb - 1) * ldx + N * g;
+    }
+
+    // one batch: columns [c0, c0 + CB); when RAGGED, columns past K are
+    // masked to zero (a 16-byte piece is loaded only when it starts before
+    // K, so it lies in the row's padded extent and in an x block holding a
+    // valid element)
+    template <bool RAGGED>
+    __device__ __forceinline__ void batch(int c0, f4 (&acc)[RG]) const
+    {
+        V wv[Q][RG];
+        f4 xa[Q], xb[Q];
+        const f4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int c = c0 + CL * q;
+            const int valid = kn - (c + N * g);
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg) {
+                if constexpr (RAGGED)
+                    wv[q][rg] = valid > 0 ? mask_from<V, N>(load_w<T>(w[rg] + c), valid) : V{};
+                else
+                    wv[q][rg] = load_w<T>(w[rg] + c);
+            }
+            if constexpr (RAGGED) {
+                xa[q] = valid > 0 ? mask_from<f4, 4>(load_x4(xv + c), valid) : z;
+                xb[q] = (N == 8 && valid > 4) ? mask_from<f4, 4>(load_x4(xv + c + 4), valid - 4)
+                                              : z;
+            } else {
+                xa[q] = load_x4(xv + c);
+                xb[q] = (N == 8) ? load_x4(xv + c + 4) : z;
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0); // the batch's loads first
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg) {
+                if constexpr (N == 4) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        acc[rg] = mfma16(wv[q][rg][e], xa[q][e], acc[rg]);
+                } else {
+                    const f8 wf = __builtin_convertvector(wv[q][rg], f8); // exact
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        acc[rg] = mfma16(wf[e], xa[q][e], acc[rg]);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        acc[rg] = mfma16(wf[4 + e], xb[q][e], acc[rg]);
+                }
+            }
+        __builtin_amdgcn_sched_barrier(0); // the next batch's loads stay below
+    }
+
+    // on return out[rg] holds D of row group rg
+    __device__ __forceinline__ void run(f4 (&out)[RG]) const
+    {
+        const f4 z = {0.f, 0.f, 0.f, 0.f};
+        f4 acc[RG], t1[RG], t2[RG];
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+            acc[rg] = t1[rg] = t2[rg] = z;
+        int c0 = 0, n1 = 0;
+        for (; c0 + CB <= kn; c0 += CB) {
+            batch<false>(c0, acc);
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg) {
+                t1[rg] += acc[rg];
+                acc[rg] = z;
+            }
+            if (++n1 == kMfmaLevel) {
+#pragma unroll
+                for (int rg = 0; rg < RG; ++rg) {
+                    t2[rg] += t1[rg];
+                    t1[rg] = z;
+                }
+                n1 = 0;
+            }
+        }
+        if (c0 < kn) // every lane reaches the MFMAs
+            batch<true>(c0, acc);
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+            out[rg] = t2[rg] + (t1[rg] + acc[rg]);
+    }
+};
+
+// One row tile of a several-vector item: WV wavefronts x RG groups of 16
+// rows, all nb <= 16 vectors.
+template <typename T, int RG, int Q, int WV>
+__device__ __forceinline__ void tile_mfma16(const DevItem &it, int row0)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wrow0 = row0 + wave * (16 * RG);
+    if (wrow0 >= it.M) return;
+    const int nb = it.nrhs < 1 ? 1 : it.nrhs;
+    f4 out[RG];
+    const Mfma16Rows<T, RG, Q> mr(static_cast<const T *>(it.W), it.ldw, wrow0, it.M, it.x,
+                                  it.ldx, nb, it.K, lane);
+    mr.run(out);
+    // D[4 g + v][i]: row wrow0 + 16 rg + 4 g + v, vector i
+    const int i = lane & 15, g = lane >> 4;
+    if (i < nb) {
+        float *yv = it.y + (int64_t)i * it.ldy;
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = wrow0 + 16 * rg + 4 * g + v;
+                if (row < it.M) yv[row] = out[rg][v];
+            }
+    }
+}
+
+template <int WM, int RG, int Q, int WV>
+__device__ __forceinline__ void tile_mfma16_w(const DevItem &it, int row0)
+{
+    if constexpr (WM == kWF32)
+        tile_mfma16<float, RG, Q, WV>(it, row0);
+    else if constexpr (WM == kWF16)
+        tile_mfma16<_Float16, RG, Q, WV>(it, row0);
+    else if (it.dtype == 1)
+        tile_mfma16<_Float16, RG, Q, WV>(it, row0);
+    else
+        tile_mfma16<float, RG, Q, WV>(it, row0);
+}
+
+template <int WM, int RG, int Q, int WV>
+__global__ __launch_bounds__(WV *kWave) void k_sweep_mfma16(const DevItem *__restrict__ items,
+                                                             const DevTile *__restrict__ tiles,
+                                                             int ntiles)
+{
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const DevTile tl = tiles[t];
+        const DevItem it = items[tl.item];
+        tile_mfma16_w<WM, RG, Q, WV>(it, tl.row0);
+        __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
+    }
+}
+
+template <int WM, int RG, int Q, int WV>
+__global__ __launch_bounds__(WV *kWave) void k_item_mfma16(const DevItem it)
+{
+    tile_mfma16_w<WM, RG, Q, WV>(it, (int)blockIdx.x * (16 * RG * WV));
+}
+
+// (rows per wavefront = 16 RG, waves per block, Q = loads per row group in
+// flight) of the 16 x 16 x 4 form; any number of vectors up to 16.  Q >= 4
+// keeps these apart from the 4 x 4 x 1 shapes (U = 1).
+#define TVL_MFMA16_SHAPES(X) X(16, 4, 8) X(32, 1, 4) X(32, 2, 4) X(64, 1, 4)
+
+template <int R, int WV, int Q>
+struct InstMfma16 {
+    static constexpr int RG = R / 16;
+    template <int WM>
+    static hipError_t sweep_w(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
+                              hipStream_t st)
+    {
+        hipLaunchKernelGGL((k_sweep_mfma16<WM, RG, Q, WV>), dim3(grid), dim3(WV * kWave), 0, st,
+                           items, tiles, ntiles);
+        return hipGetLastError();
+    }
+    static hipError_t sweep(int wm, const DevItem *items, const DevTile *tiles, int ntiles,
+                            int grid, hipStream_t st)
+    {
+        return wm == kWF32   ? sweep_w<kWF32>(items, tiles, ntiles, grid, st)
+               : wm == kWF16 ? sweep_w<kWF16>(items, tiles, ntiles, grid, st)
+                             : sweep_w<kWMixed>(items, tiles, ntiles, grid, st);
+    }
+    static hipError_t item(const DevItem &it, hipStream_t st)
+    {
+        const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
+        if (it.dtype == 1)
+            hipLaunchKernelGGL((k_item_mfma16<kWF16, RG, Q, WV>), grid, block, 0, st, it);
+        else
+            hipLaunchKernelGGL((k_item_mfma16<kWF32, RG, Q, WV>), grid, block, 0, st, it);
+        return hipGetLastError();
+    }
+};
+
 // (R, waves per block, U, B) with B x vectors per launch (B >= nrhs).
 #define TVL_MULTI_SHAPES(X)                                                                       \
     X(2, 4, 2, 2) X(2, 4, 4, 2) X(4, 4, 2, 2) X(2, 4, 1, 4) X(2, 4, 2, 4) X(4, 4, 1, 4)          \
@@ -558,6 +797,7 @@ bool multi_shape_supported(const Shape &s, int B)
     if (s.R == R_ && s.W == W_ && s.U == U_) return s.xmode == kXDirect && B <= 16;
     TVL_MULTI_SHAPES(X)
     TVL_MFMA_SHAPES(Y)
+    TVL_MFMA16_SHAPES(Y)
 #undef X
 #undef Y
     return false;
@@ -572,10 +812,15 @@ hipError_t launch_sweep_multi(const Shape &s, int B, int wmode, const DevItem *i
 #define Y(R_, W_, U_)                                                                             \
     if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
         return InstMfma<R_, W_, U_>::sweep(B, wmode, items, tiles, ntiles, grid, st);
+#define Z(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return InstMfma16<R_, W_, U_>::sweep(wmode, items, tiles, ntiles, grid, st);
     TVL_MULTI_SHAPES(X)
     TVL_MFMA_SHAPES(Y)
+    TVL_MFMA16_SHAPES(Z)
 #undef X
 #undef Y
+#undef Z
     return hipErrorInvalidValue;
 }
 
@@ -586,10 +831,14 @@ hipError_t launch_item_multi(const Shape &s, int B, const DevItem &item, hipStre
         return InstMulti<R_, W_, U_, B_>::item(item, st);
 #define Y(R_, W_, U_)                                                                             \
     if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfma<R_, W_, U_>::item(B, item, st);
+#define Z(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfma16<R_, W_, U_>::item(item, st);
     TVL_MULTI_SHAPES(X)
     TVL_MFMA_SHAPES(Y)
+    TVL_MFMA16_SHAPES(Z)
 #undef X
 #undef Y
+#undef Z
     return hipErrorInvalidValue;
 }
 

@@ -24,8 +24,11 @@ TOL = {0: 1e-5, 1: 2e-3}
 DEV = "cuda"
 MULTI = [(2, 4, 2, 2), (2, 4, 4, 2), (4, 4, 2, 2), (2, 4, 1, 4), (2, 4, 2, 4), (4, 4, 1, 4),
          (4, 4, 2, 4), (2, 4, 1, 8), (2, 4, 2, 8), (4, 4, 1, 8)]
-# matrix-core form: (rows per wavefront = 8 or 16, waves per block, unroll), any nrhs <= 16
-MFMA = [(8, 1, 1), (8, 4, 1), (16, 1, 1), (16, 2, 1), (16, 4, 1)]
+# matrix-core forms, any nrhs <= 16: 4x4x1 (rows per wavefront 8 or 16, waves
+# per block, unroll 1) and 16x16x4 (16 x row groups, waves per block, loads
+# per row group in flight >= 4)
+MFMA = [(8, 4, 1), (16, 1, 1), (16, 2, 1)]
+MFMA16 = [(16, 4, 8), (32, 1, 4), (32, 2, 4), (64, 1, 4)]
 
 
 def tunings(nrhs):
@@ -33,7 +36,7 @@ def tunings(nrhs):
     for r, w, u, b in MULTI:
         if b >= nrhs and (b == 2 or b // 2 < nrhs):  # the kernels the library would pick from
             out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
-    for r, w, u in MFMA:
+    for r, w, u in MFMA + MFMA16:
         out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
     return out
 
@@ -108,7 +111,9 @@ def test_beam4_sweep110m():
     for t in (None, dict(rows_per_wave=2, waves_per_block=4, unroll=2, flags=2),
               dict(rows_per_wave=4, waves_per_block=4, unroll=1, flags=2, grid=500),
               dict(rows_per_wave=8, waves_per_block=4, unroll=1, flags=2),
-              dict(rows_per_wave=16, waves_per_block=1, unroll=1, flags=2, grid=700)):
+              dict(rows_per_wave=16, waves_per_block=2, unroll=1, flags=2, grid=700),
+              dict(rows_per_wave=32, waves_per_block=2, unroll=4, flags=2),
+              dict(rows_per_wave=64, waves_per_block=1, unroll=4, flags=2, grid=300)):
         for d in ms:
             d.Y.fill_(float("nan"))
         plan = tvl.tvl_sweep_plan_create([d.item() for d in ms], t)
@@ -129,4 +134,40 @@ def test_beam4_sweep110m():
                     yb = Y[b]
                 r = oracle.check(yb, ref, S, 1e-5)
                 assert r["bad"] == 0, (m.name, b, t, r)
+        plan.destroy()
+
+
+def test_multi_plan_mixed_dtypes():
+    """One plan holding fp32 and fp16 several-vector items with different
+    vector counts (the mixed-dtype kernels), every output against the oracle."""
+    rng = np.random.default_rng(4242)
+    specs = [(300, 1000, 0, 5), (130, 2050, 1, 11), (77, 768, 0, 16), (1, 33, 1, 2)]
+    host, items, keep = [], [], []
+    for M, K, dt, nb in specs:
+        Wf = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+        W = Wf if dt == 0 else synth.f32_to_f16_bits(Wf)
+        X = rng.standard_normal((nb, K)).astype(np.float32)
+        buf, ldw = dev_matrix(W, dt)
+        ldx = (K + 3) // 4 * 4
+        Xd = torch.full((nb, ldx), float("nan"), device=DEV)
+        Xd[:, :K] = torch.from_numpy(X).to(DEV)
+        Yd = torch.full((nb, M + 1), -12345.0, device=DEV)
+        items.append(tvl.item(buf.data_ptr(), ldw, Xd.data_ptr(), Yd.data_ptr(), M, K, dt,
+                              nrhs=nb, ldx=ldx, ldy=M + 1))
+        host.append((W, X, dt, nb, Yd))
+        keep += [buf, Xd, Yd]
+    for t in [None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
+                       for r, w, u in MFMA + MFMA16]:
+        for *_, Yd in host:
+            Yd[:, :-1].fill_(float("nan"))
+        plan = tvl.tvl_sweep_plan_create(items, t)
+        plan.run()
+        torch.cuda.synchronize()
+        for W, X, dt, nb, Yd in host:
+            Y = Yd.cpu().numpy()
+            assert np.all(Y[:, -1] == -12345.0), ("wrote past M", t)
+            for b in range(nb):
+                ref, S = (oracle.gemv_f32 if dt == 0 else oracle.gemv_f16)(W, X[b])
+                r = oracle.check(Y[b, :-1], ref, S, TOL[dt])
+                assert r["bad"] == 0, (W.shape, dt, nb, b, t, r)
         plan.destroy()
