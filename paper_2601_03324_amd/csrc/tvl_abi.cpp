@@ -846,28 +846,30 @@ tvl_status tvl_gemv_batch_sweep(const tvl_item *items, int32_t n, hipStream_t st
     if (st != TVL_OK) return st;
     std::string key(reinterpret_cast<const char *>(&dev), sizeof dev);
     key.append(reinterpret_cast<const char *>(items), sizeof(tvl_item) * (size_t)n);
-    tvl_plan *p = nullptr;
+    // A cached plan is launched under the lock that found it: another
+    // thread's eviction (cache full) or tvl_release_workspaces would
+    // otherwise free it between the lookup and the launch.
     {
         std::lock_guard<std::mutex> lk(g_mu);
         auto it = g_cache.find(key);
-        if (it != g_cache.end()) p = it->second;
+        if (it != g_cache.end()) return plan_launch(it->second, stream);
     }
-    if (!p) {
-        st = plan_build(items, n, nullptr, &p);
-        if (st != TVL_OK) return st;
-        std::lock_guard<std::mutex> lk(g_mu);
-        if (g_cache.size() >= kCacheMax) {
-            for (auto &kv : g_cache)
-                plan_free(kv.second);
-            g_cache.clear();
-        }
-        auto ins = g_cache.emplace(key, p);
-        if (!ins.second) { // another thread built the same list meanwhile
-            plan_free(p);
-            p = ins.first->second;
-        }
+    tvl_plan *fresh = nullptr; // built outside the lock (allocates, uploads)
+    st = plan_build(items, n, nullptr, &fresh);
+    if (st != TVL_OK) return st;
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_cache.find(key);
+    if (it != g_cache.end()) { // another thread built the same list meanwhile
+        plan_free(fresh);
+        return plan_launch(it->second, stream);
     }
-    return plan_launch(p, stream);
+    if (g_cache.size() >= kCacheMax) { // plan_free waits for in-flight launches
+        for (auto &kv : g_cache)
+            plan_free(kv.second);
+        g_cache.clear();
+    }
+    g_cache.emplace(key, fresh);
+    return plan_launch(fresh, stream);
 }
 
 tvl_status tvl_release_workspaces(void)

@@ -389,3 +389,46 @@ def test_large_sweeps_sampled(name):
     plan.destroy()
     del gemvs
     torch.cuda.empty_cache()
+
+
+def test_batch_sweep_cache_under_threads():
+    """Four host threads, each on its own stream, call tvl_gemv_batch_sweep
+    over 80 distinct one-item lists: more lists than the library's plan cache
+    holds, so cached plans are evicted while other threads look them up and
+    launch them.  Every output of every call is checked against the oracle."""
+    import threading
+    rng = np.random.default_rng(99)
+    M, K, nlist, nthr = 64, 256, 80, 4
+    W = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    buf, ldw = dev_matrix(W, 0)
+    xs = rng.standard_normal((nlist, K)).astype(np.float32)
+    X = torch.from_numpy(xs).to(DEV)
+    Y = torch.full((nthr, nlist, M), float("nan"), device=DEV)
+    torch.cuda.synchronize()
+    errors = []
+
+    def worker(t):
+        try:
+            s = torch.cuda.Stream()
+            for rep in range(3):
+                for i in range(nlist):
+                    j = (7 * i + 13 * t + rep) % nlist
+                    tvl.tvl_gemv_batch_sweep([(buf, ldw, X[j], Y[t, j], M, K, 0)], s)
+            s.synchronize()
+        except Exception as exc:  # reported below
+            errors.append((t, exc))
+
+    ths = [threading.Thread(target=worker, args=(t,)) for t in range(nthr)]
+    for th in ths:
+        th.start()
+    for th in ths:
+        th.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    Yh = Y.cpu().numpy()
+    for j in range(nlist):
+        ref, S = oracle.gemv_f32(W, xs[j])
+        for t in range(nthr):
+            r = oracle.check(Yh[t, j], ref, S, 1e-5)
+            assert r["bad"] == 0, (t, j, r)
+    tvl.tvl_release_workspaces()
