@@ -181,9 +181,11 @@ typedef struct tvl_item {
  *   2: (2,4,2) (2,4,4) (4,4,2);  4: (2,4,1) (2,4,2) (4,4,1) (4,4,2);
  *   8: (2,4,1) (2,4,2) (4,4,1)
  * and, for any nrhs <= 16, on the matrix cores: the 4x4x1 form (rows in
- * groups of 4, U = 1) (8,4,1) (16,1,1) (16,2,1), and the 16x16x4 form (rows
+ * groups of 4, U = 1) (8,4,1) (16,1,1) (16,2,1); the 16x16x4 form (rows
  * in groups of 16, U = loads per group in flight) (16,4,8) (32,1,4) (32,2,4)
- * (64,1,4)
+ * (64,1,4); and the 16x16x4 form with rows staged through LDS (U = 2; fp32
+ * weights; a launch holding fp16 weights runs the previous form with the
+ * same rows and waves, U = 4) (16,1,2) (16,4,2) (32,1,2) (32,2,2) (32,4,2)
  * Launches holding block-quantised items (direct-x only; R rows per group of
  * lanes, see tvl_dtype): (2,4,2) (4,4,1) (4,4,2) (4,1,2) (8,4,1) (8,2,1) */
 typedef struct tvl_tuning {

@@ -270,13 +270,16 @@ int multi_B(int n) { return n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16; }
 // 110M decode token.  Up to 4 vectors the VALU form wins: more rows per
 // wavefront amortise each x read over more weights (R = 4), and fewer loads
 // in flight keep the R x B accumulators in registers.  From 5 vectors on,
-// the FMAs would take ~half the VALU issue slots and the matrix cores win:
-// at 8 vectors the 4 x 4 x 1 form with 16 rows per wavefront (4.70 TB/s
-// against 4.07 on the VALU and 3.84 for the 16 x 16 x 4 form), at 16
-// vectors the 16 x 16 x 4 form with 32 rows and one wavefront per block
-// (3.61 TB/s against 3.14 for the 4 x 4 x 1 form).
-Shape default_multi_shape(int B)
+// the FMAs would take ~half the VALU issue slots and the matrix cores win.
+// fp32 weights: the 16 x 16 x 4 form with LDS-staged rows, 32 rows and one
+// wavefront per block (8 vectors: 5.27 TB/s against 4.73 for the 4 x 4 x 1
+// form and 4.07 on the VALU; 16 vectors: 4.81 against 3.68 for the direct-
+// load 16 x 16 x 4 form).  Launches with fp16 weights (that form is fp32
+// only): the 4 x 4 x 1 form up to 8 vectors, the direct-load 16 x 16 x 4
+// form beyond.
+Shape default_multi_shape(int B, bool all_f32)
 {
+    if (B > 4 && all_f32) return Shape{32, 1, 2, tvl::kXDirect};
     if (B > 8) return Shape{32, 1, 4, tvl::kXDirect};
     if (B > 4) return Shape{16, 2, 1, tvl::kXDirect};
     return B == 2 ? Shape{4, 4, 2, tvl::kXDirect} : Shape{4, 4, 1, tvl::kXDirect};
@@ -392,7 +395,7 @@ Shape default_shape_items(const tvl_item *items, int32_t n)
     for (int32_t i = 0; i < n; ++i)
         quant = quant || is_quant(items[i].dtype);
     if (quant) return default_quant_shape();
-    if (nmax > 1) return default_multi_shape(multi_B(nmax));
+    if (nmax > 1) return default_multi_shape(multi_B(nmax), b16 == 0);
     if (fused) return default_fused_shape(b16, b32);
     return default_shape(b16, b32, b32 > 0 ? row32 / b32 : 0.0);
 }
@@ -772,7 +775,7 @@ tvl_status tvl_gemv_item(const tvl_item *item, const tvl_tuning *tuning, hipStre
     const int B = is_multi(*item) ? multi_B((int)item->nrhs) : 0;
     Shape shape;
     st = pick_shape(tuning,
-                    B ? default_multi_shape(B)
+                    B ? default_multi_shape(B, item->dtype == TVL_F32)
                       : default_fused_shape(f16 ? 1.0 : 0.0, f16 ? 0.0 : 1.0),
                     &shape, false);
     if (st != TVL_OK) return st;

@@ -542,9 +542,10 @@ struct InstMfma {
 // 8 whole ones (the other half comes with the next load of the same batch).
 // HBM bytes stay within 4 % of the whole-line form, but the L1 receives 1.7x
 // the requests and the address unit stalls on it (rocprofv3 on MI355X), so
-// this form tops out near 3.8 TB/s whatever the vector count.  It is the
-// faster form from 9 to 16 vectors, where the 4 x 4 x 1 form runs out of
-// registers; up to 8 vectors the 4 x 4 x 1 form is faster.
+// this form tops out near 3.8 TB/s whatever the vector count.  For fp32
+// weights the LDS-staged form below avoids the half lines and is faster; this
+// form serves launches with fp16 weights from 9 to 16 vectors, where the
+// 4 x 4 x 1 form runs out of registers.
 //
 // The x loads (vector i, columns as for the weights) hit the cache: every
 // wavefront of a matrix reads the same vectors; RG groups of 16 rows share
@@ -765,6 +766,191 @@ struct InstMfma16 {
     }
 };
 
+// -------------------------------- matrix cores, 16 x 16 x 4, LDS-staged rows
+// The same contraction as above for fp32 weights, with whole-line weight
+// loads: a wavefront load brings 512 contiguous bytes of each of two rows
+// (lanes 0-31: row 2t, lanes 32-63: row 2t + 1), so each load covers 8 whole
+// 128-byte lines.  The rows go to a wavefront-private LDS tile and come back
+// in the A-operand layout (lane 16 g + i: row i, 16-byte block 4 q + g).
+// Blocks are XOR-swizzled within a row (block b of row r at slot b ^ (r % 16))
+// so that the 16 lanes reading one block of 16 rows hit 16 different bank
+// groups, and the 32 lanes writing a row hit 32 different slots.  One
+// wavefront's LDS reads follow its writes in order: no barrier.  The x
+// vectors keep their direct B-layout loads.  Accumulation as in the form
+// above, with 32 MFMA steps per chunk.
+constexpr int kLdsCols = 128; // columns per chunk (512 bytes of a row)
+
+template <int RG>
+struct MfmaLdsRows {
+    static constexpr int NT = 8 * RG; // row-pair loads per chunk
+    const float *W;
+    int64_t ldw;
+    const float *xv; // vector i (clamped), at column 4 g
+    int wrow0, mlast, kn, lane;
+
+    __device__ __forceinline__ MfmaLdsRows(const float *W_, int64_t ldw_, int wrow0_, int M,
+                                           const float *x, int64_t ldx, int nb, int K, int lane_)
+        : W(W_), ldw(ldw_), wrow0(wrow0_), mlast(M - 1), kn(K), lane(lane_)
+    {
+        xv = x + (int64_t)min(lane & 15, nb - 1) * ldx + 4 * (lane >> 4);
+    }
+
+    // tile: this wavefront's 16 RG x 128 floats of LDS
+    template <bool RAGGED>
+    __device__ __forceinline__ void chunk(int c0, f4 *tile, f4 (&acc)[RG]) const
+    {
+        const int g = lane >> 4, i = lane & 15, h = lane >> 5, b = lane & 31;
+        const f4 z = {0.f, 0.f, 0.f, 0.f};
+        f4 w[NT], xb[8];
+        const int wcol = c0 + 4 * b;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const float *src = W + (int64_t)min(wrow0 + 2 * t + h, mlast) * ldw + wcol;
+            if constexpr (RAGGED)
+                w[t] = wcol < kn ? mask_from<f4, 4>(load_w<float>(src), kn - wcol) : z;
+            else
+                w[t] = load_w<float>(src);
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int c = c0 + 16 * q;
+            if constexpr (RAGGED) {
+                const int valid = kn - (c + 4 * g);
+                xb[q] = valid > 0 ? mask_from<f4, 4>(load_x4(xv + c), valid) : z;
+            } else {
+                xb[q] = load_x4(xv + c);
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0); // the chunk's loads first
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const int r = 2 * t + h;
+            tile[r * (kLdsCols / 4) + (b ^ (r & 15))] = w[t];
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg) {
+                const int r = 16 * rg + i;
+                const f4 a = tile[r * (kLdsCols / 4) + ((4 * q + g) ^ i)];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    acc[rg] = mfma16(a[e], xb[q][e], acc[rg]);
+            }
+        __builtin_amdgcn_sched_barrier(0); // the next chunk's loads stay below
+    }
+
+    __device__ __forceinline__ void run(f4 *tile, f4 (&out)[RG]) const
+    {
+        const f4 z = {0.f, 0.f, 0.f, 0.f};
+        f4 acc[RG], t1[RG], t2[RG];
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+            acc[rg] = t1[rg] = t2[rg] = z;
+        int c0 = 0, n1 = 0;
+        for (; c0 + kLdsCols <= kn; c0 += kLdsCols) {
+            chunk<false>(c0, tile, acc);
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg) {
+                t1[rg] += acc[rg];
+                acc[rg] = z;
+            }
+            if (++n1 == kMfmaLevel) {
+#pragma unroll
+                for (int rg = 0; rg < RG; ++rg) {
+                    t2[rg] += t1[rg];
+                    t1[rg] = z;
+                }
+                n1 = 0;
+            }
+        }
+        if (c0 < kn) // every lane reaches the MFMAs
+            chunk<true>(c0, tile, acc);
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+            out[rg] = t2[rg] + (t1[rg] + acc[rg]);
+    }
+};
+
+template <int RG, int WV>
+__device__ __forceinline__ void tile_mfma_lds(const DevItem &it, int row0, f4 *tile)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wrow0 = row0 + wave * (16 * RG);
+    if (wrow0 >= it.M) return; // no barrier follows
+    const int nb = it.nrhs < 1 ? 1 : it.nrhs;
+    f4 out[RG];
+    const MfmaLdsRows<RG> mr(static_cast<const float *>(it.W), it.ldw, wrow0, it.M, it.x, it.ldx,
+                             nb, it.K, lane);
+    mr.run(tile, out);
+    const int i = lane & 15, g = lane >> 4;
+    if (i < nb) {
+        float *yv = it.y + (int64_t)i * it.ldy;
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = wrow0 + 16 * rg + 4 * g + v;
+                if (row < it.M) yv[row] = out[rg][v];
+            }
+    }
+}
+
+// fp32 weights only (the launcher sends other launches to the direct form)
+template <int RG, int WV>
+__global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_lds(const DevItem *__restrict__ items,
+                                                               const DevTile *__restrict__ tiles,
+                                                               int ntiles)
+{
+    constexpr int kTile = 16 * RG * (kLdsCols / 4); // f4 per wavefront
+    __shared__ f4 lds[WV * kTile];
+    f4 *tile = lds + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave) * kTile;
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const DevTile tl = tiles[t];
+        const DevItem it = items[tl.item];
+        tile_mfma_lds<RG, WV>(it, tl.row0, tile);
+        __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
+    }
+}
+
+template <int RG, int WV>
+__global__ __launch_bounds__(WV *kWave) void k_item_mfma_lds(const DevItem it)
+{
+    constexpr int kTile = 16 * RG * (kLdsCols / 4);
+    __shared__ f4 lds[WV * kTile];
+    f4 *tile = lds + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave) * kTile;
+    tile_mfma_lds<RG, WV>(it, (int)blockIdx.x * (16 * RG * WV), tile);
+}
+
+// (rows per wavefront = 16 RG, waves per block, U = 2 marks this form).
+// Two variants ran slower on MI355X with 8 vectors and were not kept: the
+// next chunk's loads issued before the current chunk's products (~200 VGPRs
+// at 16 rows: 4.9-5.0 against 5.2-5.3 TB/s), and x staged through LDS too
+// (whole-line x loads: 5.05 against 5.24 TB/s).
+#define TVL_MFMA_LDS_SHAPES(X) X(16, 1, 2) X(16, 4, 2) X(32, 1, 2) X(32, 2, 2) X(32, 4, 2)
+
+template <int R, int WV, int U>
+struct InstMfmaLds {
+    static constexpr int RG = R / 16;
+    static hipError_t sweep(int wm, const DevItem *items, const DevTile *tiles, int ntiles,
+                            int grid, hipStream_t st)
+    {
+        if (wm != kWF32) // fp16 weights: the direct-load form with the same rows
+            return InstMfma16<R, WV, 4>::sweep(wm, items, tiles, ntiles, grid, st);
+        hipLaunchKernelGGL((k_sweep_mfma_lds<RG, WV>), dim3(grid), dim3(WV * kWave), 0, st, items,
+                           tiles, ntiles);
+        return hipGetLastError();
+    }
+    static hipError_t item(const DevItem &it, hipStream_t st)
+    {
+        if (it.dtype == 1) return InstMfma16<R, WV, 4>::item(it, st);
+        const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
+        hipLaunchKernelGGL((k_item_mfma_lds<RG, WV>), grid, block, 0, st, it);
+        return hipGetLastError();
+    }
+};
+
 // (R, waves per block, U, B) with B x vectors per launch (B >= nrhs).
 #define TVL_MULTI_SHAPES(X)                                                                       \
     X(2, 4, 2, 2) X(2, 4, 4, 2) X(4, 4, 2, 2) X(2, 4, 1, 4) X(2, 4, 2, 4) X(4, 4, 1, 4)          \
@@ -798,6 +984,7 @@ bool multi_shape_supported(const Shape &s, int B)
     TVL_MULTI_SHAPES(X)
     TVL_MFMA_SHAPES(Y)
     TVL_MFMA16_SHAPES(Y)
+    TVL_MFMA_LDS_SHAPES(Y)
 #undef X
 #undef Y
     return false;
@@ -815,12 +1002,17 @@ hipError_t launch_sweep_multi(const Shape &s, int B, int wmode, const DevItem *i
 #define Z(R_, W_, U_)                                                                             \
     if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
         return InstMfma16<R_, W_, U_>::sweep(wmode, items, tiles, ntiles, grid, st);
+#define V(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return InstMfmaLds<R_, W_, U_>::sweep(wmode, items, tiles, ntiles, grid, st);
     TVL_MULTI_SHAPES(X)
     TVL_MFMA_SHAPES(Y)
     TVL_MFMA16_SHAPES(Z)
+    TVL_MFMA_LDS_SHAPES(V)
 #undef X
 #undef Y
 #undef Z
+#undef V
     return hipErrorInvalidValue;
 }
 
@@ -833,12 +1025,16 @@ hipError_t launch_item_multi(const Shape &s, int B, const DevItem &item, hipStre
     if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfma<R_, W_, U_>::item(B, item, st);
 #define Z(R_, W_, U_)                                                                             \
     if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfma16<R_, W_, U_>::item(item, st);
+#define V(R_, W_, U_)                                                                             \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfmaLds<R_, W_, U_>::item(item, st);
     TVL_MULTI_SHAPES(X)
     TVL_MFMA_SHAPES(Y)
     TVL_MFMA16_SHAPES(Z)
+    TVL_MFMA_LDS_SHAPES(V)
 #undef X
 #undef Y
 #undef Z
+#undef V
     return hipErrorInvalidValue;
 }
 

@@ -29,6 +29,9 @@ MULTI = [(2, 4, 2, 2), (2, 4, 4, 2), (4, 4, 2, 2), (2, 4, 1, 4), (2, 4, 2, 4), (
 # per row group in flight >= 4)
 MFMA = [(8, 4, 1), (16, 1, 1), (16, 2, 1)]
 MFMA16 = [(16, 4, 8), (32, 1, 4), (32, 2, 4), (64, 1, 4)]
+# 16x16x4 with LDS-staged rows (U = 2; fp32 weights, fp16 launches take the
+# direct form)
+MFMA_LDS = [(16, 1, 2), (16, 4, 2), (32, 1, 2), (32, 2, 2), (32, 4, 2)]
 
 
 def tunings(nrhs):
@@ -36,7 +39,7 @@ def tunings(nrhs):
     for r, w, u, b in MULTI:
         if b >= nrhs and (b == 2 or b // 2 < nrhs):  # the kernels the library would pick from
             out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
-    for r, w, u in MFMA + MFMA16:
+    for r, w, u in MFMA + MFMA16 + MFMA_LDS:
         out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
     return out
 
@@ -113,7 +116,9 @@ def test_beam4_sweep110m():
               dict(rows_per_wave=8, waves_per_block=4, unroll=1, flags=2),
               dict(rows_per_wave=16, waves_per_block=2, unroll=1, flags=2, grid=700),
               dict(rows_per_wave=32, waves_per_block=2, unroll=4, flags=2),
-              dict(rows_per_wave=64, waves_per_block=1, unroll=4, flags=2, grid=300)):
+              dict(rows_per_wave=64, waves_per_block=1, unroll=4, flags=2, grid=300),
+              dict(rows_per_wave=16, waves_per_block=4, unroll=2, flags=2),
+              dict(rows_per_wave=32, waves_per_block=1, unroll=2, flags=2, grid=900)):
         for d in ms:
             d.Y.fill_(float("nan"))
         plan = tvl.tvl_sweep_plan_create([d.item() for d in ms], t)
@@ -157,7 +162,7 @@ def test_multi_plan_mixed_dtypes():
         host.append((W, X, dt, nb, Yd))
         keep += [buf, Xd, Yd]
     for t in [None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
-                       for r, w, u in MFMA + MFMA16]:
+                       for r, w, u in MFMA + MFMA16 + MFMA_LDS]:
         for *_, Yd in host:
             Yd[:, :-1].fill_(float("nan"))
         plan = tvl.tvl_sweep_plan_create(items, t)
