@@ -176,3 +176,27 @@ def test_multi_plan_mixed_dtypes():
                 r = oracle.check(Y[b, :-1], ref, S, TOL[dt])
                 assert r["bad"] == 0, (W.shape, dt, nb, b, t, r)
         plan.destroy()
+
+
+@pytest.mark.parametrize("nb", [8, 16])
+def test_beam_sweep110m_default(nb):
+    """The 110M decode token for 8 and 16 hypotheses in the launch the bench
+    times (the library's default several-vector kernel): every output of the
+    first 28 matrices and sampled rows of the rest, every vector."""
+    wl = synth.WORKLOADS["sweep110m"]
+    ms = sdev.load_multi(wl, nb, DEV)
+    for d in ms:
+        d.Y.fill_(float("nan"))
+    plan = tvl.tvl_sweep_plan_create([d.item() for d in ms])
+    plan.run()
+    torch.cuda.synchronize()
+    for k, d in enumerate(ms):
+        m = d.spec
+        Y = d.Y.cpu().numpy()
+        rows = np.arange(m.M) if k < 28 else sdev.sample_rows(m.M, 96, 11 + k)
+        Wh = m.weights() if k < 28 else np.stack([m.weights(int(r), 1)[0] for r in rows])
+        for b in range(nb):
+            ref, S = oracle.gemv_f32(Wh, m.x(b))
+            r = oracle.check(Y[b][rows], ref, S, 1e-5)
+            assert r["bad"] == 0, (m.name, nb, b, r)
+    plan.destroy()
