@@ -346,16 +346,22 @@ tvl_status current_device(int *dev, DevInfo *info)
 //   mostly fp16 weights                  -> direct-x, R=4, W=1, U=4
 //   fp32, rows of <= 3 KB (K <= 768)     -> direct-x, R=2, W=4, U=3 (one batch
 //                                           covers the row)
-//   fp32, rows of <= 8 KB (K <= 2048)    -> direct-x, R=2, W=4, U=4
+//   fp32, rows of <= 8 KB (K <= 2048)    -> direct-x, R=2, W=4, U=4; in a
+//                                           sweep R=2, W=8, U=3 (the 110M
+//                                           token: 7.03 against 6.91 TB/s)
 //   fp32, longer rows                    -> direct-x, R=1, W=4, U=8
 // Direct-x reads x next to the weights, so no wavefront waits on a staging
 // round trip; with fp16 weights each 16-byte load needs 32 bytes of x, so
-// more rows per wavefront (R=4) share each x read.
-Shape default_shape(double bytes_f16, double bytes_f32, double f32_row_bytes_weighted)
+// more rows per wavefront (R=4) share each x read.  `sweep`: a plan's one
+// launch over many GEMVs (a single GEMV of short rows is faster with 4
+// wavefronts per workgroup: more workgroups share the few rows).
+Shape default_shape(double bytes_f16, double bytes_f32, double f32_row_bytes_weighted,
+                    bool sweep)
 {
     if (bytes_f16 > bytes_f32) return Shape{4, 1, 4, tvl::kXDirect};
     if (f32_row_bytes_weighted <= 3072.0) return Shape{2, 4, 3, tvl::kXDirect};
-    if (f32_row_bytes_weighted <= 8192.0) return Shape{2, 4, 4, tvl::kXDirect};
+    if (f32_row_bytes_weighted <= 8192.0)
+        return sweep ? Shape{2, 8, 3, tvl::kXDirect} : Shape{2, 4, 4, tvl::kXDirect};
     return Shape{1, 4, 8, tvl::kXDirect};
 }
 
@@ -397,7 +403,7 @@ Shape default_shape_items(const tvl_item *items, int32_t n)
     if (quant) return default_quant_shape();
     if (nmax > 1) return default_multi_shape(multi_B(nmax), b16 == 0);
     if (fused) return default_fused_shape(b16, b32);
-    return default_shape(b16, b32, b32 > 0 ? row32 / b32 : 0.0);
+    return default_shape(b16, b32, b32 > 0 ? row32 / b32 : 0.0, true);
 }
 
 int64_t item_bytes_factor(const tvl_item &t) { return t.op == TVL_OP_SWIGLU ? 2 : 1; }
@@ -708,7 +714,7 @@ tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype, const float *x
         return TVL_OK;
     }
     const Shape def = default_shape(dtype == TVL_F16 ? 1.0 : 0.0, dtype == TVL_F16 ? 0.0 : 1.0,
-                                    (double)K * 4.0);
+                                    (double)K * 4.0, false);
     shape = def;
     if (user_shape || (tuning && tuning->flags)) {
         st = pick_shape(tuning, def, &shape);

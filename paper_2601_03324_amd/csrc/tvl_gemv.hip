@@ -310,7 +310,8 @@ __global__ __launch_bounds__(WV *kWave) void k_sweep_direct(const DevItem *__res
 #define TVL_DIRECT_SHAPES(X)                                                                      \
     X(1, 1, 4) X(1, 1, 8) X(2, 1, 2) X(2, 1, 3) X(2, 1, 4) X(2, 1, 8) X(4, 1, 1) X(4, 1, 2)       \
     X(4, 1, 3) X(4, 1, 4) X(8, 1, 1) X(8, 1, 2) X(1, 4, 4) X(1, 4, 8) X(2, 4, 2) X(2, 4, 3)       \
-    X(2, 4, 4) X(2, 4, 8) X(4, 4, 1) X(4, 4, 2) X(4, 4, 3) X(4, 4, 4) X(8, 4, 1) X(8, 4, 2)
+    X(2, 4, 4) X(2, 4, 8) X(4, 4, 1) X(4, 4, 2) X(4, 4, 3) X(4, 4, 4) X(8, 4, 1) X(8, 4, 2)       \
+    X(1, 8, 8) X(2, 8, 3) X(2, 8, 4) X(4, 8, 2)
 
 template <int R, int WV, int U, int XM>
 hipError_t launch_ksplit(int dtype, const void *W, int64_t ldw, const float *x, float *y, int M,

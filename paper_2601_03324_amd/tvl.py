@@ -28,7 +28,8 @@ LDS_SHAPES = ((1, 4, 4), (1, 4, 8), (2, 4, 2), (2, 4, 3), (2, 4, 4), (2, 4, 8), 
               (4, 8, 2), (1, 2, 8), (2, 2, 8), (4, 2, 4), (8, 2, 2))
 DIRECT_SHAPES = tuple((r, w, u) for w in (1, 4)
                       for (r, u) in ((1, 4), (1, 8), (2, 2), (2, 3), (2, 4), (2, 8), (4, 1),
-                                     (4, 2), (4, 3), (4, 4), (8, 1), (8, 2)))
+                                     (4, 2), (4, 3), (4, 4), (8, 1), (8, 2))) + (
+    (1, 8, 8), (2, 8, 3), (2, 8, 4), (4, 8, 2))
 
 # every symbol include/tvl.h declares
 EXPORTS = ("tvl_version", "tvl_row_stride", "tvl_pack_rows", "tvl_gemv", "tvl_gemv_ex",
