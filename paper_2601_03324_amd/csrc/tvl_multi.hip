@@ -772,30 +772,50 @@ struct InstMfma16 {
 // (lanes 0-31: row 2t, lanes 32-63: row 2t + 1), so each load covers 8 whole
 // 128-byte lines.  The rows go to a wavefront-private LDS tile and come back
 // in the A-operand layout (lane 16 g + i: row i, 16-byte block 4 q + g).
-// Blocks are XOR-swizzled within a row (block b of row r at slot b ^ (r % 16))
-// so that the 16 lanes reading one block of 16 rows hit 16 different bank
-// groups, and the 32 lanes writing a row hit 32 different slots.  One
-// wavefront's LDS reads follow its writes in order: no barrier.  The x
-// vectors keep their direct B-layout loads.  Accumulation as in the form
-// above, with 32 MFMA steps per chunk.
-constexpr int kLdsCols = 128; // columns per chunk (512 bytes of a row)
+// Rows sit 528 bytes apart (512 + 16 of padding), so row i starts 4 i banks
+// further on: the 16 lanes reading one 16-byte block of 16 rows hit 16
+// different bank groups, and every LDS access of a chunk is one base
+// register plus an immediate offset.  One wavefront's LDS reads follow its
+// writes in order: no barrier.  The x vectors keep their direct B-layout
+// loads.  Accumulation as in the form above, with 32 MFMA steps per chunk.
+constexpr int kLdsCols = 128;                   // columns per chunk (512 bytes of a row)
+constexpr int kLdsRow = kLdsCols / 4 + 1;       // f4 per LDS row, padding included
+
+// Row pairs are read through buffer descriptors: the descriptor of pair t
+// starts at the pair's first row and holds only its rows below M (0, 1 or
+// 2 rows), so the hardware's range check returns zeros for rows past M and
+// every load needs just one 32-bit lane offset (h ldw 4 + 16 b) in a VGPR,
+// the chunk's column in the scalar offset.  Two rows must then fit in the
+// descriptor's 31-bit size: rows of up to kLdsMaxLdw floats (1 GiB rows go
+// to the direct-load form).
+constexpr int64_t kLdsMaxLdw = (int64_t(1) << 28) - 64;
 
 template <int RG>
 struct MfmaLdsRows {
     static constexpr int NT = 8 * RG; // row-pair loads per chunk
-    const float *W;
+    const float *W;  // the wavefront's first row (wavefront-uniform)
     int64_t ldw;
     const float *xv; // vector i (clamped), at column 4 g
-    int wrow0, mlast, kn, lane;
+    int vrows, kn, lane;
+    int voff; // this lane's byte offset in a row pair
 
-    __device__ __forceinline__ MfmaLdsRows(const float *W_, int64_t ldw_, int wrow0_, int M,
+    __device__ __forceinline__ MfmaLdsRows(const float *W_, int64_t ldw_, int wrow0, int M,
                                            const float *x, int64_t ldx, int nb, int K, int lane_)
-        : W(W_), ldw(ldw_), wrow0(wrow0_), mlast(M - 1), kn(K), lane(lane_)
+        : W(W_ + (int64_t)wrow0 * ldw_), ldw(ldw_), vrows(M - wrow0), kn(K), lane(lane_),
+          voff((int)((lane_ >> 5) * ldw_ * 4 + 16 * (lane_ & 31)))
     {
         xv = x + (int64_t)min(lane & 15, nb - 1) * ldx + 4 * (lane >> 4);
     }
 
-    // tile: this wavefront's 16 RG x 128 floats of LDS
+    // rows 2 t, 2 t + 1 of the wavefront, those below M
+    __device__ __forceinline__ __amdgpu_buffer_rsrc_t pair(int t) const
+    {
+        const int n = min(max(vrows - 2 * t, 0), 2);
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(W + 2 * t * ldw), (short)0,
+                                                 (int)(n * ldw * 4), 0x00020000);
+    }
+
+    // tile: this wavefront's 16 LDS rows of kLdsRow float4
     template <bool RAGGED>
     __device__ __forceinline__ void chunk(int c0, f4 *tile, f4 (&acc)[RG]) const
     {
@@ -805,11 +825,16 @@ struct MfmaLdsRows {
         const int wcol = c0 + 4 * b;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            const float *src = W + (int64_t)min(wrow0 + 2 * t + h, mlast) * ldw + wcol;
+            // non-temporal (cache policy 2), like load_w
             if constexpr (RAGGED)
-                w[t] = wcol < kn ? mask_from<f4, 4>(load_w<float>(src), kn - wcol) : z;
+                w[t] = wcol < kn ? mask_from<f4, 4>(__builtin_bit_cast(
+                                       f4, __builtin_amdgcn_raw_buffer_load_b128(
+                                               pair(t), voff, 4 * c0, 2)),
+                                   kn - wcol)
+                                 : z;
             else
-                w[t] = load_w<float>(src);
+                w[t] = __builtin_bit_cast(
+                    f4, __builtin_amdgcn_raw_buffer_load_b128(pair(t), voff, 4 * c0, 2));
         }
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
@@ -822,21 +847,24 @@ struct MfmaLdsRows {
             }
         }
         __builtin_amdgcn_sched_barrier(0); // the chunk's loads first
+        // one 16-row group at a time through the same 16 LDS rows (a
+        // wavefront's LDS accesses run in order: group rg + 1 overwrites
+        // rows that group rg has finished reading)
+        f4 *wt = tile + h * kLdsRow + b;       // row h, block b (+ 2 rows per load)
+        const f4 *rt = tile + i * kLdsRow + g; // row i, block g (+ 4 q blocks)
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const int r = 2 * t + h;
-            tile[r * (kLdsCols / 4) + (b ^ (r & 15))] = w[t];
-        }
+        for (int rg = 0; rg < RG; ++rg) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
+            for (int t = 0; t < 8; ++t)
+                wt[2 * t * kLdsRow] = w[8 * rg + t];
 #pragma unroll
-            for (int rg = 0; rg < RG; ++rg) {
-                const int r = 16 * rg + i;
-                const f4 a = tile[r * (kLdsCols / 4) + ((4 * q + g) ^ i)];
+            for (int q = 0; q < 8; ++q) {
+                const f4 a = rt[4 * q];
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     acc[rg] = mfma16(a[e], xb[q][e], acc[rg]);
             }
+        }
         __builtin_amdgcn_sched_barrier(0); // the next chunk's loads stay below
     }
 
@@ -875,6 +903,10 @@ struct MfmaLdsRows {
 template <int RG, int WV>
 __device__ __forceinline__ void tile_mfma_lds(const DevItem &it, int row0, f4 *tile)
 {
+    if (it.ldw > kLdsMaxLdw) { // wavefront-uniform
+        tile_mfma16<float, RG, 4, WV>(it, row0);
+        return;
+    }
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int wrow0 = row0 + wave * (16 * RG);
@@ -903,7 +935,7 @@ __global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_lds(const DevItem *__r
                                                                const DevTile *__restrict__ tiles,
                                                                int ntiles)
 {
-    constexpr int kTile = 16 * RG * (kLdsCols / 4); // f4 per wavefront
+    constexpr int kTile = 16 * kLdsRow; // f4 per wavefront
     __shared__ f4 lds[WV * kTile];
     f4 *tile = lds + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave) * kTile;
     for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
@@ -917,7 +949,7 @@ __global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_lds(const DevItem *__r
 template <int RG, int WV>
 __global__ __launch_bounds__(WV *kWave) void k_item_mfma_lds(const DevItem it)
 {
-    constexpr int kTile = 16 * RG * (kLdsCols / 4);
+    constexpr int kTile = 16 * kLdsRow;
     __shared__ f4 lds[WV * kTile];
     f4 *tile = lds + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave) * kTile;
     tile_mfma_lds<RG, WV>(it, (int)blockIdx.x * (16 * RG * WV), tile);

@@ -200,3 +200,26 @@ def test_beam_sweep110m_default(nb):
             r = oracle.check(Y[b][rows], ref, S, 1e-5)
             assert r["bad"] == 0, (m.name, nb, b, r)
     plan.destroy()
+
+
+@pytest.mark.parametrize("ldw", [(1 << 28) - 64, 1 << 28], ids=["lds-limit", "direct"])
+def test_multi_huge_row_stride(ldw):
+    """Row strides at the matrix-core LDS form's limit (two rows in a buffer
+    descriptor's 31-bit size) and one past it (the launch falls back to the
+    direct-load form): 3 rows of 1 GiB each, 8 vectors, every launch shape."""
+    M, K, nb = 3, 300, 8
+    rng = np.random.default_rng(ldw % 1000)
+    W = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    X = rng.standard_normal((nb, K)).astype(np.float32)
+    buf = torch.empty((M, ldw), dtype=torch.float32, device=DEV)
+    buf[:, K:K + 64].fill_(float("nan"))  # padding next to the row: never read
+    buf[:, :K] = torch.from_numpy(W).to(DEV)
+    refs = [oracle.gemv_f32(W, X[b]) for b in range(nb)]
+    for t in [None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
+                       for r, w, u in MFMA_LDS + MFMA16]:
+        Y = run(buf, ldw, 0, X, M, K, nb, M, t)
+        for b in range(nb):
+            r = oracle.check(Y[b], refs[b][0], refs[b][1], 1e-5)
+            assert r["bad"] == 0, (ldw, t, b, r)
+    del buf
+    torch.cuda.empty_cache()
