@@ -449,9 +449,13 @@ struct Workspace {
 };
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
 
-tvl_status get_workspace(int dev, hipStream_t st, int64_t nfloat, int64_t ncnt, Workspace *out)
+// The caller holds g_mu, and keeps holding it until it has launched the
+// kernel that uses the workspace: another thread growing the same stream's
+// workspace, or tvl_release_workspaces, would otherwise free the buffers
+// between this lookup and that launch.
+tvl_status get_workspace_locked(int dev, hipStream_t st, int64_t nfloat, int64_t ncnt,
+                                Workspace *out)
 {
-    std::lock_guard<std::mutex> lk(g_mu);
     Workspace &w = g_ws[{dev, st}];
     if (w.partial_cap < nfloat || w.counter_cap < ncnt) {
         hipError_t e;
@@ -749,7 +753,8 @@ tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype, const float *x
     } else {
         if ((int64_t)tiles * S > kMaxDim) return fail(TVL_ERR_ARG, "tvl_gemv: grid too large");
         Workspace ws;
-        st = get_workspace(dev, stream, (int64_t)S * M, tiles, &ws);
+        std::lock_guard<std::mutex> lk(g_mu); // until the launch (see get_workspace_locked)
+        st = get_workspace_locked(dev, stream, (int64_t)S * M, tiles, &ws);
         if (st != TVL_OK) return st;
         e = tvl::launch_gemv_ksplit(shape, dtype, W, ldw, x, y, (int)M, (int)K, S, ws.partials,
                                     ws.counters, stream);

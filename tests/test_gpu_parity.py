@@ -432,3 +432,57 @@ def test_batch_sweep_cache_under_threads():
             r = oracle.check(Yh[t, j], ref, S, 1e-5)
             assert r["bad"] == 0, (t, j, r)
     tvl.tvl_release_workspaces()
+
+
+def test_ksplit_workspaces_under_threads():
+    """K-split GEMVs (few long rows) from four host threads, each on its own
+    stream, while a fifth thread frees the K-split workspaces again and
+    again: a call must never launch with a workspace another thread has just
+    freed or replaced.  Every result is checked against the oracle."""
+    import threading
+    import time
+    rng = np.random.default_rng(123)
+    M, K, nthr, reps = 64, 12288, 4, 25  # 48 KB rows, M <= 128: the library's K split
+    W = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    buf, ldw = dev_matrix(W, 0)
+    xs = rng.standard_normal((reps, K)).astype(np.float32)
+    X = torch.from_numpy(xs).to(DEV)
+    Y = torch.full((nthr, reps, M), float("nan"), device=DEV)
+    torch.cuda.synchronize()
+    errors, done = [], threading.Event()
+
+    def worker(t):
+        try:
+            s = torch.cuda.Stream()
+            for r in range(reps):
+                tvl.tvl_gemv(buf, ldw, 0, X[r], Y[t, r], M, K, stream=s)
+            s.synchronize()
+        except Exception as exc:  # reported below
+            errors.append((t, exc))
+
+    def releaser():
+        try:
+            while not done.is_set():
+                tvl.tvl_release_workspaces()
+                time.sleep(0.001)
+        except Exception as exc:
+            errors.append(("release", exc))
+
+    rel = threading.Thread(target=releaser)
+    rel.start()
+    ths = [threading.Thread(target=worker, args=(t,)) for t in range(nthr)]
+    for th in ths:
+        th.start()
+    for th in ths:
+        th.join()
+    done.set()
+    rel.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    Yh = Y.cpu().numpy()
+    for r in range(reps):
+        ref, S = oracle.gemv_f32(W, xs[r])
+        for t in range(nthr):
+            res = oracle.check(Yh[t, r], ref, S, 1e-5)
+            assert res["bad"] == 0, (t, r, res)
+    tvl.tvl_release_workspaces()
