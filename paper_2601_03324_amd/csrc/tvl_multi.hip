@@ -180,9 +180,10 @@ __global__ __launch_bounds__(WV *kWave) void k_item_multi(const DevItem it)
 // 4-float accumulator, for block b = l / 4.
 //
 // So the four lanes of a quad must hold four rows (and four vectors) at one
-// column.  Loading that layout directly has every quad touch four cache
-// lines, and the texture unit then spends four times the cycles per load;
-// instead every load here is the fully coalesced one of the VALU kernels
+// column.  Loading that layout directly would have every quad touch four
+// cache lines (the direct-load 16 x 16 x 4 form below has loads of that kind
+// and measures what they cost); instead every load here is the fully
+// coalesced one of the VALU kernels
 // (lane l reads 16 bytes at column N l of ONE row: 1 KB per wavefront load),
 // four rows (or four vectors) are loaded, and a 4 x 4 transpose across each
 // quad (two DPP exchange steps) moves row q's 16 bytes at column N (4 b + s)
