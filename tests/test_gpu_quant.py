@@ -179,3 +179,38 @@ def test_quant_7b_layer_shapes(dt):
         Wq, ldw, x = quant_case(M ^ K ^ dt, M, K, dt)
         yref, S = oracle.gemv_q(Wq, BITS[dt], ldw, M, K, x)
         check(run_item(Wq, ldw, dt, x, M, K), yref, S, f"{M}x{K}")
+
+
+@pytest.mark.parametrize("name", ["sweep110m_q8", "sweep110m_q4", "sweep7b_q4"])
+def test_quant_sweeps_in_one_launch(name):
+    """Whole decode tokens with block-quantised weights in the launch the
+    bench times (one plan, the library's default shape): 40 sampled rows of
+    every matrix (first, last, random), each regenerated and quantised on
+    its own, against the oracle."""
+    import zlib
+    import synth.device as sdev
+    wl = synth.WORKLOADS[name]
+    log(f"{name}: generating and uploading {wl.weight_bytes() / 1e9:.2f} GB")
+    gemvs = sdev.load(wl, DEV, progress=True)
+    for g in gemvs:
+        g.y.fill_(float("nan"))
+    plan = tvl.tvl_sweep_plan_create([g.item() for g in gemvs])
+    plan.run()
+    torch.cuda.synchronize()
+    worst = 0.0
+    for g in gemvs:
+        m = g.spec
+        y = g.y.cpu().numpy()
+        x = g.x.cpu().numpy()
+        idx = sdev.sample_rows(m.M, 40, zlib.crc32(m.name.encode()))
+        ys, Ss = [], []
+        for r in idx:
+            yr, Sr = oracle.gemv_q(m.weights(int(r), 1), m.bits, synth.q_row_bytes(m.K, m.bits),
+                                   1, m.K, x)
+            ys.append(yr[0])
+            Ss.append(Sr[0])
+        worst = max(worst, check(y[idx], np.array(ys), np.array(Ss), f"{name} {m.name}"))
+    log(f"{name}: max normalised error {worst:.3e}")
+    plan.destroy()
+    del gemvs
+    torch.cuda.empty_cache()
