@@ -413,12 +413,35 @@ def pin_quant_matches_dequantized():
                     assert oracle.q_weight(Wq, bits, ldw, M, K, i, j) == float(deq[i, j])
 
 
+def pin_quant_exact_rational():
+    """Arbitrary fp32 scales (not powers of two): against exact rational sums of
+    s * q * x.  A product s q x can need 24 + 8 + 24 significand bits, more
+    than double holds, so the bound is K * 2^-52 * S (product and sum
+    roundings), not equality."""
+    from fractions import Fraction
+    rng = np.random.default_rng(24)
+    for bits, lo, hi in ((8, -127, 127), (4, -7, 7)):
+        for M, K in ((1, 1), (3, 65), (4, 130), (2, 200)):
+            codes = rng.integers(lo, hi + 1, (M, K))
+            scales = rng.uniform(1e-3, 1.0, (M, (K + 63) // 64)).astype(np.float32)
+            Wq, ldw = _q_rows(codes, scales, bits)
+            x = rng.standard_normal(K).astype(np.float32)
+            y, S = oracle.gemv_q(Wq, bits, ldw, M, K, x)
+            for i in range(M):
+                exact = sum(Fraction(float(scales[i, j // 64])) * int(codes[i, j])
+                            * Fraction(float(x[j])) for j in range(K))
+                s_abs = sum(abs(Fraction(float(scales[i, j // 64])) * int(codes[i, j])
+                                * Fraction(float(x[j]))) for j in range(K))
+                assert abs(Fraction(y[i]) - exact) <= K * Fraction(2) ** -52 * s_abs, (bits, M, K, i)
+                assert abs(Fraction(S[i]) - s_abs) <= K * Fraction(2) ** -52 * s_abs
+
+
 PINS = [pin_golden, pin_products_exact, pin_brute_force_exact, pin_brute_force_exact_f16,
         pin_index_and_stride, pin_identity, pin_all_ones_rows, pin_integer_exact,
         pin_linearity, pin_one_hot, pin_zero_row, pin_f16_decode_all_patterns,
         pin_f16_subnormal_gemv, pin_check_rules, pin_rmsnorm_closed_forms,
         pin_rmsnorm_invariances, pin_rmsnorm_gemv, pin_swiglu, pin_quant_golden,
-        pin_quant_matches_dequantized]
+        pin_quant_matches_dequantized, pin_quant_exact_rational]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=[p.__name__ for p in PINS])
