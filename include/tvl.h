@@ -158,7 +158,8 @@ typedef struct tvl_item {
  *                   at once (32 and 64: several-vector launches only)
  *   waves_per_block W in {1, 2, 4, 8}: wavefronts per workgroup
  *   unroll          U in {1, 2, 3, 4, 8}: 16-byte weight loads per row kept in
- *                   flight per lane
+ *                   flight per lane (several-vector launches: selects the
+ *                   matrix-core form, below; 6 and 12 occur there only)
  *   ksplit          S >= 1: K slices per row tile (tvl_gemv only; 1 = row
  *                   split)
  *   grid            workgroups of a sweep launch (0 = one per tile); a smaller
@@ -183,9 +184,15 @@ typedef struct tvl_item {
  * and, for any nrhs <= 16, on the matrix cores: the 4x4x1 form (rows in
  * groups of 4, U = 1) (8,4,1) (16,1,1) (16,2,1); the 16x16x4 form (rows
  * in groups of 16, U = loads per group in flight) (16,4,8) (32,1,4) (32,2,4)
- * (64,1,4); and the 16x16x4 form with rows staged through LDS (U = 2; fp32
- * weights; a launch holding fp16 weights runs the previous form with the
- * same rows and waves, U = 4) (16,1,2) (16,4,2) (32,1,2) (32,2,2) (32,4,2)
+ * (64,1,4); the 16x16x4 form with rows staged through LDS from registers
+ * (U = 2; fp32 and fp16 weights) (16,1,2) (16,4,2) (32,1,2) (32,2,2)
+ * (32,4,2) (64,1,2); and the 16x16x4 form with fp32 weights streamed into
+ * LDS by the loads themselves (U = 3: 128-column chunks, 6: 64, 12: 32; a
+ * launch holding fp16 weights runs the previous form with the same rows and
+ * waves) (16,1,3) (16,2,3) (16,4,3) (16,1,6) (16,2,6) (16,4,6) (32,1,6)
+ * (32,2,6) (32,1,12) (64,1,12) (64,2,12).  Rows longer than these forms'
+ * buffer descriptors can address (a load's 2, 4 or 8 rows within 2^31
+ * bytes) run the direct-load 16x16x4 form.
  * Launches holding block-quantised items (direct-x only; R rows per group of
  * lanes, see tvl_dtype): (2,4,2) (4,4,1) (4,4,2) (4,1,2) (8,4,1) (8,2,1) */
 typedef struct tvl_tuning {

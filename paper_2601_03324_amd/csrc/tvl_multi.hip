@@ -543,10 +543,9 @@ struct InstMfma {
 // 8 whole ones (the other half comes with the next load of the same batch).
 // HBM bytes stay within 4 % of the whole-line form, but the L1 receives 1.7x
 // the requests and the address unit stalls on it (rocprofv3 on MI355X), so
-// this form tops out near 3.8 TB/s whatever the vector count.  For fp32
-// weights the LDS-staged form below avoids the half lines and is faster; this
-// form serves launches with fp16 weights from 9 to 16 vectors, where the
-// 4 x 4 x 1 form runs out of registers.
+// this form tops out near 3.8 TB/s whatever the vector count.  The LDS-staged
+// forms below avoid the half lines and are faster; this form serves their
+// rows too long for a buffer descriptor and explicit tunings.
 //
 // The x loads (vector i, columns as for the weights) hit the cache: every
 // wavefront of a matrix reads the same vectors; RG groups of 16 rows share
@@ -768,80 +767,106 @@ struct InstMfma16 {
 };
 
 // -------------------------------- matrix cores, 16 x 16 x 4, LDS-staged rows
-// The same contraction as above for fp32 weights, with whole-line weight
-// loads: a wavefront load brings 512 contiguous bytes of each of two rows
-// (lanes 0-31: row 2t, lanes 32-63: row 2t + 1), so each load covers 8 whole
-// 128-byte lines.  The rows go to a wavefront-private LDS tile and come back
-// in the A-operand layout (lane 16 g + i: row i, 16-byte block 4 q + g).
-// Rows sit 528 bytes apart (512 + 16 of padding), so row i starts 4 i banks
-// further on: the 16 lanes reading one 16-byte block of 16 rows hit 16
-// different bank groups, and every LDS access of a chunk is one base
-// register plus an immediate offset.  One wavefront's LDS reads follow its
-// writes in order: no barrier.  The x vectors keep their direct B-layout
-// loads.  Accumulation as in the form above, with 32 MFMA steps per chunk.
-constexpr int kLdsCols = 128;                   // columns per chunk (512 bytes of a row)
+// The same contraction as above with whole-line weight loads: every
+// wavefront load covers whole 128-byte lines of the rows.  fp32: lanes 0-31
+// bring 512 contiguous bytes of row 2t and lanes 32-63 those of row 2t + 1
+// (8 lines); fp16: each 16-lane quarter brings 256 bytes of one of the rows
+// 4t .. 4t + 3 (8 lines), converted exactly to fp32 in registers.  The rows
+// go to a wavefront-private LDS tile of fp32 values and come back in the
+// A-operand layout (lane 16 g + i: row i, 16-byte block 4 q + g).  Rows sit
+// 528 bytes apart (512 + 16 of padding), so row i starts 4 i banks further
+// on: the 16 lanes reading one 16-byte block of 16 rows hit 16 different
+// bank groups, and every LDS access of a chunk is one base register plus an
+// immediate offset.  One wavefront's LDS reads follow its writes in order:
+// no barrier.  The x vectors keep their direct B-layout loads.
+// Accumulation as in the form above, with 32 MFMA steps per chunk.
+//
+// Which columns an LDS block holds (the x loads follow the same map):
+//   fp32: block k holds columns 4k .. 4k + 3 of the chunk;
+//   fp16: the lane that loads columns 8j .. 8j + 7 writes their first half
+//         to block j and their second half to block 16 + j, so the 16 lanes
+//         of a row write 16 consecutive blocks.  Block k < 16 then holds
+//         columns 8k .. 8k + 3, block 16 + k columns 8k + 4 .. 8k + 7.
+constexpr int kLdsCols = 128;                   // columns per chunk (one LDS row)
 constexpr int kLdsRow = kLdsCols / 4 + 1;       // f4 per LDS row, padding included
 
-// Row pairs are read through buffer descriptors: the descriptor of pair t
-// starts at the pair's first row and holds only its rows below M (0, 1 or
-// 2 rows), so the hardware's range check returns zeros for rows past M and
-// every load needs just one 32-bit lane offset (h ldw 4 + 16 b) in a VGPR,
-// the chunk's column in the scalar offset.  Two rows must then fit in the
-// descriptor's 31-bit size: rows of up to kLdsMaxLdw floats (1 GiB rows go
-// to the direct-load form).
+// Row groups (2 fp32 or 4 fp16 rows, 1 KiB of a chunk) are read through
+// buffer descriptors: the descriptor of group t starts at the group's first
+// row and holds only its rows below M, so the hardware's range check returns
+// zeros for rows past M and every load needs just one 32-bit lane offset in
+// a VGPR, the chunk's column in the scalar offset.  A group must then fit in
+// the descriptor's 31-bit size: 8 ldw bytes, rows of up to kLdsMaxLdw
+// elements (longer rows go to the direct-load form).
 constexpr int64_t kLdsMaxLdw = (int64_t(1) << 28) - 64;
 
-template <int RG>
+template <typename T, int RG>
 struct MfmaLdsRows {
-    static constexpr int NT = 8 * RG; // row-pair loads per chunk
-    const float *W;  // the wavefront's first row (wavefront-uniform)
+    static constexpr int ES = (int)sizeof(T);
+    static constexpr int LR = kLdsCols * ES / 16; // lanes per row of a load (16 bytes each)
+    static constexpr int RL = kWave / LR;         // rows per load
+    static constexpr int NT = 16 / RL * RG;       // loads per chunk
+    static_assert(RL * LR == kWave && 16 % RL == 0, "a load covers whole rows of a chunk");
+    const T *W;      // the wavefront's first row (wavefront-uniform)
     int64_t ldw;
-    const float *xv; // vector i (clamped), at column 4 g
+    const float *xv; // vector i (clamped)
     int vrows, kn, lane;
-    int voff; // this lane's byte offset in a row pair
+    int voff; // this lane's byte offset in a row group
 
-    __device__ __forceinline__ MfmaLdsRows(const float *W_, int64_t ldw_, int wrow0, int M,
+    __device__ __forceinline__ MfmaLdsRows(const T *W_, int64_t ldw_, int wrow0, int M,
                                            const float *x, int64_t ldx, int nb, int K, int lane_)
         : W(W_ + (int64_t)wrow0 * ldw_), ldw(ldw_), vrows(M - wrow0), kn(K), lane(lane_),
-          voff((int)((lane_ >> 5) * ldw_ * 4 + 16 * (lane_ & 31)))
+          voff((int)((lane_ / LR) * ldw_ * ES + 16 * (lane_ % LR)))
     {
-        xv = x + (int64_t)min(lane & 15, nb - 1) * ldx + 4 * (lane >> 4);
+        xv = x + (int64_t)min(lane & 15, nb - 1) * ldx;
     }
 
-    // rows 2 t, 2 t + 1 of the wavefront, those below M
-    __device__ __forceinline__ __amdgpu_buffer_rsrc_t pair(int t) const
+    // chunk column of x block 4 q + g (the map above)
+    static __device__ __forceinline__ int xcol(int q, int g)
     {
-        const int n = min(max(vrows - 2 * t, 0), 2);
-        return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(W + 2 * t * ldw), (short)0,
-                                                 (int)(n * ldw * 4), 0x00020000);
+        if constexpr (ES == 4)
+            return 16 * q + 4 * g;
+        else
+            return 32 * (q & 3) + 8 * g + 4 * (q >> 2);
+    }
+
+    // rows RL t .. RL t + RL - 1 of the wavefront, those below M
+    __device__ __forceinline__ __amdgpu_buffer_rsrc_t group(int t) const
+    {
+        const int n = min(max(vrows - RL * t, 0), RL);
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<T *>(W + RL * t * ldw), (short)0,
+                                                 (int)(n * ldw * ES), 0x00020000);
+    }
+
+    // one 16-byte load: columns c0 + (16 / ES) (lane % LR) .. of its row,
+    // non-temporal (cache policy 2) like load_w
+    __device__ __forceinline__ u4 load(int t, int c0) const
+    {
+        return __builtin_bit_cast(
+            u4, __builtin_amdgcn_raw_buffer_load_b128(group(t), voff, ES * c0, 2));
     }
 
     // tile: this wavefront's 16 LDS rows of kLdsRow float4
     template <bool RAGGED>
     __device__ __forceinline__ void chunk(int c0, f4 *tile, f4 (&acc)[RG]) const
     {
-        const int g = lane >> 4, i = lane & 15, h = lane >> 5, b = lane & 31;
+        const int g = lane >> 4, i = lane & 15, b = lane % LR;
         const f4 z = {0.f, 0.f, 0.f, 0.f};
-        f4 w[NT], xb[8];
-        const int wcol = c0 + 4 * b;
+        const u4 zu = {0u, 0u, 0u, 0u};
+        u4 w[NT];
+        f4 xb[8];
+        const int wcol = c0 + (16 / ES) * b;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            // non-temporal (cache policy 2), like load_w
             if constexpr (RAGGED)
-                w[t] = wcol < kn ? mask_from<f4, 4>(__builtin_bit_cast(
-                                       f4, __builtin_amdgcn_raw_buffer_load_b128(
-                                               pair(t), voff, 4 * c0, 2)),
-                                   kn - wcol)
-                                 : z;
+                w[t] = wcol < kn ? load(t, c0) : zu;
             else
-                w[t] = __builtin_bit_cast(
-                    f4, __builtin_amdgcn_raw_buffer_load_b128(pair(t), voff, 4 * c0, 2));
+                w[t] = load(t, c0);
         }
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-            const int c = c0 + 16 * q;
+            const int c = c0 + xcol(q, g);
             if constexpr (RAGGED) {
-                const int valid = kn - (c + 4 * g);
+                const int valid = kn - c;
                 xb[q] = valid > 0 ? mask_from<f4, 4>(load_x4(xv + c), valid) : z;
             } else {
                 xb[q] = load_x4(xv + c);
@@ -851,13 +876,29 @@ struct MfmaLdsRows {
         // one 16-row group at a time through the same 16 LDS rows (a
         // wavefront's LDS accesses run in order: group rg + 1 overwrites
         // rows that group rg has finished reading)
-        f4 *wt = tile + h * kLdsRow + b;       // row h, block b (+ 2 rows per load)
-        const f4 *rt = tile + i * kLdsRow + g; // row i, block g (+ 4 q blocks)
+        f4 *wt = tile + (lane / LR) * kLdsRow + b; // row lane / LR, block b
+        const f4 *rt = tile + i * kLdsRow + g;      // row i, block g (+ 4 q blocks)
 #pragma unroll
         for (int rg = 0; rg < RG; ++rg) {
 #pragma unroll
-            for (int t = 0; t < 8; ++t)
-                wt[2 * t * kLdsRow] = w[8 * rg + t];
+            for (int t = 0; t < 16 / RL; ++t) {
+                const u4 raw = w[16 / RL * rg + t];
+                if constexpr (ES == 4) {
+                    f4 v = __builtin_bit_cast(f4, raw);
+                    if constexpr (RAGGED) v = mask_from<f4, 4>(v, kn - wcol);
+                    wt[RL * t * kLdsRow] = v;
+                } else {
+                    const f8 wf = __builtin_convertvector(__builtin_bit_cast(h8, raw), f8);
+                    f4 lo = {wf[0], wf[1], wf[2], wf[3]};
+                    f4 hi = {wf[4], wf[5], wf[6], wf[7]};
+                    if constexpr (RAGGED) {
+                        lo = mask_from<f4, 4>(lo, kn - wcol);
+                        hi = mask_from<f4, 4>(hi, kn - wcol - 4);
+                    }
+                    wt[RL * t * kLdsRow] = lo;
+                    wt[RL * t * kLdsRow + 16] = hi;
+                }
+            }
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
                 const f4 a = rt[4 * q];
@@ -901,11 +942,11 @@ struct MfmaLdsRows {
     }
 };
 
-template <int RG, int WV>
+template <typename T, int RG, int WV>
 __device__ __forceinline__ void tile_mfma_lds(const DevItem &it, int row0, f4 *tile)
 {
     if (it.ldw > kLdsMaxLdw) { // wavefront-uniform
-        tile_mfma16<float, RG, 4, WV>(it, row0);
+        tile_mfma16<T, RG, 4, WV>(it, row0);
         return;
     }
     const int lane = threadIdx.x & (kWave - 1);
@@ -914,8 +955,8 @@ __device__ __forceinline__ void tile_mfma_lds(const DevItem &it, int row0, f4 *t
     if (wrow0 >= it.M) return; // no barrier follows
     const int nb = it.nrhs < 1 ? 1 : it.nrhs;
     f4 out[RG];
-    const MfmaLdsRows<RG> mr(static_cast<const float *>(it.W), it.ldw, wrow0, it.M, it.x, it.ldx,
-                             nb, it.K, lane);
+    const MfmaLdsRows<T, RG> mr(static_cast<const T *>(it.W), it.ldw, wrow0, it.M, it.x, it.ldx,
+                                nb, it.K, lane);
     mr.run(tile, out);
     const int i = lane & 15, g = lane >> 4;
     if (i < nb) {
@@ -930,8 +971,20 @@ __device__ __forceinline__ void tile_mfma_lds(const DevItem &it, int row0, f4 *t
     }
 }
 
-// fp32 weights only (the launcher sends other launches to the direct form)
-template <int RG, int WV>
+template <int WM, int RG, int WV>
+__device__ __forceinline__ void tile_mfma_lds_w(const DevItem &it, int row0, f4 *tile)
+{
+    if constexpr (WM == kWF32)
+        tile_mfma_lds<float, RG, WV>(it, row0, tile);
+    else if constexpr (WM == kWF16)
+        tile_mfma_lds<_Float16, RG, WV>(it, row0, tile);
+    else if (it.dtype == 1)
+        tile_mfma_lds<_Float16, RG, WV>(it, row0, tile);
+    else
+        tile_mfma_lds<float, RG, WV>(it, row0, tile);
+}
+
+template <int WM, int RG, int WV>
 __global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_lds(const DevItem *__restrict__ items,
                                                                const DevTile *__restrict__ tiles,
                                                                int ntiles)
@@ -942,18 +995,286 @@ __global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_lds(const DevItem *__r
     for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const DevTile tl = tiles[t];
         const DevItem it = items[tl.item];
-        tile_mfma_lds<RG, WV>(it, tl.row0, tile);
+        tile_mfma_lds_w<WM, RG, WV>(it, tl.row0, tile);
         __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
     }
 }
 
-template <int RG, int WV>
+template <int WM, int RG, int WV>
 __global__ __launch_bounds__(WV *kWave) void k_item_mfma_lds(const DevItem it)
 {
     constexpr int kTile = 16 * kLdsRow;
     __shared__ f4 lds[WV * kTile];
     f4 *tile = lds + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave) * kTile;
-    tile_mfma_lds<RG, WV>(it, (int)blockIdx.x * (16 * RG * WV), tile);
+    tile_mfma_lds_w<WM, RG, WV>(it, (int)blockIdx.x * (16 * RG * WV), tile);
+}
+
+// ------------------- matrix cores, 16 x 16 x 4, weights streamed into LDS
+// fp32 weights in the same contraction, with the weight loads writing LDS
+// directly: a buffer load with the LDS bit puts lane l's 16 bytes at
+// M0 + 16 l and holds no VGPR, so a wavefront keeps the next two chunks in
+// flight while it multiplies the current one (three LDS stages per
+// wavefront).  One load covers 1 KiB: the chunk of RPL rows (CC * 4 bytes
+// each), lane l landing in row l / LPR at 16-byte position l % LPR.  Rows
+// are stored without padding, so the blocks of row r are XOR-swizzled (the
+// lane at position p reads block p ^ f(r)) such that the 16 lanes that read
+// one block of 16 rows hit the 16 different 16-byte bank groups of a 256-
+// byte LDS line: f(r) = r for rows of 256 bytes or more, f(r) = r / 2 for
+// 128-byte rows (two rows per line).  x: direct B-layout loads one chunk
+// ahead, in registers; more rows per wavefront share each x load (x from
+// the cache adds nb 4 CC bytes per chunk of 16 RG rows to the weights'
+// 16 RG 4 CC).
+//
+// Each chunk step issues, in this order, the x loads of the next chunk (NQ)
+// and the weight loads of the chunk after that (NL); near the end of the
+// rows the same loads go to empty descriptors (no memory access; they fill
+// a stage that is no longer read) and to the last chunk's x.  So 2 NQ + 2 NL
+// loads always follow a chunk's weight loads when its products start, and
+// one fixed vmcnt wait brings them in while two chunks stay in flight.  A
+// ragged last chunk drains the loads and goes through registers (masked) into
+// the same layout.  Accumulation as in the forms above (4 NQ MFMA steps per
+// chunk).
+#define TVL_LDS __attribute__((address_space(3)))
+
+// 16 bytes per lane from a buffer into LDS at lds + 16 lane (non-temporal)
+__device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, TVL_LDS void *lds, int voff,
+                                          int soff)
+{
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, voff, soff, 0, 2);
+}
+
+template <int RG, int CC>
+struct MfmaDmaRows {
+    static constexpr int RB = CC * 4;          // bytes of a row's chunk (one LDS row)
+    static constexpr int RPL = 1024 / RB;      // rows per load
+    static constexpr int LPR = kWave / RPL;    // lanes (16-byte positions) per row
+    static constexpr int TPG = 16 / RPL;       // loads per 16-row group
+    static constexpr int NL = TPG * RG;        // weight loads per chunk
+    static constexpr int NQ = CC / 16;         // x loads and MFMA column steps per chunk
+    static constexpr int STAGE = 16 * RG * RB; // bytes per stage
+    static constexpr int kStages = 3;
+    static constexpr int WAIT = 2 * NL + 2 * NQ;
+    static constexpr int SH = RB < 256 ? 1 : 0; // rows per 256-byte line, log2
+    // RPL rows in a buffer descriptor's 31-bit size
+    static constexpr int64_t MAXLDW = (int64_t(1) << 31) / (4 * RPL) - 32;
+    static_assert(RB >= 128 && LPR * RPL == kWave && WAIT < 64, "chunk shape");
+
+    // the swizzle of row r (0..15 in its group)
+    static __device__ __forceinline__ int swz(int r) { return (r >> SH) & (LPR - 1); }
+
+    const float *W; // the wavefront's first row (wavefront-uniform)
+    int64_t ldw;
+    const float *xv; // vector i (clamped), at column 4 g
+    int vrows, kn, lane;
+    TVL_LDS char *lds; // this wavefront's stages
+    int voff[TPG];     // per load of a row group: the lane's byte offset in it
+    int raddr[NQ];     // per MFMA column step: the lane's A block in a stage
+
+    __device__ __forceinline__ MfmaDmaRows(const float *W_, int64_t ldw_, int wrow0, int M,
+                                           const float *x, int64_t ldx, int nb, int K, int lane_,
+                                           TVL_LDS char *lds_)
+        : W(W_ + (int64_t)wrow0 * ldw_), ldw(ldw_), vrows(M - wrow0), kn(K), lane(lane_),
+          lds(lds_)
+    {
+        xv = x + (int64_t)min(lane & 15, nb - 1) * ldx + 4 * (lane >> 4);
+        const int h = lane / LPR, p = lane % LPR, g = lane >> 4, i = lane & 15;
+#pragma unroll
+        for (int t = 0; t < TPG; ++t)
+            voff[t] = (int)(h * ldw_ * 4) + 16 * (p ^ swz(RPL * t + h));
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+            raddr[q] = i * RB + 16 * ((4 * q + g) ^ swz(i));
+    }
+
+    // rows RPL j .. RPL j + RPL - 1 of the wavefront, those below M; none if
+    // !live
+    __device__ __forceinline__ __amdgpu_buffer_rsrc_t group(int j, bool live) const
+    {
+        const int n = live ? min(max(vrows - RPL * j, 0), RPL) : 0;
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(W + RPL * j * ldw), (short)0,
+                                                 (int)(n * ldw * 4), 0x00020000);
+    }
+
+    // the chunk at column c0 into stage ST (non-temporal, cache policy 2)
+    template <int ST>
+    __device__ __forceinline__ void issue(int c0, bool live) const
+    {
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+            for (int t = 0; t < TPG; ++t)
+                lds_dma16(group(TPG * rg + t, live),
+                          (TVL_LDS void *)(lds + ST * STAGE + rg * 16 * RB + t * 1024), voff[t],
+                          4 * c0);
+    }
+
+    __device__ __forceinline__ void load_x(int c0, f4 (&xb)[NQ]) const
+    {
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+            xb[q] = load_x4(xv + c0 + 16 * q);
+    }
+
+    template <int ST>
+    __device__ __forceinline__ void multiply(const f4 (&xb)[NQ], f4 (&acc)[RG]) const
+    {
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+                const f4 a =
+                    *(const TVL_LDS f4 *)(lds + ST * STAGE + rg * 16 * RB + raddr[q]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    acc[rg] = mfma16(a[e], xb[q][e], acc[rg]);
+            }
+    }
+
+    // one chunk step (chunk c in stage ST, its x in X, the next x into Y);
+    // true after the last full chunk
+    template <int ST>
+    __device__ __forceinline__ bool step(int &c, int nfull, f4 (&X)[NQ], f4 (&Y)[NQ],
+                                         f4 (&acc)[RG], f4 (&t1)[RG], f4 (&t2)[RG],
+                                         int &n1) const
+    {
+        const f4 z = {0.f, 0.f, 0.f, 0.f};
+        load_x(min(c + 1, nfull - 1) * CC, Y);
+        issue<(ST + 2) % kStages>((c + 2) * CC, c + 2 < nfull);
+        __builtin_amdgcn_sched_barrier(0);
+        // vmcnt(WAIT): expcnt and lgkmcnt left alone
+        __builtin_amdgcn_s_waitcnt((WAIT & 15) | ((WAIT >> 4) << 14) | 0x0F70);
+        __builtin_amdgcn_sched_barrier(0);
+        multiply<ST>(X, acc);
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg) {
+            t1[rg] += acc[rg];
+            acc[rg] = z;
+        }
+        if (++n1 == kMfmaLevel) {
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg) {
+                t2[rg] += t1[rg];
+                t1[rg] = z;
+            }
+            n1 = 0;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        return ++c == nfull;
+    }
+
+    // the ragged last chunk at c0 (after every load has landed), through
+    // registers into stage 0
+    __device__ __forceinline__ void tail(int c0, f4 (&acc)[RG]) const
+    {
+        const f4 z = {0.f, 0.f, 0.f, 0.f};
+        const int h = lane / LPR, p = lane % LPR, g = lane >> 4;
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+            for (int t = 0; t < TPG; ++t) {
+                const int wcol = c0 + 4 * (p ^ swz(RPL * t + h));
+                f4 w = z;
+                if (wcol < kn)
+                    w = mask_from<f4, 4>(
+                        __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                   group(TPG * rg + t, true), voff[t], 4 * c0, 2)),
+                        kn - wcol);
+                *(TVL_LDS f4 *)(lds + rg * 16 * RB + t * 1024 + 16 * lane) = w;
+            }
+        f4 xb[NQ];
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int valid = kn - (c0 + 16 * q + 4 * g);
+            xb[q] = valid > 0 ? mask_from<f4, 4>(load_x4(xv + c0 + 16 * q), valid) : z;
+        }
+        multiply<0>(xb, acc);
+    }
+
+    __device__ __forceinline__ void run(f4 (&out)[RG]) const
+    {
+        const f4 z = {0.f, 0.f, 0.f, 0.f};
+        f4 acc[RG], t1[RG], t2[RG];
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+            acc[rg] = t1[rg] = t2[rg] = z;
+        const int nfull = kn / CC;
+        int c = 0, n1 = 0;
+        if (nfull > 0) {
+            f4 xa[NQ], xb[NQ];
+            issue<0>(0, true);
+            load_x(0, xa);
+            issue<1>(CC, nfull > 1);
+            // stages rotate by 3 and x buffers by 2: six steps per turn
+            for (;;) {
+                if (step<0>(c, nfull, xa, xb, acc, t1, t2, n1)) break;
+                if (step<1>(c, nfull, xb, xa, acc, t1, t2, n1)) break;
+                if (step<2>(c, nfull, xa, xb, acc, t1, t2, n1)) break;
+                if (step<0>(c, nfull, xb, xa, acc, t1, t2, n1)) break;
+                if (step<1>(c, nfull, xa, xb, acc, t1, t2, n1)) break;
+                if (step<2>(c, nfull, xb, xa, acc, t1, t2, n1)) break;
+            }
+            __builtin_amdgcn_s_waitcnt(0x0F70); // the empty loads too, before LDS is reused
+        }
+        if (c * CC < kn)
+            tail(c * CC, acc);
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+            out[rg] = t2[rg] + (t1[rg] + acc[rg]);
+    }
+};
+
+template <int RG, int WV, int CC>
+__device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_LDS char *lds)
+{
+    using Rows = MfmaDmaRows<RG, CC>;
+    if (it.ldw > Rows::MAXLDW) { // wavefront-uniform
+        tile_mfma16<float, RG, 4, WV>(it, row0);
+        return;
+    }
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wrow0 = row0 + wave * (16 * RG);
+    if (wrow0 >= it.M) return; // no barrier follows
+    const int nb = it.nrhs < 1 ? 1 : it.nrhs;
+    f4 out[RG];
+    const Rows mr(static_cast<const float *>(it.W), it.ldw, wrow0, it.M, it.x, it.ldx, nb, it.K,
+                  lane, lds + wave * (Rows::kStages * Rows::STAGE));
+    mr.run(out);
+    const int i = lane & 15, g = lane >> 4;
+    if (i < nb) {
+        float *yv = it.y + (int64_t)i * it.ldy;
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = wrow0 + 16 * rg + 4 * g + v;
+                if (row < it.M) yv[row] = out[rg][v];
+            }
+    }
+}
+
+// fp32 weights only (the launcher sends other launches to the LDS-staged form)
+template <int RG, int WV, int CC>
+__global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_dma(const DevItem *__restrict__ items,
+                                                               const DevTile *__restrict__ tiles,
+                                                               int ntiles)
+{
+    using Rows = MfmaDmaRows<RG, CC>;
+    __shared__ f4 lds[WV * Rows::kStages * Rows::STAGE / 16];
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+        const DevTile tl = tiles[t];
+        const DevItem it = items[tl.item];
+        tile_mfma_dma<RG, WV, CC>(it, tl.row0, (TVL_LDS char *)lds);
+        __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
+    }
+}
+
+template <int RG, int WV, int CC>
+__global__ __launch_bounds__(WV *kWave) void k_item_mfma_dma(const DevItem it)
+{
+    using Rows = MfmaDmaRows<RG, CC>;
+    __shared__ f4 lds[WV * Rows::kStages * Rows::STAGE / 16];
+    tile_mfma_dma<RG, WV, CC>(it, (int)blockIdx.x * (16 * RG * WV), (TVL_LDS char *)lds);
 }
 
 // (rows per wavefront = 16 RG, waves per block, U = 2 marks this form).
@@ -961,25 +1282,62 @@ __global__ __launch_bounds__(WV *kWave) void k_item_mfma_lds(const DevItem it)
 // next chunk's loads issued before the current chunk's products (~200 VGPRs
 // at 16 rows: 4.9-5.0 against 5.2-5.3 TB/s), and x staged through LDS too
 // (whole-line x loads: 5.05 against 5.24 TB/s).
-#define TVL_MFMA_LDS_SHAPES(X) X(16, 1, 2) X(16, 4, 2) X(32, 1, 2) X(32, 2, 2) X(32, 4, 2)
+#define TVL_MFMA_LDS_SHAPES(X) X(16, 1, 2) X(16, 4, 2) X(32, 1, 2) X(32, 2, 2) X(32, 4, 2) X(64, 1, 2)
+
+// (rows per wavefront = 16 RG, waves per block, U, columns per chunk) of the
+// form with weights streamed into LDS: U = 3 for 128-column chunks, 6 for
+// 64, 12 for 32.
+#define TVL_MFMA_DMA_SHAPES(X)                                                                    \
+    X(16, 1, 3, 128) X(16, 2, 3, 128) X(16, 4, 3, 128) X(16, 1, 6, 64) X(16, 2, 6, 64)            \
+        X(16, 4, 6, 64) X(32, 1, 6, 64) X(32, 2, 6, 64) X(32, 1, 12, 32) X(64, 1, 12, 32)         \
+            X(64, 2, 12, 32)
 
 template <int R, int WV, int U>
 struct InstMfmaLds {
     static constexpr int RG = R / 16;
+    template <int WM>
+    static hipError_t sweep_w(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
+                              hipStream_t st)
+    {
+        hipLaunchKernelGGL((k_sweep_mfma_lds<WM, RG, WV>), dim3(grid), dim3(WV * kWave), 0, st,
+                           items, tiles, ntiles);
+        return hipGetLastError();
+    }
     static hipError_t sweep(int wm, const DevItem *items, const DevTile *tiles, int ntiles,
                             int grid, hipStream_t st)
     {
-        if (wm != kWF32) // fp16 weights: the direct-load form with the same rows
-            return InstMfma16<R, WV, 4>::sweep(wm, items, tiles, ntiles, grid, st);
-        hipLaunchKernelGGL((k_sweep_mfma_lds<RG, WV>), dim3(grid), dim3(WV * kWave), 0, st, items,
-                           tiles, ntiles);
+        return wm == kWF32   ? sweep_w<kWF32>(items, tiles, ntiles, grid, st)
+               : wm == kWF16 ? sweep_w<kWF16>(items, tiles, ntiles, grid, st)
+                             : sweep_w<kWMixed>(items, tiles, ntiles, grid, st);
+    }
+    static hipError_t item(const DevItem &it, hipStream_t st)
+    {
+        const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
+        if (it.dtype == 1)
+            hipLaunchKernelGGL((k_item_mfma_lds<kWF16, RG, WV>), grid, block, 0, st, it);
+        else
+            hipLaunchKernelGGL((k_item_mfma_lds<kWF32, RG, WV>), grid, block, 0, st, it);
+        return hipGetLastError();
+    }
+};
+
+template <int R, int WV, int CC>
+struct InstMfmaDma {
+    static constexpr int RG = R / 16;
+    static hipError_t sweep(int wm, const DevItem *items, const DevTile *tiles, int ntiles,
+                            int grid, hipStream_t st)
+    {
+        if (wm != kWF32) // fp16 weights: the LDS-staged form with the same rows
+            return InstMfmaLds<R, WV, 2>::sweep(wm, items, tiles, ntiles, grid, st);
+        hipLaunchKernelGGL((k_sweep_mfma_dma<RG, WV, CC>), dim3(grid), dim3(WV * kWave), 0, st,
+                           items, tiles, ntiles);
         return hipGetLastError();
     }
     static hipError_t item(const DevItem &it, hipStream_t st)
     {
-        if (it.dtype == 1) return InstMfma16<R, WV, 4>::item(it, st);
+        if (it.dtype != 0) return InstMfmaLds<R, WV, 2>::item(it, st);
         const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
-        hipLaunchKernelGGL((k_item_mfma_lds<RG, WV>), grid, block, 0, st, it);
+        hipLaunchKernelGGL((k_item_mfma_dma<RG, WV, CC>), grid, block, 0, st, it);
         return hipGetLastError();
     }
 };
@@ -1018,6 +1376,9 @@ bool multi_shape_supported(const Shape &s, int B)
     TVL_MFMA_SHAPES(Y)
     TVL_MFMA16_SHAPES(Y)
     TVL_MFMA_LDS_SHAPES(Y)
+#define D(R_, W_, U_, CC_) Y(R_, W_, U_)
+    TVL_MFMA_DMA_SHAPES(D)
+#undef D
 #undef X
 #undef Y
     return false;
@@ -1042,6 +1403,11 @@ hipError_t launch_sweep_multi(const Shape &s, int B, int wmode, const DevItem *i
     TVL_MFMA_SHAPES(Y)
     TVL_MFMA16_SHAPES(Z)
     TVL_MFMA_LDS_SHAPES(V)
+#define D(R_, W_, U_, CC_)                                                                        \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return InstMfmaDma<R_, W_, CC_>::sweep(wmode, items, tiles, ntiles, grid, st);
+    TVL_MFMA_DMA_SHAPES(D)
+#undef D
 #undef X
 #undef Y
 #undef Z
@@ -1064,6 +1430,10 @@ hipError_t launch_item_multi(const Shape &s, int B, const DevItem &item, hipStre
     TVL_MFMA_SHAPES(Y)
     TVL_MFMA16_SHAPES(Z)
     TVL_MFMA_LDS_SHAPES(V)
+#define D(R_, W_, U_, CC_)                                                                        \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfmaDma<R_, W_, CC_>::item(item, st);
+    TVL_MFMA_DMA_SHAPES(D)
+#undef D
 #undef X
 #undef Y
 #undef Z

@@ -29,9 +29,12 @@ MULTI = [(2, 4, 2, 2), (2, 4, 4, 2), (4, 4, 2, 2), (2, 4, 1, 4), (2, 4, 2, 4), (
 # per row group in flight >= 4)
 MFMA = [(8, 4, 1), (16, 1, 1), (16, 2, 1)]
 MFMA16 = [(16, 4, 8), (32, 1, 4), (32, 2, 4), (64, 1, 4)]
-# 16x16x4 with LDS-staged rows (U = 2; fp32 weights, fp16 launches take the
-# direct form)
-MFMA_LDS = [(16, 1, 2), (16, 4, 2), (32, 1, 2), (32, 2, 2), (32, 4, 2)]
+# 16x16x4 with LDS-staged rows (U = 2)
+MFMA_LDS = [(16, 1, 2), (16, 4, 2), (32, 1, 2), (32, 2, 2), (32, 4, 2), (64, 1, 2)]
+# 16x16x4 with weights streamed into LDS (U = 3: 128-column chunks, 6: 64,
+# 12: 32; fp32 weights, fp16 launches take the LDS-staged form)
+MFMA_DMA = [(16, 1, 3), (16, 2, 3), (16, 4, 3), (16, 1, 6), (16, 2, 6), (16, 4, 6), (32, 1, 6),
+            (32, 2, 6), (32, 1, 12), (64, 1, 12), (64, 2, 12)]
 
 
 def tunings(nrhs):
@@ -39,7 +42,7 @@ def tunings(nrhs):
     for r, w, u, b in MULTI:
         if b >= nrhs and (b == 2 or b // 2 < nrhs):  # the kernels the library would pick from
             out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
-    for r, w, u in MFMA + MFMA16 + MFMA_LDS:
+    for r, w, u in MFMA + MFMA16 + MFMA_LDS + MFMA_DMA:
         out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
     return out
 
@@ -118,7 +121,10 @@ def test_beam4_sweep110m():
               dict(rows_per_wave=32, waves_per_block=2, unroll=4, flags=2),
               dict(rows_per_wave=64, waves_per_block=1, unroll=4, flags=2, grid=300),
               dict(rows_per_wave=16, waves_per_block=4, unroll=2, flags=2),
-              dict(rows_per_wave=32, waves_per_block=1, unroll=2, flags=2, grid=900)):
+              dict(rows_per_wave=32, waves_per_block=1, unroll=2, flags=2, grid=900),
+              dict(rows_per_wave=16, waves_per_block=2, unroll=3, flags=2),
+              dict(rows_per_wave=32, waves_per_block=1, unroll=6, flags=2, grid=600),
+              dict(rows_per_wave=64, waves_per_block=1, unroll=12, flags=2)):
         for d in ms:
             d.Y.fill_(float("nan"))
         plan = tvl.tvl_sweep_plan_create([d.item() for d in ms], t)
@@ -162,7 +168,7 @@ def test_multi_plan_mixed_dtypes():
         host.append((W, X, dt, nb, Yd))
         keep += [buf, Xd, Yd]
     for t in [None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
-                       for r, w, u in MFMA + MFMA16 + MFMA_LDS]:
+                       for r, w, u in MFMA + MFMA16 + MFMA_LDS + MFMA_DMA]:
         for *_, Yd in host:
             Yd[:, :-1].fill_(float("nan"))
         plan = tvl.tvl_sweep_plan_create(items, t)
@@ -202,24 +208,37 @@ def test_beam_sweep110m_default(nb):
     plan.destroy()
 
 
-@pytest.mark.parametrize("ldw", [(1 << 28) - 64, 1 << 28], ids=["lds-limit", "direct"])
-def test_multi_huge_row_stride(ldw):
-    """Row strides at the matrix-core LDS form's limit (two rows in a buffer
-    descriptor's 31-bit size) and one past it (the launch falls back to the
-    direct-load form): 3 rows of 1 GiB each, 8 vectors, every launch shape."""
-    M, K, nb = 3, 300, 8
-    rng = np.random.default_rng(ldw % 1000)
-    W = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+@pytest.mark.parametrize("dt,ldw,M", [(0, (1 << 26) - 32, 9), (0, (1 << 27) - 32, 5),
+                                       (0, (1 << 28) - 64, 3), (0, 1 << 28, 3),
+                                       (1, (1 << 28) - 64, 5), (1, 1 << 28, 5)],
+                         ids=["f32-dma32-limit", "f32-dma64-limit", "f32-lds-limit", "f32-direct",
+                              "f16-lds-limit", "f16-direct"])
+def test_multi_huge_row_stride(dt, ldw, M):
+    """Row strides at the limits of the matrix-core forms that address a
+    load's rows through one buffer descriptor (31-bit size): 2 fp32 or 4 fp16
+    rows for the LDS-staged form and 128-column streamed chunks, 4 or 8 fp32
+    rows for 64- or 32-column streamed chunks, and one past (those launches
+    fall back to the direct-load form).  3, 5 or 9 rows (a partial group) of
+    0.25-1 GiB, 8 vectors, every launch shape."""
+    K, nb = 300, 8
+    rng = np.random.default_rng(ldw % 1000 + dt)
+    Wf = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    W = Wf if dt == 0 else synth.f32_to_f16_bits(Wf)
     X = rng.standard_normal((nb, K)).astype(np.float32)
-    buf = torch.empty((M, ldw), dtype=torch.float32, device=DEV)
-    buf[:, K:K + 64].fill_(float("nan"))  # padding next to the row: never read
-    buf[:, :K] = torch.from_numpy(W).to(DEV)
-    refs = [oracle.gemv_f32(W, X[b]) for b in range(nb)]
+    if dt == 0:
+        buf = torch.empty((M, ldw), dtype=torch.float32, device=DEV)
+        buf[:, K:K + 64].fill_(float("nan"))  # padding next to the row: never used
+        buf[:, :K] = torch.from_numpy(W).to(DEV)
+    else:
+        buf = torch.empty((M, ldw), dtype=torch.int16, device=DEV)
+        buf[:, K:K + 64].fill_(0x7E00)
+        buf[:, :K] = torch.from_numpy(W.view(np.int16)).to(DEV)
+    refs = [(oracle.gemv_f32 if dt == 0 else oracle.gemv_f16)(W, X[b]) for b in range(nb)]
     for t in [None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
-                       for r, w, u in MFMA_LDS + MFMA16]:
-        Y = run(buf, ldw, 0, X, M, K, nb, M, t)
+                       for r, w, u in MFMA_LDS + MFMA16 + MFMA_DMA]:
+        Y = run(buf, ldw, dt, X, M, K, nb, M, t)
         for b in range(nb):
-            r = oracle.check(Y[b], refs[b][0], refs[b][1], 1e-5)
-            assert r["bad"] == 0, (ldw, t, b, r)
+            r = oracle.check(Y[b], refs[b][0], refs[b][1], TOL[dt])
+            assert r["bad"] == 0, (dt, ldw, t, b, r)
     del buf
     torch.cuda.empty_cache()
