@@ -159,7 +159,7 @@ typedef struct tvl_item {
  *   waves_per_block W in {1, 2, 4, 8}: wavefronts per workgroup
  *   unroll          U in {1, 2, 3, 4, 8}: 16-byte weight loads per row kept in
  *                   flight per lane (several-vector launches: selects the
- *                   matrix-core form, below; 6 and 12 occur there only)
+ *                   matrix-core form, below, where U can exceed 8)
  *   ksplit          S >= 1: K slices per row tile (tvl_gemv only; 1 = row
  *                   split)
  *   grid            workgroups of a sweep launch (0 = one per tile); a smaller
@@ -187,10 +187,10 @@ typedef struct tvl_item {
  * (64,1,4); the 16x16x4 form with rows staged through LDS from registers
  * (U = 2; fp32 and fp16 weights) (16,1,2) (16,4,2) (32,1,2) (32,2,2)
  * (32,4,2) (64,1,2); and the 16x16x4 form with fp32 weights streamed into
- * LDS by the loads themselves (U = 3: 128-column chunks, 6: 64, 12: 32; a
- * launch holding fp16 weights runs the previous form with the same rows and
- * waves) (16,1,3) (16,2,3) (16,4,3) (16,1,6) (16,2,6) (16,4,6) (32,1,6)
- * (32,2,6) (32,1,12) (64,1,12) (64,2,12).  Rows longer than these forms'
+ * LDS by the loads themselves (U = 10 S + log2(C / 16) for S LDS stages and
+ * chunks of C columns; a launch holding fp16 weights runs the previous form
+ * with the same rows and waves) (16,2,33) (16,4,32) (32,1,32) (32,2,32)
+ * (64,1,31) (16,4,42) (32,1,42) (32,1,52).  Rows longer than these forms'
  * buffer descriptors can address (a load's 2, 4 or 8 rows within 2^31
  * bytes) run the direct-load 16x16x4 form.
  * Launches holding block-quantised items (direct-x only; R rows per group of

@@ -283,7 +283,7 @@ int multi_B(int n) { return n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16; }
 // core steps as an fp32 chunk of twice the bytes.
 Shape default_multi_shape(int B, bool all_f32)
 {
-    if (B > 4 && all_f32) return Shape{32, 1, 6, tvl::kXDirect};
+    if (B > 4 && all_f32) return Shape{32, 1, 32, tvl::kXDirect};
     if (B > 8) return Shape{16, 1, 2, tvl::kXDirect};
     if (B > 4) return Shape{16, 2, 1, tvl::kXDirect};
     return B == 2 ? Shape{4, 4, 2, tvl::kXDirect} : Shape{4, 4, 1, tvl::kXDirect};

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 #include "tvl_device.h"
 
 namespace tvl {
@@ -1013,24 +1015,26 @@ __global__ __launch_bounds__(WV *kWave) void k_item_mfma_lds(const DevItem it)
 // fp32 weights in the same contraction, with the weight loads writing LDS
 // directly: a buffer load with the LDS bit puts lane l's 16 bytes at
 // M0 + 16 l and holds no VGPR, so a wavefront keeps the next two chunks in
-// flight while it multiplies the current one (three LDS stages per
-// wavefront).  One load covers 1 KiB: the chunk of RPL rows (CC * 4 bytes
+// flight while it multiplies the current one (S LDS stages per wavefront:
+// S - 1 chunks in flight).  One load covers 1 KiB: the chunk of RPL rows (CC * 4 bytes
 // each), lane l landing in row l / LPR at 16-byte position l % LPR.  Rows
 // are stored without padding, so the blocks of row r are XOR-swizzled (the
 // lane at position p reads block p ^ f(r)) such that the 16 lanes that read
 // one block of 16 rows hit the 16 different 16-byte bank groups of a 256-
 // byte LDS line: f(r) = r for rows of 256 bytes or more, f(r) = r / 2 for
-// 128-byte rows (two rows per line).  x: direct B-layout loads one chunk
-// ahead, in registers; more rows per wavefront share each x load (x from
+// 128-byte rows (two rows per line).  x: direct B-layout loads S - 2 chunks
+// ahead, in S - 1 register buffers; more rows per wavefront share each x load (x from
 // the cache adds nb 4 CC bytes per chunk of 16 RG rows to the weights'
 // 16 RG 4 CC).
 //
-// Each chunk step issues, in this order, the x loads of the next chunk (NQ)
-// and the weight loads of the chunk after that (NL); near the end of the
-// rows the same loads go to empty descriptors (no memory access; they fill
-// a stage that is no longer read) and to the last chunk's x.  So 2 NQ + 2 NL
+// Chunk step c issues, in this order, the x loads of chunk c + S - 2 (NQ)
+// and the weight loads of chunk c + S - 1 (NL); near the end of the rows the
+// same loads go to empty descriptors (no memory access; they fill a stage
+// that is no longer read) and to the last chunk's x.  So (S - 1)(NQ + NL)
 // loads always follow a chunk's weight loads when its products start, and
-// one fixed vmcnt wait brings them in while two chunks stay in flight.  A
+// one fixed vmcnt wait brings them in while S - 1 chunks stay in flight (the
+// compiler's own waits for x, NQ loads stricter, leave the same chunks in
+// flight).  A
 // ragged last chunk drains the loads and goes through registers (masked) into
 // the same layout.  Accumulation as in the forms above (4 NQ MFMA steps per
 // chunk).
@@ -1043,7 +1047,7 @@ __device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, TVL_LDS void
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, voff, soff, 0, 2);
 }
 
-template <int RG, int CC>
+template <int RG, int CC, int S>
 struct MfmaDmaRows {
     static constexpr int RB = CC * 4;          // bytes of a row's chunk (one LDS row)
     static constexpr int RPL = 1024 / RB;      // rows per load
@@ -1052,12 +1056,13 @@ struct MfmaDmaRows {
     static constexpr int NL = TPG * RG;        // weight loads per chunk
     static constexpr int NQ = CC / 16;         // x loads and MFMA column steps per chunk
     static constexpr int STAGE = 16 * RG * RB; // bytes per stage
-    static constexpr int kStages = 3;
-    static constexpr int WAIT = 2 * NL + 2 * NQ;
+    static constexpr int kStages = S;
+    static constexpr int NX = S - 1; // x buffers
+    static constexpr int WAIT = (S - 1) * (NL + NQ);
     static constexpr int SH = RB < 256 ? 1 : 0; // rows per 256-byte line, log2
     // RPL rows in a buffer descriptor's 31-bit size
     static constexpr int64_t MAXLDW = (int64_t(1) << 31) / (4 * RPL) - 32;
-    static_assert(RB >= 128 && LPR * RPL == kWave && WAIT < 64, "chunk shape");
+    static_assert(RB >= 128 && LPR * RPL == kWave && S >= 3 && WAIT < 64, "chunk shape");
 
     // the swizzle of row r (0..15 in its group)
     static __device__ __forceinline__ int swz(int r) { return (r >> SH) & (LPR - 1); }
@@ -1130,21 +1135,20 @@ struct MfmaDmaRows {
             }
     }
 
-    // one chunk step (chunk c in stage ST, its x in X, the next x into Y);
+    // one chunk step: chunk c (stage ST = c % S, x buffer XB = c % NX);
     // true after the last full chunk
-    template <int ST>
-    __device__ __forceinline__ bool step(int &c, int nfull, f4 (&X)[NQ], f4 (&Y)[NQ],
-                                         f4 (&acc)[RG], f4 (&t1)[RG], f4 (&t2)[RG],
-                                         int &n1) const
+    template <int ST, int XB>
+    __device__ __forceinline__ bool step(int &c, int nfull, f4 (&xs)[NX][NQ], f4 (&acc)[RG],
+                                         f4 (&t1)[RG], f4 (&t2)[RG], int &n1) const
     {
         const f4 z = {0.f, 0.f, 0.f, 0.f};
-        load_x(min(c + 1, nfull - 1) * CC, Y);
-        issue<(ST + 2) % kStages>((c + 2) * CC, c + 2 < nfull);
+        load_x(min(c + S - 2, nfull - 1) * CC, xs[(XB + S - 2) % NX]);
+        issue<(ST + S - 1) % S>((c + S - 1) * CC, c + S - 1 < nfull);
         __builtin_amdgcn_sched_barrier(0);
         // vmcnt(WAIT): expcnt and lgkmcnt left alone
         __builtin_amdgcn_s_waitcnt((WAIT & 15) | ((WAIT >> 4) << 14) | 0x0F70);
         __builtin_amdgcn_sched_barrier(0);
-        multiply<ST>(X, acc);
+        multiply<ST>(xs[XB], acc);
 #pragma unroll
         for (int rg = 0; rg < RG; ++rg) {
             t1[rg] += acc[rg];
@@ -1160,6 +1164,25 @@ struct MfmaDmaRows {
         }
         __builtin_amdgcn_sched_barrier(0);
         return ++c == nfull;
+    }
+
+    // S NX steps: stages and x buffers back where they started
+    template <int... J>
+    __device__ __forceinline__ bool turn(std::integer_sequence<int, J...>, int &c, int nfull,
+                                         f4 (&xs)[NX][NQ], f4 (&acc)[RG], f4 (&t1)[RG],
+                                         f4 (&t2)[RG], int &n1) const
+    {
+        return (step<J % S, J % NX>(c, nfull, xs, acc, t1, t2, n1) || ...);
+    }
+
+    // prologue: after the weights of chunk 0, x of chunk j - 1 and the
+    // weights of chunk j for j = 1 .. S - 2
+    template <int... J>
+    __device__ __forceinline__ void start(std::integer_sequence<int, J...>, int nfull,
+                                          f4 (&xs)[NX][NQ]) const
+    {
+        ((load_x(min(J, nfull - 1) * CC, xs[J]), issue<J + 1>((J + 1) * CC, J + 1 < nfull)),
+         ...);
     }
 
     // the ragged last chunk at c0 (after every load has landed), through
@@ -1200,18 +1223,10 @@ struct MfmaDmaRows {
         const int nfull = kn / CC;
         int c = 0, n1 = 0;
         if (nfull > 0) {
-            f4 xa[NQ], xb[NQ];
+            f4 xs[NX][NQ];
             issue<0>(0, true);
-            load_x(0, xa);
-            issue<1>(CC, nfull > 1);
-            // stages rotate by 3 and x buffers by 2: six steps per turn
-            for (;;) {
-                if (step<0>(c, nfull, xa, xb, acc, t1, t2, n1)) break;
-                if (step<1>(c, nfull, xb, xa, acc, t1, t2, n1)) break;
-                if (step<2>(c, nfull, xa, xb, acc, t1, t2, n1)) break;
-                if (step<0>(c, nfull, xb, xa, acc, t1, t2, n1)) break;
-                if (step<1>(c, nfull, xa, xb, acc, t1, t2, n1)) break;
-                if (step<2>(c, nfull, xb, xa, acc, t1, t2, n1)) break;
+            start(std::make_integer_sequence<int, S - 2>{}, nfull, xs);
+            while (!turn(std::make_integer_sequence<int, S * NX>{}, c, nfull, xs, acc, t1, t2, n1)) {
             }
             __builtin_amdgcn_s_waitcnt(0x0F70); // the empty loads too, before LDS is reused
         }
@@ -1223,10 +1238,10 @@ struct MfmaDmaRows {
     }
 };
 
-template <int RG, int WV, int CC>
+template <int RG, int WV, int CC, int S>
 __device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_LDS char *lds)
 {
-    using Rows = MfmaDmaRows<RG, CC>;
+    using Rows = MfmaDmaRows<RG, CC, S>;
     if (it.ldw > Rows::MAXLDW) { // wavefront-uniform
         tile_mfma16<float, RG, 4, WV>(it, row0);
         return;
@@ -1254,27 +1269,27 @@ __device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_L
 }
 
 // fp32 weights only (the launcher sends other launches to the LDS-staged form)
-template <int RG, int WV, int CC>
+template <int RG, int WV, int CC, int S>
 __global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_dma(const DevItem *__restrict__ items,
                                                                const DevTile *__restrict__ tiles,
                                                                int ntiles)
 {
-    using Rows = MfmaDmaRows<RG, CC>;
+    using Rows = MfmaDmaRows<RG, CC, S>;
     __shared__ f4 lds[WV * Rows::kStages * Rows::STAGE / 16];
     for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const DevTile tl = tiles[t];
         const DevItem it = items[tl.item];
-        tile_mfma_dma<RG, WV, CC>(it, tl.row0, (TVL_LDS char *)lds);
+        tile_mfma_dma<RG, WV, CC, S>(it, tl.row0, (TVL_LDS char *)lds);
         __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
     }
 }
 
-template <int RG, int WV, int CC>
+template <int RG, int WV, int CC, int S>
 __global__ __launch_bounds__(WV *kWave) void k_item_mfma_dma(const DevItem it)
 {
-    using Rows = MfmaDmaRows<RG, CC>;
+    using Rows = MfmaDmaRows<RG, CC, S>;
     __shared__ f4 lds[WV * Rows::kStages * Rows::STAGE / 16];
-    tile_mfma_dma<RG, WV, CC>(it, (int)blockIdx.x * (16 * RG * WV), (TVL_LDS char *)lds);
+    tile_mfma_dma<RG, WV, CC, S>(it, (int)blockIdx.x * (16 * RG * WV), (TVL_LDS char *)lds);
 }
 
 // (rows per wavefront = 16 RG, waves per block, U = 2 marks this form).
@@ -1284,13 +1299,11 @@ __global__ __launch_bounds__(WV *kWave) void k_item_mfma_dma(const DevItem it)
 // (whole-line x loads: 5.05 against 5.24 TB/s).
 #define TVL_MFMA_LDS_SHAPES(X) X(16, 1, 2) X(16, 4, 2) X(32, 1, 2) X(32, 2, 2) X(32, 4, 2) X(64, 1, 2)
 
-// (rows per wavefront = 16 RG, waves per block, U, columns per chunk) of the
-// form with weights streamed into LDS: U = 3 for 128-column chunks, 6 for
-// 64, 12 for 32.
+// (rows per wavefront = 16 RG, waves per block, U, columns per chunk, stages)
+// of the form with weights streamed into LDS: U = 10 S + log2(CC / 16).
 #define TVL_MFMA_DMA_SHAPES(X)                                                                    \
-    X(16, 1, 3, 128) X(16, 2, 3, 128) X(16, 4, 3, 128) X(16, 1, 6, 64) X(16, 2, 6, 64)            \
-        X(16, 4, 6, 64) X(32, 1, 6, 64) X(32, 2, 6, 64) X(32, 1, 12, 32) X(64, 1, 12, 32)         \
-            X(64, 2, 12, 32)
+    X(16, 2, 33, 128, 3) X(16, 4, 32, 64, 3) X(32, 1, 32, 64, 3) X(32, 2, 32, 64, 3)             \
+        X(64, 1, 31, 32, 3) X(16, 4, 42, 64, 4) X(32, 1, 42, 64, 4) X(32, 1, 52, 64, 5)
 
 template <int R, int WV, int U>
 struct InstMfmaLds {
@@ -1321,7 +1334,7 @@ struct InstMfmaLds {
     }
 };
 
-template <int R, int WV, int CC>
+template <int R, int WV, int CC, int S>
 struct InstMfmaDma {
     static constexpr int RG = R / 16;
     static hipError_t sweep(int wm, const DevItem *items, const DevTile *tiles, int ntiles,
@@ -1329,7 +1342,7 @@ struct InstMfmaDma {
     {
         if (wm != kWF32) // fp16 weights: the LDS-staged form with the same rows
             return InstMfmaLds<R, WV, 2>::sweep(wm, items, tiles, ntiles, grid, st);
-        hipLaunchKernelGGL((k_sweep_mfma_dma<RG, WV, CC>), dim3(grid), dim3(WV * kWave), 0, st,
+        hipLaunchKernelGGL((k_sweep_mfma_dma<RG, WV, CC, S>), dim3(grid), dim3(WV * kWave), 0, st,
                            items, tiles, ntiles);
         return hipGetLastError();
     }
@@ -1337,7 +1350,7 @@ struct InstMfmaDma {
     {
         if (it.dtype != 0) return InstMfmaLds<R, WV, 2>::item(it, st);
         const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
-        hipLaunchKernelGGL((k_item_mfma_dma<RG, WV, CC>), grid, block, 0, st, it);
+        hipLaunchKernelGGL((k_item_mfma_dma<RG, WV, CC, S>), grid, block, 0, st, it);
         return hipGetLastError();
     }
 };
@@ -1376,7 +1389,7 @@ bool multi_shape_supported(const Shape &s, int B)
     TVL_MFMA_SHAPES(Y)
     TVL_MFMA16_SHAPES(Y)
     TVL_MFMA_LDS_SHAPES(Y)
-#define D(R_, W_, U_, CC_) Y(R_, W_, U_)
+#define D(R_, W_, U_, CC_, S_) Y(R_, W_, U_)
     TVL_MFMA_DMA_SHAPES(D)
 #undef D
 #undef X
@@ -1403,9 +1416,9 @@ hipError_t launch_sweep_multi(const Shape &s, int B, int wmode, const DevItem *i
     TVL_MFMA_SHAPES(Y)
     TVL_MFMA16_SHAPES(Z)
     TVL_MFMA_LDS_SHAPES(V)
-#define D(R_, W_, U_, CC_)                                                                        \
+#define D(R_, W_, U_, CC_, S_)                                                                    \
     if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
-        return InstMfmaDma<R_, W_, CC_>::sweep(wmode, items, tiles, ntiles, grid, st);
+        return InstMfmaDma<R_, W_, CC_, S_>::sweep(wmode, items, tiles, ntiles, grid, st);
     TVL_MFMA_DMA_SHAPES(D)
 #undef D
 #undef X
@@ -1430,8 +1443,8 @@ hipError_t launch_item_multi(const Shape &s, int B, const DevItem &item, hipStre
     TVL_MFMA_SHAPES(Y)
     TVL_MFMA16_SHAPES(Z)
     TVL_MFMA_LDS_SHAPES(V)
-#define D(R_, W_, U_, CC_)                                                                        \
-    if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfmaDma<R_, W_, CC_>::item(item, st);
+#define D(R_, W_, U_, CC_, S_)                                                                    \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfmaDma<R_, W_, CC_, S_>::item(item, st);
     TVL_MFMA_DMA_SHAPES(D)
 #undef D
 #undef X

@@ -31,10 +31,10 @@ MFMA = [(8, 4, 1), (16, 1, 1), (16, 2, 1)]
 MFMA16 = [(16, 4, 8), (32, 1, 4), (32, 2, 4), (64, 1, 4)]
 # 16x16x4 with LDS-staged rows (U = 2)
 MFMA_LDS = [(16, 1, 2), (16, 4, 2), (32, 1, 2), (32, 2, 2), (32, 4, 2), (64, 1, 2)]
-# 16x16x4 with weights streamed into LDS (U = 3: 128-column chunks, 6: 64,
-# 12: 32; fp32 weights, fp16 launches take the LDS-staged form)
-MFMA_DMA = [(16, 1, 3), (16, 2, 3), (16, 4, 3), (16, 1, 6), (16, 2, 6), (16, 4, 6), (32, 1, 6),
-            (32, 2, 6), (32, 1, 12), (64, 1, 12), (64, 2, 12)]
+# 16x16x4 with weights streamed into LDS (U = 10 stages + log2(columns per
+# chunk / 16); fp32 weights, fp16 launches take the LDS-staged form)
+MFMA_DMA = [(16, 2, 33), (16, 4, 32), (32, 1, 32), (32, 2, 32), (64, 1, 31), (16, 4, 42),
+            (32, 1, 42), (32, 1, 52)]
 
 
 def tunings(nrhs):
@@ -122,9 +122,10 @@ def test_beam4_sweep110m():
               dict(rows_per_wave=64, waves_per_block=1, unroll=4, flags=2, grid=300),
               dict(rows_per_wave=16, waves_per_block=4, unroll=2, flags=2),
               dict(rows_per_wave=32, waves_per_block=1, unroll=2, flags=2, grid=900),
-              dict(rows_per_wave=16, waves_per_block=2, unroll=3, flags=2),
-              dict(rows_per_wave=32, waves_per_block=1, unroll=6, flags=2, grid=600),
-              dict(rows_per_wave=64, waves_per_block=1, unroll=12, flags=2)):
+              dict(rows_per_wave=16, waves_per_block=2, unroll=33, flags=2),
+              dict(rows_per_wave=32, waves_per_block=1, unroll=32, flags=2, grid=600),
+              dict(rows_per_wave=64, waves_per_block=1, unroll=31, flags=2),
+              dict(rows_per_wave=32, waves_per_block=1, unroll=52, flags=2, grid=500)):
         for d in ms:
             d.Y.fill_(float("nan"))
         plan = tvl.tvl_sweep_plan_create([d.item() for d in ms], t)
