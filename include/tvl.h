@@ -186,13 +186,12 @@ typedef struct tvl_item {
  * in groups of 16, U = loads per group in flight) (16,4,8) (32,1,4) (32,2,4)
  * (64,1,4); the 16x16x4 form with rows staged through LDS from registers
  * (U = 2; fp32 and fp16 weights) (16,1,2) (16,4,2) (32,1,2) (32,2,2)
- * (32,4,2) (64,1,2); and the 16x16x4 form with fp32 weights streamed into
+ * (32,4,2) (64,1,2); and the 16x16x4 form with the weights streamed into
  * LDS by the loads themselves (U = 10 S + log2(C / 16) for S LDS stages and
- * chunks of C columns; a launch holding fp16 weights runs the previous form
- * with the same rows and waves) (16,2,33) (16,4,32) (32,1,32) (32,2,32)
- * (64,1,31) (16,4,42) (32,1,42) (32,1,52).  Rows longer than these forms'
- * buffer descriptors can address (a load's 2, 4 or 8 rows within 2^31
- * bytes) run the direct-load 16x16x4 form.
+ * chunks of C columns; fp32 and fp16 weights) (16,1,33) (16,2,33) (32,1,33)
+ * (16,1,32) (16,4,32) (32,1,32) (32,2,32) (16,4,42) (32,1,42) (32,1,52).
+ * Rows longer than these forms' buffer descriptors can address (a load's 2,
+ * 4 or 8 rows within 2^31 bytes) run the direct-load 16x16x4 form.
  * Launches holding block-quantised items (direct-x only; R rows per group of
  * lanes, see tvl_dtype): (2,4,2) (4,4,1) (4,4,2) (4,1,2) (8,4,1) (8,2,1) */
 typedef struct tvl_tuning {

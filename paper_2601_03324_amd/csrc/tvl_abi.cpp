@@ -276,16 +276,17 @@ int multi_B(int n) { return n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16; }
 // 5.92 TB/s against 5.43-5.49 for the LDS-staged form, 4.73 for the 4 x 4 x 1
 // form and 4.07 on the VALU; 16 vectors: 5.08 against 4.88-4.90 LDS-staged
 // and 3.68 for the direct-load form).  Launches with fp16 weights (one 70B-shaped
-// layer): the 4 x 4 x 1 form up to 8 vectors (8: 4.36 TB/s against 4.22 for
-// the LDS-staged form), the LDS-staged form with 16 rows per wavefront beyond
-// (16 vectors: 3.61 against 2.70 for the direct-load 16 x 16 x 4 form and
-// 3.22 with 32 rows), where each converted fp16 chunk costs as many matrix-
-// core steps as an fp32 chunk of twice the bytes.
+// layer): from 5 to 8 vectors the streamed form with 16 rows, two wavefronts
+// per block and 128-column chunks (8: 4.60 TB/s against 4.37-4.41 for the
+// 4 x 4 x 1 form and 4.20-4.33 LDS-staged); beyond, the LDS-staged form with
+// 16 rows per wavefront (16 vectors: 3.61 against 3.42-3.60 streamed, 2.70
+// for the direct-load form and 3.22 with 32 rows), where each converted fp16
+// chunk costs as many matrix-core steps as an fp32 chunk of twice the bytes.
 Shape default_multi_shape(int B, bool all_f32)
 {
     if (B > 4 && all_f32) return Shape{32, 1, 32, tvl::kXDirect};
     if (B > 8) return Shape{16, 1, 2, tvl::kXDirect};
-    if (B > 4) return Shape{16, 2, 1, tvl::kXDirect};
+    if (B > 4) return Shape{16, 2, 33, tvl::kXDirect};
     return B == 2 ? Shape{4, 4, 2, tvl::kXDirect} : Shape{4, 4, 1, tvl::kXDirect};
 }
 

@@ -1047,9 +1047,12 @@ __device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, TVL_LDS void
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, voff, soff, 0, 2);
 }
 
-template <int RG, int CC, int S>
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+
+template <typename T, int RG, int CC, int S>
 struct MfmaDmaRows {
-    static constexpr int RB = CC * 4;          // bytes of a row's chunk (one LDS row)
+    static constexpr int ES = (int)sizeof(T);
+    static constexpr int RB = CC * ES;         // bytes of a row's chunk (one LDS row)
     static constexpr int RPL = 1024 / RB;      // rows per load
     static constexpr int LPR = kWave / RPL;    // lanes (16-byte positions) per row
     static constexpr int TPG = 16 / RPL;       // loads per 16-row group
@@ -1061,21 +1064,21 @@ struct MfmaDmaRows {
     static constexpr int WAIT = (S - 1) * (NL + NQ);
     static constexpr int SH = RB < 256 ? 1 : 0; // rows per 256-byte line, log2
     // RPL rows in a buffer descriptor's 31-bit size
-    static constexpr int64_t MAXLDW = (int64_t(1) << 31) / (4 * RPL) - 32;
+    static constexpr int64_t MAXLDW = (int64_t(1) << 31) / (ES * RPL) - 64;
     static_assert(RB >= 128 && LPR * RPL == kWave && S >= 3 && WAIT < 64, "chunk shape");
 
     // the swizzle of row r (0..15 in its group)
     static __device__ __forceinline__ int swz(int r) { return (r >> SH) & (LPR - 1); }
 
-    const float *W; // the wavefront's first row (wavefront-uniform)
+    const T *W; // the wavefront's first row (wavefront-uniform)
     int64_t ldw;
     const float *xv; // vector i (clamped), at column 4 g
     int vrows, kn, lane;
     TVL_LDS char *lds; // this wavefront's stages
     int voff[TPG];     // per load of a row group: the lane's byte offset in it
-    int raddr[NQ];     // per MFMA column step: the lane's A block in a stage
+    int raddr[NQ];     // per MFMA column step: the lane's A operand in a stage
 
-    __device__ __forceinline__ MfmaDmaRows(const float *W_, int64_t ldw_, int wrow0, int M,
+    __device__ __forceinline__ MfmaDmaRows(const T *W_, int64_t ldw_, int wrow0, int M,
                                            const float *x, int64_t ldx, int nb, int K, int lane_,
                                            TVL_LDS char *lds_)
         : W(W_ + (int64_t)wrow0 * ldw_), ldw(ldw_), vrows(M - wrow0), kn(K), lane(lane_),
@@ -1085,10 +1088,13 @@ struct MfmaDmaRows {
         const int h = lane / LPR, p = lane % LPR, g = lane >> 4, i = lane & 15;
 #pragma unroll
         for (int t = 0; t < TPG; ++t)
-            voff[t] = (int)(h * ldw_ * 4) + 16 * (p ^ swz(RPL * t + h));
+            voff[t] = (int)(h * ldw_ * ES) + 16 * (p ^ swz(RPL * t + h));
+        // columns 16 q + 4 g .. + 3 of row i: 16-byte block 4 q + g (fp32),
+        // the (g & 1) half of block 2 q + g / 2 (fp16)
 #pragma unroll
         for (int q = 0; q < NQ; ++q)
-            raddr[q] = i * RB + 16 * ((4 * q + g) ^ swz(i));
+            raddr[q] = ES == 4 ? i * RB + 16 * ((4 * q + g) ^ swz(i))
+                               : i * RB + 16 * ((2 * q + (g >> 1)) ^ swz(i)) + 8 * (g & 1);
     }
 
     // rows RPL j .. RPL j + RPL - 1 of the wavefront, those below M; none if
@@ -1096,8 +1102,8 @@ struct MfmaDmaRows {
     __device__ __forceinline__ __amdgpu_buffer_rsrc_t group(int j, bool live) const
     {
         const int n = live ? min(max(vrows - RPL * j, 0), RPL) : 0;
-        return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(W + RPL * j * ldw), (short)0,
-                                                 (int)(n * ldw * 4), 0x00020000);
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<T *>(W + RPL * j * ldw), (short)0,
+                                                 (int)(n * ldw * ES), 0x00020000);
     }
 
     // the chunk at column c0 into stage ST (non-temporal, cache policy 2)
@@ -1110,7 +1116,7 @@ struct MfmaDmaRows {
             for (int t = 0; t < TPG; ++t)
                 lds_dma16(group(TPG * rg + t, live),
                           (TVL_LDS void *)(lds + ST * STAGE + rg * 16 * RB + t * 1024), voff[t],
-                          4 * c0);
+                          ES * c0);
     }
 
     __device__ __forceinline__ void load_x(int c0, f4 (&xb)[NQ]) const
@@ -1127,8 +1133,12 @@ struct MfmaDmaRows {
         for (int rg = 0; rg < RG; ++rg)
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
-                const f4 a =
-                    *(const TVL_LDS f4 *)(lds + ST * STAGE + rg * 16 * RB + raddr[q]);
+                const TVL_LDS char *ap = lds + ST * STAGE + rg * 16 * RB + raddr[q];
+                f4 a;
+                if constexpr (ES == 4)
+                    a = *(const TVL_LDS f4 *)ap;
+                else // exact conversion
+                    a = __builtin_convertvector(*(const TVL_LDS h4 *)ap, f4);
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     acc[rg] = mfma16(a[e], xb[q][e], acc[rg]);
@@ -1195,14 +1205,19 @@ struct MfmaDmaRows {
         for (int rg = 0; rg < RG; ++rg)
 #pragma unroll
             for (int t = 0; t < TPG; ++t) {
-                const int wcol = c0 + 4 * (p ^ swz(RPL * t + h));
-                f4 w = z;
-                if (wcol < kn)
-                    w = mask_from<f4, 4>(
-                        __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                   group(TPG * rg + t, true), voff[t], 4 * c0, 2)),
-                        kn - wcol);
-                *(TVL_LDS f4 *)(lds + rg * 16 * RB + t * 1024 + 16 * lane) = w;
+                const int wcol = c0 + 16 / ES * (p ^ swz(RPL * t + h));
+                u4 w = {0u, 0u, 0u, 0u};
+                if (wcol < kn) {
+                    w = __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                   group(TPG * rg + t, true), voff[t], ES * c0, 2));
+                    if constexpr (ES == 4)
+                        w = __builtin_bit_cast(
+                            u4, mask_from<f4, 4>(__builtin_bit_cast(f4, w), kn - wcol));
+                    else
+                        w = __builtin_bit_cast(
+                            u4, mask_from<h8, 8>(__builtin_bit_cast(h8, w), kn - wcol));
+                }
+                *(TVL_LDS u4 *)(lds + rg * 16 * RB + t * 1024 + 16 * lane) = w;
             }
         f4 xb[NQ];
 #pragma unroll
@@ -1238,12 +1253,12 @@ struct MfmaDmaRows {
     }
 };
 
-template <int RG, int WV, int CC, int S>
+template <typename T, int RG, int WV, int CC, int S>
 __device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_LDS char *lds)
 {
-    using Rows = MfmaDmaRows<RG, CC, S>;
+    using Rows = MfmaDmaRows<T, RG, CC, S>;
     if (it.ldw > Rows::MAXLDW) { // wavefront-uniform
-        tile_mfma16<float, RG, 4, WV>(it, row0);
+        tile_mfma16<T, RG, 4, WV>(it, row0);
         return;
     }
     const int lane = threadIdx.x & (kWave - 1);
@@ -1252,7 +1267,7 @@ __device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_L
     if (wrow0 >= it.M) return; // no barrier follows
     const int nb = it.nrhs < 1 ? 1 : it.nrhs;
     f4 out[RG];
-    const Rows mr(static_cast<const float *>(it.W), it.ldw, wrow0, it.M, it.x, it.ldx, nb, it.K,
+    const Rows mr(static_cast<const T *>(it.W), it.ldw, wrow0, it.M, it.x, it.ldx, nb, it.K,
                   lane, lds + wave * (Rows::kStages * Rows::STAGE));
     mr.run(out);
     const int i = lane & 15, g = lane >> 4;
@@ -1268,28 +1283,47 @@ __device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_L
     }
 }
 
-// fp32 weights only (the launcher sends other launches to the LDS-staged form)
-template <int RG, int WV, int CC, int S>
+// LDS bytes per wavefront of a launch with weight dtypes WM
+template <int WM, int RG, int CC, int S>
+constexpr int dma_wave_lds()
+{
+    return WM == kWF16 ? S * MfmaDmaRows<_Float16, RG, CC, S>::STAGE
+                       : S * MfmaDmaRows<float, RG, CC, S>::STAGE;
+}
+
+template <int WM, int RG, int WV, int CC, int S>
+__device__ __forceinline__ void tile_mfma_dma_w(const DevItem &it, int row0, TVL_LDS char *lds)
+{
+    if constexpr (WM == kWF32)
+        tile_mfma_dma<float, RG, WV, CC, S>(it, row0, lds);
+    else if constexpr (WM == kWF16)
+        tile_mfma_dma<_Float16, RG, WV, CC, S>(it, row0, lds);
+    else if (it.dtype == 1)
+        tile_mfma_dma<_Float16, RG, WV, CC, S>(it, row0, lds);
+    else
+        tile_mfma_dma<float, RG, WV, CC, S>(it, row0, lds);
+}
+
+template <int WM, int RG, int WV, int CC, int S>
 __global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_dma(const DevItem *__restrict__ items,
                                                                const DevTile *__restrict__ tiles,
                                                                int ntiles)
 {
-    using Rows = MfmaDmaRows<RG, CC, S>;
-    __shared__ f4 lds[WV * Rows::kStages * Rows::STAGE / 16];
+    __shared__ f4 lds[WV * dma_wave_lds<WM, RG, CC, S>() / 16];
     for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const DevTile tl = tiles[t];
         const DevItem it = items[tl.item];
-        tile_mfma_dma<RG, WV, CC, S>(it, tl.row0, (TVL_LDS char *)lds);
+        tile_mfma_dma_w<WM, RG, WV, CC, S>(it, tl.row0, (TVL_LDS char *)lds);
         __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
     }
 }
 
-template <int RG, int WV, int CC, int S>
+template <int WM, int RG, int WV, int CC, int S>
 __global__ __launch_bounds__(WV *kWave) void k_item_mfma_dma(const DevItem it)
 {
-    using Rows = MfmaDmaRows<RG, CC, S>;
-    __shared__ f4 lds[WV * Rows::kStages * Rows::STAGE / 16];
-    tile_mfma_dma<RG, WV, CC, S>(it, (int)blockIdx.x * (16 * RG * WV), (TVL_LDS char *)lds);
+    __shared__ f4 lds[WV * dma_wave_lds<WM, RG, CC, S>() / 16];
+    tile_mfma_dma_w<WM, RG, WV, CC, S>(it, (int)blockIdx.x * (16 * RG * WV),
+                                       (TVL_LDS char *)lds);
 }
 
 // (rows per wavefront = 16 RG, waves per block, U = 2 marks this form).
@@ -1301,9 +1335,11 @@ __global__ __launch_bounds__(WV *kWave) void k_item_mfma_dma(const DevItem it)
 
 // (rows per wavefront = 16 RG, waves per block, U, columns per chunk, stages)
 // of the form with weights streamed into LDS: U = 10 S + log2(CC / 16).
+// Chunks of at least 64 columns (a 128-byte fp16 row chunk).
 #define TVL_MFMA_DMA_SHAPES(X)                                                                    \
-    X(16, 2, 33, 128, 3) X(16, 4, 32, 64, 3) X(32, 1, 32, 64, 3) X(32, 2, 32, 64, 3)             \
-        X(64, 1, 31, 32, 3) X(16, 4, 42, 64, 4) X(32, 1, 42, 64, 4) X(32, 1, 52, 64, 5)
+    X(16, 1, 33, 128, 3) X(16, 2, 33, 128, 3) X(32, 1, 33, 128, 3) X(16, 1, 32, 64, 3)           \
+        X(16, 4, 32, 64, 3) X(32, 1, 32, 64, 3) X(32, 2, 32, 64, 3) X(16, 4, 42, 64, 4)           \
+            X(32, 1, 42, 64, 4) X(32, 1, 52, 64, 5)
 
 template <int R, int WV, int U>
 struct InstMfmaLds {
@@ -1337,20 +1373,28 @@ struct InstMfmaLds {
 template <int R, int WV, int CC, int S>
 struct InstMfmaDma {
     static constexpr int RG = R / 16;
+    template <int WM>
+    static hipError_t sweep_w(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
+                              hipStream_t st)
+    {
+        hipLaunchKernelGGL((k_sweep_mfma_dma<WM, RG, WV, CC, S>), dim3(grid), dim3(WV * kWave), 0,
+                           st, items, tiles, ntiles);
+        return hipGetLastError();
+    }
     static hipError_t sweep(int wm, const DevItem *items, const DevTile *tiles, int ntiles,
                             int grid, hipStream_t st)
     {
-        if (wm != kWF32) // fp16 weights: the LDS-staged form with the same rows
-            return InstMfmaLds<R, WV, 2>::sweep(wm, items, tiles, ntiles, grid, st);
-        hipLaunchKernelGGL((k_sweep_mfma_dma<RG, WV, CC, S>), dim3(grid), dim3(WV * kWave), 0, st,
-                           items, tiles, ntiles);
-        return hipGetLastError();
+        return wm == kWF32   ? sweep_w<kWF32>(items, tiles, ntiles, grid, st)
+               : wm == kWF16 ? sweep_w<kWF16>(items, tiles, ntiles, grid, st)
+                             : sweep_w<kWMixed>(items, tiles, ntiles, grid, st);
     }
     static hipError_t item(const DevItem &it, hipStream_t st)
     {
-        if (it.dtype != 0) return InstMfmaLds<R, WV, 2>::item(it, st);
         const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
-        hipLaunchKernelGGL((k_item_mfma_dma<RG, WV, CC, S>), grid, block, 0, st, it);
+        if (it.dtype == 1)
+            hipLaunchKernelGGL((k_item_mfma_dma<kWF16, RG, WV, CC, S>), grid, block, 0, st, it);
+        else
+            hipLaunchKernelGGL((k_item_mfma_dma<kWF32, RG, WV, CC, S>), grid, block, 0, st, it);
         return hipGetLastError();
     }
 };

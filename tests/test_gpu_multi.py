@@ -32,9 +32,9 @@ MFMA16 = [(16, 4, 8), (32, 1, 4), (32, 2, 4), (64, 1, 4)]
 # 16x16x4 with LDS-staged rows (U = 2)
 MFMA_LDS = [(16, 1, 2), (16, 4, 2), (32, 1, 2), (32, 2, 2), (32, 4, 2), (64, 1, 2)]
 # 16x16x4 with weights streamed into LDS (U = 10 stages + log2(columns per
-# chunk / 16); fp32 weights, fp16 launches take the LDS-staged form)
-MFMA_DMA = [(16, 2, 33), (16, 4, 32), (32, 1, 32), (32, 2, 32), (64, 1, 31), (16, 4, 42),
-            (32, 1, 42), (32, 1, 52)]
+# chunk / 16); fp32 and fp16 weights)
+MFMA_DMA = [(16, 1, 33), (16, 2, 33), (32, 1, 33), (16, 1, 32), (16, 4, 32), (32, 1, 32),
+            (32, 2, 32), (16, 4, 42), (32, 1, 42), (32, 1, 52)]
 
 
 def tunings(nrhs):
@@ -124,7 +124,7 @@ def test_beam4_sweep110m():
               dict(rows_per_wave=32, waves_per_block=1, unroll=2, flags=2, grid=900),
               dict(rows_per_wave=16, waves_per_block=2, unroll=33, flags=2),
               dict(rows_per_wave=32, waves_per_block=1, unroll=32, flags=2, grid=600),
-              dict(rows_per_wave=64, waves_per_block=1, unroll=31, flags=2),
+              dict(rows_per_wave=16, waves_per_block=1, unroll=33, flags=2),
               dict(rows_per_wave=32, waves_per_block=1, unroll=52, flags=2, grid=500)):
         for d in ms:
             d.Y.fill_(float("nan"))
@@ -209,18 +209,18 @@ def test_beam_sweep110m_default(nb):
     plan.destroy()
 
 
-@pytest.mark.parametrize("dt,ldw,M", [(0, (1 << 26) - 32, 9), (0, (1 << 27) - 32, 5),
-                                       (0, (1 << 28) - 64, 3), (0, 1 << 28, 3),
+@pytest.mark.parametrize("dt,ldw,M", [(0, (1 << 27) - 64, 5), (0, (1 << 28) - 64, 3),
+                                       (0, 1 << 28, 3), (1, (1 << 27) - 64, 9),
                                        (1, (1 << 28) - 64, 5), (1, 1 << 28, 5)],
-                         ids=["f32-dma32-limit", "f32-dma64-limit", "f32-lds-limit", "f32-direct",
-                              "f16-lds-limit", "f16-direct"])
+                         ids=["f32-4rows-limit", "f32-2rows-limit", "f32-direct",
+                              "f16-8rows-limit", "f16-4rows-limit", "f16-direct"])
 def test_multi_huge_row_stride(dt, ldw, M):
     """Row strides at the limits of the matrix-core forms that address a
     load's rows through one buffer descriptor (31-bit size): 2 fp32 or 4 fp16
-    rows for the LDS-staged form and 128-column streamed chunks, 4 or 8 fp32
-    rows for 64- or 32-column streamed chunks, and one past (those launches
-    fall back to the direct-load form).  3, 5 or 9 rows (a partial group) of
-    0.25-1 GiB, 8 vectors, every launch shape."""
+    rows (LDS-staged form, 128-column streamed chunks), 4 fp32 or 8 fp16 rows
+    (64-column streamed chunks), and one past (those launches fall back to the
+    direct-load form).  3, 5 or 9 rows (a partial group) of 0.25-1 GiB, 8
+    vectors, every launch shape."""
     K, nb = 300, 8
     rng = np.random.default_rng(ldw % 1000 + dt)
     Wf = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
