@@ -1012,20 +1012,21 @@ __global__ __launch_bounds__(WV *kWave) void k_item_mfma_lds(const DevItem it)
 }
 
 // ------------------- matrix cores, 16 x 16 x 4, weights streamed into LDS
-// fp32 weights in the same contraction, with the weight loads writing LDS
-// directly: a buffer load with the LDS bit puts lane l's 16 bytes at
-// M0 + 16 l and holds no VGPR, so a wavefront keeps the next two chunks in
-// flight while it multiplies the current one (S LDS stages per wavefront:
-// S - 1 chunks in flight).  One load covers 1 KiB: the chunk of RPL rows (CC * 4 bytes
-// each), lane l landing in row l / LPR at 16-byte position l % LPR.  Rows
-// are stored without padding, so the blocks of row r are XOR-swizzled (the
-// lane at position p reads block p ^ f(r)) such that the 16 lanes that read
-// one block of 16 rows hit the 16 different 16-byte bank groups of a 256-
-// byte LDS line: f(r) = r for rows of 256 bytes or more, f(r) = r / 2 for
-// 128-byte rows (two rows per line).  x: direct B-layout loads S - 2 chunks
-// ahead, in S - 1 register buffers; more rows per wavefront share each x load (x from
-// the cache adds nb 4 CC bytes per chunk of 16 RG rows to the weights'
-// 16 RG 4 CC).
+// The same contraction with the weight loads writing LDS directly: a buffer
+// load with the LDS bit puts lane l's 16 bytes at M0 + 16 l and holds no
+// VGPR, so with S LDS stages a wavefront keeps S - 1 chunks in flight while
+// it multiplies the current one.  One load covers 1 KiB: the chunk of RPL
+// rows (CC columns, RB = CC * sizeof(T) bytes each), lane l landing in row
+// l / LPR at 16-byte position l % LPR.  Rows are stored without padding, so
+// the blocks of row r are XOR-swizzled (the lane at position p reads block
+// p ^ f(r)) such that the 16 lanes that read one column block of 16 rows hit
+// the 16 different 16-byte bank groups of a 256-byte LDS line: f(r) = r for
+// rows of 256 bytes or more, f(r) = r / 2 for 128-byte rows (two rows per
+// line).  fp16 weights stay fp16 in LDS: the A operand of a step is then 8
+// bytes (4 columns), converted exactly after the LDS read.  x: direct
+// B-layout loads S - 2 chunks ahead, in S - 1 register buffers; more rows
+// per wavefront share each x load (x from the cache adds nb 4 CC bytes per
+// chunk of 16 RG rows to the weights' 16 RG RB).
 //
 // Chunk step c issues, in this order, the x loads of chunk c + S - 2 (NQ)
 // and the weight loads of chunk c + S - 1 (NL); near the end of the rows the
@@ -1034,9 +1035,9 @@ __global__ __launch_bounds__(WV *kWave) void k_item_mfma_lds(const DevItem it)
 // loads always follow a chunk's weight loads when its products start, and
 // one fixed vmcnt wait brings them in while S - 1 chunks stay in flight (the
 // compiler's own waits for x, NQ loads stricter, leave the same chunks in
-// flight).  A
-// ragged last chunk drains the loads and goes through registers (masked) into
-// the same layout.  Accumulation as in the forms above (4 NQ MFMA steps per
+// flight; the compiler does not track these loads' LDS writes).  A ragged
+// last chunk drains the loads and goes through registers (masked) into the
+// same layout.  Accumulation as in the forms above (4 NQ MFMA steps per
 // chunk).
 #define TVL_LDS __attribute__((address_space(3)))
 
@@ -1253,6 +1254,7 @@ struct MfmaDmaRows {
     }
 };
 
+// lds: this wavefront's stages
 template <typename T, int RG, int WV, int CC, int S>
 __device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_LDS char *lds)
 {
@@ -1268,7 +1270,7 @@ __device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_L
     const int nb = it.nrhs < 1 ? 1 : it.nrhs;
     f4 out[RG];
     const Rows mr(static_cast<const T *>(it.W), it.ldw, wrow0, it.M, it.x, it.ldx, nb, it.K,
-                  lane, lds + wave * (Rows::kStages * Rows::STAGE));
+                  lane, lds);
     mr.run(out);
     const int i = lane & 15, g = lane >> 4;
     if (i < nb) {
@@ -1283,12 +1285,22 @@ __device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_L
     }
 }
 
-// LDS bytes per wavefront of a launch with weight dtypes WM
+// LDS bytes per wavefront of a launch with weight dtypes WM.  A mixed launch
+// gives every wavefront the fp32 size: the wavefronts of a block move on to
+// their next tiles independently, so one may run an fp32 tile while another
+// still runs an fp16 one.
 template <int WM, int RG, int CC, int S>
 constexpr int dma_wave_lds()
 {
     return WM == kWF16 ? S * MfmaDmaRows<_Float16, RG, CC, S>::STAGE
                        : S * MfmaDmaRows<float, RG, CC, S>::STAGE;
+}
+
+template <int WM, int RG, int CC, int S>
+__device__ __forceinline__ TVL_LDS char *dma_wave_base(f4 *lds)
+{
+    return (TVL_LDS char *)lds +
+           __builtin_amdgcn_readfirstlane(threadIdx.x / kWave) * dma_wave_lds<WM, RG, CC, S>();
 }
 
 template <int WM, int RG, int WV, int CC, int S>
@@ -1313,7 +1325,7 @@ __global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_dma(const DevItem *__r
     for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const DevTile tl = tiles[t];
         const DevItem it = items[tl.item];
-        tile_mfma_dma_w<WM, RG, WV, CC, S>(it, tl.row0, (TVL_LDS char *)lds);
+        tile_mfma_dma_w<WM, RG, WV, CC, S>(it, tl.row0, dma_wave_base<WM, RG, CC, S>(lds));
         __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
     }
 }
@@ -1323,7 +1335,7 @@ __global__ __launch_bounds__(WV *kWave) void k_item_mfma_dma(const DevItem it)
 {
     __shared__ f4 lds[WV * dma_wave_lds<WM, RG, CC, S>() / 16];
     tile_mfma_dma_w<WM, RG, WV, CC, S>(it, (int)blockIdx.x * (16 * RG * WV),
-                                       (TVL_LDS char *)lds);
+                                       dma_wave_base<WM, RG, CC, S>(lds));
 }
 
 // (rows per wavefront = 16 RG, waves per block, U = 2 marks this form).

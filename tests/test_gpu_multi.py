@@ -151,7 +151,8 @@ def test_beam4_sweep110m():
 
 def test_multi_plan_mixed_dtypes():
     """One plan holding fp32 and fp16 several-vector items with different
-    vector counts (the mixed-dtype kernels), every output against the oracle."""
+    vector counts (the mixed-dtype kernels), every output against the oracle,
+    also with grids of 1 and 3 workgroups looping over all tiles."""
     rng = np.random.default_rng(4242)
     specs = [(300, 1000, 0, 5), (130, 2050, 1, 11), (77, 768, 0, 16), (1, 33, 1, 2)]
     host, items, keep = [], [], []
@@ -168,8 +169,12 @@ def test_multi_plan_mixed_dtypes():
                               nrhs=nb, ldx=ldx, ldy=M + 1))
         host.append((W, X, dt, nb, Yd))
         keep += [buf, Xd, Yd]
+    # small grids: each workgroup loops over tiles of both dtypes, and its
+    # wavefronts drift apart (one may run an fp32 tile next to an fp16 one)
     for t in [None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
-                       for r, w, u in MFMA + MFMA16 + MFMA_LDS + MFMA_DMA]:
+                       for r, w, u in MFMA + MFMA16 + MFMA_LDS + MFMA_DMA] + [
+            dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2, grid=g)
+            for r, w, u in MFMA_LDS + MFMA_DMA if w > 1 for g in (1, 3)]:
         for *_, Yd in host:
             Yd[:, :-1].fill_(float("nan"))
         plan = tvl.tvl_sweep_plan_create(items, t)
