@@ -129,7 +129,14 @@ typedef enum tvl_status {
  *     the weights are read once for all vectors.  Only for plain GEMV items
  *     (op == TVL_OP_GEMV, g == NULL).  Up to 4 vectors the products run on
  *     the vector ALUs, from 5 on (by default) on the matrix cores, in fp32
- *     with fp32 accumulation either way.
+ *     with fp32 accumulation either way; except that launches holding only
+ *     fp16 weights use the fp16 matrix cores from 5 vectors on (by default):
+ *     each 64- or 128-column chunk of each x vector is scaled by 2^k, which
+ *     puts its largest |x| 2^k in [2^13, 2^14), and split into two fp16 parts,
+ *     x 2^k = hi + lo + r with |r| <= 2^-22 |x 2^k| + 2^-25; the fp16 products
+ *     are exact and accumulate in fp32, and the sum is scaled back exactly.
+ *     The split adds at most 2^-22 sum_j |W_ij x_j| + 2^-38 sum_j |W_ij| m_j
+ *     to the error bound above (m_j: the largest |x| in column j's chunk).
  *   Block-quantised weights (dtype TVL_Q8 / TVL_Q4): plain one-vector GEMV
  *     items only (op == TVL_OP_GEMV, g == NULL, nrhs <= 1).
  * One launch (plan or batch) may hold plain fp32/fp16 items together with
@@ -189,9 +196,13 @@ typedef struct tvl_item {
  * (32,4,2) (64,1,2); and the 16x16x4 form with the weights streamed into
  * LDS by the loads themselves (U = 10 S + log2(C / 16) for S LDS stages and
  * chunks of C columns; fp32 and fp16 weights) (16,1,33) (16,2,33) (32,1,33)
- * (16,1,32) (16,4,32) (32,1,32) (32,2,32) (16,4,42) (32,1,42) (32,1,52).
- * Rows longer than these forms' buffer descriptors can address (a load's 2,
- * 4 or 8 rows within 2^31 bytes) run the direct-load 16x16x4 form.
+ * (16,1,32) (16,4,32) (32,1,32) (32,2,32) (16,4,42) (32,1,42) (32,1,52);
+ * and with U + 100 the same for fp16 weights on the fp16 matrix cores with
+ * split x (launches holding fp32 weights run the LDS-staged form with the
+ * same rows and waves) (16,1,133) (16,2,133) (32,1,133) (32,2,133)
+ * (64,1,133) (32,1,132) (64,1,132).  Rows longer than these forms' buffer
+ * descriptors can address (a load's 2, 4 or 8 rows within 2^31 bytes) run
+ * the direct-load 16x16x4 form.
  * Launches holding block-quantised items (direct-x only; R rows per group of
  * lanes, see tvl_dtype): (2,4,2) (4,4,1) (4,4,2) (4,1,2) (8,4,1) (8,2,1) */
 typedef struct tvl_tuning {

@@ -275,18 +275,21 @@ int multi_B(int n) { return n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16; }
 // 32 rows in 64-column chunks and one wavefront per block (8 vectors: 5.70-
 // 5.92 TB/s against 5.43-5.49 for the LDS-staged form, 4.73 for the 4 x 4 x 1
 // form and 4.07 on the VALU; 16 vectors: 5.08 against 4.88-4.90 LDS-staged
-// and 3.68 for the direct-load form).  Launches with fp16 weights (one 70B-shaped
-// layer): from 5 to 8 vectors the streamed form with 16 rows, two wavefronts
-// per block and 128-column chunks (8: 4.60 TB/s against 4.37-4.41 for the
-// 4 x 4 x 1 form and 4.20-4.33 LDS-staged); beyond, the LDS-staged form with
-// 16 rows per wavefront (16 vectors: 3.61 against 3.42-3.60 streamed, 2.70
-// for the direct-load form and 3.22 with 32 rows), where each converted fp16
-// chunk costs as many matrix-core steps as an fp32 chunk of twice the bytes.
-Shape default_multi_shape(int B, bool all_f32)
+// and 3.68 for the direct-load form).  Launches with only fp16 weights (one
+// 70B-shaped layer), 5-16 vectors: the streamed form on the fp16 matrix
+// cores with x split in two fp16 parts, 32 rows per wavefront, 128-column
+// chunks (8 vectors: 5.57 TB/s against 4.64 for the same form on the fp32
+// matrix cores and 4.48 for 4 x 4 x 1; 16: 4.78 against 3.60 for the
+// LDS-staged form, where each converted fp16 chunk costs as many fp32
+// matrix-core steps as an fp32 chunk of twice the bytes).  Launches mixing
+// fp32 and fp16 weights: the fp32 choice with 5-8 vectors, the LDS-staged
+// form with 16 rows beyond.
+Shape default_multi_shape(int B, bool all_f32, bool all_f16)
 {
     if (B > 4 && all_f32) return Shape{32, 1, 32, tvl::kXDirect};
+    if (B > 4 && all_f16) return Shape{32, 1, 133, tvl::kXDirect};
     if (B > 8) return Shape{16, 1, 2, tvl::kXDirect};
-    if (B > 4) return Shape{16, 2, 33, tvl::kXDirect};
+    if (B > 4) return Shape{32, 1, 32, tvl::kXDirect};
     return B == 2 ? Shape{4, 4, 2, tvl::kXDirect} : Shape{4, 4, 1, tvl::kXDirect};
 }
 
@@ -406,7 +409,7 @@ Shape default_shape_items(const tvl_item *items, int32_t n)
     for (int32_t i = 0; i < n; ++i)
         quant = quant || is_quant(items[i].dtype);
     if (quant) return default_quant_shape();
-    if (nmax > 1) return default_multi_shape(multi_B(nmax), b16 == 0);
+    if (nmax > 1) return default_multi_shape(multi_B(nmax), b16 == 0, b32 == 0);
     if (fused) return default_fused_shape(b16, b32);
     return default_shape(b16, b32, b32 > 0 ? row32 / b32 : 0.0, true);
 }
@@ -791,7 +794,7 @@ tvl_status tvl_gemv_item(const tvl_item *item, const tvl_tuning *tuning, hipStre
     const int B = is_multi(*item) ? multi_B((int)item->nrhs) : 0;
     Shape shape;
     st = pick_shape(tuning,
-                    B ? default_multi_shape(B, item->dtype == TVL_F32)
+                    B ? default_multi_shape(B, item->dtype == TVL_F32, item->dtype == TVL_F16)
                       : default_fused_shape(f16 ? 1.0 : 0.0, f16 ? 0.0 : 1.0),
                     &shape, false);
     if (st != TVL_OK) return st;

@@ -1050,8 +1050,25 @@ __device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, TVL_LDS void
 
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 
-template <typename T, int RG, int CC, int S>
+// fp16 weights on the fp16 matrix cores (HX): each chunk's x values are
+// scaled per vector by a power of two 2^k (k = 14 - e for the chunk's
+// largest |x| in [2^(e-1), 2^e), clamped to +-126), which puts the largest
+// in [2^13, 2^14), far below the fp16 maximum, and split into a high and a
+// low fp16 part, both rounded to nearest: x 2^k = hi + lo + r with
+// |r| <= 2^-11 |x 2^k - hi| <= 2^-22 |x 2^k| while lo is normal, and
+// |r| <= 2^-25 (half the smallest fp16 subnormal) below.  Products of fp16 values are
+// exact in fp32, so one v_mfma_f32_16x16x32_f16 per part does the work of
+// eight fp32 16 x 16 x 4 steps; the chunk's sum is then scaled back by 2^-k
+// (exact).  A operand: lane 16 g + i holds row i, columns 8 g .. 8 g + 7 of
+// the 32-column step (one 16-byte LDS read); B: vector i, the same columns.
+__device__ __forceinline__ f4 mfma16h(h8 a, h8 b, f4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+template <typename T, int RG, int CC, int S, bool HX = false>
 struct MfmaDmaRows {
+    static_assert(!HX || sizeof(T) == 2, "split x with fp16 weights only");
     static constexpr int ES = (int)sizeof(T);
     static constexpr int RB = CC * ES;         // bytes of a row's chunk (one LDS row)
     static constexpr int RPL = 1024 / RB;      // rows per load
@@ -1073,11 +1090,17 @@ struct MfmaDmaRows {
 
     const T *W; // the wavefront's first row (wavefront-uniform)
     int64_t ldw;
-    const float *xv; // vector i (clamped), at column 4 g
+    const float *xv; // vector i (clamped), at column 4 g (8 g with HX)
     int vrows, kn, lane;
     TVL_LDS char *lds; // this wavefront's stages
     int voff[TPG];     // per load of a row group: the lane's byte offset in it
     int raddr[NQ];     // per MFMA column step: the lane's A operand in a stage
+
+    // chunk column of the lane's x load k, relative to xv
+    static __device__ __forceinline__ int xoff(int k)
+    {
+        return HX ? 32 * (k >> 1) + 4 * (k & 1) : 16 * k;
+    }
 
     __device__ __forceinline__ MfmaDmaRows(const T *W_, int64_t ldw_, int wrow0, int M,
                                            const float *x, int64_t ldx, int nb, int K, int lane_,
@@ -1085,17 +1108,19 @@ struct MfmaDmaRows {
         : W(W_ + (int64_t)wrow0 * ldw_), ldw(ldw_), vrows(M - wrow0), kn(K), lane(lane_),
           lds(lds_)
     {
-        xv = x + (int64_t)min(lane & 15, nb - 1) * ldx + 4 * (lane >> 4);
+        xv = x + (int64_t)min(lane & 15, nb - 1) * ldx + (HX ? 8 : 4) * (lane >> 4);
         const int h = lane / LPR, p = lane % LPR, g = lane >> 4, i = lane & 15;
 #pragma unroll
         for (int t = 0; t < TPG; ++t)
             voff[t] = (int)(h * ldw_ * ES) + 16 * (p ^ swz(RPL * t + h));
         // columns 16 q + 4 g .. + 3 of row i: 16-byte block 4 q + g (fp32),
-        // the (g & 1) half of block 2 q + g / 2 (fp16)
+        // the (g & 1) half of block 2 q + g / 2 (fp16); HX: columns
+        // 32 q + 8 g .. + 7, block 4 q + g
 #pragma unroll
         for (int q = 0; q < NQ; ++q)
-            raddr[q] = ES == 4 ? i * RB + 16 * ((4 * q + g) ^ swz(i))
-                               : i * RB + 16 * ((2 * q + (g >> 1)) ^ swz(i)) + 8 * (g & 1);
+            raddr[q] = ES == 4 || HX
+                           ? i * RB + 16 * ((4 * q + g) ^ swz(i))
+                           : i * RB + 16 * ((2 * q + (g >> 1)) ^ swz(i)) + 8 * (g & 1);
     }
 
     // rows RPL j .. RPL j + RPL - 1 of the wavefront, those below M; none if
@@ -1124,12 +1149,16 @@ struct MfmaDmaRows {
     {
 #pragma unroll
         for (int q = 0; q < NQ; ++q)
-            xb[q] = load_x4(xv + c0 + 16 * q);
+            xb[q] = load_x4(xv + c0 + xoff(q));
     }
 
     template <int ST>
     __device__ __forceinline__ void multiply(const f4 (&xb)[NQ], f4 (&acc)[RG]) const
     {
+        if constexpr (HX) {
+            multiply_hx<ST>(xb, acc);
+            return;
+        }
 #pragma unroll
         for (int rg = 0; rg < RG; ++rg)
 #pragma unroll
@@ -1144,6 +1173,46 @@ struct MfmaDmaRows {
                 for (int e = 0; e < 4; ++e)
                     acc[rg] = mfma16(a[e], xb[q][e], acc[rg]);
             }
+    }
+
+    // HX: the chunk's products on the fp16 matrix cores (scaled, split x)
+    template <int ST>
+    __device__ __forceinline__ void multiply_hx(const f4 (&xb)[NQ], f4 (&acc)[RG]) const
+    {
+        float m = 0.f;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                m = fmaxf(m, fabsf(xb[q][e]));
+        // the vector's 4 lanes (g = 0..3) hold the chunk's columns
+        m = fmaxf(m, __shfl_xor(m, 16));
+        m = fmaxf(m, __shfl_xor(m, 32));
+        int e2 = 0;
+        if (m > 0.f && m <= 3.4028235e38f) e2 = __builtin_amdgcn_frexp_expf(m);
+        const int k = min(max(14 - e2, -126), 126);
+        const float sc = __builtin_ldexpf(1.f, k), inv = __builtin_ldexpf(1.f, -k);
+        h8 hi[NQ / 2], lo[NQ / 2];
+#pragma unroll
+        for (int q = 0; q < NQ / 2; ++q)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float v = xb[2 * q + e / 4][e % 4] * sc;
+                const _Float16 vh = (_Float16)v;
+                hi[q][e] = vh;
+                lo[q][e] = (_Float16)(v - (float)vh);
+            }
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg) {
+            f4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < NQ / 2; ++q) {
+                const h8 a = *(const TVL_LDS h8 *)(lds + ST * STAGE + rg * 16 * RB + raddr[q]);
+                c = mfma16h(a, hi[q], c);
+                c = mfma16h(a, lo[q], c);
+            }
+            acc[rg] += c * inv;
+        }
     }
 
     // one chunk step: chunk c (stage ST = c % S, x buffer XB = c % NX);
@@ -1223,8 +1292,8 @@ struct MfmaDmaRows {
         f4 xb[NQ];
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
-            const int valid = kn - (c0 + 16 * q + 4 * g);
-            xb[q] = valid > 0 ? mask_from<f4, 4>(load_x4(xv + c0 + 16 * q), valid) : z;
+            const int valid = kn - (c0 + xoff(q) + (HX ? 8 : 4) * g);
+            xb[q] = valid > 0 ? mask_from<f4, 4>(load_x4(xv + c0 + xoff(q)), valid) : z;
         }
         multiply<0>(xb, acc);
     }
@@ -1255,10 +1324,10 @@ struct MfmaDmaRows {
 };
 
 // lds: this wavefront's stages
-template <typename T, int RG, int WV, int CC, int S>
+template <typename T, int RG, int WV, int CC, int S, bool HX>
 __device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_LDS char *lds)
 {
-    using Rows = MfmaDmaRows<T, RG, CC, S>;
+    using Rows = MfmaDmaRows<T, RG, CC, S, HX>;
     if (it.ldw > Rows::MAXLDW) { // wavefront-uniform
         tile_mfma16<T, RG, 4, WV>(it, row0);
         return;
@@ -1292,8 +1361,10 @@ __device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_L
 template <int WM, int RG, int CC, int S>
 constexpr int dma_wave_lds()
 {
-    return WM == kWF16 ? S * MfmaDmaRows<_Float16, RG, CC, S>::STAGE
-                       : S * MfmaDmaRows<float, RG, CC, S>::STAGE;
+    if constexpr (WM == kWF16)
+        return S * MfmaDmaRows<_Float16, RG, CC, S>::STAGE;
+    else
+        return S * MfmaDmaRows<float, RG, CC, S>::STAGE;
 }
 
 template <int WM, int RG, int CC, int S>
@@ -1303,20 +1374,21 @@ __device__ __forceinline__ TVL_LDS char *dma_wave_base(f4 *lds)
            __builtin_amdgcn_readfirstlane(threadIdx.x / kWave) * dma_wave_lds<WM, RG, CC, S>();
 }
 
-template <int WM, int RG, int WV, int CC, int S>
+// HX: fp16 items on the fp16 matrix cores (fp32 items are unaffected)
+template <int WM, int RG, int WV, int CC, int S, bool HX>
 __device__ __forceinline__ void tile_mfma_dma_w(const DevItem &it, int row0, TVL_LDS char *lds)
 {
     if constexpr (WM == kWF32)
-        tile_mfma_dma<float, RG, WV, CC, S>(it, row0, lds);
+        tile_mfma_dma<float, RG, WV, CC, S, false>(it, row0, lds);
     else if constexpr (WM == kWF16)
-        tile_mfma_dma<_Float16, RG, WV, CC, S>(it, row0, lds);
+        tile_mfma_dma<_Float16, RG, WV, CC, S, HX>(it, row0, lds);
     else if (it.dtype == 1)
-        tile_mfma_dma<_Float16, RG, WV, CC, S>(it, row0, lds);
+        tile_mfma_dma<_Float16, RG, WV, CC, S, HX>(it, row0, lds);
     else
-        tile_mfma_dma<float, RG, WV, CC, S>(it, row0, lds);
+        tile_mfma_dma<float, RG, WV, CC, S, false>(it, row0, lds);
 }
 
-template <int WM, int RG, int WV, int CC, int S>
+template <int WM, int RG, int WV, int CC, int S, bool HX>
 __global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_dma(const DevItem *__restrict__ items,
                                                                const DevTile *__restrict__ tiles,
                                                                int ntiles)
@@ -1325,17 +1397,17 @@ __global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_dma(const DevItem *__r
     for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const DevTile tl = tiles[t];
         const DevItem it = items[tl.item];
-        tile_mfma_dma_w<WM, RG, WV, CC, S>(it, tl.row0, dma_wave_base<WM, RG, CC, S>(lds));
+        tile_mfma_dma_w<WM, RG, WV, CC, S, HX>(it, tl.row0, dma_wave_base<WM, RG, CC, S>(lds));
         __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
     }
 }
 
-template <int WM, int RG, int WV, int CC, int S>
+template <int WM, int RG, int WV, int CC, int S, bool HX>
 __global__ __launch_bounds__(WV *kWave) void k_item_mfma_dma(const DevItem it)
 {
     __shared__ f4 lds[WV * dma_wave_lds<WM, RG, CC, S>() / 16];
-    tile_mfma_dma_w<WM, RG, WV, CC, S>(it, (int)blockIdx.x * (16 * RG * WV),
-                                       dma_wave_base<WM, RG, CC, S>(lds));
+    tile_mfma_dma_w<WM, RG, WV, CC, S, HX>(it, (int)blockIdx.x * (16 * RG * WV),
+                                           dma_wave_base<WM, RG, CC, S>(lds));
 }
 
 // (rows per wavefront = 16 RG, waves per block, U = 2 marks this form).
@@ -1345,13 +1417,18 @@ __global__ __launch_bounds__(WV *kWave) void k_item_mfma_dma(const DevItem it)
 // (whole-line x loads: 5.05 against 5.24 TB/s).
 #define TVL_MFMA_LDS_SHAPES(X) X(16, 1, 2) X(16, 4, 2) X(32, 1, 2) X(32, 2, 2) X(32, 4, 2) X(64, 1, 2)
 
-// (rows per wavefront = 16 RG, waves per block, U, columns per chunk, stages)
-// of the form with weights streamed into LDS: U = 10 S + log2(CC / 16).
-// Chunks of at least 64 columns (a 128-byte fp16 row chunk).
+// (rows per wavefront = 16 RG, waves per block, U, columns per chunk, stages,
+// HX) of the form with weights streamed into LDS: U = 10 S + log2(CC / 16),
+// + 100 for fp16 weights on the fp16 matrix cores (HX).  Chunks of at least
+// 64 columns (a 128-byte fp16 row chunk).
 #define TVL_MFMA_DMA_SHAPES(X)                                                                    \
-    X(16, 1, 33, 128, 3) X(16, 2, 33, 128, 3) X(32, 1, 33, 128, 3) X(16, 1, 32, 64, 3)           \
-        X(16, 4, 32, 64, 3) X(32, 1, 32, 64, 3) X(32, 2, 32, 64, 3) X(16, 4, 42, 64, 4)           \
-            X(32, 1, 42, 64, 4) X(32, 1, 52, 64, 5)
+    X(16, 1, 33, 128, 3, false) X(16, 2, 33, 128, 3, false) X(32, 1, 33, 128, 3, false)          \
+        X(16, 1, 32, 64, 3, false) X(16, 4, 32, 64, 3, false) X(32, 1, 32, 64, 3, false)          \
+            X(32, 2, 32, 64, 3, false) X(16, 4, 42, 64, 4, false) X(32, 1, 42, 64, 4, false)      \
+                X(32, 1, 52, 64, 5, false) X(16, 1, 133, 128, 3, true)                            \
+                    X(16, 2, 133, 128, 3, true) X(32, 1, 133, 128, 3, true)                       \
+                        X(32, 2, 133, 128, 3, true) X(64, 1, 133, 128, 3, true)                   \
+                            X(32, 1, 132, 64, 3, true) X(64, 1, 132, 64, 3, true)
 
 template <int R, int WV, int U>
 struct InstMfmaLds {
@@ -1382,31 +1459,43 @@ struct InstMfmaLds {
     }
 };
 
-template <int R, int WV, int CC, int S>
+template <int R, int WV, int CC, int S, bool HX>
 struct InstMfmaDma {
     static constexpr int RG = R / 16;
     template <int WM>
     static hipError_t sweep_w(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
                               hipStream_t st)
     {
-        hipLaunchKernelGGL((k_sweep_mfma_dma<WM, RG, WV, CC, S>), dim3(grid), dim3(WV * kWave), 0,
-                           st, items, tiles, ntiles);
+        hipLaunchKernelGGL((k_sweep_mfma_dma<WM, RG, WV, CC, S, HX>), dim3(grid), dim3(WV * kWave),
+                           0, st, items, tiles, ntiles);
         return hipGetLastError();
     }
+    // HX shapes serve launches of fp16 weights only; others run the
+    // LDS-staged form with the same rows and waves
     static hipError_t sweep(int wm, const DevItem *items, const DevTile *tiles, int ntiles,
                             int grid, hipStream_t st)
     {
-        return wm == kWF32   ? sweep_w<kWF32>(items, tiles, ntiles, grid, st)
-               : wm == kWF16 ? sweep_w<kWF16>(items, tiles, ntiles, grid, st)
-                             : sweep_w<kWMixed>(items, tiles, ntiles, grid, st);
+        if constexpr (HX) {
+            if (wm != kWF16) return InstMfmaLds<R, WV, 2>::sweep(wm, items, tiles, ntiles, grid, st);
+            return sweep_w<kWF16>(items, tiles, ntiles, grid, st);
+        } else {
+            return wm == kWF32   ? sweep_w<kWF32>(items, tiles, ntiles, grid, st)
+                   : wm == kWF16 ? sweep_w<kWF16>(items, tiles, ntiles, grid, st)
+                                 : sweep_w<kWMixed>(items, tiles, ntiles, grid, st);
+        }
     }
     static hipError_t item(const DevItem &it, hipStream_t st)
     {
         const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
-        if (it.dtype == 1)
-            hipLaunchKernelGGL((k_item_mfma_dma<kWF16, RG, WV, CC, S>), grid, block, 0, st, it);
-        else
-            hipLaunchKernelGGL((k_item_mfma_dma<kWF32, RG, WV, CC, S>), grid, block, 0, st, it);
+        if (it.dtype == 1) {
+            hipLaunchKernelGGL((k_item_mfma_dma<kWF16, RG, WV, CC, S, HX>), grid, block, 0, st, it);
+        } else {
+            if constexpr (HX)
+                return InstMfmaLds<R, WV, 2>::item(it, st);
+            else
+                hipLaunchKernelGGL((k_item_mfma_dma<kWF32, RG, WV, CC, S, HX>), grid, block, 0, st,
+                                   it);
+        }
         return hipGetLastError();
     }
 };
@@ -1445,7 +1534,7 @@ bool multi_shape_supported(const Shape &s, int B)
     TVL_MFMA_SHAPES(Y)
     TVL_MFMA16_SHAPES(Y)
     TVL_MFMA_LDS_SHAPES(Y)
-#define D(R_, W_, U_, CC_, S_) Y(R_, W_, U_)
+#define D(R_, W_, U_, CC_, S_, HX_) Y(R_, W_, U_)
     TVL_MFMA_DMA_SHAPES(D)
 #undef D
 #undef X
@@ -1472,9 +1561,9 @@ hipError_t launch_sweep_multi(const Shape &s, int B, int wmode, const DevItem *i
     TVL_MFMA_SHAPES(Y)
     TVL_MFMA16_SHAPES(Z)
     TVL_MFMA_LDS_SHAPES(V)
-#define D(R_, W_, U_, CC_, S_)                                                                    \
+#define D(R_, W_, U_, CC_, S_, HX_)                                                               \
     if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
-        return InstMfmaDma<R_, W_, CC_, S_>::sweep(wmode, items, tiles, ntiles, grid, st);
+        return InstMfmaDma<R_, W_, CC_, S_, HX_>::sweep(wmode, items, tiles, ntiles, grid, st);
     TVL_MFMA_DMA_SHAPES(D)
 #undef D
 #undef X
@@ -1499,8 +1588,9 @@ hipError_t launch_item_multi(const Shape &s, int B, const DevItem &item, hipStre
     TVL_MFMA_SHAPES(Y)
     TVL_MFMA16_SHAPES(Z)
     TVL_MFMA_LDS_SHAPES(V)
-#define D(R_, W_, U_, CC_, S_)                                                                    \
-    if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfmaDma<R_, W_, CC_, S_>::item(item, st);
+#define D(R_, W_, U_, CC_, S_, HX_)                                                               \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return InstMfmaDma<R_, W_, CC_, S_, HX_>::item(item, st);
     TVL_MFMA_DMA_SHAPES(D)
 #undef D
 #undef X

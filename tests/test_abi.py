@@ -61,6 +61,7 @@ def test_item_layout_matches_header():
 
 
 D = 4 << 40  # another fake, far-away device address (g, W3)
+E = 5 << 40
 
 
 @pytest.mark.parametrize("kw,st", [
@@ -85,11 +86,17 @@ def test_fused_item_rejects(kw, st):
 
 @pytest.mark.parametrize("nrhs", list(range(2, 17)))
 def test_multi_item_default_shape_exists(nrhs):
-    """Every vector count has a default several-vector kernel: validation
-    passes and the call only fails at the device query of a GPU-less host."""
-    it = tvl.item(A, 768, B, C, 768, 768, 0, nrhs=nrhs, ldx=768, ldy=768)
-    assert L.tvl_gemv_item(ctypes.byref(it), None, None) == HIP
-    arr, n = tvl.make_items([it])
+    """Every vector count has a default several-vector kernel, for fp32,
+    fp16 and mixed launches: validation passes and the call only fails at the
+    device query of a GPU-less host."""
+    for dt in (0, 1):
+        it = tvl.item(A, 768, B, C, 768, 768, dt, nrhs=nrhs, ldx=768, ldy=768)
+        assert L.tvl_gemv_item(ctypes.byref(it), None, None) == HIP
+        arr, n = tvl.make_items([it])
+        assert L.tvl_gemv_batch_sweep(arr, n, None) == HIP
+    mixed = [tvl.item(A, 768, B, C, 768, 768, 0, nrhs=nrhs, ldx=768, ldy=768),
+             tvl.item(D, 768, B, E, 768, 768, 1, nrhs=nrhs, ldx=768, ldy=768)]
+    arr, n = tvl.make_items(mixed)
     assert L.tvl_gemv_batch_sweep(arr, n, None) == HIP
 
 

@@ -35,6 +35,10 @@ MFMA_LDS = [(16, 1, 2), (16, 4, 2), (32, 1, 2), (32, 2, 2), (32, 4, 2), (64, 1, 
 # chunk / 16); fp32 and fp16 weights)
 MFMA_DMA = [(16, 1, 33), (16, 2, 33), (32, 1, 33), (16, 1, 32), (16, 4, 32), (32, 1, 32),
             (32, 2, 32), (16, 4, 42), (32, 1, 42), (32, 1, 52)]
+# the same with fp16 weights on the fp16 matrix cores, x split in two fp16
+# parts (U + 100; launches holding fp32 weights take the LDS-staged form)
+MFMA_HX = [(16, 1, 133), (16, 2, 133), (32, 1, 133), (32, 2, 133), (64, 1, 133), (32, 1, 132),
+           (64, 1, 132)]
 
 
 def tunings(nrhs):
@@ -42,7 +46,7 @@ def tunings(nrhs):
     for r, w, u, b in MULTI:
         if b >= nrhs and (b == 2 or b // 2 < nrhs):  # the kernels the library would pick from
             out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
-    for r, w, u in MFMA + MFMA16 + MFMA_LDS + MFMA_DMA:
+    for r, w, u in MFMA + MFMA16 + MFMA_LDS + MFMA_DMA + MFMA_HX:
         out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
     return out
 
@@ -172,9 +176,9 @@ def test_multi_plan_mixed_dtypes():
     # small grids: each workgroup loops over tiles of both dtypes, and its
     # wavefronts drift apart (one may run an fp32 tile next to an fp16 one)
     for t in [None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
-                       for r, w, u in MFMA + MFMA16 + MFMA_LDS + MFMA_DMA] + [
+                       for r, w, u in MFMA + MFMA16 + MFMA_LDS + MFMA_DMA + MFMA_HX] + [
             dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2, grid=g)
-            for r, w, u in MFMA_LDS + MFMA_DMA if w > 1 for g in (1, 3)]:
+            for r, w, u in MFMA_LDS + MFMA_DMA + MFMA_HX if w > 1 for g in (1, 3)]:
         for *_, Yd in host:
             Yd[:, :-1].fill_(float("nan"))
         plan = tvl.tvl_sweep_plan_create(items, t)
@@ -241,10 +245,34 @@ def test_multi_huge_row_stride(dt, ldw, M):
         buf[:, :K] = torch.from_numpy(W.view(np.int16)).to(DEV)
     refs = [(oracle.gemv_f32 if dt == 0 else oracle.gemv_f16)(W, X[b]) for b in range(nb)]
     for t in [None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
-                       for r, w, u in MFMA_LDS + MFMA16 + MFMA_DMA]:
+                       for r, w, u in MFMA_LDS + MFMA16 + MFMA_DMA + MFMA_HX]:
         Y = run(buf, ldw, dt, X, M, K, nb, M, t)
         for b in range(nb):
             r = oracle.check(Y[b], refs[b][0], refs[b][1], TOL[dt])
             assert r["bad"] == 0, (dt, ldw, t, b, r)
     del buf
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("M,K", [(100, 1000), (37, 4099), (300, 768)])
+def test_split_x_keeps_fp32_accuracy(M, K):
+    """fp16 weights on the fp16 matrix cores with x split into two scaled fp16
+    parts: the result stays within the fp32 parity bar (1e-5 of the norm), for
+    x spanning 10^-20 .. 10^20 (each 128-column chunk with its own scale;
+    chunks of zeros and of tiny values included)."""
+    rng = np.random.default_rng(M + K)
+    W = synth.f32_to_f16_bits((rng.standard_normal((M, K)) * 0.02).astype(np.float32))
+    nb = 16
+    mag = 10.0 ** rng.uniform(-20, 20, size=(nb, K))
+    X = (rng.standard_normal((nb, K)) * mag).astype(np.float32)
+    X[0, :256] = 0.0                 # two zero chunks
+    X[1, 128:256] *= 1e-18           # a chunk of tiny values
+    X[2] = rng.standard_normal(K).astype(np.float32)  # plain N(0, 1)
+    refs = [oracle.gemv_f16(W, X[b]) for b in range(nb)]
+    buf, ldw = dev_matrix(W, 1)
+    for r, w, u in MFMA_HX:
+        Y = run(buf, ldw, 1, X, M, K, nb, M, dict(rows_per_wave=r, waves_per_block=w,
+                                                  unroll=u, flags=2))
+        for b in range(nb):
+            res = oracle.check(Y[b], refs[b][0], refs[b][1], 1e-5)
+            assert res["bad"] == 0, (M, K, (r, w, u), b, res)
