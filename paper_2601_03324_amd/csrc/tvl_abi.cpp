@@ -271,22 +271,23 @@ int multi_B(int n) { return n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16; }
 // wavefront amortise each x read over more weights (R = 4), and fewer loads
 // in flight keep the R x B accumulators in registers.  From 5 vectors on,
 // the FMAs would take ~half the VALU issue slots and the matrix cores win.
-// fp32 weights: the 16 x 16 x 4 form with the weights streamed into LDS,
-// 32 rows in 64-column chunks and one wavefront per block (8 vectors: 5.70-
-// 5.92 TB/s against 5.43-5.49 for the LDS-staged form, 4.73 for the 4 x 4 x 1
-// form and 4.07 on the VALU; 16 vectors: 5.08 against 4.88-4.90 LDS-staged
-// and 3.68 for the direct-load form).  Launches with only fp16 weights (one
+// fp32 weights: the 16 x 16 x 4 form with the weights streamed into LDS and
+// x shared by the block's four wavefronts (16 rows each, 64-column chunks;
+// 8 vectors: 6.05-6.10 TB/s against 5.55-5.92 streamed with x per wavefront,
+// 5.43-5.49 for the LDS-staged form, 4.73 for the 4 x 4 x 1 form and 4.07 on
+// the VALU; 16 vectors: 5.48-5.51 against 4.96-5.08 streamed, 4.88-4.90
+// LDS-staged and 3.68 for the direct-load form).  Launches with only fp16 weights (one
 // 70B-shaped layer), 5-16 vectors: the streamed form on the fp16 matrix
 // cores with x split in two fp16 parts, 32 rows per wavefront, 128-column
 // chunks (8 vectors: 5.57 TB/s against 4.64 for the same form on the fp32
 // matrix cores and 4.48 for 4 x 4 x 1; 16: 4.78 against 3.60 for the
 // LDS-staged form, where each converted fp16 chunk costs as many fp32
 // matrix-core steps as an fp32 chunk of twice the bytes).  Launches mixing
-// fp32 and fp16 weights: the fp32 choice with 5-8 vectors, the LDS-staged
-// form with 16 rows beyond.
+// fp32 and fp16 weights: the streamed form with x per wavefront (32 rows)
+// with 5-8 vectors, the LDS-staged form with 16 rows beyond.
 Shape default_multi_shape(int B, bool all_f32, bool all_f16)
 {
-    if (B > 4 && all_f32) return Shape{32, 1, 32, tvl::kXDirect};
+    if (B > 4 && all_f32) return Shape{16, 4, 202, tvl::kXDirect};
     if (B > 4 && all_f16) return Shape{32, 1, 133, tvl::kXDirect};
     if (B > 8) return Shape{16, 1, 2, tvl::kXDirect};
     if (B > 4) return Shape{32, 1, 32, tvl::kXDirect};

@@ -1041,11 +1041,14 @@ __global__ __launch_bounds__(WV *kWave) void k_item_mfma_lds(const DevItem it)
 // chunk).
 #define TVL_LDS __attribute__((address_space(3)))
 
-// 16 bytes per lane from a buffer into LDS at lds + 16 lane (non-temporal)
+// 16 bytes per lane from a buffer into LDS at lds + 16 lane; weights
+// non-temporal (cache policy 2, streamed once), x (NT = false) with the
+// default policy (every block of a matrix reads it)
+template <bool NT = true>
 __device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, TVL_LDS void *lds, int voff,
                                           int soff)
 {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, voff, soff, 0, 2);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, voff, soff, 0, NT ? 2 : 0);
 }
 
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
@@ -1354,6 +1357,221 @@ __device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_L
     }
 }
 
+// x shared by the wavefronts of a block (fp32 weights, three stages).  The
+// WV wavefronts of a block work on one row tile, so they need the same x
+// chunks: each loads 1/WV of every x chunk into a shared LDS ring (buffer
+// loads with the LDS bit, vector v in an LDS row of CC * 4 bytes, swizzled
+// like the weight rows), and the B operand comes from there.  L1/L2 then
+// deliver nb 4 CC x bytes per chunk of the block's 16 RG WV rows instead of
+// per wavefront.  One s_barrier per chunk step: after a wavefront's own loads
+// of chunk c have landed (vmcnt) every wavefront's have, and every
+// wavefront has finished chunk c - 1, whose stages (x shared, weights
+// private) the step's new loads overwrite.  Every wavefront of the block
+// takes part in every barrier: wavefronts with no rows left stream empty
+// descriptors and store nothing, and all choices of path depend only on the
+// item.
+template <int RG, int CC, int WV>
+struct MfmaDmaXsRows : MfmaDmaRows<float, RG, CC, 3> {
+    using Base = MfmaDmaRows<float, RG, CC, 3>;
+    using Base::LPR;
+    using Base::NL;
+    using Base::NQ;
+    using Base::RB;
+    using Base::STAGE;
+    static constexpr int XVPL = 1024 / RB;        // vectors per x load
+    static constexpr int XNL = 16 / XVPL;         // x loads per chunk, whole block
+    static constexpr int XW = (XNL + WV - 1) / WV; // x loads per chunk, per wavefront (at most)
+    static constexpr int XSTAGE = 16 * RB;         // bytes of an x stage (16 vectors)
+    static constexpr int WAIT = NL + XW;           // loads of one chunk step (at most)
+    static constexpr int64_t MAXLDX = (int64_t(1) << 31) / (4 * XVPL) - 64;
+    static_assert((XNL % WV == 0 || XW == 1) && WAIT < 64, "x loads: all or one per wavefront");
+
+    const float *X; // vector 0 of the item
+    int64_t ldx;
+    int nb, wave;
+    TVL_LDS char *xlds; // the block's x stages
+    int xvoff[XW];      // per x load of this wavefront: the lane's byte offset
+
+    __device__ __forceinline__ MfmaDmaXsRows(const float *W_, int64_t ldw_, int wrow0, int M,
+                                             const float *x, int64_t ldx_, int nb_, int K,
+                                             int lane_, int wave_, TVL_LDS char *lds_,
+                                             TVL_LDS char *xlds_)
+        : Base(W_, ldw_, wrow0, M, x, ldx_, nb_, K, lane_, lds_), X(x), ldx(ldx_), nb(nb_),
+          wave(wave_), xlds(xlds_)
+    {
+        const int h = lane_ / LPR, p = lane_ % LPR;
+#pragma unroll
+        for (int u = 0; u < XW; ++u) {
+            const int v = XVPL * (wave_ + WV * u) + h; // vector, < 16
+            xvoff[u] = (int)(h * ldx_ * 4) + 16 * (p ^ Base::swz(v));
+        }
+    }
+
+    // vectors XVPL j .. XVPL j + XVPL - 1 below nb; none if !live
+    __device__ __forceinline__ __amdgpu_buffer_rsrc_t xgroup(int j, bool live) const
+    {
+        const int n = live ? min(max(nb - XVPL * j, 0), XVPL) : 0;
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(X + XVPL * j * ldx), (short)0,
+                                                 (int)(n * ldx * 4), 0x00020000);
+    }
+
+    // x loads this wavefront issues per chunk: XW, or (more wavefronts than x
+    // loads) 1 for the first XNL wavefronts and 0 for the others
+    __device__ __forceinline__ bool loads_x() const { return XNL % WV == 0 || wave < XNL; }
+
+    // this wavefront's share of the weights (all its rows) and of x for the
+    // chunk at c0, into stage ST
+    template <int ST>
+    __device__ __forceinline__ void issue_all(int c0, bool live) const
+    {
+        Base::template issue<ST>(c0, live);
+        if (!loads_x()) return; // wavefront-uniform
+#pragma unroll
+        for (int u = 0; u < XW; ++u) {
+            const int j = wave + WV * u;
+            lds_dma16<false>(xgroup(j, live), (TVL_LDS void *)(xlds + ST * XSTAGE + j * 1024),
+                             xvoff[u], 4 * c0);
+        }
+    }
+
+    template <int ST>
+    __device__ __forceinline__ void multiply_xs(f4 (&acc)[RG]) const
+    {
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const f4 b = *(const TVL_LDS f4 *)(xlds + ST * XSTAGE + this->raddr[q]);
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg) {
+                const f4 a =
+                    *(const TVL_LDS f4 *)(this->lds + ST * STAGE + rg * 16 * RB + this->raddr[q]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    acc[rg] = mfma16(a[e], b[e], acc[rg]);
+            }
+        }
+    }
+
+    template <int ST>
+    __device__ __forceinline__ bool step(int &c, int nfull, f4 (&acc)[RG], f4 (&t1)[RG],
+                                         f4 (&t2)[RG], int &n1) const
+    {
+        const f4 z = {0.f, 0.f, 0.f, 0.f};
+        __builtin_amdgcn_sched_barrier(0);
+        // vmcnt(loads of one step): this wavefront's loads of chunk c have landed
+        if (loads_x())
+            __builtin_amdgcn_s_waitcnt((WAIT & 15) | ((WAIT >> 4) << 14) | 0x0F70);
+        else
+            __builtin_amdgcn_s_waitcnt((NL & 15) | ((NL >> 4) << 14) | 0x0F70);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        issue_all<(ST + 2) % 3>((c + 2) * CC, c + 2 < nfull);
+        __builtin_amdgcn_sched_barrier(0);
+        multiply_xs<ST>(acc);
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg) {
+            t1[rg] += acc[rg];
+            acc[rg] = z;
+        }
+        if (++n1 == kMfmaLevel) {
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg) {
+                t2[rg] += t1[rg];
+                t1[rg] = z;
+            }
+            n1 = 0;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        return ++c == nfull;
+    }
+
+    __device__ __forceinline__ void run(f4 (&out)[RG]) const
+    {
+        const f4 z = {0.f, 0.f, 0.f, 0.f};
+        f4 acc[RG], t1[RG], t2[RG];
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+            acc[rg] = t1[rg] = t2[rg] = z;
+        const int nfull = this->kn / CC;
+        int c = 0, n1 = 0;
+        // the previous tile's readers of the shared stages are done
+        __builtin_amdgcn_s_barrier();
+        if (nfull > 0) {
+            issue_all<0>(0, true);
+            issue_all<1>(CC, nfull > 1);
+            for (;;) {
+                if (step<0>(c, nfull, acc, t1, t2, n1)) break;
+                if (step<1>(c, nfull, acc, t1, t2, n1)) break;
+                if (step<2>(c, nfull, acc, t1, t2, n1)) break;
+            }
+            __builtin_amdgcn_s_waitcnt(0x0F70); // the empty loads too
+        }
+        if (c * CC < this->kn) // private: weights stage 0, x in registers
+            Base::tail(c * CC, acc);
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+            out[rg] = t2[rg] + (t1[rg] + acc[rg]);
+    }
+};
+
+// One row tile with x shared by the block; every wavefront runs it to the
+// end (see above).  lds: the block's LDS (weight stages, then x stages).
+template <int RG, int WV, int CC>
+__device__ __forceinline__ void tile_mfma_dma_xs(const DevItem &it, int row0, TVL_LDS char *lds)
+{
+    using Rows = MfmaDmaXsRows<RG, CC, WV>;
+    if (it.ldw > Rows::MAXLDW || it.ldx > Rows::MAXLDX) { // the item decides, no barrier
+        tile_mfma16<float, RG, 4, WV>(it, row0);
+        return;
+    }
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wrow0 = row0 + wave * (16 * RG); // may be past M: empty loads, no stores
+    const int nb = it.nrhs < 1 ? 1 : it.nrhs;
+    f4 out[RG];
+    const Rows mr(static_cast<const float *>(it.W), it.ldw, wrow0, it.M, it.x, it.ldx, nb, it.K,
+                  lane, wave, lds + wave * (3 * Rows::STAGE), lds + WV * (3 * Rows::STAGE));
+    mr.run(out);
+    const int i = lane & 15, g = lane >> 4;
+    if (i < nb) {
+        float *yv = it.y + (int64_t)i * it.ldy;
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = wrow0 + 16 * rg + 4 * g + v;
+                if (row < it.M) yv[row] = out[rg][v];
+            }
+    }
+}
+
+template <int RG, int WV, int CC>
+constexpr int dma_xs_lds()
+{
+    using Rows = MfmaDmaXsRows<RG, CC, WV>;
+    return WV * 3 * Rows::STAGE + 3 * Rows::XSTAGE;
+}
+
+template <int RG, int WV, int CC>
+__global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_xs(const DevItem *__restrict__ items,
+                                                              const DevTile *__restrict__ tiles,
+                                                              int ntiles)
+{
+    __shared__ f4 lds[dma_xs_lds<RG, WV, CC>() / 16];
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) { // block-uniform
+        const DevTile tl = tiles[t];
+        const DevItem it = items[tl.item];
+        tile_mfma_dma_xs<RG, WV, CC>(it, tl.row0, (TVL_LDS char *)lds);
+        __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
+    }
+}
+
+template <int RG, int WV, int CC>
+__global__ __launch_bounds__(WV *kWave) void k_item_mfma_xs(const DevItem it)
+{
+    __shared__ f4 lds[dma_xs_lds<RG, WV, CC>() / 16];
+    tile_mfma_dma_xs<RG, WV, CC>(it, (int)blockIdx.x * (16 * RG * WV), (TVL_LDS char *)lds);
+}
+
 // LDS bytes per wavefront of a launch with weight dtypes WM.  A mixed launch
 // gives every wavefront the fp32 size: the wavefronts of a block move on to
 // their next tiles independently, so one may run an fp32 tile while another
@@ -1459,6 +1677,33 @@ struct InstMfmaLds {
     }
 };
 
+// (rows per wavefront = 16 RG, waves per block, U, columns per chunk) of the
+// streamed form with x shared by the block: U = 200 + log2(CC / 16); fp32
+// weights (launches holding fp16 weights run the LDS-staged form).
+#define TVL_MFMA_XS_SHAPES(X)                                                                     \
+    X(16, 4, 202, 64) X(32, 2, 202, 64) X(32, 4, 202, 64) X(16, 2, 203, 128) X(16, 4, 203, 128)   \
+        X(16, 8, 202, 64)
+
+template <int R, int WV, int CC>
+struct InstMfmaXs {
+    static constexpr int RG = R / 16;
+    static hipError_t sweep(int wm, const DevItem *items, const DevTile *tiles, int ntiles,
+                            int grid, hipStream_t st)
+    {
+        if (wm != kWF32) return InstMfmaLds<R, WV, 2>::sweep(wm, items, tiles, ntiles, grid, st);
+        hipLaunchKernelGGL((k_sweep_mfma_xs<RG, WV, CC>), dim3(grid), dim3(WV * kWave), 0, st,
+                           items, tiles, ntiles);
+        return hipGetLastError();
+    }
+    static hipError_t item(const DevItem &it, hipStream_t st)
+    {
+        if (it.dtype != 0) return InstMfmaLds<R, WV, 2>::item(it, st);
+        const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
+        hipLaunchKernelGGL((k_item_mfma_xs<RG, WV, CC>), grid, block, 0, st, it);
+        return hipGetLastError();
+    }
+};
+
 template <int R, int WV, int CC, int S, bool HX>
 struct InstMfmaDma {
     static constexpr int RG = R / 16;
@@ -1537,6 +1782,9 @@ bool multi_shape_supported(const Shape &s, int B)
 #define D(R_, W_, U_, CC_, S_, HX_) Y(R_, W_, U_)
     TVL_MFMA_DMA_SHAPES(D)
 #undef D
+#define D(R_, W_, U_, CC_) Y(R_, W_, U_)
+    TVL_MFMA_XS_SHAPES(D)
+#undef D
 #undef X
 #undef Y
     return false;
@@ -1566,6 +1814,11 @@ hipError_t launch_sweep_multi(const Shape &s, int B, int wmode, const DevItem *i
         return InstMfmaDma<R_, W_, CC_, S_, HX_>::sweep(wmode, items, tiles, ntiles, grid, st);
     TVL_MFMA_DMA_SHAPES(D)
 #undef D
+#define D(R_, W_, U_, CC_)                                                                        \
+    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
+        return InstMfmaXs<R_, W_, CC_>::sweep(wmode, items, tiles, ntiles, grid, st);
+    TVL_MFMA_XS_SHAPES(D)
+#undef D
 #undef X
 #undef Y
 #undef Z
@@ -1592,6 +1845,10 @@ hipError_t launch_item_multi(const Shape &s, int B, const DevItem &item, hipStre
     if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
         return InstMfmaDma<R_, W_, CC_, S_, HX_>::item(item, st);
     TVL_MFMA_DMA_SHAPES(D)
+#undef D
+#define D(R_, W_, U_, CC_)                                                                        \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfmaXs<R_, W_, CC_>::item(item, st);
+    TVL_MFMA_XS_SHAPES(D)
 #undef D
 #undef X
 #undef Y

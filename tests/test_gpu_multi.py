@@ -39,6 +39,10 @@ MFMA_DMA = [(16, 1, 33), (16, 2, 33), (32, 1, 33), (16, 1, 32), (16, 4, 32), (32
 # parts (U + 100; launches holding fp32 weights take the LDS-staged form)
 MFMA_HX = [(16, 1, 133), (16, 2, 133), (32, 1, 133), (32, 2, 133), (64, 1, 133), (32, 1, 132),
            (64, 1, 132)]
+# streamed, x shared by the block's wavefronts through LDS (U = 200 +
+# log2(columns per chunk / 16); fp32 weights, fp16 launches take the
+# LDS-staged form)
+MFMA_XS = [(16, 4, 202), (32, 2, 202), (32, 4, 202), (16, 2, 203), (16, 4, 203), (16, 8, 202)]
 
 
 def tunings(nrhs):
@@ -46,7 +50,7 @@ def tunings(nrhs):
     for r, w, u, b in MULTI:
         if b >= nrhs and (b == 2 or b // 2 < nrhs):  # the kernels the library would pick from
             out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
-    for r, w, u in MFMA + MFMA16 + MFMA_LDS + MFMA_DMA + MFMA_HX:
+    for r, w, u in MFMA + MFMA16 + MFMA_LDS + MFMA_DMA + MFMA_HX + MFMA_XS:
         out.append(dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2))
     return out
 
@@ -129,6 +133,8 @@ def test_beam4_sweep110m():
               dict(rows_per_wave=16, waves_per_block=2, unroll=33, flags=2),
               dict(rows_per_wave=32, waves_per_block=1, unroll=32, flags=2, grid=600),
               dict(rows_per_wave=16, waves_per_block=1, unroll=33, flags=2),
+              dict(rows_per_wave=16, waves_per_block=4, unroll=202, flags=2),
+              dict(rows_per_wave=32, waves_per_block=2, unroll=202, flags=2, grid=400),
               dict(rows_per_wave=32, waves_per_block=1, unroll=52, flags=2, grid=500)):
         for d in ms:
             d.Y.fill_(float("nan"))
@@ -176,9 +182,10 @@ def test_multi_plan_mixed_dtypes():
     # small grids: each workgroup loops over tiles of both dtypes, and its
     # wavefronts drift apart (one may run an fp32 tile next to an fp16 one)
     for t in [None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
-                       for r, w, u in MFMA + MFMA16 + MFMA_LDS + MFMA_DMA + MFMA_HX] + [
+                       for r, w, u in MFMA + MFMA16 + MFMA_LDS + MFMA_DMA + MFMA_HX + MFMA_XS] + [
             dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2, grid=g)
-            for r, w, u in MFMA_LDS + MFMA_DMA + MFMA_HX if w > 1 for g in (1, 3)]:
+            for r, w, u in MFMA_LDS + MFMA_DMA + MFMA_HX + MFMA_XS if w > 1
+            for g in (1, 3)]:
         for *_, Yd in host:
             Yd[:, :-1].fill_(float("nan"))
         plan = tvl.tvl_sweep_plan_create(items, t)
@@ -245,7 +252,7 @@ def test_multi_huge_row_stride(dt, ldw, M):
         buf[:, :K] = torch.from_numpy(W.view(np.int16)).to(DEV)
     refs = [(oracle.gemv_f32 if dt == 0 else oracle.gemv_f16)(W, X[b]) for b in range(nb)]
     for t in [None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
-                       for r, w, u in MFMA_LDS + MFMA16 + MFMA_DMA + MFMA_HX]:
+                       for r, w, u in MFMA_LDS + MFMA16 + MFMA_DMA + MFMA_HX + MFMA_XS]:
         Y = run(buf, ldw, dt, X, M, K, nb, M, t)
         for b in range(nb):
             r = oracle.check(Y[b], refs[b][0], refs[b][1], TOL[dt])
