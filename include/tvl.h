@@ -201,10 +201,13 @@ typedef struct tvl_item {
  * split x (launches holding fp32 weights run the LDS-staged form with the
  * same rows and waves) (16,1,133) (16,2,133) (32,1,133) (32,2,133)
  * (64,1,133) (32,1,132) (64,1,132); and with U = 200 + log2(C / 16) the
- * streamed form for fp32 weights with x shared by the block's wavefronts
- * through LDS (launches holding fp16 weights run the LDS-staged form with the
- * same rows and waves) (16,4,202) (32,2,202) (32,4,202) (16,2,203) (16,4,203)
- * (16,8,202).  Rows (and x strides) longer than these forms' buffer
+ * streamed form with x shared by the block's wavefronts through LDS, fp32 or
+ * fp16 weights (launches mixing them run the LDS-staged form with the same
+ * rows and waves) (16,4,202) (32,2,202) (32,4,202) (16,2,203) (16,4,203)
+ * (16,8,202), and with U + 100 its split-x form for fp16 weights (launches
+ * holding fp32 weights run the LDS-staged form) (16,4,303) (32,2,303)
+ * (32,4,303) (16,8,303) (16,4,302) (32,4,302).  Rows (and x strides) longer
+ * than these forms' buffer
  * descriptors can address (a load's 2, 4 or 8 rows within 2^31 bytes) run
  * the direct-load 16x16x4 form.
  * Launches holding block-quantised items (direct-x only; R rows per group of

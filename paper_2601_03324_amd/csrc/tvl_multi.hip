@@ -1370,40 +1370,52 @@ __device__ __forceinline__ void tile_mfma_dma(const DevItem &it, int row0, TVL_L
 // takes part in every barrier: wavefronts with no rows left stream empty
 // descriptors and store nothing, and all choices of path depend only on the
 // item.
-template <int RG, int CC, int WV>
-struct MfmaDmaXsRows : MfmaDmaRows<float, RG, CC, 3> {
-    using Base = MfmaDmaRows<float, RG, CC, 3>;
-    using Base::LPR;
+template <typename T, int RG, int CC, int WV, bool HX>
+struct MfmaDmaXsRows : MfmaDmaRows<T, RG, CC, 3, HX> {
+    using Base = MfmaDmaRows<T, RG, CC, 3, HX>;
     using Base::NL;
     using Base::NQ;
-    using Base::RB;
     using Base::STAGE;
-    static constexpr int XVPL = 1024 / RB;        // vectors per x load
-    static constexpr int XNL = 16 / XVPL;         // x loads per chunk, whole block
+    static constexpr int XRB = CC * 4;             // bytes of a vector's chunk (an x LDS row)
+    static constexpr int XVPL = 1024 / XRB;        // vectors per x load
+    static constexpr int XLPR = kWave / XVPL;      // lanes per vector of an x load
+    static constexpr int XNL = 16 / XVPL;          // x loads per chunk, whole block
     static constexpr int XW = (XNL + WV - 1) / WV; // x loads per chunk, per wavefront (at most)
-    static constexpr int XSTAGE = 16 * RB;         // bytes of an x stage (16 vectors)
+    static constexpr int XSTAGE = 16 * XRB;        // bytes of an x stage (16 vectors)
     static constexpr int WAIT = NL + XW;           // loads of one chunk step (at most)
     static constexpr int64_t MAXLDX = (int64_t(1) << 31) / (4 * XVPL) - 64;
-    static_assert((XNL % WV == 0 || XW == 1) && WAIT < 64, "x loads: all or one per wavefront");
+    static_assert(XRB >= 256 && ((XNL % WV == 0) || XW == 1) && WAIT < 64,
+                  "x rows of >= 256 bytes; x loads: all or one per wavefront");
+
+    // x rows are >= 256 bytes: the swizzle of vector v is v itself
+    static __device__ __forceinline__ int xswz(int v) { return v & (XLPR - 1); }
 
     const float *X; // vector 0 of the item
     int64_t ldx;
     int nb, wave;
     TVL_LDS char *xlds; // the block's x stages
     int xvoff[XW];      // per x load of this wavefront: the lane's byte offset
+    int xraddr[NQ];     // per x operand load: the lane's 16 bytes in an x stage
 
-    __device__ __forceinline__ MfmaDmaXsRows(const float *W_, int64_t ldw_, int wrow0, int M,
+    __device__ __forceinline__ MfmaDmaXsRows(const T *W_, int64_t ldw_, int wrow0, int M,
                                              const float *x, int64_t ldx_, int nb_, int K,
                                              int lane_, int wave_, TVL_LDS char *lds_,
                                              TVL_LDS char *xlds_)
         : Base(W_, ldw_, wrow0, M, x, ldx_, nb_, K, lane_, lds_), X(x), ldx(ldx_), nb(nb_),
           wave(wave_), xlds(xlds_)
     {
-        const int h = lane_ / LPR, p = lane_ % LPR;
+        const int h = lane_ / XLPR, p = lane_ % XLPR, g = lane_ >> 4, j = lane_ & 15;
 #pragma unroll
         for (int u = 0; u < XW; ++u) {
-            const int v = XVPL * (wave_ + WV * u) + h; // vector, < 16
-            xvoff[u] = (int)(h * ldx_ * 4) + 16 * (p ^ Base::swz(v));
+            const int v = XVPL * (wave_ + WV * u) + h; // vector, < 16 when loaded
+            xvoff[u] = (int)(h * ldx_ * 4) + 16 * (p ^ xswz(v));
+        }
+        // the B operand's columns (Base::xoff(k) + 4 or 8 g): 16-byte block
+        // 4 k + g, or with HX 8 (k / 2) + 2 g + k % 2, of vector j's row
+#pragma unroll
+        for (int k = 0; k < NQ; ++k) {
+            const int blk = HX ? 8 * (k >> 1) + 2 * g + (k & 1) : 4 * k + g;
+            xraddr[k] = j * XRB + 16 * (blk ^ xswz(j));
         }
     }
 
@@ -1435,23 +1447,6 @@ struct MfmaDmaXsRows : MfmaDmaRows<float, RG, CC, 3> {
     }
 
     template <int ST>
-    __device__ __forceinline__ void multiply_xs(f4 (&acc)[RG]) const
-    {
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const f4 b = *(const TVL_LDS f4 *)(xlds + ST * XSTAGE + this->raddr[q]);
-#pragma unroll
-            for (int rg = 0; rg < RG; ++rg) {
-                const f4 a =
-                    *(const TVL_LDS f4 *)(this->lds + ST * STAGE + rg * 16 * RB + this->raddr[q]);
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    acc[rg] = mfma16(a[e], b[e], acc[rg]);
-            }
-        }
-    }
-
-    template <int ST>
     __device__ __forceinline__ bool step(int &c, int nfull, f4 (&acc)[RG], f4 (&t1)[RG],
                                          f4 (&t2)[RG], int &n1) const
     {
@@ -1466,7 +1461,11 @@ struct MfmaDmaXsRows : MfmaDmaRows<float, RG, CC, 3> {
         __builtin_amdgcn_sched_barrier(0);
         issue_all<(ST + 2) % 3>((c + 2) * CC, c + 2 < nfull);
         __builtin_amdgcn_sched_barrier(0);
-        multiply_xs<ST>(acc);
+        f4 xb[NQ];
+#pragma unroll
+        for (int k = 0; k < NQ; ++k)
+            xb[k] = *(const TVL_LDS f4 *)(xlds + ST * XSTAGE + xraddr[k]);
+        Base::template multiply<ST>(xb, acc);
 #pragma unroll
         for (int rg = 0; rg < RG; ++rg) {
             t1[rg] += acc[rg];
@@ -1515,12 +1514,12 @@ struct MfmaDmaXsRows : MfmaDmaRows<float, RG, CC, 3> {
 
 // One row tile with x shared by the block; every wavefront runs it to the
 // end (see above).  lds: the block's LDS (weight stages, then x stages).
-template <int RG, int WV, int CC>
+template <typename T, int RG, int WV, int CC, bool HX>
 __device__ __forceinline__ void tile_mfma_dma_xs(const DevItem &it, int row0, TVL_LDS char *lds)
 {
-    using Rows = MfmaDmaXsRows<RG, CC, WV>;
+    using Rows = MfmaDmaXsRows<T, RG, CC, WV, HX>;
     if (it.ldw > Rows::MAXLDW || it.ldx > Rows::MAXLDX) { // the item decides, no barrier
-        tile_mfma16<float, RG, 4, WV>(it, row0);
+        tile_mfma16<T, RG, 4, WV>(it, row0);
         return;
     }
     const int lane = threadIdx.x & (kWave - 1);
@@ -1528,7 +1527,7 @@ __device__ __forceinline__ void tile_mfma_dma_xs(const DevItem &it, int row0, TV
     const int wrow0 = row0 + wave * (16 * RG); // may be past M: empty loads, no stores
     const int nb = it.nrhs < 1 ? 1 : it.nrhs;
     f4 out[RG];
-    const Rows mr(static_cast<const float *>(it.W), it.ldw, wrow0, it.M, it.x, it.ldx, nb, it.K,
+    const Rows mr(static_cast<const T *>(it.W), it.ldw, wrow0, it.M, it.x, it.ldx, nb, it.K,
                   lane, wave, lds + wave * (3 * Rows::STAGE), lds + WV * (3 * Rows::STAGE));
     mr.run(out);
     const int i = lane & 15, g = lane >> 4;
@@ -1544,32 +1543,34 @@ __device__ __forceinline__ void tile_mfma_dma_xs(const DevItem &it, int row0, TV
     }
 }
 
-template <int RG, int WV, int CC>
+template <typename T, int RG, int WV, int CC, bool HX>
 constexpr int dma_xs_lds()
 {
-    using Rows = MfmaDmaXsRows<RG, CC, WV>;
+    using Rows = MfmaDmaXsRows<T, RG, CC, WV, HX>;
     return WV * 3 * Rows::STAGE + 3 * Rows::XSTAGE;
 }
 
-template <int RG, int WV, int CC>
+// launches of one weight dtype (T); HX with fp16 only
+template <typename T, int RG, int WV, int CC, bool HX>
 __global__ __launch_bounds__(WV *kWave) void k_sweep_mfma_xs(const DevItem *__restrict__ items,
                                                               const DevTile *__restrict__ tiles,
                                                               int ntiles)
 {
-    __shared__ f4 lds[dma_xs_lds<RG, WV, CC>() / 16];
+    __shared__ f4 lds[dma_xs_lds<T, RG, WV, CC, HX>() / 16];
     for (int t = blockIdx.x; t < ntiles; t += gridDim.x) { // block-uniform
         const DevTile tl = tiles[t];
         const DevItem it = items[tl.item];
-        tile_mfma_dma_xs<RG, WV, CC>(it, tl.row0, (TVL_LDS char *)lds);
+        tile_mfma_dma_xs<T, RG, WV, CC, HX>(it, tl.row0, (TVL_LDS char *)lds);
         __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
     }
 }
 
-template <int RG, int WV, int CC>
+template <typename T, int RG, int WV, int CC, bool HX>
 __global__ __launch_bounds__(WV *kWave) void k_item_mfma_xs(const DevItem it)
 {
-    __shared__ f4 lds[dma_xs_lds<RG, WV, CC>() / 16];
-    tile_mfma_dma_xs<RG, WV, CC>(it, (int)blockIdx.x * (16 * RG * WV), (TVL_LDS char *)lds);
+    __shared__ f4 lds[dma_xs_lds<T, RG, WV, CC, HX>() / 16];
+    tile_mfma_dma_xs<T, RG, WV, CC, HX>(it, (int)blockIdx.x * (16 * RG * WV),
+                                        (TVL_LDS char *)lds);
 }
 
 // LDS bytes per wavefront of a launch with weight dtypes WM.  A mixed launch
@@ -1677,30 +1678,50 @@ struct InstMfmaLds {
     }
 };
 
-// (rows per wavefront = 16 RG, waves per block, U, columns per chunk) of the
-// streamed form with x shared by the block: U = 200 + log2(CC / 16); fp32
-// weights (launches holding fp16 weights run the LDS-staged form).
+// (rows per wavefront = 16 RG, waves per block, U, columns per chunk, HX)
+// of the streamed form with x shared by the block: U = 200 + log2(CC / 16),
+// + 100 for fp16 weights on the fp16 matrix cores (HX).  Launches mixing
+// weight dtypes, and for HX shapes launches holding fp32 weights, run the
+// LDS-staged form with the same rows and waves.
 #define TVL_MFMA_XS_SHAPES(X)                                                                     \
-    X(16, 4, 202, 64) X(32, 2, 202, 64) X(32, 4, 202, 64) X(16, 2, 203, 128) X(16, 4, 203, 128)   \
-        X(16, 8, 202, 64)
+    X(16, 4, 202, 64, false) X(32, 2, 202, 64, false) X(32, 4, 202, 64, false)                    \
+        X(16, 2, 203, 128, false) X(16, 4, 203, 128, false) X(16, 8, 202, 64, false)              \
+            X(16, 4, 303, 128, true) X(32, 2, 303, 128, true) X(32, 4, 303, 128, true)            \
+                X(16, 8, 303, 128, true) X(16, 4, 302, 64, true) X(32, 4, 302, 64, true)
 
-template <int R, int WV, int CC>
+template <int R, int WV, int CC, bool HX>
 struct InstMfmaXs {
     static constexpr int RG = R / 16;
     static hipError_t sweep(int wm, const DevItem *items, const DevTile *tiles, int ntiles,
                             int grid, hipStream_t st)
     {
-        if (wm != kWF32) return InstMfmaLds<R, WV, 2>::sweep(wm, items, tiles, ntiles, grid, st);
-        hipLaunchKernelGGL((k_sweep_mfma_xs<RG, WV, CC>), dim3(grid), dim3(WV * kWave), 0, st,
-                           items, tiles, ntiles);
-        return hipGetLastError();
+        const dim3 g(grid), b(WV * kWave);
+        if (wm == kWF16) {
+            hipLaunchKernelGGL((k_sweep_mfma_xs<_Float16, RG, WV, CC, HX>), g, b, 0, st, items,
+                               tiles, ntiles);
+            return hipGetLastError();
+        }
+        if constexpr (!HX) {
+            if (wm == kWF32) {
+                hipLaunchKernelGGL((k_sweep_mfma_xs<float, RG, WV, CC, false>), g, b, 0, st,
+                                   items, tiles, ntiles);
+                return hipGetLastError();
+            }
+        }
+        return InstMfmaLds<R, WV, 2>::sweep(wm, items, tiles, ntiles, grid, st);
     }
     static hipError_t item(const DevItem &it, hipStream_t st)
     {
-        if (it.dtype != 0) return InstMfmaLds<R, WV, 2>::item(it, st);
         const dim3 grid((it.M + R * WV - 1) / (R * WV)), block(WV * kWave);
-        hipLaunchKernelGGL((k_item_mfma_xs<RG, WV, CC>), grid, block, 0, st, it);
-        return hipGetLastError();
+        if (it.dtype == 1) {
+            hipLaunchKernelGGL((k_item_mfma_xs<_Float16, RG, WV, CC, HX>), grid, block, 0, st, it);
+            return hipGetLastError();
+        }
+        if constexpr (!HX) {
+            hipLaunchKernelGGL((k_item_mfma_xs<float, RG, WV, CC, false>), grid, block, 0, st, it);
+            return hipGetLastError();
+        }
+        return InstMfmaLds<R, WV, 2>::item(it, st);
     }
 };
 
@@ -1782,7 +1803,7 @@ bool multi_shape_supported(const Shape &s, int B)
 #define D(R_, W_, U_, CC_, S_, HX_) Y(R_, W_, U_)
     TVL_MFMA_DMA_SHAPES(D)
 #undef D
-#define D(R_, W_, U_, CC_) Y(R_, W_, U_)
+#define D(R_, W_, U_, CC_, HX_) Y(R_, W_, U_)
     TVL_MFMA_XS_SHAPES(D)
 #undef D
 #undef X
@@ -1814,9 +1835,9 @@ hipError_t launch_sweep_multi(const Shape &s, int B, int wmode, const DevItem *i
         return InstMfmaDma<R_, W_, CC_, S_, HX_>::sweep(wmode, items, tiles, ntiles, grid, st);
     TVL_MFMA_DMA_SHAPES(D)
 #undef D
-#define D(R_, W_, U_, CC_)                                                                        \
+#define D(R_, W_, U_, CC_, HX_)                                                                   \
     if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
-        return InstMfmaXs<R_, W_, CC_>::sweep(wmode, items, tiles, ntiles, grid, st);
+        return InstMfmaXs<R_, W_, CC_, HX_>::sweep(wmode, items, tiles, ntiles, grid, st);
     TVL_MFMA_XS_SHAPES(D)
 #undef D
 #undef X
@@ -1846,8 +1867,8 @@ hipError_t launch_item_multi(const Shape &s, int B, const DevItem &item, hipStre
         return InstMfmaDma<R_, W_, CC_, S_, HX_>::item(item, st);
     TVL_MFMA_DMA_SHAPES(D)
 #undef D
-#define D(R_, W_, U_, CC_)                                                                        \
-    if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfmaXs<R_, W_, CC_>::item(item, st);
+#define D(R_, W_, U_, CC_, HX_)                                                                   \
+    if (s.R == R_ && s.W == W_ && s.U == U_) return InstMfmaXs<R_, W_, CC_, HX_>::item(item, st);
     TVL_MFMA_XS_SHAPES(D)
 #undef D
 #undef X

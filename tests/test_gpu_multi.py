@@ -40,9 +40,10 @@ MFMA_DMA = [(16, 1, 33), (16, 2, 33), (32, 1, 33), (16, 1, 32), (16, 4, 32), (32
 MFMA_HX = [(16, 1, 133), (16, 2, 133), (32, 1, 133), (32, 2, 133), (64, 1, 133), (32, 1, 132),
            (64, 1, 132)]
 # streamed, x shared by the block's wavefronts through LDS (U = 200 +
-# log2(columns per chunk / 16); fp32 weights, fp16 launches take the
-# LDS-staged form)
-MFMA_XS = [(16, 4, 202), (32, 2, 202), (32, 4, 202), (16, 2, 203), (16, 4, 203), (16, 8, 202)]
+# log2(columns per chunk / 16), + 100 for fp16 weights with split x; mixed
+# launches, and fp32 ones for the split-x shapes, take the LDS-staged form)
+MFMA_XS = [(16, 4, 202), (32, 2, 202), (32, 4, 202), (16, 2, 203), (16, 4, 203), (16, 8, 202),
+           (16, 4, 303), (32, 2, 303), (32, 4, 303), (16, 8, 303), (16, 4, 302), (32, 4, 302)]
 
 
 def tunings(nrhs):
@@ -277,7 +278,7 @@ def test_split_x_keeps_fp32_accuracy(M, K):
     X[2] = rng.standard_normal(K).astype(np.float32)  # plain N(0, 1)
     refs = [oracle.gemv_f16(W, X[b]) for b in range(nb)]
     buf, ldw = dev_matrix(W, 1)
-    for r, w, u in MFMA_HX:
+    for r, w, u in MFMA_HX + [t for t in MFMA_XS if t[2] > 300]:
         Y = run(buf, ldw, 1, X, M, K, nb, M, dict(rows_per_wave=r, waves_per_block=w,
                                                   unroll=u, flags=2))
         for b in range(nb):
