@@ -21,8 +21,9 @@ decode tokens with RMSNorm and SwiGLU fused into the GEMVs: fused110m (fp32,
 2 weight copies alternated) and fused70b8 (fp16 weights); the 110M and 7B
 tokens with block-quantised 8-bit / 4-bit weights (sweep110m_q8, sweep110m_q4,
 sweep7b_q8, sweep7b_q4; small weight sets are rotated over enough copies to
-span 1 GB); and beam4_110m / beam8_110m / beam16_110m (several x vectors per
-weight read).
+span 1 GB); beam4_110m / beam8_110m / beam16_110m (several x vectors per
+weight read) and beam8_70b / beam16_70b (the same over one 70B-shaped fp16
+layer).
 
 Prints ONE JSON line with the metric, a roofline object for the dominant
 kernel and the CPU oracle's throughput on a bounded sample of the workload.
@@ -48,7 +49,8 @@ CSRC = os.path.join(ROOT, "paper_2601_03324_amd", "csrc")
 KERNEL_COMMON = ("tvl_internal.h", "tvl_device.h")
 KERNEL_FAMILY = {"fused110m": "tvl_fused.hip", "fused70b8": "tvl_fused.hip",
                  "beam4_110m": "tvl_multi.hip", "beam8_110m": "tvl_multi.hip",
-                 "beam16_110m": "tvl_multi.hip"}
+                 "beam16_110m": "tvl_multi.hip", "beam8_70b": "tvl_multi.hip",
+                 "beam16_70b": "tvl_multi.hip"}
 
 DESCRIBE = {
     "sweep110m": "sweep110m: one decode token of Llama-2 110M, 85 fp32 GEMVs "
@@ -71,13 +73,21 @@ DESCRIBE = {
                   "GEMVs x 8 x vectors, weights read once, one launch",
     "beam16_110m": "beam16_110m: one decode token of Llama-2 110M for 16 beam hypotheses: 85 "
                    "fp32 GEMVs x 16 x vectors, weights read once, one launch",
+    "beam8_70b": "beam8_70b: one Llama-2 70B-shaped decoder layer for 8 beam hypotheses: 7 "
+                 "GEMVs (wq, wk, wv, wo, w1, w3, w2; 1.71 GB of fp16 weights) x 8 x vectors, "
+                 "weights read once, one launch",
+    "beam16_70b": "beam16_70b: one Llama-2 70B-shaped decoder layer for 16 beam hypotheses: 7 "
+                  "GEMVs (1.71 GB of fp16 weights) x 16 x vectors, weights read once, one launch",
 }
 for _nm, _tok, _n in (("110m", "Llama-2 110M", 85), ("7b", "Llama-2 7B", 225)):
     for _b in (8, 4):
         DESCRIBE[f"sweep{_nm}_q{_b}"] = (
             f"sweep{_nm}_q{_b}: one decode token of {_tok}, {_n} GEMVs with {_b}-bit "
             f"block-quantised weights (one fp32 scale per 64 columns), one launch")
-BEAMS = {"beam4_110m": 4, "beam8_110m": 8, "beam16_110m": 16}
+# beam workloads: (source workload, x vectors, leading matrices used or None)
+BEAMS = {"beam4_110m": ("sweep110m", 4, None), "beam8_110m": ("sweep110m", 8, None),
+         "beam16_110m": ("sweep110m", 16, None), "beam8_70b": ("stack70b8", 8, 7),
+         "beam16_70b": ("stack70b8", 16, 7)}
 
 
 def oracle_rows(oracle, synth, m, rows, x):
@@ -515,14 +525,18 @@ def time_steps(step, steps, warmup, torch, np, stream):
 
 
 def run_beam(args, tvl, torch, np, oracle, synth, sdev) -> int:
-    """The 110M decode token for B beam hypotheses (several x vectors per GEMV)."""
-    B = BEAMS[args.workload]
-    wl = synth.WORKLOADS["sweep110m"]
+    """A decode token (or one layer) for B beam hypotheses (several x vectors
+    per GEMV)."""
+    src, B, nmats = BEAMS[args.workload]
+    wl = synth.WORKLOADS[src]
+    if nmats:
+        wl = synth.Workload(f"{src}[:{nmats}]", wl.cfg, tuple(wl.mats[:nmats]))
+    big = wl.weight_bytes() > 1e9  # far beyond the caches: one copy is cold
     algo = sum(m.wbytes + B * (4 * m.K + 4 * m.M) for m in wl.mats)
     log(f"generating {args.workload}: {len(wl.mats)} GEMVs x {B} vectors")
     a = sdev.load_multi(wl, B, "cuda")
     copies = [a]
-    if not args.warm:
+    if not (args.warm or big):
         copies.append(sdev.load_multi(wl, B, "cuda", share_from=[
             sdev.DevGemv(d.spec, tvl.TvlMatrix(d.W.buf.clone(), d.W.M, d.W.K, d.W.ldw, d.W.dtype),
                          None, None) for d in a]))
@@ -543,15 +557,14 @@ def run_beam(args, tvl, torch, np, oracle, synth, sdev) -> int:
     plans[0].run()
     torch.cuda.synchronize()
     worst = 0.0
-    for j in (0, 6, 84):
+    for j in sorted({0, min(6, len(a) - 1), len(a) - 1}):
         d = a[j]
         m = d.spec
         rows = sdev.sample_rows(m.M, 64, 13)
-        Wr = np.stack([m.weights(int(r), 1)[0] for r in rows])
         Y = d.Y.cpu().numpy()
         for b in range(B):
-            ref, S = oracle.gemv_f32(Wr, m.x(b))
-            r = oracle.check(Y[b][rows], ref, S, 1e-5)
+            ref, S = oracle_rows(oracle, synth, m, rows, m.x(b))
+            r = oracle.check(Y[b][rows], ref, S, 2e-3 if m.dtype == "f16" else 1e-5)
             worst = max(worst, r["max_err"])
             if r["bad"]:
                 log(f"PARITY FAILURE in {m.name} vector {b}: {r}")
@@ -561,7 +574,8 @@ def run_beam(args, tvl, torch, np, oracle, synth, sdev) -> int:
     out = {
         "metric": METRIC, "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 6),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": dtype_label(wl.mats[0]),
         "data": "synthetic (seeded SplitMix64; W ~ N(0, 0.02^2), x ~ N(0, 1) per vector)",
         "config": {"workload": DESCRIBE[args.workload], "algorithmic_bytes_per_step": algo,
                    "vectors": B, "weight_copies_rotated": len(copies), "tiles": info["ntiles"],
@@ -580,7 +594,7 @@ def run_beam(args, tvl, torch, np, oracle, synth, sdev) -> int:
     }
     if not args.no_cpu_baseline:
         samples = [(m, m.weights(), m.x(0)) for m in wl.mats[:7]]
-        out["cpu_baseline"] = cpu_baseline(samples, args.cpu_seconds, "sweep110m (per vector)")
+        out["cpu_baseline"] = cpu_baseline(samples, args.cpu_seconds, f"{wl.name} (per vector)")
     for p in plans:
         p.destroy()
     emit(out)

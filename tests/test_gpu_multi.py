@@ -226,6 +226,34 @@ def test_beam_sweep110m_default(nb):
     plan.destroy()
 
 
+@pytest.mark.parametrize("nb", [8, 16])
+def test_beam_70b_layer_default(nb):
+    """One 70B-shaped fp16 layer (7 GEMVs, 1.71 GB) for 8 and 16 hypotheses in
+    the launch the bench times (the library's default: split x on the fp16
+    matrix cores, x shared by the block): 48 sampled rows of every matrix,
+    every vector, within the fp32 parity bar (1e-5 of the norm)."""
+    src = synth.WORKLOADS["stack70b8"]
+    wl = synth.Workload("stack70b8[:7]", src.cfg, tuple(src.mats[:7]))
+    ms = sdev.load_multi(wl, nb, DEV)
+    for d in ms:
+        d.Y.fill_(float("nan"))
+    plan = tvl.tvl_sweep_plan_create([d.item() for d in ms])
+    plan.run()
+    torch.cuda.synchronize()
+    for k, d in enumerate(ms):
+        m = d.spec
+        rows = sdev.sample_rows(m.M, 48, 21 + k)
+        Wr = np.stack([m.weights(int(r), 1)[0] for r in rows])
+        Y = d.Y.cpu().numpy()
+        for b in range(nb):
+            ref, S = oracle.gemv_f16(Wr, m.x(b))
+            r = oracle.check(Y[b][rows], ref, S, 1e-5)
+            assert r["bad"] == 0, (m.name, nb, b, r)
+    plan.destroy()
+    del ms
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("dt,ldw,M", [(0, (1 << 27) - 64, 5), (0, (1 << 28) - 64, 3),
                                        (0, 1 << 28, 3), (1, (1 << 27) - 64, 9),
                                        (1, (1 << 28) - 64, 5), (1, 1 << 28, 5)],
