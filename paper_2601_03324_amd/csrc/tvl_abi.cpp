@@ -386,8 +386,17 @@ Shape default_fused_shape(double bytes_f16, double bytes_f32)
 }
 
 // Default shape for plans or items with block-quantised weights (from
-// sweeps of the 110M and 7B tokens, 8- and 4-bit, on MI355X).
-Shape default_quant_shape() { return Shape{8, 4, 1, tvl::kXDirect}; }
+// sweeps of the 110M and 7B tokens, 8- and 4-bit, on MI355X): 8 rows per
+// lane group, except for 8-bit launches of under 1 GB of codes, which get 4
+// (twice the wavefronts for a launch too short to reach full bandwidth;
+// 110M token: 5.64 against 5.34-5.38 TB/s; 7B: 6.34 against 6.51, 4-bit 7B:
+// 4.16 against 5.73, 4-bit 110M: 3.14 against 3.82).  qbytes: code bytes of
+// the launch's quantised items; q4: any of them 4-bit.
+Shape default_quant_shape(double qbytes, bool q4)
+{
+    if (!q4 && qbytes < 1e9) return Shape{4, 4, 1, tvl::kXDirect};
+    return Shape{8, 4, 1, tvl::kXDirect};
+}
 
 Shape default_shape_items(const tvl_item *items, int32_t n)
 {
@@ -407,10 +416,15 @@ Shape default_shape_items(const tvl_item *items, int32_t n)
         fused = fused || is_fused(items[i]);
         nmax = std::max<int>(nmax, (int)nvec(items[i]));
     }
-    bool quant = false;
+    bool quant = false, q4 = false;
+    double qbytes = 0;
     for (int32_t i = 0; i < n; ++i)
-        quant = quant || is_quant(items[i].dtype);
-    if (quant) return default_quant_shape();
+        if (is_quant(items[i].dtype)) {
+            quant = true;
+            q4 = q4 || items[i].dtype == TVL_Q4;
+            qbytes += (double)items[i].M * (double)items[i].K * quant_bits(items[i].dtype) / 8;
+        }
+    if (quant) return default_quant_shape(qbytes, q4);
     if (nmax > 1) return default_multi_shape(multi_B(nmax), b16 == 0, b32 == 0);
     if (fused) return default_fused_shape(b16, b32);
     return default_shape(b16, b32, b32 > 0 ? row32 / b32 : 0.0, true);
@@ -714,7 +728,10 @@ tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype, const float *x
         if (tuning && (tuning->flags & TVL_FLAG_X_LDS))
             return fail(TVL_ERR_ARG, "tvl_gemv: quantised weights read x directly (direct-x)");
         Shape qs;
-        st = pick_shape(tuning, default_quant_shape(), &qs, false);
+        st = pick_shape(tuning,
+                        default_quant_shape((double)M * (double)K * quant_bits(dtype) / 8,
+                                            dtype == TVL_Q4),
+                        &qs, false);
         if (st != TVL_OK) return st;
         if (!tvl::quant_shape_supported(qs))
             return fail(TVL_ERR_ARG, "tvl_gemv: no quantised-weight kernel for (%d, %d, %d)", qs.R,
