@@ -525,6 +525,32 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
     Shape shape;
     tvl_status st = pick_shape(tuning, default_shape_items(items, n), &shape, !special);
     if (st != TVL_OK) return st;
+    // every argument check before the first HIP call
+    bool fused = false, quant = false, f32 = false, f16 = false;
+    int nmax = 1;
+    for (int32_t i = 0; i < n; ++i) {
+        fused = fused || is_fused(items[i]);
+        quant = quant || is_quant(items[i].dtype);
+        nmax = std::max<int>(nmax, (int)nvec(items[i]));
+        (items[i].dtype == TVL_F16 ? f16 : f32) = true;
+    }
+    const int multiB = nmax > 1 ? multi_B(nmax) : 0;
+    if (nmax > 1) {
+        if (fused)
+            return fail(TVL_ERR_ARG, "plan: several-vector items cannot share a plan with "
+                                     "RMSNorm or SwiGLU items");
+        if (!tvl::multi_shape_supported(shape, multiB))
+            return fail(TVL_ERR_ARG, "plan: no several-vector kernel for (%d, %d, %d) with %d "
+                                     "vectors",
+                        shape.R, shape.W, shape.U, multiB);
+    }
+    if (quant && !tvl::quant_shape_supported(shape))
+        return fail(TVL_ERR_ARG, "plan: no quantised-weight kernel for (%d, %d, %d)", shape.R,
+                    shape.W, shape.U);
+    if (fused && !tvl::fused_shape_supported(shape))
+        return fail(TVL_ERR_ARG, "plan: items with RMSNorm or SwiGLU need a direct-x shape with "
+                                 "fused support; (%d, %d, %d) %s has none",
+                    shape.R, shape.W, shape.U, shape.xmode == tvl::kXLds ? "LDS-x" : "direct-x");
     int dev = 0;
     DevInfo info;
     st = current_device(&dev, &info);
@@ -535,44 +561,10 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
     p->device = dev;
     p->shape = shape;
     p->items.assign(items, items + n);
-    int nmax = 1;
-    for (int32_t i = 0; i < n; ++i) {
-        p->fused = p->fused || is_fused(items[i]);
-        nmax = std::max<int>(nmax, (int)nvec(items[i]));
-    }
-    {
-        bool f32 = false, f16 = false;
-        for (int32_t i = 0; i < n; ++i)
-            (items[i].dtype == TVL_F16 ? f16 : f32) = true;
-        p->wmode = f32 && f16 ? 2 : f16 ? 1 : 0;
-    }
-    if (nmax > 1) {
-        p->multiB = multi_B(nmax);
-        if (p->fused) {
-            delete p;
-            return fail(TVL_ERR_ARG, "plan: several-vector items cannot share a plan with "
-                                     "RMSNorm or SwiGLU items");
-        }
-        if (!tvl::multi_shape_supported(shape, p->multiB)) {
-            delete p;
-            return fail(TVL_ERR_ARG, "plan: no several-vector kernel for (%d, %d, %d) with %d "
-                                     "vectors",
-                        shape.R, shape.W, shape.U, p->multiB);
-        }
-    }
-    for (int32_t i = 0; i < n; ++i)
-        p->quant = p->quant || is_quant(items[i].dtype);
-    if (p->quant && !tvl::quant_shape_supported(shape)) {
-        delete p;
-        return fail(TVL_ERR_ARG, "plan: no quantised-weight kernel for (%d, %d, %d)", shape.R,
-                    shape.W, shape.U);
-    }
-    if (p->fused && !tvl::fused_shape_supported(shape)) {
-        delete p;
-        return fail(TVL_ERR_ARG, "plan: items with RMSNorm or SwiGLU need a direct-x shape with "
-                                 "fused support; (%d, %d, %d) %s has none",
-                    shape.R, shape.W, shape.U, shape.xmode == tvl::kXLds ? "LDS-x" : "direct-x");
-    }
+    p->fused = fused;
+    p->quant = quant;
+    p->multiB = multiB;
+    p->wmode = f32 && f16 ? 2 : f16 ? 1 : 0;
     // output rows per tile: a SwiGLU tile streams R rows of W and of W3 per
     // wavefront, i.e. R/2 output rows; a quantised item whose rows share a
     // wavefront in groups of G lanes covers 64 / G times R rows per wavefront

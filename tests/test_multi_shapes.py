@@ -1,0 +1,74 @@
+"""The several-vector launch shapes (CPU only): include/tvl.h lists exactly the
+matrix-core shapes the GPU tests run, and the library accepts every listed
+shape, for fp32 and fp16 items, single items and plans, and rejects others.
+No GPU here: an accepted call fails only at the device query (TVL_ERR_HIP).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from multi_shapes import MFMA, MFMA16, MFMA_DMA, MFMA_HX, MFMA_LDS, MFMA_XS, MULTI
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+tvl = pytest.importorskip("paper_2601_03324_amd.tvl",
+                          reason="libtvl.so not built (run __graft_entry__.build())")
+L = tvl.lib
+HIP, ARG = -6, -8
+A, B, C = 1 << 40, 2 << 40, 3 << 40  # fake device addresses, never dereferenced
+
+MATRIX = MFMA + MFMA16 + MFMA_LDS + MFMA_DMA + MFMA_HX + MFMA_XS
+
+
+def header_section(start, end):
+    text = open(os.path.join(ROOT, "include", "tvl.h")).read()
+    return text[text.index(start):text.index(end)]
+
+
+def test_header_lists_the_tested_matrix_core_shapes():
+    sec = header_section("on the matrix cores:", "Launches holding block-quantised")
+    listed = {tuple(map(int, m)) for m in re.findall(r"\((\d+),(\d+),(\d+)\)", sec)}
+    assert listed == set(MATRIX)
+    assert len(MATRIX) == len(set(MATRIX))
+
+
+def test_header_lists_the_tested_valu_shapes():
+    sec = header_section("on the vector ALUs:", "on the matrix cores:")
+    listed = set()
+    for cls, body in re.findall(r"(\d+): ((?:\(\d+,\d+,\d+\)\s*)+)", sec):
+        listed |= {(*map(int, m), int(cls)) for m in re.findall(r"\((\d+),(\d+),(\d+)\)", body)}
+    assert listed == set(MULTI)
+
+
+def call(shape, nrhs, dt):
+    r, w, u = shape
+    it = tvl.item(A, 768, B, C, 768, 768, dt, nrhs=nrhs, ldx=768, ldy=768)
+    t = tvl.tvl_tuning(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
+    single = L.tvl_gemv_item(ctypes.byref(it), ctypes.byref(t), None)
+    arr, n = tvl.make_items([it])
+    h = ctypes.c_void_p()
+    plan = L.tvl_sweep_plan_create(arr, n, ctypes.byref(t), ctypes.byref(h))
+    assert not h.value
+    return single, plan
+
+
+@pytest.mark.parametrize("dt", [0, 1], ids=["f32", "f16"])
+@pytest.mark.parametrize("shape", MATRIX, ids=[f"{r}-{w}-{u}" for r, w, u in MATRIX])
+def test_library_accepts_every_matrix_core_shape(shape, dt):
+    for nrhs in (2, 9, 16):
+        assert call(shape, nrhs, dt) == (HIP, HIP), (shape, nrhs)
+
+
+@pytest.mark.parametrize("shape", MULTI, ids=[f"{r}-{w}-{u}-{b}" for r, w, u, b in MULTI])
+def test_library_accepts_every_valu_shape(shape):
+    r, w, u, b = shape
+    assert call((r, w, u), b, 0) == (HIP, HIP)
+
+
+@pytest.mark.parametrize("shape", [(16, 4, 99), (16, 3, 202), (64, 2, 202), (16, 8, 203),
+                                   (64, 4, 303), (32, 1, 62), (16, 2, 8), (128, 1, 2)])
+def test_unlisted_shapes_are_rejected(shape):
+    assert call(shape, 8, 0) == (ARG, ARG)
