@@ -291,3 +291,34 @@ def test_split_x_keeps_fp32_accuracy(M, K):
         for b in range(nb):
             res = oracle.check(Y[b], refs[b][0], refs[b][1], 1e-5)
             assert res["bad"] == 0, (M, K, (r, w, u), b, res)
+
+
+@pytest.mark.parametrize("ldx", [(1 << 27) - 64, 1 << 27], ids=["xs-limit", "fallback"])
+def test_multi_huge_x_stride(ldx):
+    """x strides at the shared-x forms' limit (4 x vectors of one 64-column
+    chunk row in a buffer descriptor's 31-bit size) and one past it (those
+    launches fall back to the direct-load form): 5 vectors of 0.5 GiB each (a
+    partial group of 4), fp32 and fp16 weights, every launch shape."""
+    M, K, nb = 100, 300, 5
+    rng = np.random.default_rng(ldx % 1000)
+    Xh = rng.standard_normal((nb, K)).astype(np.float32)
+    Xd = torch.empty((nb, ldx), dtype=torch.float32, device=DEV)
+    Xd[:, K:K + 64].fill_(float("nan"))  # next to each vector: never used
+    Xd[:, :K] = torch.from_numpy(Xh).to(DEV)
+    for dt in (0, 1):
+        Wf = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+        W = Wf if dt == 0 else synth.f32_to_f16_bits(Wf)
+        buf, ldw = dev_matrix(W, dt)
+        refs = [(oracle.gemv_f32 if dt == 0 else oracle.gemv_f16)(W, Xh[b]) for b in range(nb)]
+        for t in [None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
+                           for r, w, u in MFMA_XS + MFMA_DMA + MFMA_HX + MFMA_LDS]:
+            Yd = torch.full((nb, M), float("nan"), device=DEV)
+            tvl.tvl_gemv_item(dict(W=buf, ldw=ldw, x=Xd, y=Yd, M=M, K=K, dtype=dt, nrhs=nb,
+                                   ldx=ldx, ldy=M), t)
+            torch.cuda.synchronize()
+            Y = Yd.cpu().numpy()
+            for b in range(nb):
+                r = oracle.check(Y[b], refs[b][0], refs[b][1], TOL[dt])
+                assert r["bad"] == 0, (ldx, dt, t, b, r)
+    del Xd
+    torch.cuda.empty_cache()
