@@ -183,7 +183,8 @@ typedef struct tvl_item {
  *   direct-x: W=1 and W=4: (1,4) (1,8) (2,2) (2,3) (2,4) (2,8) (4,1) (4,2)
  *                  (4,3) (4,4) (8,1) (8,2);  W=8: (1,8) (2,3) (2,4) (4,2)
  * Launches holding RMSNorm or SwiGLU items (direct-x only):
- *   (2,4,2) (2,4,3) (2,4,4) (2,1,4) (4,1,2) (4,1,4) (4,4,2) (2,1,8)
+ *   (2,4,2) (2,4,3) (2,4,4) (2,1,4) (4,1,2) (4,1,4) (4,4,2) (2,1,8) (8,4,1)
+ *   (8,2,1) (4,4,3)
  * Launches holding several-vector items (direct-x only), per vector class
  * (nrhs <= 2, <= 4, <= 8) on the vector ALUs:
  *   2: (2,4,2) (2,4,4) (4,4,2);  4: (2,4,1) (2,4,2) (4,4,1) (4,4,2);

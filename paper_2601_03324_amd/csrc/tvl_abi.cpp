@@ -378,11 +378,13 @@ Shape default_shape(double bytes_f16, double bytes_f32, double f32_row_bytes_wei
 // Default shape for items with a fused RMSNorm or SwiGLU (direct-x only,
 // an even R so a SwiGLU pair fits in one wavefront).  Measured on MI355X
 // over every fused shape: the 110M decode token (fp32) runs best at
-// (2, 4, 3), the 70B-shaped layers (fp16) at (4, 4, 2); the extra g loads
-// make the fused forms a little more register-hungry than the plain ones.
+// (4, 4, 3) (6.88-6.91 TB/s against 6.53-6.61 at (2, 4, 3)), the 70B-shaped
+// layers (fp16) at (8, 2, 1) (6.92 against 6.72 at (4, 4, 2)).  A fused item
+// reads g next to x, so more rows per wavefront share both (x and g bytes
+// per weight byte: 2 / (R · weight size) per 16-byte load).
 Shape default_fused_shape(double bytes_f16, double bytes_f32)
 {
-    return bytes_f16 > bytes_f32 ? Shape{4, 4, 2, tvl::kXDirect} : Shape{2, 4, 3, tvl::kXDirect};
+    return bytes_f16 > bytes_f32 ? Shape{8, 2, 1, tvl::kXDirect} : Shape{4, 4, 3, tvl::kXDirect};
 }
 
 // Default shape for plans or items with block-quantised weights (from

@@ -41,7 +41,8 @@ __global__ __launch_bounds__(WV *kWave) void k_item(const DevItem it)
 
 // (R, waves per block, U) triples with fused RMSNorm / SwiGLU support.
 #define TVL_FUSED_SHAPES(X)                                                                       \
-    X(2, 4, 2) X(2, 4, 3) X(2, 4, 4) X(2, 1, 4) X(4, 1, 2) X(4, 1, 4) X(4, 4, 2) X(2, 1, 8)
+    X(2, 4, 2) X(2, 4, 3) X(2, 4, 4) X(2, 1, 4) X(4, 1, 2) X(4, 1, 4) X(4, 4, 2) X(2, 1, 8)          \
+        X(8, 4, 1) X(8, 2, 1) X(4, 4, 3)
 
 template <int R, int WV, int U>
 struct InstFused {

@@ -29,8 +29,7 @@ import synth.device as sdev  # noqa: E402
 
 TOL = {0: 1e-5, 1: 2e-3}
 DEV = "cuda"
-FUSED_SHAPES = [(2, 4, 2), (2, 4, 3), (2, 4, 4), (2, 1, 4), (4, 1, 2), (4, 1, 4), (4, 4, 2),
-                (2, 1, 8)]
+from multi_shapes import FUSED_SHAPES  # noqa: E402
 TUNINGS = [None] + [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
                     for r, w, u in FUSED_SHAPES]
 

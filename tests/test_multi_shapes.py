@@ -1,5 +1,5 @@
-"""The several-vector launch shapes (CPU only): include/tvl.h lists exactly the
-matrix-core shapes the GPU tests run, and the library accepts every listed
+"""The several-vector and fused launch shapes (CPU only): include/tvl.h lists
+exactly the shapes the GPU tests run, and the library accepts every listed
 shape, for fp32 and fp16 items, single items and plans, and rejects others.
 No GPU here: an accepted call fails only at the device query (TVL_ERR_HIP).
 """
@@ -11,7 +11,7 @@ import re
 
 import pytest
 
-from multi_shapes import MFMA, MFMA16, MFMA_DMA, MFMA_HX, MFMA_LDS, MFMA_XS, MULTI
+from multi_shapes import FUSED_SHAPES, MFMA, MFMA16, MFMA_DMA, MFMA_HX, MFMA_LDS, MFMA_XS, MULTI
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 tvl = pytest.importorskip("paper_2601_03324_amd.tvl",
@@ -72,3 +72,22 @@ def test_library_accepts_every_valu_shape(shape):
                                    (64, 4, 303), (32, 1, 62), (16, 2, 8), (128, 1, 2)])
 def test_unlisted_shapes_are_rejected(shape):
     assert call(shape, 8, 0) == (ARG, ARG)
+
+
+def test_header_lists_the_tested_fused_shapes():
+    sec = header_section("Launches holding RMSNorm or SwiGLU items", "Launches holding several")
+    listed = {tuple(map(int, m)) for m in re.findall(r"\((\d+),(\d+),(\d+)\)", sec)}
+    assert listed == set(FUSED_SHAPES)
+
+
+@pytest.mark.parametrize("shape", FUSED_SHAPES, ids=[f"{r}-{w}-{u}" for r, w, u in FUSED_SHAPES])
+def test_library_accepts_every_fused_shape(shape):
+    r, w, u = shape
+    D = 4 << 40
+    for dt in (0, 1):
+        it = tvl.item(A, 768, B, C, 768, 768, dt, g=D, eps=1e-5)
+        t = tvl.tvl_tuning(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
+        assert L.tvl_gemv_item(ctypes.byref(it), ctypes.byref(t), None) == HIP
+        arr, n = tvl.make_items([it])
+        h = ctypes.c_void_p()
+        assert L.tvl_sweep_plan_create(arr, n, ctypes.byref(t), ctypes.byref(h)) == HIP
