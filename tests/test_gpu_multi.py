@@ -144,7 +144,9 @@ def test_multi_plan_mixed_dtypes():
     vector counts (the mixed-dtype kernels), every output against the oracle,
     also with grids of 1 and 3 workgroups looping over all tiles."""
     rng = np.random.default_rng(4242)
-    specs = [(300, 1000, 0, 5), (130, 2050, 1, 11), (77, 768, 0, 16), (1, 33, 1, 2)]
+    # (M, K, dtype, vectors); one-vector items share several-vector launches too
+    specs = [(300, 1000, 0, 5), (130, 2050, 1, 11), (77, 768, 0, 16), (1, 33, 1, 2),
+             (50, 300, 0, 1), (40, 640, 1, 1)]
     host, items, keep = [], [], []
     for M, K, dt, nb in specs:
         Wf = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
