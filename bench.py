@@ -181,7 +181,7 @@ def cpu_baseline(samples, seconds: float, what: str, threads: int = 1) -> dict:
 
 def host_threads() -> int:
     """Host threads for the all-cores leg: the CPUs this process may run on,
-    capped by OMP_NUM_THREADS when set (a GPU machine's share of its host)."""
+    capped by OMP_NUM_THREADS when set (a container's share of its host)."""
     n = len(os.sched_getaffinity(0))
     omp = os.environ.get("OMP_NUM_THREADS", "")
     return min(n, int(omp)) if omp.isdigit() and int(omp) > 0 else n
