@@ -7,9 +7,10 @@
  * Steps: allocate dense weights and vectors with hipMalloc, pack them into the
  * 128-byte row layout (tvl_pack_rows), run a three-item plan (fp32 ragged,
  * fp16 ragged, fp32 768 x 768) in one launch, run the same items through
- * tvl_gemv_batch_sweep and tvl_gemv, and check every output against the
- * oracle (y = W x, Sec. 6.1; normalised error <= 1e-5 fp32, 2e-3 fp16).  One
- * bad call (a misaligned x) must return TVL_ERR_ALIGN with a message.
+ * tvl_gemv_batch_sweep and tvl_gemv, run two several-vector items (8 fp32 and
+ * 16 fp16 beam vectors), and check every output against the oracle (y = W x,
+ * Sec. 6.1; normalised error <= 1e-5 fp32, 2e-3 fp16, 1e-5 for the beams).
+ * One bad call (a misaligned x) must return TVL_ERR_ALIGN with a message.
  *
  * Exit status: 0 all checks passed, 1 a check failed, 77 no GPU.
  */
@@ -131,6 +132,64 @@ static int check_case(const case_t *c, const char *what)
     return bad != 0;
 }
 
+/* A several-vector item (beam search with nrhs hypotheses): nrhs x vectors
+ * at a stride of ldx floats (the padding holds NaN, never used), nrhs
+ * outputs at a stride of M; every vector against the oracle's GEMV of it,
+ * at the fp32 bar (1e-5 of the norm) for both weight types. */
+static int run_multi(int64_t M, int64_t K, int32_t dtype, int nrhs, uint64_t seed, int single,
+                     hipStream_t st)
+{
+    case_t c;
+    make_case(&c, M, K, dtype, seed);
+    TVL_OK_(tvl_pack_rows(c.packed, c.ldw, c.dense, c.M, c.K, c.dtype, st));
+    const int64_t ldx = (K + 3) / 4 * 4;
+    uint64_t s = seed * 7919u;
+    float *hx = malloc((size_t)(nrhs * ldx) * 4);
+    for (int64_t i = 0; i < nrhs * ldx; ++i) hx[i] = (i % ldx) < K ? uniform(&s, -2.f, 2.f) : NAN;
+    float *dx = NULL, *dy = NULL;
+    HIP_OK(hipMalloc((void **)&dx, (size_t)(nrhs * ldx) * 4));
+    HIP_OK(hipMalloc((void **)&dy, (size_t)(nrhs * M) * 4));
+    HIP_OK(hipMemcpy(dx, hx, (size_t)(nrhs * ldx) * 4, hipMemcpyHostToDevice));
+    HIP_OK(hipMemsetAsync(dy, 0xff, (size_t)(nrhs * M) * 4, st));
+    tvl_item it;
+    memset(&it, 0, sizeof it);
+    it.W = c.packed, it.ldw = c.ldw, it.x = dx, it.y = dy, it.M = M, it.K = K, it.dtype = dtype;
+    it.nrhs = nrhs, it.ldx = ldx, it.ldy = M;
+    if (single)
+        TVL_OK_(tvl_gemv_item(&it, NULL, st));
+    else
+        TVL_OK_(tvl_gemv_batch_sweep(&it, 1, st));
+    HIP_OK(hipStreamSynchronize(st));
+    float *y = malloc((size_t)(nrhs * M) * 4);
+    double *ref = malloc((size_t)M * 8), *S = malloc((size_t)M * 8);
+    HIP_OK(hipMemcpy(y, dy, (size_t)(nrhs * M) * 4, hipMemcpyDeviceToHost));
+    double worst = 0.0;
+    int64_t bad = 0;
+    for (int b = 0; b < nrhs; ++b) {
+        if (dtype == TVL_F16)
+            oracle_gemv_f16(c.host, K, hx + b * ldx, M, K, ref, S);
+        else
+            oracle_gemv_f32(c.host, K, hx + b * ldx, M, K, ref, S);
+        double w = 0.0, mean = 0.0;
+        int64_t at = -1;
+        bad += oracle_check(y + b * M, ref, S, M, 1e-5, &w, &at, &mean);
+        if (w > worst) worst = w;
+    }
+    printf("%s: %lld x %lld %s, %d vectors, max normalised error %.3e%s\n",
+           single ? "multi item" : "multi batch", (long long)M, (long long)K,
+           dtype == TVL_F16 ? "fp16" : "fp32", nrhs, worst, bad ? "  FAIL" : "");
+    free(hx), free(y), free(ref), free(S);
+    HIP_OK(hipFree(dx));
+    HIP_OK(hipFree(dy));
+    HIP_OK(hipFree(c.dense));
+    HIP_OK(hipFree(c.packed));
+    HIP_OK(hipFree(c.dx));
+    HIP_OK(hipFree(c.dy));
+    free(c.host);
+    free(c.hx);
+    return bad != 0;
+}
+
 int main(void)
 {
     int ndev = 0;
@@ -186,6 +245,11 @@ int main(void)
         HIP_OK(hipStreamSynchronize(st));
         fails += check_case(c, "gemv");
     }
+
+    /* beam search: 8 fp32 vectors through the batch entry point, 16 fp16
+     * vectors through the single-item one (the library's default kernels) */
+    fails += run_multi(300, 1000, TVL_F32, 8, 4, 0, st);
+    fails += run_multi(130, 2050, TVL_F16, 16, 5, 1, st);
 
     /* an error is returned, not raised, and nothing is enqueued */
     const tvl_status bad = tvl_gemv(cs[0].packed, cs[0].ldw, TVL_F32, cs[0].dx + 1, cs[0].dy,

@@ -4,8 +4,8 @@
 
 On a host without a GPU the driver must load both libraries and report that
 there is no device (exit status 77); on a GPU it packs three matrices, runs a
-plan, a cached batch and single GEMVs, and checks every output against the C
-oracle.
+plan, a cached batch and single GEMVs, then two several-vector items (8 fp32
+and 16 fp16 beam vectors), and checks every output against the C oracle.
 """
 from __future__ import annotations
 
@@ -45,4 +45,5 @@ def test_c_driver_on_gpu():
     print(r.stdout)
     assert r.returncode == 0, (r.returncode, r.stdout, r.stderr)
     assert "all checks passed" in r.stdout
-    assert r.stdout.count("max normalised error") == 12  # 3 items x (plan + 2 batches + gemv)
+    # 3 items x (plan + 2 batches + gemv), and 2 several-vector items
+    assert r.stdout.count("max normalised error") == 14
