@@ -187,7 +187,7 @@ typedef struct tvl_item {
  *   (8,2,1) (4,4,3)
  * Launches holding several-vector items (direct-x only), per vector class
  * (nrhs <= 2, <= 4, <= 8) on the vector ALUs:
- *   2: (2,4,2) (2,4,4) (4,4,2);  8: (2,4,1) (2,4,2) (4,4,1);
+ *   2: (2,4,2) (2,4,4) (4,4,2) (8,2,1);  8: (2,4,1) (2,4,2) (4,4,1);
  *   4: (2,4,1) (2,4,2) (4,4,1) (4,4,2) (8,4,1) (8,2,1)
  * and, for any nrhs <= 16, on the matrix cores: the 4x4x1 form (rows in
  * groups of 4, U = 1) (8,4,1) (16,1,1) (16,2,1); the 16x16x4 form (rows

@@ -270,8 +270,10 @@ int multi_B(int n) { return n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16; }
 // 110M decode token and a 70B-shaped fp16 layer.  Up to 4 vectors the VALU
 // form wins: more rows per wavefront amortise each x read over more weights
 // (3-4 vectors: 8 rows, 6.36-6.39 TB/s against 6.09-6.10 with 4 rows on the
-// 110M token; fp16, 2 wavefronts per block: 6.02-6.10 against 5.62-5.75),
-// and one load in flight keeps the R x B accumulators in registers.  From 5 vectors on,
+// 110M token; fp16, 2 wavefronts per block: 6.02-6.10 against 5.62-5.75;
+// 2 fp16 vectors: 6.36 against 6.09-6.17, while 2 fp32 vectors keep 4 rows,
+// 7.00-7.01 against 6.90-6.91), and one load in flight keeps the R x B
+// accumulators in registers.  From 5 vectors on,
 // the FMAs would take ~half the VALU issue slots and the matrix cores win.
 // fp32 weights: the 16 x 16 x 4 form with the weights streamed into LDS and
 // x shared by the block's four wavefronts (16 rows each, 64-column chunks;
@@ -295,7 +297,7 @@ Shape default_multi_shape(int B, bool all_f32, bool all_f16)
     if (B > 8) return Shape{16, 1, 2, tvl::kXDirect};
     if (B > 4) return Shape{32, 1, 32, tvl::kXDirect};
     if (B == 4) return all_f16 ? Shape{8, 2, 1, tvl::kXDirect} : Shape{8, 4, 1, tvl::kXDirect};
-    return Shape{4, 4, 2, tvl::kXDirect};
+    return all_f16 ? Shape{8, 2, 1, tvl::kXDirect} : Shape{4, 4, 2, tvl::kXDirect};
 }
 
 int quant_bits(int32_t dt) { return dt == TVL_Q4 ? 4 : 8; }

@@ -1769,7 +1769,8 @@ struct InstMfmaDma {
 // (R, waves per block, U, B) with B x vectors per launch (B >= nrhs).
 #define TVL_MULTI_SHAPES(X)                                                                       \
     X(2, 4, 2, 2) X(2, 4, 4, 2) X(4, 4, 2, 2) X(2, 4, 1, 4) X(2, 4, 2, 4) X(4, 4, 1, 4)          \
-        X(4, 4, 2, 4) X(2, 4, 1, 8) X(2, 4, 2, 8) X(4, 4, 1, 8) X(8, 4, 1, 4) X(8, 2, 1, 4)
+        X(4, 4, 2, 4) X(2, 4, 1, 8) X(2, 4, 2, 8) X(4, 4, 1, 8) X(8, 4, 1, 4) X(8, 2, 1, 4)      \
+            X(8, 2, 1, 2)
 
 template <int R, int WV, int U, int B>
 struct InstMulti {

@@ -7,7 +7,8 @@ forms: (rows per wavefront, waves per block, U), any nrhs <= 16.
 """
 
 MULTI = [(2, 4, 2, 2), (2, 4, 4, 2), (4, 4, 2, 2), (2, 4, 1, 4), (2, 4, 2, 4), (4, 4, 1, 4),
-         (4, 4, 2, 4), (2, 4, 1, 8), (2, 4, 2, 8), (4, 4, 1, 8), (8, 4, 1, 4), (8, 2, 1, 4)]
+         (4, 4, 2, 4), (2, 4, 1, 8), (2, 4, 2, 8), (4, 4, 1, 8), (8, 4, 1, 4), (8, 2, 1, 4),
+         (8, 2, 1, 2)]
 # matrix-core forms, any nrhs <= 16: 4x4x1 (rows per wavefront 8 or 16, waves
 # per block, unroll 1) and 16x16x4 (16 x row groups, waves per block, loads
 # per row group in flight >= 4)
