@@ -17,12 +17,13 @@ namespace {
 // and scaled once.
 //
 // Decoding costs VALU work per code (a 4-bit row streams two codes per byte),
-// so every code converts with ONE sign-extending SDWA conversion of a byte
-// (v_cvt_f32_i32 with a byte select) and one FMA, exactly:
-//   8-bit: the bytes are the codes;
-//   4-bit: (v << 4) & 0xF0F0F0F0 and v & 0xF0F0F0F0 put 16 * q of the low
-//          and of the high nibbles in the top of each byte; the factor 16
-//          is folded into the scale (a power of two, exact).
+// so every code converts with ONE conversion instruction and one FMA, exactly:
+//   8-bit: a sign-extending SDWA conversion of a byte (v_cvt_f32_i32 with a
+//          byte select); the bytes are the codes;
+//   4-bit: v_cvt_off_f32_i4 turns the signed nibble in bits 3:0 of its
+//          operand into q / 16; an SDWA byte select reaches the low nibble
+//          of each byte of a dword v, and of v >> 4 (its high nibbles).  The
+//          factor 1/16 is folded into the scale (a power of two, exact).
 //
 // Short rows: a wavefront splits into 64 / G groups of G lanes, one row per
 // group (G from quant_lanes), so a 384-byte row still fills its lanes.
@@ -43,33 +44,40 @@ __device__ __forceinline__ float qdot8(const u4 w, const f4 (&xv)[4])
     return ta + tb;
 }
 
-// 4-bit: 16 * sum_j q_j x_j over the 32 columns of one 16-byte vector.  Dword
+// q / 16 for the signed nibble in bits 3:0 of byte B of v
+#define TVL_NIB16(B)                                                                              \
+    __device__ __forceinline__ float nib16_##B(unsigned v)                                        \
+    {                                                                                             \
+        float r;                                                                                  \
+        asm("v_cvt_off_f32_i4_sdwa %0, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_" #B \
+            : "=v"(r) : "v"(v));                                                                  \
+        return r;                                                                                 \
+    }
+TVL_NIB16(0)
+TVL_NIB16(1)
+TVL_NIB16(2)
+TVL_NIB16(3)
+#undef TVL_NIB16
+
+// 4-bit: sum_j q_j x_j / 16 over the 32 columns of one 16-byte vector.  Dword
 // d holds columns 8d .. 8d+7, column 8d + 2b in the low nibble of byte b and
-// 8d + 2b + 1 in its high nibble.
+// 8d + 2b + 1 in its high nibble.  Per 8 codes: one shift, 8 conversions and
+// 8 FMAs.
 __device__ __forceinline__ float qdot4(const u4 w, const f4 (&xv)[8])
 {
     float ta = 0.f, tb = 0.f; // even columns; odd columns
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
-        // lo = (w << 4) & 0xF0F0F0F0, hi = w & 0xF0F0F0F0, formed here and
-        // only here: written plainly, the optimiser moves each mask past the
-        // byte sign extension (an AND per code instead of per dword) and
-        // hoists every row's masks together (registers)
-        unsigned lo, hi;
-        asm volatile("v_lshlrev_b32 %0, 4, %2\n\t"
-                     "v_and_b32 %0, 0xf0f0f0f0, %0\n\t"
-                     "v_and_b32 %1, 0xf0f0f0f0, %2"
-                     : "=&v"(lo), "=v"(hi)
-                     : "v"(w[d]));
+        const unsigned lo = w[d], hi = w[d] >> 4;
         const f4 x0 = xv[2 * d], x1 = xv[2 * d + 1];
-        ta = fmaf(sbyte(lo, 0), x0.x, ta);
-        tb = fmaf(sbyte(hi, 0), x0.y, tb);
-        ta = fmaf(sbyte(lo, 1), x0.z, ta);
-        tb = fmaf(sbyte(hi, 1), x0.w, tb);
-        ta = fmaf(sbyte(lo, 2), x1.x, ta);
-        tb = fmaf(sbyte(hi, 2), x1.y, tb);
-        ta = fmaf(sbyte(lo, 3), x1.z, ta);
-        tb = fmaf(sbyte(hi, 3), x1.w, tb);
+        ta = fmaf(nib16_0(lo), x0.x, ta);
+        tb = fmaf(nib16_0(hi), x0.y, tb);
+        ta = fmaf(nib16_1(lo), x0.z, ta);
+        tb = fmaf(nib16_1(hi), x0.w, tb);
+        ta = fmaf(nib16_2(lo), x1.x, ta);
+        tb = fmaf(nib16_2(hi), x1.y, tb);
+        ta = fmaf(nib16_3(lo), x1.z, ta);
+        tb = fmaf(nib16_3(hi), x1.w, tb);
     }
     return ta + tb;
 }
@@ -160,7 +168,7 @@ struct QuantRows {
     __device__ __forceinline__ void accumulate(float &acc, const u4 w, float sc, const f4 (&xv)[NX]) const
     {
         if constexpr (BITS == 4)
-            acc = fmaf(sc * 0.0625f, qdot4(w, xv), acc);
+            acc = fmaf(sc * 16.f, qdot4(w, xv), acc);
         else
             acc = fmaf(sc, qdot8(w, xv), acc);
     }
