@@ -654,7 +654,7 @@ def run_fused(args, tvl, torch, np, oracle, synth, sdev) -> int:
         else:
             W3 = np.stack([it.W3.weights(int(rr), 1)[0] for rr in rows])
             href, a, b, Sa, Sb = oracle.swiglu_ffn_in(W, W3, x, g, it.eps)
-            r = oracle.check(y, href, oracle.swiglu_bound(a, b, Sa, Sb, href), tol)
+            r = oracle.check(y, href, oracle.swiglu_bound(a, b, Sa, Sb), tol)
         worst = max(worst, r["max_err"])
         if r["bad"]:
             log(f"PARITY FAILURE in {it.name}: {r}")

@@ -99,7 +99,7 @@ def test_swiglu_item(M, K, norm, dt):
     x = (rng.standard_normal(K) * 4).astype(np.float32)
     g = rng.uniform(0.5, 1.5, K).astype(np.float32) if norm else None
     href, a, b, Sa, Sb = oracle.swiglu_ffn_in(W1, W3, x, g, 1e-5)
-    bound = oracle.swiglu_bound(a, b, Sa, Sb, href)
+    bound = oracle.swiglu_bound(a, b, Sa, Sb)
     b1, ldw = dev_matrix(W1, dt)
     b3, _ = dev_matrix(W3, dt)
     xd = torch.from_numpy(x).to(DEV)
@@ -193,7 +193,7 @@ def _check_fused_gemvs(gemvs, what, rows=None):
             W3 = (it.W3.weights() if rows is None
                   else np.stack([it.W3.weights(int(i), 1)[0] for i in idx]))
             href, a, b, Sa, Sb = oracle.swiglu_ffn_in(W, W3, x, g, it.eps)
-            bound = oracle.swiglu_bound(a, b, Sa, Sb, href)
+            bound = oracle.swiglu_bound(a, b, Sa, Sb)
             worst = max(worst, check_swiglu(y, href, bound, dt, f"{what} {it.name}"))
     return worst
 
@@ -263,6 +263,6 @@ def test_mixed_plain_and_fused_plan():
                 check_gemv(y.cpu().numpy(), yref, S, dt, f"mixed gemv {t}")
             else:
                 href, a, b, Sa, Sb = oracle.swiglu_ffn_in(W1, W3, x, g, 1e-5)
-                check_swiglu(y.cpu().numpy(), href, oracle.swiglu_bound(a, b, Sa, Sb, href), dt,
+                check_swiglu(y.cpu().numpy(), href, oracle.swiglu_bound(a, b, Sa, Sb), dt,
                              f"mixed swiglu {t}")
         plan.destroy()

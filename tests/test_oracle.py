@@ -341,6 +341,84 @@ def pin_swiglu():
     assert np.all(oracle.swiglu(np.array([1.0, -2.0, 3.0]), np.zeros(3)) == 0.0)
 
 
+def _h_exact(a: float, b: float) -> float:
+    """h = silu(a) b written out with math.exp (independent of the oracle)."""
+    return a * b / (1.0 + math.exp(-a))
+
+
+def pin_swiglu_bound(o=oracle):
+    """The gate's normaliser N = |silu'(a)| |b| Sa + |silu(a)| Sb (Sec. 2.1
+    FFN; the GEMV parity norm carried through h = silu(a) b).
+
+    * hand-worked: at a = 0, silu = 0 and silu' = 1/2, so N = |b| Sa / 2; at
+      a = 40 (saturated), silu' = 1 and silu = 40 to double precision; at
+      a = -40, s = e^-40 / (1 + e^-40), silu = -40 s, silu' = s (1 - 40 (1 - s));
+    * tightness: the largest change of h over the four corners
+      (a +- t Sa, b +- t Sb), computed with math.exp, is t N to first order
+      (within 1e-3 at t = 1e-7) for random a, b, Sa, Sb on both sides of
+      silu's minimum (a = -1.278...) and on both signs of b;
+    * the corner bound holds for a GPU-like error too: h moves by at most
+      t N (1 + 1e-3) for every perturbation inside the box."""
+    a = np.array([0.0, 0.0, 40.0, -40.0])
+    b = np.array([3.0, -2.0, -0.5, 2.0])
+    Sa = np.array([5.0, 1.0, 7.0, 3.0])
+    Sb = np.array([4.0, 6.0, 1.5, 9.0])
+    N = o.swiglu_bound(a, b, Sa, Sb)
+    assert N[0] == 3.0 * 5.0 / 2 and N[1] == 2.0 * 1.0 / 2
+    assert abs(N[2] - (0.5 * 7.0 + 40.0 * 1.5)) <= 1e-14 * N[2]
+    s = math.exp(-40.0) / (1.0 + math.exp(-40.0))
+    ref = abs(s * (1.0 - 40.0 * (1.0 - s))) * 2.0 * 3.0 + abs(-40.0 * s) * 9.0
+    assert abs(N[3] - ref) <= 1e-12 * ref
+    rng = np.random.default_rng(31)
+    n = 400
+    a = rng.uniform(-8.0, 8.0, n)
+    a[:40] = rng.uniform(-1.6, -1.0, 40)  # around silu's minimum (silu' = 0)
+    b = rng.uniform(-3.0, 3.0, n)
+    Sa = np.abs(a) * rng.uniform(1.0, 4.0, n) + rng.uniform(0.0, 1.0, n)
+    Sb = np.abs(b) * rng.uniform(1.0, 4.0, n) + rng.uniform(0.0, 1.0, n)
+    N = o.swiglu_bound(a, b, Sa, Sb)
+    t = 1e-7
+    for i in range(n):
+        h0 = _h_exact(a[i], b[i])
+        dmax = max(abs(_h_exact(a[i] + sa * t * Sa[i], b[i] + sb * t * Sb[i]) - h0)
+                   for sa in (-1.0, 1.0) for sb in (-1.0, 1.0))
+        assert abs(dmax - t * N[i]) <= 1e-3 * t * N[i], (i, a[i], b[i], dmax, t * N[i])
+        for da, db in rng.uniform(-1.0, 1.0, (4, 2)):
+            d = abs(_h_exact(a[i] + da * t * Sa[i], b[i] + db * t * Sb[i]) - h0)
+            assert d <= t * N[i] * (1 + 1e-3)
+
+
+def pin_swiglu_ffn_in(o=oracle):
+    """swiglu_ffn_in composes RMSNorm, both GEMVs and the gate: W1 and W3 see
+    the same normalised x.  With x = c (a constant) the normalised x is
+    g c / sqrt(c^2 + eps) (closed form); with W1 = 2 I and W3 = I,
+    a = 2 xn and b = xn exactly, and h = silu(a) b."""
+    K = 8
+    c, eps = 3.0, 0.25
+    x = np.full(K, c, np.float32)
+    g = np.array([0.5, 1.0, 1.5, 2.0, -1.0, 0.25, 4.0, 3.0], np.float32)
+    xn = [float(gj) * c / math.sqrt(c * c + eps) for gj in g]
+    I = np.eye(K, dtype=np.float32)
+    h, a, b, Sa, Sb = o.swiglu_ffn_in(2 * I, I, x, g, eps)
+    for j in range(K):
+        assert abs(a[j] - 2 * xn[j]) <= 4 * U * abs(xn[j])
+        assert abs(b[j] - xn[j]) <= 4 * U * abs(xn[j])
+        assert Sa[j] == abs(a[j]) and Sb[j] == abs(b[j])
+        assert abs(h[j] - _h_exact(2 * xn[j], xn[j])) <= 16 * U * abs(h[j])
+    # without g the raw x goes to both GEMVs
+    h, a, b, _, _ = o.swiglu_ffn_in(2 * I, I, x)
+    assert np.all(a == 2 * c) and np.all(b == c)
+    assert np.allclose(h, _h_exact(2 * c, c), rtol=16 * U, atol=0)
+    # a fp16 W1 (bit patterns) and a fp32 W3 of the same values agree
+    rng = np.random.default_rng(32)
+    Wi = rng.integers(-3, 4, (5, 40)).astype(np.float16)
+    xr = rng.standard_normal(40).astype(np.float32)
+    gr = rng.uniform(0.5, 1.5, 40).astype(np.float32)
+    h16, a16, b16, _, _ = o.swiglu_ffn_in(Wi.view(np.uint16), Wi.astype(np.float32), xr, gr)
+    assert np.array_equal(a16, b16)
+    assert np.allclose(h16, [_h_exact(v, v) for v in a16], rtol=16 * U, atol=0)
+
+
 # --------------------------------------------------- quantised-weight pins
 def _q_rows(codes: np.ndarray, scales: np.ndarray, bits: int, extra: int = 0):
     """Build a quantised matrix by hand (not with the generator's quantiser):
@@ -440,7 +518,8 @@ PINS = [pin_golden, pin_products_exact, pin_brute_force_exact, pin_brute_force_e
         pin_index_and_stride, pin_identity, pin_all_ones_rows, pin_integer_exact,
         pin_linearity, pin_one_hot, pin_zero_row, pin_f16_decode_all_patterns,
         pin_f16_subnormal_gemv, pin_check_rules, pin_rmsnorm_closed_forms,
-        pin_rmsnorm_invariances, pin_rmsnorm_gemv, pin_swiglu, pin_quant_golden,
+        pin_rmsnorm_invariances, pin_rmsnorm_gemv, pin_swiglu, pin_swiglu_bound,
+        pin_swiglu_ffn_in, pin_quant_golden,
         pin_quant_matches_dequantized, pin_quant_exact_rational]
 
 
@@ -518,6 +597,52 @@ def test_mutants_are_caught(tmp_path):
                     # a pin that cannot even evaluate the mutant's output
                     # (NaN or Inf where an exact value belongs) catches it too
                     caught.append(pin.__name__)
+        if not caught:
+            survivors.append(name)
+    assert not survivors, f"mutants not caught by any pin: {survivors}"
+
+
+# Plausible mistakes in the Python part of the oracle (the SwiGLU gate's
+# normaliser and the FFN-input composition), each applied to a private copy of
+# oracle/__init__.py that still calls the real C library.
+PY_MUTANTS = {
+    "bound_dsilu_abs_dropped": ("np.abs(dsilu) * np.abs(b) * Sa", "dsilu * np.abs(b) * Sa"),
+    "bound_silu_abs_dropped": ("np.abs(a * sig) * Sb", "a * sig * Sb"),
+    "bound_Sa_Sb_swapped": ("np.abs(dsilu) * np.abs(b) * Sa + np.abs(a * sig) * Sb",
+                            "np.abs(dsilu) * np.abs(b) * Sb + np.abs(a * sig) * Sa"),
+    "bound_b_dropped": ("np.abs(dsilu) * np.abs(b) * Sa", "np.abs(dsilu) * Sa"),
+    "bound_dsilu_is_sigmoid": ("dsilu = sig * (1.0 + a * (1.0 - sig))", "dsilu = sig"),
+    "bound_dsilu_sign": ("dsilu = sig * (1.0 + a * (1.0 - sig))",
+                         "dsilu = sig * (1.0 - a * (1.0 - sig))"),
+    "bound_sigmoid_sign": ("sig = 1.0 / (1.0 + np.exp(-a))", "sig = 1.0 / (1.0 + np.exp(a))"),
+    "bound_second_term_dropped": ("np.abs(dsilu) * np.abs(b) * Sa + np.abs(a * sig) * Sb",
+                                  "np.abs(dsilu) * np.abs(b) * Sa"),
+    "ffn_W3_sees_raw_x": ("b, Sb = gemv_dx(W3, xd, K)",
+                          "b, Sb = gemv_dx(W3, np.asarray(x, np.float32).astype(np.float64), K)"),
+    "ffn_W1_sees_raw_x": ("a, Sa = gemv_dx(W1, xd, K)",
+                          "a, Sa = gemv_dx(W1, np.asarray(x, np.float32).astype(np.float64), K)"),
+    "ffn_W1_W3_swapped": ("a, Sa = gemv_dx(W1, xd, K)\n    b, Sb = gemv_dx(W3, xd, K)",
+                          "a, Sa = gemv_dx(W3, xd, K)\n    b, Sb = gemv_dx(W1, xd, K)"),
+    "ffn_gate_on_b": ("return swiglu(a, b), a, b, Sa, Sb", "return swiglu(b, a), a, b, Sa, Sb"),
+}
+PY_PINS = [pin_swiglu_bound, pin_swiglu_ffn_in]
+
+
+def test_python_mutants_are_caught():
+    import types
+    src = open(oracle.__file__).read()
+    survivors = []
+    for name, (old, new) in PY_MUTANTS.items():
+        assert src.count(old) == 1, name
+        mod = types.ModuleType("oracle_mutant_" + name)
+        mod.__file__ = oracle.__file__  # same liboracle.so
+        exec(compile(src.replace(old, new, 1), oracle.__file__, "exec"), mod.__dict__)
+        caught = []
+        for pin in PY_PINS:
+            try:
+                pin(mod)
+            except (AssertionError, ValueError, OverflowError):
+                caught.append(pin.__name__)
         if not caught:
             survivors.append(name)
     assert not survivors, f"mutants not caught by any pin: {survivors}"
