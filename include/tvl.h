@@ -31,7 +31,8 @@
  * the caller; the library never allocates, frees or retains them.  The same
  * W or x may appear in several items (a tied classifier, Sec. 5.1; a shared
  * activation).  The library owns only what it allocates itself: plan objects
- * and the K-split workspace (see tvl_gemv).
+ * and the K-split workspace (see tvl_gemv), plus one static scratch array per
+ * GPU for tvl_gemv_noalloc.
  *
  * Streams.  Every compute call enqueues work on `stream` (0 = the null
  * stream) and returns without synchronising; results are valid once the
@@ -264,6 +265,30 @@ TVL_API tvl_status tvl_gemv(const void *W, int64_t ldw, int32_t dtype,
 TVL_API tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype,
                                const float *x, float *y, int64_t M, int64_t K,
                                const tvl_tuning *tuning, hipStream_t stream);
+
+/* tvl_gemv_ex for callers that cannot allocate device memory: code that is
+ * being captured into a HIP graph, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, same variant choice, same kernels and
+ * bitwise the same results as tvl_gemv_ex; it never calls hipMalloc,
+ * hipFree or any allocating routine.  Where the variant is a K split, its
+ * partials and arrival counters live in a static array of the library
+ * (one per GPU, 4.25 MiB, held until the process ends) instead of a
+ * per-stream workspace:
+ *   - a K split needs S * M <= 2^20 partials and at most 2^16 row tiles
+ *     (S: slices, from `tuning` or by shape); larger splits return
+ *     TVL_ERR_SHAPE and enqueue nothing.  The default split (M <= 128 rows
+ *     of >= 32 KB, S <= 4) always fits;
+ *   - every call on one GPU shares that GPU's array, so calls that overlap
+ *     on one GPU (concurrent streams or host threads) race and may return
+ *     wrong results: order them;
+ *   - each launch leaves the counters at zero again; the first call on a
+ *     device looks the array up and clears the counters on `stream`, then
+ *     synchronises `stream`.  That first call must not be captured: while
+ *     `stream` is capturing it returns TVL_ERR_ARG and enqueues nothing.
+ *     Later calls make no HIP call besides the launch. */
+TVL_API tvl_status tvl_gemv_noalloc(const void *W, int64_t ldw, int32_t dtype,
+                                    const float *x, float *y, int64_t M, int64_t K,
+                                    const tvl_tuning *tuning, hipStream_t stream);
 
 /* One item (any op, with or without RMSNorm) in one launch.  A plain GEMV
  * item is the same as tvl_gemv_ex; fused items use the direct-x row split.

@@ -662,6 +662,136 @@ void plan_free(tvl_plan *p)
 std::map<std::string, tvl_plan *> g_cache;
 constexpr size_t kCacheMax = 64;
 
+// First tvl_gemv_noalloc call on a device: look up its static scratch and
+// clear the counters (tvl::noalloc_scratch; later calls make no HIP call).
+tvl_status noalloc_setup(int dev, hipStream_t stream, float **partials, int **counters)
+{
+    const hipError_t e = tvl::noalloc_scratch(dev, stream, partials, counters);
+    if (e == hipErrorStreamCaptureUnsupported)
+        return fail(TVL_ERR_ARG, "tvl_gemv_noalloc: the first call on device %d clears the "
+                                 "static scratch and synchronises its stream, so it cannot be "
+                                 "captured; make one call before capturing", dev);
+    if (e != hipSuccess) return fail_hip(e, "tvl_gemv_noalloc scratch set-up");
+    return TVL_OK;
+}
+
+// tvl_gemv_ex and tvl_gemv_noalloc: the same variant choice; `noalloc` puts
+// the K split's partials and counters in the library's static per-device
+// scratch instead of a per-stream workspace.
+tvl_status gemv_impl(const void *W, int64_t ldw, int32_t dtype, const float *x, float *y,
+                     int64_t M, int64_t K, const tvl_tuning *tuning, hipStream_t stream,
+                     bool noalloc)
+{
+    const char *who = noalloc ? "tvl_gemv_noalloc" : "tvl_gemv";
+    tvl_status st = check_one(W, ldw, dtype, x, y, M, K, who);
+    if (st != TVL_OK) return st;
+    tvl_item it{W, ldw, x, y, M, K, dtype, TVL_OP_GEMV, nullptr, nullptr, 0.f, 1, 0, 0};
+    st = check_alias(&it, 1);
+    if (st != TVL_OK) return st;
+    st = check_tuning(tuning, true);
+    if (st != TVL_OK) return st;
+
+    // Variant by shape.  Row split when there are enough row tiles to give
+    // every CU several workgroups; otherwise split K so that small-M GEMVs
+    // still spread over the whole GPU.
+    Shape shape;
+    int S = 1;
+    const bool user_shape =
+        tuning && (tuning->rows_per_wave || tuning->waves_per_block || tuning->unroll);
+    if (is_quant(dtype)) {
+        if (tuning && tuning->ksplit > 1)
+            return fail(TVL_ERR_ARG, "%s: quantised weights have no K split", who);
+        if (tuning && (tuning->flags & TVL_FLAG_X_LDS))
+            return fail(TVL_ERR_ARG, "%s: quantised weights read x directly (direct-x)", who);
+        Shape qs;
+        st = pick_shape(tuning,
+                        default_quant_shape((double)M * (double)K * quant_bits(dtype) / 8,
+                                            dtype == TVL_Q4),
+                        &qs, false);
+        if (st != TVL_OK) return st;
+        if (!tvl::quant_shape_supported(qs))
+            return fail(TVL_ERR_ARG, "%s: no quantised-weight kernel for (%d, %d, %d)", who,
+                        qs.R, qs.W, qs.U);
+        int qdev = 0;
+        DevInfo qinfo;
+        st = current_device(&qdev, &qinfo);
+        if (st != TVL_OK) return st;
+        if (noalloc) { // no scratch here; the first call on a device still sets it up
+            float *p = nullptr;
+            int *c = nullptr;
+            st = noalloc_setup(qdev, stream, &p, &c);
+            if (st != TVL_OK) return st;
+        }
+        const hipError_t qe = tvl::launch_item_quant(qs, dev_item(it), stream);
+        if (qe != hipSuccess) return fail_hip(qe, "quantised gemv launch");
+        return TVL_OK;
+    }
+    const Shape def = default_shape(dtype == TVL_F16 ? 1.0 : 0.0, dtype == TVL_F16 ? 0.0 : 1.0,
+                                    (double)K * 4.0, false);
+    shape = def;
+    if (user_shape || (tuning && tuning->flags)) {
+        st = pick_shape(tuning, def, &shape);
+        if (st != TVL_OK) return st;
+    }
+
+    int dev = 0;
+    DevInfo info;
+    st = current_device(&dev, &info);
+    if (st != TVL_OK) return st;
+    const bool auto_shape = !(user_shape || (tuning && tuning->flags));
+    if (auto_shape) {
+        // Few rows of more than 4 KB (measured on MI355X for M = 16 .. 1024):
+        // one row per single-wavefront workgroup, 8 loads in flight, beats
+        // both the large-M shapes and a K split: the split's publish-and-
+        // combine step costs more than it saves unless rows are long and
+        // very few.  Rows of <= 4 KB take one batch of loads anyway.
+        const int64_t blocks = (M + def.R * def.W - 1) / (def.R * def.W);
+        const int64_t row_bytes = K * elem_size(dtype);
+        if (blocks < 2LL * info.cus && row_bytes > 4096) shape = Shape{1, 1, 8, tvl::kXDirect};
+        if (!(tuning && tuning->ksplit) && M <= 128 && row_bytes >= 32768) {
+            shape = Shape{1, 1, 4, tvl::kXDirect};
+            S = (int)std::min<int64_t>(4, std::max<int64_t>(2, 256 / M));
+        }
+    }
+    const int rows_per_tile = shape.R * shape.W;
+    const int64_t tiles = (M + rows_per_tile - 1) / rows_per_tile;
+    if (tuning && tuning->ksplit) S = tuning->ksplit;
+    if (S > 1 && (int64_t)tiles * S > kMaxDim)
+        return fail(TVL_ERR_ARG, "%s: grid too large", who);
+    if (noalloc && S > 1 &&
+        ((int64_t)S * M > tvl::kNoallocPartials || tiles > tvl::kNoallocCounters))
+        return fail(TVL_ERR_SHAPE,
+                    "tvl_gemv_noalloc: a K split of %lld rows into %d slices needs %lld partials "
+                    "and %lld counters; the static scratch holds %lld and %lld",
+                    (long long)M, S, (long long)S * M, (long long)tiles,
+                    (long long)tvl::kNoallocPartials, (long long)tvl::kNoallocCounters);
+    float *ns_partials = nullptr;
+    int *ns_counters = nullptr;
+    if (noalloc) { // every check done: the first call on a device sets the scratch up
+        st = noalloc_setup(dev, stream, &ns_partials, &ns_counters);
+        if (st != TVL_OK) return st;
+    }
+    hipError_t e;
+    if (S <= 1) {
+        e = tvl::launch_gemv_rows(shape, dtype, W, ldw, x, y, (int)M, (int)K, stream);
+    } else {
+        if (noalloc) {
+            e = tvl::launch_gemv_ksplit(shape, dtype, W, ldw, x, y, (int)M, (int)K, S,
+                                        ns_partials, ns_counters, stream);
+        } else {
+            Workspace ws;
+            std::lock_guard<std::mutex> lk(g_mu); // until the launch (see get_workspace_locked)
+            st = get_workspace_locked(dev, stream, (int64_t)S * M, tiles, &ws);
+            if (st != TVL_OK) return st;
+            e = tvl::launch_gemv_ksplit(shape, dtype, W, ldw, x, y, (int)M, (int)K, S,
+                                        ws.partials, ws.counters, stream);
+        }
+    }
+    if (e != hipSuccess) return fail_hip(e, noalloc ? "tvl_gemv_noalloc launch" : "gemv launch");
+    return TVL_OK;
+}
+
+
 }  // namespace
 
 // ================================================================== ABI
@@ -706,87 +836,14 @@ tvl_status tvl_gemv_ex(const void *W, int64_t ldw, int32_t dtype, const float *x
                        int64_t M, int64_t K, const tvl_tuning *tuning, hipStream_t stream)
 {
     g_err[0] = 0;
-    tvl_status st = check_one(W, ldw, dtype, x, y, M, K, "tvl_gemv");
-    if (st != TVL_OK) return st;
-    tvl_item it{W, ldw, x, y, M, K, dtype, TVL_OP_GEMV, nullptr, nullptr, 0.f, 1, 0, 0};
-    st = check_alias(&it, 1);
-    if (st != TVL_OK) return st;
-    st = check_tuning(tuning, true);
-    if (st != TVL_OK) return st;
+    return gemv_impl(W, ldw, dtype, x, y, M, K, tuning, stream, false);
+}
 
-    // Variant by shape.  Row split when there are enough row tiles to give
-    // every CU several workgroups; otherwise split K so that small-M GEMVs
-    // still spread over the whole GPU.
-    Shape shape;
-    int S = 1;
-    const bool user_shape =
-        tuning && (tuning->rows_per_wave || tuning->waves_per_block || tuning->unroll);
-    if (is_quant(dtype)) {
-        if (tuning && tuning->ksplit > 1)
-            return fail(TVL_ERR_ARG, "tvl_gemv: quantised weights have no K split");
-        if (tuning && (tuning->flags & TVL_FLAG_X_LDS))
-            return fail(TVL_ERR_ARG, "tvl_gemv: quantised weights read x directly (direct-x)");
-        Shape qs;
-        st = pick_shape(tuning,
-                        default_quant_shape((double)M * (double)K * quant_bits(dtype) / 8,
-                                            dtype == TVL_Q4),
-                        &qs, false);
-        if (st != TVL_OK) return st;
-        if (!tvl::quant_shape_supported(qs))
-            return fail(TVL_ERR_ARG, "tvl_gemv: no quantised-weight kernel for (%d, %d, %d)", qs.R,
-                        qs.W, qs.U);
-        int qdev = 0;
-        DevInfo qinfo;
-        st = current_device(&qdev, &qinfo);
-        if (st != TVL_OK) return st;
-        const hipError_t qe = tvl::launch_item_quant(qs, dev_item(it), stream);
-        if (qe != hipSuccess) return fail_hip(qe, "quantised gemv launch");
-        return TVL_OK;
-    }
-    const Shape def = default_shape(dtype == TVL_F16 ? 1.0 : 0.0, dtype == TVL_F16 ? 0.0 : 1.0,
-                                    (double)K * 4.0, false);
-    shape = def;
-    if (user_shape || (tuning && tuning->flags)) {
-        st = pick_shape(tuning, def, &shape);
-        if (st != TVL_OK) return st;
-    }
-
-    int dev = 0;
-    DevInfo info;
-    st = current_device(&dev, &info);
-    if (st != TVL_OK) return st;
-    const bool auto_shape = !(user_shape || (tuning && tuning->flags));
-    if (auto_shape) {
-        // Few rows of more than 4 KB (measured on MI355X for M = 16 .. 1024):
-        // one row per single-wavefront workgroup, 8 loads in flight, beats
-        // both the large-M shapes and a K split: the split's publish-and-
-        // combine step costs more than it saves unless rows are long and
-        // very few.  Rows of <= 4 KB take one batch of loads anyway.
-        const int64_t blocks = (M + def.R * def.W - 1) / (def.R * def.W);
-        const int64_t row_bytes = K * elem_size(dtype);
-        if (blocks < 2LL * info.cus && row_bytes > 4096) shape = Shape{1, 1, 8, tvl::kXDirect};
-        if (!(tuning && tuning->ksplit) && M <= 128 && row_bytes >= 32768) {
-            shape = Shape{1, 1, 4, tvl::kXDirect};
-            S = (int)std::min<int64_t>(4, std::max<int64_t>(2, 256 / M));
-        }
-    }
-    const int rows_per_tile = shape.R * shape.W;
-    const int64_t tiles = (M + rows_per_tile - 1) / rows_per_tile;
-    if (tuning && tuning->ksplit) S = tuning->ksplit;
-    hipError_t e;
-    if (S <= 1) {
-        e = tvl::launch_gemv_rows(shape, dtype, W, ldw, x, y, (int)M, (int)K, stream);
-    } else {
-        if ((int64_t)tiles * S > kMaxDim) return fail(TVL_ERR_ARG, "tvl_gemv: grid too large");
-        Workspace ws;
-        std::lock_guard<std::mutex> lk(g_mu); // until the launch (see get_workspace_locked)
-        st = get_workspace_locked(dev, stream, (int64_t)S * M, tiles, &ws);
-        if (st != TVL_OK) return st;
-        e = tvl::launch_gemv_ksplit(shape, dtype, W, ldw, x, y, (int)M, (int)K, S, ws.partials,
-                                    ws.counters, stream);
-    }
-    if (e != hipSuccess) return fail_hip(e, "gemv launch");
-    return TVL_OK;
+tvl_status tvl_gemv_noalloc(const void *W, int64_t ldw, int32_t dtype, const float *x, float *y,
+                            int64_t M, int64_t K, const tvl_tuning *tuning, hipStream_t stream)
+{
+    g_err[0] = 0;
+    return gemv_impl(W, ldw, dtype, x, y, M, K, tuning, stream, true);
 }
 
 tvl_status tvl_gemv(const void *W, int64_t ldw, int32_t dtype, const float *x, float *y,

@@ -6,7 +6,19 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <map>
+#include <mutex>
+
 #include "tvl_device.h"
+
+// Scratch of the allocation-free K split (tvl_gemv_noalloc): the fp32
+// partials of every slice, then one int arrival counter per row tile, for
+// callers that cannot allocate device memory.  Each GPU the library runs on
+// holds its own copy until the process ends.  In host code this name stands
+// for a host-side shadow, not a device address: kernels are given the address
+// that hipGetSymbolAddress returns for the current device (noalloc_scratch).
+static __device__ __align__(256) unsigned char
+    scratch[(tvl::kNoallocPartials + tvl::kNoallocCounters) * 4];
 
 namespace tvl {
 namespace {
@@ -446,6 +458,37 @@ hipError_t launch_gemv_ksplit(const Shape &s, int dtype, const void *W, int64_t 
 #undef X
 #undef Y
     return hipErrorInvalidValue;
+}
+
+namespace {
+std::mutex g_scratch_mu;
+std::map<int, unsigned char *> g_scratch; // device -> its copy of `scratch`
+}  // namespace
+
+hipError_t noalloc_scratch(int dev, hipStream_t st, float **partials, int **counters)
+{
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    auto it = g_scratch.find(dev);
+    if (it == g_scratch.end()) {
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        hipError_t e = hipStreamIsCapturing(st, &cap);
+        if (e != hipSuccess) return e;
+        if (cap != hipStreamCaptureStatusNone) return hipErrorStreamCaptureUnsupported;
+        unsigned char *p = nullptr;
+        e = hipGetSymbolAddress(reinterpret_cast<void **>(&p), HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        // Every K-split launch leaves its counters at zero; they must start
+        // there.  The synchronisation makes the cleared counters visible to
+        // launches on any stream of this device.
+        e = launch_zero_i32(reinterpret_cast<int *>(p + kNoallocPartials * 4), kNoallocCounters,
+                            st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        if (e != hipSuccess) return e;
+        it = g_scratch.emplace(dev, p).first;
+    }
+    *partials = reinterpret_cast<float *>(it->second);
+    *counters = reinterpret_cast<int *>(it->second + kNoallocPartials * 4);
+    return hipSuccess;
 }
 
 hipError_t launch_sweep(const Shape &s, const DevItem *items, const DevTile *tiles, int ntiles,

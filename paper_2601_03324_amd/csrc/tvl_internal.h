@@ -104,6 +104,18 @@ hipError_t launch_gemv_ksplit(const Shape &s, int dtype, const void *W, int64_t 
 hipError_t launch_sweep(const Shape &s, const DevItem *items, const DevTile *tiles,
                         int ntiles, int grid, int ks_cap, hipStream_t st);
 
+// Scratch of the allocation-free K split (tvl_gemv_noalloc): one file-scope
+// device array per GPU holding kNoallocPartials fp32 partials followed by
+// kNoallocCounters int arrival counters (4.25 MiB).
+constexpr int64_t kNoallocPartials = int64_t(1) << 20;
+constexpr int64_t kNoallocCounters = int64_t(1) << 16;
+// Device address of the current device's scratch (device `dev` must be
+// current).  The first call per device looks the array up with
+// hipGetSymbolAddress, clears its counters on `st` and synchronises `st`;
+// it returns hipErrorStreamCaptureUnsupported, doing nothing, if `st` is
+// being captured.  Later calls make no HIP call.
+hipError_t noalloc_scratch(int dev, hipStream_t st, float **partials, int **counters);
+
 // Sweep with fused RMSNorm / SwiGLU items (direct-x mode, R even).
 bool fused_shape_supported(const Shape &s);
 hipError_t launch_sweep_fused(const Shape &s, const DevItem *items, const DevTile *tiles,

@@ -33,7 +33,7 @@ DIRECT_SHAPES = tuple((r, w, u) for w in (1, 4)
 
 # every symbol include/tvl.h declares
 EXPORTS = ("tvl_version", "tvl_row_stride", "tvl_pack_rows", "tvl_gemv", "tvl_gemv_ex",
-           "tvl_gemv_item",
+           "tvl_gemv_noalloc", "tvl_gemv_item",
            "tvl_gemv_batch_sweep", "tvl_sweep_plan_create", "tvl_sweep_plan_run",
            "tvl_sweep_plan_info", "tvl_sweep_plan_destroy", "tvl_release_workspaces",
            "tvl_util_read_stream", "tvl_util_copy", "tvl_status_str", "tvl_last_error")
@@ -93,6 +93,7 @@ def _load() -> ctypes.CDLL:
         "tvl_pack_rows": ([P, I64, P, I64, I64, I32, P], I32),
         "tvl_gemv": ([P, I64, I32, P, P, I64, I64, P], I32),
         "tvl_gemv_ex": ([P, I64, I32, P, P, I64, I64, P, P], I32),
+        "tvl_gemv_noalloc": ([P, I64, I32, P, P, I64, I64, P, P], I32),
         "tvl_gemv_item": ([P, P, P], I32),
         "tvl_gemv_batch_sweep": ([P, I32, P], I32),
         "tvl_sweep_plan_create": ([P, I32, P, P], I32),
@@ -169,6 +170,14 @@ def tvl_gemv_ex(W, ldw: int, dtype: int, x, y, M: int, K: int, tuning=None, stre
     _chk(lib.tvl_gemv_ex(_p(W), ldw, dtype, _p(x), _p(y), M, K,
                          ctypes.byref(t) if t is not None else None, _stream(stream)),
          "tvl_gemv_ex")
+
+
+def tvl_gemv_noalloc(W, ldw: int, dtype: int, x, y, M: int, K: int, tuning=None,
+                     stream=None) -> None:
+    t = _tuning(tuning)
+    _chk(lib.tvl_gemv_noalloc(_p(W), ldw, dtype, _p(x), _p(y), M, K,
+                              ctypes.byref(t) if t is not None else None, _stream(stream)),
+         "tvl_gemv_noalloc")
 
 
 def item(W, ldw: int, x, y, M: int, K: int, dtype: int, op: int = TVL_OP_GEMV, W3=None,

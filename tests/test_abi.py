@@ -153,12 +153,12 @@ def test_row_stride_rejects():
     assert tvl.tvl_row_stride(-3, 1) == -1
 
 
-def gemv(W=A, ldw=768, dt=0, x=B, y=C, M=768, K=768, tuning=None):
+def gemv(W=A, ldw=768, dt=0, x=B, y=C, M=768, K=768, tuning=None, fn="tvl_gemv_ex"):
     t = None if tuning is None else ctypes.byref(tvl.tvl_tuning(**tuning))
-    return L.tvl_gemv_ex(W, ldw, dt, x, y, M, K, t, None)
+    return getattr(L, fn)(W, ldw, dt, x, y, M, K, t, None)
 
 
-@pytest.mark.parametrize("kw,st", [
+REJECTS = [
     (dict(W=0), NULL), (dict(x=0), NULL), (dict(y=0), NULL),
     (dict(dt=4), DTYPE), (dict(dt=-1), DTYPE),
     (dict(dt=2, ldw=640), SHAPE), (dict(dt=3, ldw=256), SHAPE), (dict(dt=2, ldw=896, tuning=dict(ksplit=2)), ARG),
@@ -174,9 +174,14 @@ def gemv(W=A, ldw=768, dt=0, x=B, y=C, M=768, K=768, tuning=None):
     (dict(tuning=dict(rows_per_wave=8, unroll=16)), ARG), (dict(tuning=dict(flags=4)), ARG),
     (dict(tuning=dict(flags=3)), ARG),
     (dict(tuning=dict(ksplit=5000)), ARG),
-])
-def test_gemv_rejects(kw, st):
-    assert gemv(**kw) == st
+]
+
+
+@pytest.mark.parametrize("fn", ["tvl_gemv_ex", "tvl_gemv_noalloc"])
+@pytest.mark.parametrize("kw,st", REJECTS)
+def test_gemv_rejects(kw, st, fn):
+    """tvl_gemv_noalloc validates exactly like tvl_gemv_ex."""
+    assert gemv(fn=fn, **kw) == st
     assert tvl.tvl_last_error() != ""
     assert tvl.tvl_status_str(st).startswith(tvl.STATUS[st])
 
