@@ -136,8 +136,10 @@ typedef enum tvl_status {
  *     puts its largest |x| 2^k in [2^13, 2^14), and split into two fp16 parts,
  *     x 2^k = hi + lo + r with |r| <= 2^-22 |x 2^k| + 2^-25; the fp16 products
  *     are exact and accumulate in fp32, and the sum is scaled back exactly.
- *     The split adds at most 2^-22 sum_j |W_ij x_j| + 2^-38 sum_j |W_ij| m_j
- *     to the error bound above (m_j: the largest |x| in column j's chunk).
+ *     A chunk in which any nonzero |x 2^k| of any vector is below 2^-7 (a
+ *     range wider than the two parts hold) runs on the fp32 matrix cores
+ *     instead, so the split adds at most 2^-18 sum_j |W_ij x_j| to the error
+ *     bound above, for every finite x.
  *   Block-quantised weights (dtype TVL_Q8 / TVL_Q4): plain one-vector GEMV
  *     items only (op == TVL_OP_GEMV, g == NULL, nrhs <= 1).
  * One launch (plan or batch) may hold plain fp32/fp16 items together with

@@ -1064,6 +1064,19 @@ typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 // eight fp32 16 x 16 x 4 steps; the chunk's sum is then scaled back by 2^-k
 // (exact).  A operand: lane 16 g + i holds row i, columns 8 g .. 8 g + 7 of
 // the 32-column step (one 16-byte LDS read); B: vector i, the same columns.
+//
+// The absolute 2^-25 would lose the small entries of a chunk whose range is
+// wider than the two parts hold (an entry 2^40 beside ones rounds the ones
+// to zero), and S = sum_j |W_ij x_j| need not see the large entry (its
+// weight may be zero), so such a chunk runs on the fp32 matrix cores
+// instead: any nonzero |x 2^k| below kSplitMin in any vector of the
+// wavefront sends the whole chunk there.  On the split path every entry then
+// has |r| <= max(2^-22, 2^-25 / kSplitMin) |x 2^k| = 2^-18 |x 2^k|, so the
+// split adds at most 2^-18 S to the fp32 forms' error bound, for any finite
+// x.  For x ~ N(0, 1), ~0.3 % of 128-column chunks of 16 vectors take the
+// fp32 path (each costs four times the matrix-core steps of a split chunk).
+constexpr float kSplitMin = 0x1p-7f;
+
 __device__ __forceinline__ f4 mfma16h(h8 a, h8 b, f4 c)
 {
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
@@ -1178,33 +1191,41 @@ struct MfmaDmaRows {
             }
     }
 
-    // HX: the chunk's products on the fp16 matrix cores (scaled, split x)
+    // HX: the chunk's products on the fp16 matrix cores (scaled, split x),
+    // or on the fp32 ones when the chunk's range is too wide (kSplitMin)
     template <int ST>
     __device__ __forceinline__ void multiply_hx(const f4 (&xb)[NQ], f4 (&acc)[RG]) const
     {
+        // the vector's largest |x| over its 4 lanes (g = 0..3 hold the
+        // chunk's columns) sets the scale
         float m = 0.f;
 #pragma unroll
         for (int q = 0; q < NQ; ++q)
 #pragma unroll
             for (int e = 0; e < 4; ++e)
                 m = fmaxf(m, fabsf(xb[q][e]));
-        // the vector's 4 lanes (g = 0..3) hold the chunk's columns
         m = fmaxf(m, __shfl_xor(m, 16));
         m = fmaxf(m, __shfl_xor(m, 32));
         int e2 = 0;
         if (m > 0.f && m <= 3.4028235e38f) e2 = __builtin_amdgcn_frexp_expf(m);
         const int k = min(max(14 - e2, -126), 126);
         const float sc = __builtin_ldexpf(1.f, k), inv = __builtin_ldexpf(1.f, -k);
+        // the split path first (speculatively: a chunk too wide for it, rare,
+        // is redone below and this result dropped), so the range check does
+        // not stand between the scale and the matrix-core steps.
+        // hi = f16(x 2^k), lo = f16(x 2^k - hi): each one fused multiply-add
+        // with an fp16 result (v_fma_mix); x 2^k is exact (a power of two)
         h8 hi[NQ / 2], lo[NQ / 2];
 #pragma unroll
         for (int q = 0; q < NQ / 2; ++q)
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const float v = xb[2 * q + e / 4][e % 4] * sc;
-                const _Float16 vh = (_Float16)v;
+                const float xv = xb[2 * q + e / 4][e % 4];
+                const _Float16 vh = (_Float16)__builtin_fmaf(xv, sc, 0.f);
                 hi[q][e] = vh;
-                lo[q][e] = (_Float16)(v - (float)vh);
+                lo[q][e] = (_Float16)__builtin_fmaf(xv, sc, -(float)vh);
             }
+        f4 cs[RG];
 #pragma unroll
         for (int rg = 0; rg < RG; ++rg) {
             f4 c = {0.f, 0.f, 0.f, 0.f};
@@ -1214,8 +1235,51 @@ struct MfmaDmaRows {
                 c = mfma16h(a, hi[q], c);
                 c = mfma16h(a, lo[q], c);
             }
-            acc[rg] += c * inv;
+            cs[rg] = c;
         }
+        // a nonzero |x| below kSplitMin 2^-k (a power of two, >= 2^-131)?
+        // Only if the lane's smallest |x| is below it: then (rare for dense
+        // x) look again without the zeros, as (bits << 1) - 2, where the sign
+        // bit drops out, magnitudes keep their order and zero wraps to the top
+        // (four independent running minima keep the chain short)
+        float mzq[4] = {3.4028235e38f, 3.4028235e38f, 3.4028235e38f, 3.4028235e38f};
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                mzq[q & 3] = fminf(mzq[q & 3], fabsf(xb[q][e]));
+        const float mz = fminf(fminf(mzq[0], mzq[1]), fminf(mzq[2], mzq[3]));
+        const float thr = __builtin_ldexpf(kSplitMin, -k);
+        if (__builtin_expect(__builtin_amdgcn_ballot_w64(mz < thr) != 0, 0)) { // wave-uniform
+            uint32_t mn = 0xFFFFFFFFu;
+#pragma unroll
+            for (int q = 0; q < NQ; ++q)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    mn = min(mn, (__builtin_bit_cast(uint32_t, xb[q][e]) << 1) - 2u);
+            const bool wide = mn < (__builtin_bit_cast(uint32_t, thr) << 1) - 2u;
+            if (__builtin_amdgcn_ballot_w64(wide) != 0) { // wave-uniform
+                // fp32 matrix cores: step e multiplies column 8 g + e of the
+                // lane's 8 weights (converted exactly) by the same column of x
+#pragma unroll
+                for (int rg = 0; rg < RG; ++rg) {
+                    f4 c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int q = 0; q < NQ / 2; ++q) {
+                        const h8 a =
+                            *(const TVL_LDS h8 *)(lds + ST * STAGE + rg * 16 * RB + raddr[q]);
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            c = mfma16((float)a[e], xb[2 * q + e / 4][e % 4], c);
+                    }
+                    acc[rg] += c;
+                }
+                return;
+            }
+        }
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+            acc[rg] += cs[rg] * inv;
     }
 
     // one chunk step: chunk c (stage ST = c % S, x buffer XB = c % NX);

@@ -295,6 +295,40 @@ def test_split_x_keeps_fp32_accuracy(M, K):
             assert res["bad"] == 0, (M, K, (r, w, u), b, res)
 
 
+def test_split_x_wide_chunks():
+    """Chunks whose range two fp16 parts cannot hold: a huge entry beside
+    small ones, the weight under the huge entry zero and every other weight
+    positive (so S is the small entries' sum).  Split as is, the small
+    entries would round to zero (normalised error 1); such chunks take the
+    fp32 matrix cores, so every output stays within the fp32 bar (1e-5 of the
+    norm).  Full chunks and the ragged last chunk (K = 1000: 896 + 104 at 128
+    columns, 960 + 40 at 64), every split-x launch shape, 16 vectors."""
+    M, K, nb = 300, 1000, 16
+    rng = np.random.default_rng(1000)
+    X = rng.standard_normal((nb, K)).astype(np.float32)
+    huge = {0: (0, 2.0 ** 40, 1.0), 1: (200, -1e10, 3e-30), 5: (700, 2.0 ** 60, 1.0),
+            9: (990, 1e30, 1e-3), 12: (64, 2.0 ** 37, 1.0)}
+    Wf = np.abs(rng.standard_normal((M, K)) * 0.02).astype(np.float32) + 1e-3
+    for b, (col, big, small) in huge.items():
+        c0 = col // 128 * 128
+        X[b, c0:c0 + 128] = small
+        X[b, col] = big
+        Wf[:, col] = 0.0
+    W = synth.f32_to_f16_bits(Wf)
+    refs = [oracle.gemv_f16(W, X[b]) for b in range(nb)]
+    buf, ldw = dev_matrix(W, 1)
+    for r, w, u in MFMA_HX + [t for t in MFMA_XS if t[2] > 300]:
+        Y = run(buf, ldw, 1, X, M, K, nb, M, dict(rows_per_wave=r, waves_per_block=w,
+                                                  unroll=u, flags=2))
+        for b in range(nb):
+            res = oracle.check(Y[b], refs[b][0], refs[b][1], 1e-5)
+            assert res["bad"] == 0, ((r, w, u), b, res)
+    # the library's default for only fp16 weights and 16 vectors is a split-x form
+    Y = run(buf, ldw, 1, X, M, K, nb, M, None)
+    for b in range(nb):
+        assert oracle.check(Y[b], refs[b][0], refs[b][1], 1e-5)["bad"] == 0, b
+
+
 @pytest.mark.parametrize("ldx", [(1 << 27) - 64, 1 << 27], ids=["xs-limit", "fallback"])
 def test_multi_huge_x_stride(ldx):
     """x strides at the shared-x forms' limit (4 x vectors of one 64-column
