@@ -366,6 +366,7 @@ def main() -> int:
         del src, sink
     except Exception as exc:  # context only; never fatal
         log(f"read ceiling skipped: {exc}")
+    same = read_ceiling_same_bytes(algo, tvl, torch, stream)
 
     for i in range(args.warmup):
         step(i)
@@ -476,6 +477,7 @@ def main() -> int:
                        "p95": round(float(np.percentile(lat, 95)), 3),
                        "p99": round(float(np.percentile(lat, 99)), 3)},
         "read_ceiling_GBs": None if ceil_gbs is None else round(ceil_gbs, 1),
+        "read_ceiling_same_bytes": same,
         "parity_spot_max_err": worst,
         "roofline": {
             "bound": "hbm",
@@ -500,6 +502,37 @@ def main() -> int:
             p.destroy()
     emit(out)
     return 0
+
+
+def read_ceiling_same_bytes(nbytes: int, tvl, torch, stream) -> dict:
+    """The plain streaming read (the GEMV's load kind, no arithmetic) over the
+    same number of bytes as one launch of the workload: what this GPU reads
+    in a launch of that size, ramp-up and drain included.  Copies are rotated
+    over >= 1 GB (4x the last-level cache), so every launch reads from HBM;
+    the best of several grids is reported (context for the roofline
+    fraction, not a target)."""
+    nb = min(int(nbytes) // 256 * 256, 2 << 30)
+    ncopy = max(2, -(-1_000_000_000 // nb)) if nb < (1 << 30) else 1
+    src = torch.ones(nb * ncopy // 4, dtype=torch.float32, device="cuda")
+    base = int(src.data_ptr())
+    sink = torch.empty(1 << 16, dtype=torch.float32, device="cuda")
+    sid = int(stream.cuda_stream)
+    best = (0.0, 0)
+    for grid in (512, 1024, 2048, 4096, 8192, 16384, 32768):
+        for i in range(2 * ncopy):
+            tvl.tvl_util_read_stream(base + (i % ncopy) * nb, nb, sink, grid, sid)
+        reps = max(20, 2 * ncopy)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(reps):
+            tvl.tvl_util_read_stream(base + (i % ncopy) * nb, nb, sink, grid, sid)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        gbs = nb * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+        best = max(best, (gbs, grid))
+    del src, sink
+    return {"GBs": round(best[0], 1), "bytes": nb, "grid": best[1], "copies_rotated": ncopy,
+            "frac_of_peak": round(best[0] / PEAK_GBS, 4)}
 
 
 def time_steps(step, steps, warmup, torch, np, stream):
@@ -554,6 +587,7 @@ def run_beam(args, tvl, torch, np, oracle, synth, sdev) -> int:
         plans[i % len(plans)].run(sid)
 
     ms, lat = time_steps(step, args.steps, args.warmup, torch, np, stream)
+    same = read_ceiling_same_bytes(algo, tvl, torch, stream)
     plans[0].run()
     torch.cuda.synchronize()
     worst = 0.0
@@ -587,6 +621,7 @@ def run_beam(args, tvl, torch, np, oracle, synth, sdev) -> int:
                        "p50": round(float(np.percentile(lat, 50)), 3),
                        "p95": round(float(np.percentile(lat, 95)), 3),
                        "p99": round(float(np.percentile(lat, 99)), 3)},
+        "read_ceiling_same_bytes": same,
         "parity_spot_max_err": worst,
         "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / PEAK_GBS, 4),
@@ -631,6 +666,7 @@ def run_fused(args, tvl, torch, np, oracle, synth, sdev) -> int:
         plans[i % len(plans)].run(sid)
 
     ms, lat = time_steps(step, args.steps, args.warmup, torch, np, stream)
+    same = read_ceiling_same_bytes(algo, tvl, torch, stream)
     # spot parity: three items of copy 0 (a normalised GEMV, a SwiGLU pair, a plain GEMV)
     plans[0].run()
     torch.cuda.synchronize()
@@ -678,6 +714,7 @@ def run_fused(args, tvl, torch, np, oracle, synth, sdev) -> int:
                        "p50": round(float(np.percentile(lat, 50)), 3),
                        "p95": round(float(np.percentile(lat, 95)), 3),
                        "p99": round(float(np.percentile(lat, 99)), 3)},
+        "read_ceiling_same_bytes": same,
         "parity_spot_max_err": worst,
         "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / PEAK_GBS, 4),

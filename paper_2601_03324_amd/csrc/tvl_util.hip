@@ -28,7 +28,9 @@ __global__ __launch_bounds__(256) void k_zero_i32(int *p, int64_t n)
 
 // Read-only streaming with the GEMV's load kind: workgroup b reads the
 // contiguous span [b*per, (b+1)*per) of 16-byte vectors, eight loads in
-// flight per lane, and writes one float so the loads cannot be optimised away.
+// flight per lane (the last batch of a span with its loads past the span
+// switched off, so a short span keeps its loads in flight too), and writes
+// one float so the loads cannot be optimised away.
 __global__ __launch_bounds__(256) void k_read_stream(const f4 *__restrict__ src, int64_t nvec,
                                                      int64_t per, float *__restrict__ sink)
 {
@@ -48,8 +50,17 @@ __global__ __launch_bounds__(256) void k_read_stream(const f4 *__restrict__ src,
         for (int u = 0; u < 8; ++u)
             acc += a[u];
     }
-    for (; i < end; i += 256)
-        acc += __builtin_nontemporal_load(g + i);
+    if (i < end) {
+        f4 a[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            a[u] = i + u * 256 < end ? __builtin_nontemporal_load(g + i + u * 256)
+                                     : f4{0.f, 0.f, 0.f, 0.f};
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            acc += a[u];
+    }
     float v = (acc.x + acc.y) + (acc.z + acc.w);
     for (int o = 32; o >= 1; o >>= 1)
         v += __shfl_xor(v, o);
