@@ -181,36 +181,31 @@ def test_quant_7b_layer_shapes(dt):
         check(run_item(Wq, ldw, dt, x, M, K), yref, S, f"{M}x{K}")
 
 
-@pytest.mark.parametrize("name", ["sweep110m_q8", "sweep110m_q4", "sweep7b_q4"])
+@pytest.mark.parametrize("name", ["sweep110m_q8", "sweep110m_q4", "sweep7b_q8", "sweep7b_q4"])
 def test_quant_sweeps_in_one_launch(name):
     """Whole decode tokens with block-quantised weights in the launch the
-    bench times (one plan, the library's default shape): 40 sampled rows of
-    every matrix (first, last, random), each regenerated and quantised on
-    its own, against the oracle."""
-    import zlib
+    bench times (one plan, the library's default shape): every output of
+    every matrix against the oracle, on the very bytes uploaded."""
+    import host_oracle
     import synth.device as sdev
     wl = synth.WORKLOADS[name]
     log(f"{name}: generating and uploading {wl.weight_bytes() / 1e9:.2f} GB")
-    gemvs = sdev.load(wl, DEV, progress=True)
-    for g in gemvs:
-        g.y.fill_(float("nan"))
-    plan = tvl.tvl_sweep_plan_create([g.item() for g in gemvs])
+    cases = []
+    for i, m in enumerate(wl.mats):
+        Wq = m.weights()
+        x = m.x(0)
+        g = sdev.DevGemv(m, sdev.upload(m, Wq, DEV), torch.from_numpy(x).to(DEV),
+                         torch.full((m.M,), float("nan"), dtype=torch.float32, device=DEV))
+        yref, S = host_oracle.gemv_q(Wq, m.bits, synth.q_row_bytes(m.K, m.bits), m.M, m.K, x)
+        cases.append((g, yref, S))
+        del Wq
+    plan = tvl.tvl_sweep_plan_create([g.item() for g, _, _ in cases])
     plan.run()
     torch.cuda.synchronize()
     worst = 0.0
-    for g in gemvs:
-        m = g.spec
-        y = g.y.cpu().numpy()
-        x = g.x.cpu().numpy()
-        idx = sdev.sample_rows(m.M, 40, zlib.crc32(m.name.encode()))
-        ys, Ss = [], []
-        for r in idx:
-            yr, Sr = oracle.gemv_q(m.weights(int(r), 1), m.bits, synth.q_row_bytes(m.K, m.bits),
-                                   1, m.K, x)
-            ys.append(yr[0])
-            Ss.append(Sr[0])
-        worst = max(worst, check(y[idx], np.array(ys), np.array(Ss), f"{name} {m.name}"))
-    log(f"{name}: max normalised error {worst:.3e}")
+    for g, yref, S in cases:
+        worst = max(worst, check(g.y.cpu().numpy(), yref, S, f"{name} {g.spec.name}"))
+    log(f"{name}: every output, max normalised error {worst:.3e}")
     plan.destroy()
-    del gemvs
+    del cases
     torch.cuda.empty_cache()
