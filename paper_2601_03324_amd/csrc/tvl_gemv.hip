@@ -218,14 +218,19 @@ __global__ __launch_bounds__(WV *kWave) void k_gemv_rows_direct(const T *__restr
 // slice's row sums go to partials[split * M + row] with device-coherent
 // stores; every thread waits for its stores to be acknowledged, the
 // workgroup meets at a barrier, and one thread bumps the tile's counter.  The
-// workgroup that brings the counter to S adds the S partials in the order
-// 0..S-1 (device-coherent loads) and resets the counter for the next launch.
+// workgroup that brings the counter to S takes an agent-scope acquire fence,
+// adds the S partials in the order 0..S-1 (device-coherent loads) and resets
+// the counter for the next launch.
 //
-// An agent-scope release/acquire fence would be the textbook way to publish
-// the partials, but on a multi-XCD part it compiles to a write-back and an
-// invalidation of the whole L2, once per workgroup: measured 20-100x slower
-// than the row split.  Coherent stores plus the store wait give the same
-// guarantee for exactly the data that needs it.
+// The publishing side has no release fence: on a multi-XCD part an
+// agent-scope release compiles to a write-back of the whole L2, once per
+// workgroup (measured 20-100x slower than the row split).  It is not needed
+// for exactly the data published here: the partials are agent-scope atomic
+// stores, written through to the coherence point (sc1), and the wait for
+// their acknowledgement before the barrier and the counter update is what
+// the release would add for them.  The acquire fence (an L2 invalidation in
+// the last workgroup only, once per row tile) orders the partial loads after
+// the counter.  A CPU test compiles this kernel and checks that code.
 template <typename T, int R, int WV, int U, int XM>
 __global__ __launch_bounds__(WV *kWave) void k_gemv_ksplit(
     const T *__restrict__ W, int64_t ldw, const float *__restrict__ x, float *__restrict__ y,
@@ -254,6 +259,9 @@ __global__ __launch_bounds__(WV *kWave) void k_gemv_ksplit(
     }
     __syncthreads();
     if (is_last) {
+        // acquire (agent scope) for the partials the other slices published:
+        // one per row tile, in the last workgroup only
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         const int rows = min(R * WV, M - row0);
         for (int r = threadIdx.x; r < rows; r += blockDim.x) {
             float s = 0.f;
