@@ -258,7 +258,9 @@ TVL_API tvl_status tvl_pack_rows(void *dst, int64_t ldw, const void *src,
  * counter per row tile) is allocated by the library on first use per
  * (device, stream) and kept until tvl_release_workspaces() or process exit;
  * a first K-split call on a stream that is being captured into a graph
- * fails with TVL_ERR_NOMEM (make one call before capturing). */
+ * fails with TVL_ERR_NOMEM (make one call before capturing).  A workspace
+ * replaced by a larger one is not freed either (graphs captured with it
+ * stay valid) until tvl_release_workspaces(). */
 TVL_API tvl_status tvl_gemv(const void *W, int64_t ldw, int32_t dtype,
                             const float *x, float *y, int64_t M, int64_t K,
                             hipStream_t stream);
@@ -304,6 +306,10 @@ TVL_API tvl_status tvl_gemv_item(const tvl_item *item, const tvl_tuning *tuning,
  * item list builds a device tile table (one synchronous upload) and caches
  * it; later calls with an identical list launch at once.  The cache holds 64
  * lists; when it is full the device is synchronised and the cache emptied.
+ * While `stream` is being captured into a graph, only a list that already
+ * has a cached plan launches (any other returns TVL_ERR_ARG and enqueues
+ * nothing: building a plan allocates and uploads); a plan launched into a
+ * capture is kept past eviction, until tvl_release_workspaces().
  * No output y may overlap any W, x or other y of the batch. */
 TVL_API tvl_status tvl_gemv_batch_sweep(const tvl_item *items, int32_t n,
                                         hipStream_t stream);
@@ -313,7 +319,8 @@ TVL_API tvl_status tvl_gemv_batch_sweep(const tvl_item *items, int32_t n,
  * G lanes each; ordered by bytes per tile, largest first) and upload it once.  The item
  * list is copied; the W, x, y buffers it names must stay valid for every
  * run.  `tuning` may be NULL.  The plan belongs to the device current at
- * creation. */
+ * creation.  Not while a stream of that device is being captured (the table
+ * is uploaded synchronously); running a plan may be captured. */
 TVL_API tvl_status tvl_sweep_plan_create(const tvl_item *items, int32_t n,
                                          const tvl_tuning *tuning,
                                          tvl_plan **plan);
@@ -322,11 +329,14 @@ TVL_API tvl_status tvl_sweep_plan_run(const tvl_plan *plan, hipStream_t stream);
 /* Number of tiles and the launch grid of a plan (either pointer may be NULL). */
 TVL_API tvl_status tvl_sweep_plan_info(const tvl_plan *plan, int64_t *ntiles,
                                        int64_t *grid, int32_t *rows_per_tile);
-/* Free a plan (synchronises its device first).  NULL is a no-op. */
+/* Free a plan (synchronises its device first).  NULL is a no-op.  Graphs
+ * that captured a run of the plan must not be replayed afterwards. */
 TVL_API tvl_status tvl_sweep_plan_destroy(tvl_plan *plan);
 
-/* Free the K-split workspaces and the batch-sweep cache (synchronises every
- * device that holds one). */
+/* Free the K-split workspaces and the batch-sweep cache, including those
+ * kept for captured graphs (synchronises every device that holds one).
+ * Graphs that captured K-split or tvl_gemv_batch_sweep calls must not be
+ * replayed afterwards. */
 TVL_API tvl_status tvl_release_workspaces(void);
 
 /* Diagnostics (not part of the GEMV path; used to calibrate measurements).

@@ -35,6 +35,7 @@ struct tvl_plan {
     int ks_cap = 0;
     int ntiles = 0;
     int grid = 0;
+    bool captured = false; // a cached plan launched into a graph capture
     DevItem *d_items = nullptr;
     DevTile *d_tiles = nullptr;
     std::vector<tvl_item> items;
@@ -75,7 +76,8 @@ int64_t q_row_bytes(int64_t K, int32_t dt)
     const int bits = dt == TVL_Q4 ? 4 : 8;
     return ((K * bits + 7) / 8 + 127) / 128 * 128;
 }
-// Scale plane: ceil(K/64) groups of M rounded up to 4 floats (group-major).
+// Scale plane: M rounded up to 4 rows of ceil(K/64) fp32 scales, in blocks of
+// 4 rows (the scale of row i, group g at (i/4)*4*ng + 4*g + i%4).
 int64_t q_scale_bytes(int64_t M, int64_t K) { return 4 * ((M + 3) / 4 * 4) * ((K + 63) / 64); }
 
 struct Range {
@@ -479,6 +481,10 @@ struct Workspace {
     int64_t counter_cap = 0; // ints
 };
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+// Workspaces replaced by larger ones.  They are not freed until
+// tvl_release_workspaces: a graph captured earlier may still use them, and
+// launches already enqueued on the stream may too.
+std::vector<std::pair<int, Workspace>> g_ws_retired;
 
 // The caller holds g_mu, and keeps holding it until it has launched the
 // kernel that uses the workspace: another thread growing the same stream's
@@ -496,28 +502,28 @@ tvl_status get_workspace_locked(int dev, hipStream_t st, int64_t nfloat, int64_t
                                        "workspace (%lld floats) is not allocated yet; run the "
                                        "same K-split call once on this stream before capture",
                         (void *)st, (long long)nfloat);
-        if (w.partials || w.counters) {
-            // earlier launches on this stream may still use the old buffers
-            e = hipStreamSynchronize(st);
-            if (e != hipSuccess) return fail_hip(e, "hipStreamSynchronize");
-            (void)hipFree(w.partials);
-            (void)hipFree(w.counters);
-            w = Workspace{};
-        }
-        const int64_t pf = std::max<int64_t>(nfloat, 1 << 16);
-        const int64_t pc = std::max<int64_t>(ncnt, 1 << 12);
-        e = hipMalloc(&w.partials, pf * sizeof(float));
+        const int64_t pf = std::max<int64_t>({nfloat, w.partial_cap, 1 << 16});
+        const int64_t pc = std::max<int64_t>({ncnt, w.counter_cap, 1 << 12});
+        Workspace nw;
+        e = hipMalloc(&nw.partials, pf * sizeof(float));
         if (e != hipSuccess) return fail(TVL_ERR_NOMEM, "K-split workspace: %s", hipGetErrorString(e));
-        e = hipMalloc(&w.counters, pc * sizeof(int));
+        e = hipMalloc(&nw.counters, pc * sizeof(int));
         if (e != hipSuccess) {
-            (void)hipFree(w.partials);
-            w = Workspace{};
+            (void)hipFree(nw.partials);
             return fail(TVL_ERR_NOMEM, "K-split workspace: %s", hipGetErrorString(e));
         }
-        e = tvl::launch_zero_i32(w.counters, pc, st);
-        if (e != hipSuccess) return fail_hip(e, "counter reset launch");
-        w.partial_cap = pf;
-        w.counter_cap = pc;
+        e = tvl::launch_zero_i32(nw.counters, pc, st);
+        if (e != hipSuccess) {
+            (void)hipFree(nw.partials);
+            (void)hipFree(nw.counters);
+            return fail_hip(e, "counter reset launch");
+        }
+        nw.partial_cap = pf;
+        nw.counter_cap = pc;
+        // the old buffers stay allocated (earlier launches and captured
+        // graphs may use them) until tvl_release_workspaces
+        if (w.partials || w.counters) g_ws_retired.emplace_back(dev, w);
+        w = nw;
     }
     *out = w;
     return TVL_OK;
@@ -661,6 +667,9 @@ void plan_free(tvl_plan *p)
 // batch-sweep cache: item list bytes + device -> plan
 std::map<std::string, tvl_plan *> g_cache;
 constexpr size_t kCacheMax = 64;
+// evicted plans that were launched into a graph capture (freed only by
+// tvl_release_workspaces)
+std::vector<tvl_plan *> g_plans_retired;
 
 // First tvl_gemv_noalloc call on a device: look up its static scratch and
 // clear the counters (tvl::noalloc_scratch; later calls make no HIP call).
@@ -946,11 +955,24 @@ tvl_status tvl_gemv_batch_sweep(const tvl_item *items, int32_t n, hipStream_t st
     // A cached plan is launched under the lock that found it: another
     // thread's eviction (cache full) or tvl_release_workspaces would
     // otherwise free it between the lookup and the launch.
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    const hipError_t ce = hipStreamIsCapturing(stream, &cap);
+    if (ce != hipSuccess) return fail_hip(ce, "hipStreamIsCapturing");
+    const bool capturing = cap != hipStreamCaptureStatusNone;
     {
         std::lock_guard<std::mutex> lk(g_mu);
         auto it = g_cache.find(key);
-        if (it != g_cache.end()) return plan_launch(it->second, stream);
+        if (it != g_cache.end()) {
+            // a graph now holds the plan's tables: kept at eviction
+            if (capturing) it->second->captured = true;
+            return plan_launch(it->second, stream);
+        }
     }
+    if (capturing)
+        return fail(TVL_ERR_ARG, "tvl_gemv_batch_sweep: stream %p is being captured and this item "
+                                 "list has no plan yet (building one allocates and uploads); "
+                                 "make the same call once before capturing",
+                    (void *)stream);
     tvl_plan *fresh = nullptr; // built outside the lock (allocates, uploads)
     st = plan_build(items, n, nullptr, &fresh);
     if (st != TVL_OK) return st;
@@ -961,8 +983,12 @@ tvl_status tvl_gemv_batch_sweep(const tvl_item *items, int32_t n, hipStream_t st
         return plan_launch(it->second, stream);
     }
     if (g_cache.size() >= kCacheMax) { // plan_free waits for in-flight launches
-        for (auto &kv : g_cache)
-            plan_free(kv.second);
+        for (auto &kv : g_cache) {
+            if (kv.second->captured)
+                g_plans_retired.push_back(kv.second); // a graph may still launch it
+            else
+                plan_free(kv.second);
+        }
         g_cache.clear();
     }
     g_cache.emplace(key, fresh);
@@ -982,9 +1008,19 @@ tvl_status tvl_release_workspaces(void)
         (void)hipFree(kv.second.counters);
     }
     g_ws.clear();
+    for (auto &dw : g_ws_retired) {
+        (void)hipSetDevice(dw.first);
+        (void)hipDeviceSynchronize();
+        (void)hipFree(dw.second.partials);
+        (void)hipFree(dw.second.counters);
+    }
+    g_ws_retired.clear();
     for (auto &kv : g_cache)
         plan_free(kv.second);
     g_cache.clear();
+    for (tvl_plan *p : g_plans_retired)
+        plan_free(p);
+    g_plans_retired.clear();
     if (cur >= 0) (void)hipSetDevice(cur);
     return TVL_OK;
 }

@@ -1,0 +1,112 @@
+"""HIP graph capture of library calls (MI355X).
+
+A graph captured from tvl_gemv_batch_sweep (cached plan) and a K-split
+tvl_gemv keeps using the library's plan tables and K-split workspace.  Those
+must stay valid when the plan cache is later emptied (more item lists than
+it holds) and when the stream's workspace is replaced by a larger one: the
+library keeps such buffers until tvl_release_workspaces.  Each replay, with
+eager work and synchronisations between replays, must equal the eager
+result bit for bit, and the eager result must match the oracle.  Building a
+plan while the stream is capturing is refused and enqueues nothing.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2601_03324_amd import tvl  # noqa: E402
+
+DEV = "cuda"
+ARG = -8
+
+
+def matrix(rng, M, K):
+    W = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    return W, torch.from_numpy(W).to(DEV)
+
+
+def test_capture_survives_eviction_and_workspace_growth():
+    rng = np.random.default_rng(2024)
+    s = torch.cuda.Stream()
+    sid = int(s.cuda_stream)
+    # a two-item batch sweep and a K split (64 rows of 48 KB: split by default)
+    specs = [(300, 704), (129, 2048)]  # K * 4 bytes a multiple of 128: ldw = K
+    hosts, items, ys, xs = [], [], [], []
+    for M, K in specs:
+        W, Wd = matrix(rng, M, K)
+        x = rng.standard_normal(K).astype(np.float32)
+        xd = torch.from_numpy(x).to(DEV)
+        y = torch.full((M,), float("nan"), device=DEV)
+        hosts.append((W, x, Wd, xd))
+        ys.append(y)
+        items.append((Wd, K, xd, y, M, K, 0))
+    Mk, Kk = 64, 12288
+    Wk, Wkd = matrix(rng, Mk, Kk)
+    xk = rng.standard_normal(Kk).astype(np.float32)
+    xkd = torch.from_numpy(xk).to(DEV)
+    yk = torch.full((Mk,), float("nan"), device=DEV)
+    outs = ys + [yk]
+
+    def calls():
+        tvl.tvl_gemv_batch_sweep(items, sid)
+        tvl.tvl_gemv(Wkd, Kk, 0, xkd, yk, Mk, Kk, stream=sid)
+
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        calls()  # eager: builds the plan and the stream's workspace
+    s.synchronize()
+    eager = [y.clone() for y in outs]
+    for (W, x, _, _), y in zip(hosts + [(Wk, xk, None, None)], eager):
+        yref, S = oracle.gemv_f32(W, x)
+        r = oracle.check(y.cpu().numpy(), yref, S, 1e-5)
+        assert r["bad"] == 0, r
+
+    # an item list without a plan cannot be captured: refused, nothing enqueued
+    other, n_other = tvl.make_items([(hosts[0][2], 704, hosts[0][3], ys[0], 300, 699, 0)])
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        calls()
+        st = tvl.lib.tvl_gemv_batch_sweep(ctypes.cast(other, ctypes.c_void_p), n_other, sid)
+    assert st == ARG
+    assert b"captured" in tvl.lib.tvl_last_error()
+
+    # empty the plan cache (more lists than it holds) and grow the stream's
+    # K-split workspace (8192 rows x 16 slices: twice its first size)
+    big_y = torch.empty(8192, device=DEV)
+    with torch.cuda.stream(s):
+        for i in range(70):
+            tvl.tvl_gemv_batch_sweep([(hosts[0][2], 704, hosts[0][3], big_y, 300 - i, 704, 0)],
+                                     sid)
+        W2, W2d = matrix(rng, 8192, 1024)
+        x2d = torch.from_numpy(rng.standard_normal(1024).astype(np.float32)).to(DEV)
+        tvl.tvl_gemv_ex(W2d, 1024, 0, x2d, big_y, 8192, 1024, dict(ksplit=16), sid)
+    s.synchronize()
+    yref, S = oracle.gemv_f32(W2, x2d.cpu().numpy())
+    assert oracle.check(big_y.cpu().numpy(), yref, S, 1e-5)["bad"] == 0
+
+    for rep in range(3):
+        for y in outs:
+            y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for y, e in zip(outs, eager):
+            assert torch.equal(y, e), rep
+        with torch.cuda.stream(s):  # eager work between replays
+            calls()
+        s.synchronize()
+        for y, e in zip(outs, eager):
+            assert torch.equal(y, e), rep
+    del g
+    torch.cuda.synchronize()
+    tvl.tvl_release_workspaces()
