@@ -172,11 +172,23 @@ def cpu_baseline(samples, seconds: float, what: str, threads: int = 1) -> dict:
     gbs = nbytes / el / 1e9
     out = {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
            "sample": f"{ngemv} GEMVs of {what} ({nbytes / 1e9:.2f} GB algorithmic) in "
-                     f"{el:.1f} s on one host thread "
-                     f"({platform.processor() or platform.machine()})"}
+                     f"{el:.1f} s on one host thread",
+           "cpu": cpu_model()}
     if threads > 1:
         out["all_cores"] = cpu_baseline_threads(samples, seconds / 2, what, threads)
     return out
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), else the platform's."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
 
 def host_threads() -> int:
@@ -740,7 +752,7 @@ def run_fused(args, tvl, torch, np, oracle, synth, sdev) -> int:
             "value": round(nbytes / el / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"{n} fused items of {wl.name} (a normalised GEMV, a SwiGLU pair, a plain "
                       f"GEMV in turn; {nbytes / 1e9:.2f} GB algorithmic) in {el:.1f} s on one "
-                      f"host thread"}
+                      f"host thread", "cpu": cpu_model()}
     for p in plans:
         p.destroy()
     emit(out)

@@ -317,7 +317,8 @@ def upload_matrix(host, dtype: int, device="cuda", stream=None) -> TvlMatrix:
 
 def quant_matrix_bytes(M: int, K: int, dtype: int, ldw: int | None = None) -> int:
     """Bytes of a block-quantised matrix: M code rows of ldw bytes, then the
-    group-major fp32 scale plane (ceil(K/64) groups of M rounded up to 4)."""
+    fp32 scale plane in blocks of 4 rows (M rounded up to 4 rows, each with
+    ceil(K/64) scales; a block holds its 4 rows' scales group by group)."""
     ldw = tvl_row_stride(K, dtype) if ldw is None else ldw
     return M * ldw + 4 * ((M + 3) // 4 * 4) * ((K + 63) // 64)
 
