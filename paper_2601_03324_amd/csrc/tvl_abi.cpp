@@ -335,6 +335,7 @@ tvl_status check_tuning(const tvl_tuning *t, bool allow_ksplit)
 // ---------------------------------------------------------------- devices
 struct DevInfo {
     int cus = 256;
+    int xcds = 8; // gfx950: 32 compute units per XCD
 };
 
 std::mutex g_mu;
@@ -352,6 +353,7 @@ tvl_status current_device(int *dev, DevInfo *info)
         e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, *dev);
         if (e != hipSuccess) return fail_hip(e, "hipDeviceGetAttribute");
         if (cus > 0) d.cus = cus;
+        d.xcds = d.cus >= 64 ? d.cus / 32 : 1;
         it = g_dev.emplace(*dev, d).first;
     }
     *info = it->second;
@@ -529,6 +531,48 @@ tvl_status get_workspace_locked(int dev, hipStream_t st, int64_t nfloat, int64_t
     return TVL_OK;
 }
 
+// XCD-aware tile order.  The dispatcher deals a launch's workgroups to the
+// XCDs in turn (workgroup b to XCD b mod nx), and with one tile per
+// workgroup tile b runs there too.  Each XCD's L2 fetches an item's x vectors
+// once for the tiles it runs, so an item whose tiles are dealt over all XCDs
+// has its x fetched nx times: at 16 x vectors that is several percent of a
+// launch's bytes.  `tiles` is ordered longest tile first, each item's tiles
+// contiguous, and key[t] is the bytes per row of tile t.  Each class of
+// equally long tiles is cut into nx contiguous runs of equal length (the
+// remainders going to XCDs in rotation), run c to XCD c, so an item spans one
+// or two XCDs unless it is longer than a run; the XCD lists are then dealt
+// back into the table (entry nx j + c: XCD c's j-th tile).  Every XCD gets as
+// many tiles of every class as the others, plus at most one, so their bytes
+// stay balanced, and each list keeps the longest tiles first.
+std::vector<DevTile> xcd_order(const std::vector<DevTile> &tiles, const std::vector<int64_t> &key,
+                               int nx)
+{
+    std::vector<std::vector<DevTile>> lists(nx);
+    size_t a = 0;
+    int rot = 0;
+    while (a < tiles.size()) {
+        size_t b = a;
+        while (b < tiles.size() && key[b] == key[a])
+            ++b;
+        const size_t n = b - a, base = n / nx;
+        const int rem = (int)(n % nx);
+        size_t pos = a;
+        for (int c = 0; c < nx; ++c) {
+            const size_t len = base + (((c - rot) % nx + nx) % nx < rem ? 1 : 0);
+            lists[c].insert(lists[c].end(), tiles.begin() + pos, tiles.begin() + pos + len);
+            pos += len;
+        }
+        rot = (rot + rem) % nx;
+        a = b;
+    }
+    std::vector<DevTile> out;
+    out.reserve(tiles.size());
+    for (size_t j = 0; out.size() < tiles.size(); ++j)
+        for (int c = 0; c < nx; ++c)
+            if (j < lists[c].size()) out.push_back(lists[c][j]);
+    return out;
+}
+
 // -------------------------------------------------------------- plans
 tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning, tvl_plan **out)
 {
@@ -607,11 +651,21 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
         return fail(TVL_ERR_SHAPE, "plan: %lld tiles exceed 2^31-1", (long long)ntiles);
     }
     htiles.reserve((size_t)ntiles);
+    std::vector<int64_t> tkey;
+    tkey.reserve((size_t)ntiles);
     for (int32_t k = 0; k < n; ++k) {
         const int32_t i = ord[k];
-        for (int64_t r = 0; r < items[i].M; r += rows_of(items[i]))
+        for (int64_t r = 0; r < items[i].M; r += rows_of(items[i])) {
             htiles.push_back(DevTile{i, (int32_t)r});
+            tkey.push_back(items[i].K * elem_size(items[i].dtype) * item_bytes_factor(items[i]));
+        }
     }
+    // Several x vectors per item, or quantised rows (32 x floats per 16 code
+    // bytes): each XCD fetches the x of the items it runs, so keep every item
+    // on as few XCDs as possible (measured on MI355X: +5 % for 8 and 16
+    // vectors, +7 % for 4, +1-2 % for the 8- and 4-bit 110M tokens; the plain
+    // fp32 sweep, whose x is 0.5 % of its bytes, keeps one global order)
+    if ((multiB || quant) && info.xcds > 1) htiles = xcd_order(htiles, tkey, info.xcds);
     p->ntiles = (int)ntiles;
     p->ks_cap = tvl::slice_cap(kmax);
     p->grid = (tuning && tuning->grid) ? std::min<int>(tuning->grid, std::max(p->ntiles, 1))

@@ -8,6 +8,7 @@ from __future__ import annotations
 import numpy as np
 import pytest
 
+import host_oracle
 import oracle
 import synth
 
@@ -102,6 +103,7 @@ def test_beam4_sweep110m():
     launch; every output of every vector against the oracle."""
     wl = synth.WORKLOADS["sweep110m"]
     ms = sdev.load_multi(wl, 4, DEV)
+    hosts = [m.weights() for m in wl.mats]
     for t in (None, dict(rows_per_wave=2, waves_per_block=4, unroll=2, flags=2),
               dict(rows_per_wave=4, waves_per_block=4, unroll=1, flags=2, grid=500),
               dict(rows_per_wave=8, waves_per_block=4, unroll=1, flags=2),
@@ -121,20 +123,12 @@ def test_beam4_sweep110m():
         plan = tvl.tvl_sweep_plan_create([d.item() for d in ms], t)
         plan.run()
         torch.cuda.synchronize()
-        for d in ms:
+        for d, Wh in zip(ms, hosts):
             m = d.spec
-            Wh = m.weights() if m.M < 32000 else None
             Y = d.Y.cpu().numpy()
             for b in range(4):
-                if Wh is None:  # the classifier: sampled rows
-                    rows = sdev.sample_rows(m.M, 256, 5)
-                    ref, S = oracle.gemv_f32(np.stack([m.weights(int(r), 1)[0] for r in rows]),
-                                             m.x(b))
-                    yb = Y[b][rows]
-                else:
-                    ref, S = oracle.gemv_f32(Wh, m.x(b))
-                    yb = Y[b]
-                r = oracle.check(yb, ref, S, 1e-5)
+                ref, S = host_oracle.gemv(Wh, m.x(b), 0)
+                r = oracle.check(Y[b], ref, S, 1e-5)
                 assert r["bad"] == 0, (m.name, b, t, r)
         plan.destroy()
 
@@ -186,8 +180,8 @@ def test_multi_plan_mixed_dtypes():
 @pytest.mark.parametrize("nb", [8, 16])
 def test_beam_sweep110m_default(nb):
     """The 110M decode token for 8 and 16 hypotheses in the launch the bench
-    times (the library's default several-vector kernel): every output of the
-    first 28 matrices and sampled rows of the rest, every vector."""
+    times (the library's default several-vector kernel, tiles in XCD-aware
+    order): every output of every matrix and every vector."""
     wl = synth.WORKLOADS["sweep110m"]
     ms = sdev.load_multi(wl, nb, DEV)
     for d in ms:
@@ -195,14 +189,13 @@ def test_beam_sweep110m_default(nb):
     plan = tvl.tvl_sweep_plan_create([d.item() for d in ms])
     plan.run()
     torch.cuda.synchronize()
-    for k, d in enumerate(ms):
+    for d in ms:
         m = d.spec
         Y = d.Y.cpu().numpy()
-        rows = np.arange(m.M) if k < 28 else sdev.sample_rows(m.M, 96, 11 + k)
-        Wh = m.weights() if k < 28 else np.stack([m.weights(int(r), 1)[0] for r in rows])
+        Wh = m.weights()
         for b in range(nb):
-            ref, S = oracle.gemv_f32(Wh, m.x(b))
-            r = oracle.check(Y[b][rows], ref, S, 1e-5)
+            ref, S = host_oracle.gemv(Wh, m.x(b), 0)
+            r = oracle.check(Y[b], ref, S, 1e-5)
             assert r["bad"] == 0, (m.name, nb, b, r)
     plan.destroy()
 
@@ -211,7 +204,7 @@ def test_beam_sweep110m_default(nb):
 def test_beam_70b_layer_default(nb):
     """One 70B-shaped fp16 layer (7 GEMVs, 1.71 GB) for 8 and 16 hypotheses in
     the launch the bench times (the library's default: split x on the fp16
-    matrix cores, x shared by the block): 48 sampled rows of every matrix,
+    matrix cores, x shared by the block): every output of every matrix and
     every vector, within the fp32 parity bar (1e-5 of the norm)."""
     src = synth.WORKLOADS["stack70b8"]
     wl = synth.Workload("stack70b8[:7]", src.cfg, tuple(src.mats[:7]))
@@ -221,15 +214,15 @@ def test_beam_70b_layer_default(nb):
     plan = tvl.tvl_sweep_plan_create([d.item() for d in ms])
     plan.run()
     torch.cuda.synchronize()
-    for k, d in enumerate(ms):
+    for d in ms:
         m = d.spec
-        rows = sdev.sample_rows(m.M, 48, 21 + k)
-        Wr = np.stack([m.weights(int(r), 1)[0] for r in rows])
+        Wh = m.weights()
         Y = d.Y.cpu().numpy()
         for b in range(nb):
-            ref, S = oracle.gemv_f16(Wr, m.x(b))
-            r = oracle.check(Y[b][rows], ref, S, 1e-5)
+            ref, S = host_oracle.gemv(Wh, m.x(b), 1)
+            r = oracle.check(Y[b], ref, S, 1e-5)
             assert r["bad"] == 0, (m.name, nb, b, r)
+        del Wh
     plan.destroy()
     del ms
     torch.cuda.empty_cache()
