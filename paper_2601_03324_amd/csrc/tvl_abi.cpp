@@ -306,16 +306,16 @@ int quant_bits(int32_t dt) { return dt == TVL_Q4 ? 4 : 8; }
 
 // Lanes per row of an item (block-quantised weights may share a wavefront
 // between several short rows; every other item uses all 64 lanes).
-int item_lanes(const tvl_item &t)
+int item_lanes(const tvl_item &t, bool few_lanes = false)
 {
-    return is_quant(t.dtype) ? tvl::quant_lanes(t.K, quant_bits(t.dtype)) : 64;
+    return is_quant(t.dtype) ? tvl::quant_lanes(t.K, quant_bits(t.dtype), few_lanes) : 64;
 }
 
-tvl::DevItem dev_item(const tvl_item &t)
+tvl::DevItem dev_item(const tvl_item &t, bool few_lanes = false)
 {
     return tvl::DevItem{t.W,    t.ldw, t.x,   t.y,        (int32_t)t.M, (int32_t)t.K,
                         t.dtype, t.op, t.W3, t.g,        t.eps,        (int32_t)nvec(t),
-                        t.ldx,  t.ldy, item_lanes(t), 0};
+                        t.ldx,  t.ldy, item_lanes(t, few_lanes && t.dtype == TVL_Q4), 0};
 }
 
 tvl_status check_tuning(const tvl_tuning *t, bool allow_ksplit)
@@ -625,8 +625,18 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
     // output rows per tile: a SwiGLU tile streams R rows of W and of W3 per
     // wavefront, i.e. R/2 output rows; a quantised item whose rows share a
     // wavefront in groups of G lanes covers 64 / G times R rows per wavefront
+    // 4-bit rows in launches of >= 1 GB of codes take the fewest lanes per
+    // row that pad no more (see tvl::quant_lanes)
+    double qbytes = 0;
+    for (int32_t i = 0; i < n; ++i)
+        if (is_quant(items[i].dtype))
+            qbytes += (double)items[i].M * (double)items[i].K * quant_bits(items[i].dtype) / 8;
+    const bool few_lanes = qbytes >= 1e9;
+    auto lanes_of = [&](const tvl_item &t) {
+        return item_lanes(t, few_lanes && t.dtype == TVL_Q4);
+    };
     auto rows_of = [&](const tvl_item &t) {
-        return (t.op == TVL_OP_SWIGLU ? shape.R / 2 : shape.R) * shape.W * (64 / item_lanes(t));
+        return (t.op == TVL_OP_SWIGLU ? shape.R / 2 : shape.R) * shape.W * (64 / lanes_of(t));
     };
     // bytes per tile, largest first, so the longest tiles start first
     std::vector<int32_t> ord(n);
@@ -642,7 +652,7 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
     int64_t kmax = 1;
     for (int32_t i = 0; i < n; ++i) {
         const tvl_item &t = items[i];
-        hitems[i] = dev_item(t);
+        hitems[i] = dev_item(t, few_lanes);
         ntiles += (t.M + rows_of(t) - 1) / rows_of(t);
         kmax = std::max<int64_t>(kmax, t.K);
     }

@@ -48,15 +48,22 @@ static_assert(sizeof(DevItem) == 96, "DevItem layout");
 // nv = ceil(K * bits / 128) loads.  Short rows would leave most of a
 // 64-lane wavefront idle (a 4-bit row of 768 columns is 24 loads), so a
 // wavefront splits into 64 / G groups of G lanes, one row per group: G is
-// the group size in {64, 32, 16, 8} that pads nv the least (ties: larger G).
-inline int quant_lanes(int64_t K, int bits)
+// the group size in {64, 32, 16, 8} that pads nv the least.  Ties go to the
+// larger G (more tiles, shorter chains of loads per lane), except with
+// `few_lanes`: then to the smaller G.  A lane's 32 4-bit codes need 128
+// contiguous bytes of x, so one x load instruction touches G cache lines
+// (the code load it serves touches 8): for 4-bit rows in launches long
+// enough to hide the longer per-lane chains, G = 8 keeps x from costing the
+// load pipeline more than the codes do (the 4-bit Llama-2 7B token: 5.74 ->
+// 6.33 TB/s; the 110M one, 62 MB, loses a third with it).
+inline int quant_lanes(int64_t K, int bits, bool few_lanes = false)
 {
     const int64_t nv = (K * bits + 127) / 128;
     int best = 64;
     int64_t best_pad = (nv + 63) / 64 * 64;
     for (int g = 32; g >= 8; g /= 2) {
         const int64_t pad = (nv + g - 1) / g * g;
-        if (pad < best_pad) {
+        if (pad < best_pad || (few_lanes && pad == best_pad)) {
             best = g;
             best_pad = pad;
         }
