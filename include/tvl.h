@@ -343,8 +343,9 @@ TVL_API tvl_status tvl_release_workspaces(void);
  * tvl_util_read_stream: read `bytes` (a multiple of 16) at `src` (16-byte
  *   aligned) with the same streaming loads as the GEMV, in `sink_len`
  *   workgroups each reading one contiguous span, and write one float per
- *   workgroup to `sink` (`sink_len` floats).  *grid_out (may be NULL)
- *   receives the grid, which equals sink_len.
+ *   workgroup to `sink` (`sink_len` floats; the sum read by its first
+ *   thread).  *grid_out (may be NULL) receives the grid, which equals
+ *   sink_len.
  * tvl_util_copy: copy `bytes` (multiple of 16, both 16-byte aligned, no
  *   overlap) from src to dst. */
 TVL_API tvl_status tvl_util_read_stream(const void *src, int64_t bytes,

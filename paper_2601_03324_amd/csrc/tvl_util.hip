@@ -29,12 +29,14 @@ __global__ __launch_bounds__(256) void k_zero_i32(int *p, int64_t n)
 // Read-only streaming with the GEMV's load kind: workgroup b reads the
 // contiguous span [b*per, (b+1)*per) of 16-byte vectors, eight loads in
 // flight per lane (the last batch of a span with its loads past the span
-// switched off, so a short span keeps its loads in flight too), and writes
-// one float so the loads cannot be optimised away.
+// switched off, so a short span keeps its loads in flight too).  The
+// workgroup's first thread writes its own partial sum to sink[b]: every
+// thread's loads are still issued (they feed the same code), and a
+// workgroup ends without a reduction or barrier, which for short launches
+// of many small workgroups is part of what is measured.
 __global__ __launch_bounds__(256) void k_read_stream(const f4 *__restrict__ src, int64_t nvec,
                                                      int64_t per, float *__restrict__ sink)
 {
-    __shared__ float red[4];
     const int64_t beg = (int64_t)blockIdx.x * per;
     const int64_t end = min(beg + per, nvec);
     const TVL_GLOBAL f4 *g = (const TVL_GLOBAL f4 *)(src);
@@ -61,12 +63,7 @@ __global__ __launch_bounds__(256) void k_read_stream(const f4 *__restrict__ src,
         for (int u = 0; u < 8; ++u)
             acc += a[u];
     }
-    float v = (acc.x + acc.y) + (acc.z + acc.w);
-    for (int o = 32; o >= 1; o >>= 1)
-        v += __shfl_xor(v, o);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x / 64] = v;
-    __syncthreads();
-    if (threadIdx.x == 0) sink[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+    if (threadIdx.x == 0) sink[blockIdx.x] = (acc.x + acc.y) + (acc.z + acc.w);
 }
 
 __global__ __launch_bounds__(256) void k_copy(f4 *__restrict__ dst, const f4 *__restrict__ src,
@@ -108,7 +105,9 @@ hipError_t launch_read_stream(const void *src, int64_t bytes, float *sink, int g
                               hipStream_t st)
 {
     const int64_t nvec = bytes / 16;
-    const int64_t per = (nvec + grid - 1) / grid;
+    // spans of whole 128-byte lines, so each wavefront load covers 8 lines
+    // (trailing workgroups may get empty spans)
+    const int64_t per = ((nvec + grid - 1) / grid + 7) / 8 * 8;
     hipLaunchKernelGGL(k_read_stream, dim3(grid), dim3(256), 0, st,
                        static_cast<const f4 *>(src), nvec, per, sink);
     return hipGetLastError();
