@@ -210,9 +210,12 @@ typedef struct tvl_item {
  * rows and waves) (16,4,202) (32,2,202) (32,4,202) (16,2,203) (16,4,203)
  * (16,8,202), and with U + 100 its split-x form for fp16 weights (launches
  * holding fp32 weights run the LDS-staged form) (16,4,303) (32,2,303)
- * (32,4,303) (16,8,303) (16,4,302) (32,4,302).  Rows (and x strides) longer
- * than these forms' buffer descriptors can address (a load's 2, 4 or 8 rows
- * within 2^31 bytes) run the direct-load 16x16x4 form.
+ * (32,4,303) (16,8,303) (16,4,302) (32,4,302), where each wavefront splits
+ * x for a quarter (an eighth, a half) of the vectors once per block.  Rows
+ * (and, except in the split-x shared form, which reads x through plain
+ * pointers, x strides) longer than these forms' buffer descriptors can
+ * address (a load's 2, 4 or 8 rows within 2^31 bytes) run the direct-load
+ * 16x16x4 form.
  * Launches holding block-quantised items (direct-x only; R rows per group of
  * lanes, see tvl_dtype): (2,4,2) (4,4,1) (4,4,2) (4,1,2) (8,4,1) (8,2,1) */
 typedef struct tvl_tuning {

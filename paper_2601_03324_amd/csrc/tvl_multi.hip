@@ -1576,12 +1576,334 @@ struct MfmaDmaXsRows : MfmaDmaRows<T, RG, CC, 3, HX> {
     }
 };
 
+// DPP move within rows of 16 lanes (CTRL: quad permutation 0x00-0xFF,
+// 0x140 row mirror, 0x141 half-row mirror)
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
+}
+
+// the largest of v >= 0 (not NaN) over each group of N consecutive lanes (N =
+// 4, 8, 16, 32), in every lane of the group, as the largest bit pattern (the
+// order of non-negative floats): lane pairs and quads by quad permutations,
+// then half rows and rows by mirrors (each lane meets a lane of the other
+// half), then across two rows by one lane exchange
+template <int N>
+__device__ __forceinline__ float group_max(float v)
+{
+    static_assert(N == 4 || N == 8 || N == 16 || N == 32, "group of 4 .. 32 lanes");
+    uint32_t u = __builtin_bit_cast(uint32_t, v);
+    u = max(u, dpp_u32<0xB1>(u)); // quad permutation 1 0 3 2
+    u = max(u, dpp_u32<0x4E>(u)); // quad permutation 2 3 0 1
+    if constexpr (N >= 8) u = max(u, dpp_u32<0x141>(u));
+    if constexpr (N >= 16) u = max(u, dpp_u32<0x140>(u));
+    if constexpr (N == 32) u = max(u, (uint32_t)__shfl_xor((int)u, 16));
+    return __builtin_bit_cast(float, u);
+}
+
+// fp16 weights with x split once per block (the split-x form with x shared
+// by the block).  The WV wavefronts of a block need the same split x, and the
+// analysis and split of a chunk cost more vector operations than its
+// matrix-core steps: so each wavefront splits only vectors VPW w .. VPW w +
+// VPW - 1 (LPV lanes per vector, CPL columns per lane), one chunk ahead, from
+// x it loads into registers, and writes the two fp16 parts straight into the
+// B-operand layout in LDS (MFMA lane L = 16 g + j at 32-column step s finds
+// columns 32 s + 8 g .. + 7 of vector j at byte s * 1024 + 16 L of a part),
+// with each vector's 2^-k and a flag per wavefront for a chunk too wide for
+// the split (kSplitMin).  After the next step's barrier every wavefront reads
+// its B operands there.  Each value is scaled and split exactly as in the
+// per-wavefront form (the same per-vector maximum), and the matrix-core
+// steps are the same, so the results are the same bit for bit; a chunk any
+// wavefront flagged goes to the fp32 matrix cores with x read from global
+// memory (rare for dense x).  Per chunk step (c): wait for the weights of c
+// and this wavefront's x of c + 1 (the weights of c + 1 stay in flight), one
+// s_barrier, issue x of c + 2 (registers) and the weights of c + 2, issue the
+// matrix-core steps of chunk c (weight stage c % 3, split stage c % 2), split
+// x of c + 1 into split stage (c + 1) % 2 while they run, then add chunk c's
+// products.  The barrier of step c + 1 separates the writes of a split stage
+// from the reads of the step before and after.  The maximum over a vector's
+// lanes uses DPP moves (no LDS round trips on the split's critical path).
+template <int RG, int CC, int WV>
+struct MfmaXsHxRows : MfmaDmaRows<_Float16, RG, CC, 3, true> {
+    using Base = MfmaDmaRows<_Float16, RG, CC, 3, true>;
+    using Base::NL;
+    using Base::STAGE;
+    static constexpr int NS = CC / 32;        // 32-column matrix-core steps per chunk
+    static constexpr int VPW = 16 / WV;       // vectors split by each wavefront
+    static constexpr int LPV = kWave / VPW;   // lanes per vector
+    static constexpr int CPL = CC / LPV;      // columns per lane
+    static constexpr int XL = CPL / 4;        // 16-byte x loads per lane per chunk
+    static constexpr int HPART = NS * 1024;   // bytes of one fp16 part of a chunk
+    static constexpr int HSCALE = 2 * HPART;  // 16 floats: 2^-k of each vector
+    static constexpr int HFLAG = HSCALE + 64; // WV ints: a wavefront found a wide chunk
+    static constexpr int HSTAGE = (HFLAG + 4 * WV + 15) / 16 * 16;
+    static constexpr int64_t MAXLDX = int64_t(1) << 62; // x is read through plain pointers
+    static_assert(CPL == 4 || CPL == 8 || CPL == 16, "columns per lane");
+    static_assert(2 * NL + XL < 64, "vmcnt range");
+
+    const float *X; // vector 0 of the item
+    int64_t ldx;
+    int nb, wave;
+    TVL_LDS char *hl; // the block's two split stages
+    const float *xs; // this lane's vector (clamped to nb - 1) at its first column
+    int woff;        // byte offset of the lane's first column in a part
+
+    __device__ __forceinline__ MfmaXsHxRows(const _Float16 *W_, int64_t ldw_, int wrow0, int M,
+                                            const float *x, int64_t ldx_, int nb_, int K,
+                                            int lane_, int wave_, TVL_LDS char *lds_,
+                                            TVL_LDS char *hl_)
+        : Base(W_, ldw_, wrow0, M, x, ldx_, nb_, K, lane_, lds_), X(x), ldx(ldx_), nb(nb_),
+          wave(wave_), hl(hl_)
+    {
+        // vectors past nb repeat vector nb - 1, as in the per-wavefront
+        // form: same scale and range decisions, columns never stored
+        const int v = VPW * wave_ + lane_ / LPV, col = (lane_ % LPV) * CPL;
+        xs = x + (int64_t)min(v, nb_ - 1) * ldx_ + col;
+        woff = (col / 32) * 1024 + (16 * ((col % 32) / 8) + v) * 16 + 2 * (col % 8);
+    }
+
+    // this lane's x of chunk c
+    __device__ __forceinline__ void load_xs(int c, f4 (&xr)[XL]) const
+    {
+#pragma unroll
+        for (int u = 0; u < XL; ++u)
+            xr[u] = load_x4(xs + c * CC + 4 * u);
+    }
+
+    // scale and split this lane's x into split stage HS (see MfmaDmaRows'
+    // multiply_hx for the arithmetic and the range test)
+    template <int HS>
+    __device__ __forceinline__ void split(const f4 (&xr)[XL]) const
+    {
+        float m = 0.f, mz = 3.4028235e38f;
+#pragma unroll
+        for (int u = 0; u < XL; ++u)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                m = fmaxf(m, fabsf(xr[u][e]));
+                mz = fminf(mz, fabsf(xr[u][e]));
+            }
+        m = group_max<LPV>(m); // the vector's lanes are consecutive; m >= 0, never NaN
+        int e2 = 0;
+        if (m > 0.f && m <= 3.4028235e38f) e2 = __builtin_amdgcn_frexp_expf(m);
+        const int k = min(max(14 - e2, -126), 126);
+        const float sc = __builtin_ldexpf(1.f, k);
+        const float thr = __builtin_ldexpf(kSplitMin, -k);
+        bool wide = false;
+        if (__builtin_expect(__builtin_amdgcn_ballot_w64(mz < thr) != 0, 0)) { // wave-uniform
+            uint32_t mn = 0xFFFFFFFFu;
+#pragma unroll
+            for (int u = 0; u < XL; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    mn = min(mn, (__builtin_bit_cast(uint32_t, xr[u][e]) << 1) - 2u);
+            wide = mn < (__builtin_bit_cast(uint32_t, thr) << 1) - 2u;
+        }
+        const int any = __builtin_amdgcn_ballot_w64(wide) != 0; // all lanes take part
+        TVL_LDS char *hb = hl + HS * HSTAGE;
+        const int lane = this->lane;
+        if (lane == 0) *(TVL_LDS int *)(hb + HFLAG + 4 * wave) = any;
+        if (lane % LPV == 0)
+            ((TVL_LDS float *)(hb + HSCALE))[VPW * wave + lane / LPV] = __builtin_ldexpf(1.f, -k);
+        // hi = f16(x 2^k), lo = f16(x 2^k - hi), CPL values, in pieces of up
+        // to 8 columns (one B-operand slot each)
+        constexpr int PC = CPL < 8 ? CPL : 8;
+#pragma unroll
+        for (int p = 0; p < CPL / PC; ++p) {
+            _Float16 hv[PC], lv[PC];
+#pragma unroll
+            for (int e = 0; e < PC; ++e) {
+                const float xv = xr[(p * PC + e) / 4][(p * PC + e) % 4];
+                const _Float16 vh = (_Float16)__builtin_fmaf(xv, sc, 0.f);
+                hv[e] = vh;
+                lv[e] = (_Float16)__builtin_fmaf(xv, sc, -(float)vh);
+            }
+            const int off = woff + p * 256; // the next 8 columns: slot g + 1
+            if constexpr (PC == 8) {
+                *(TVL_LDS h8 *)(hb + off) = h8{hv[0], hv[1], hv[2], hv[3], hv[4], hv[5], hv[6], hv[7]};
+                *(TVL_LDS h8 *)(hb + HPART + off) =
+                    h8{lv[0], lv[1], lv[2], lv[3], lv[4], lv[5], lv[6], lv[7]};
+            } else {
+                *(TVL_LDS h4 *)(hb + off) = h4{hv[0], hv[1], hv[2], hv[3]};
+                *(TVL_LDS h4 *)(hb + HPART + off) = h4{lv[0], lv[1], lv[2], lv[3]};
+            }
+        }
+    }
+
+    // some wavefront found chunk c too wide for the split (split stage HS)
+    template <int HS>
+    __device__ __forceinline__ bool wide_chunk() const
+    {
+        const TVL_LDS char *hb = hl + HS * HSTAGE;
+        int wide = 0;
+#pragma unroll
+        for (int w = 0; w < WV; ++w)
+            wide |= *(const TVL_LDS int *)(hb + HFLAG + 4 * w);
+        return __builtin_amdgcn_readfirstlane(wide) != 0;
+    }
+
+    // chunk c on the fp32 matrix cores (weight stage ST): x of vector
+    // lane & 15, columns 32 q + 8 g + e, read from global memory
+    template <int ST>
+    __device__ __forceinline__ void products_fp32(int c, f4 (&cf)[RG]) const
+    {
+        const int lane = this->lane, j = lane & 15, g = lane >> 4;
+        const float *xq = X + (int64_t)min(j, nb - 1) * ldx + c * CC + 8 * g;
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg) {
+            f4 t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < NS; ++q) {
+                const f4 x0 = load_x4(xq + 32 * q), x1 = load_x4(xq + 32 * q + 4);
+                const h8 a = *(const TVL_LDS h8 *)(this->lds + ST * STAGE + rg * 16 * Base::RB +
+                                                  this->raddr[q]);
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    t = mfma16((float)a[e], e < 4 ? x0[e] : x1[e - 4], t);
+            }
+            cf[rg] = t;
+        }
+    }
+
+    // chunk c on the fp16 matrix cores (weight stage ST, split stage HS):
+    // cf times the returned 2^-k is the chunk's contribution
+    template <int ST, int HS>
+    __device__ __forceinline__ float products_split(f4 (&cf)[RG]) const
+    {
+        const TVL_LDS char *hb = hl + HS * HSTAGE;
+        const int lane = this->lane;
+        const float inv = ((const TVL_LDS float *)(hb + HSCALE))[lane & 15];
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg) {
+            f4 t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < NS; ++q) {
+                const h8 a = *(const TVL_LDS h8 *)(this->lds + ST * STAGE + rg * 16 * Base::RB +
+                                                  this->raddr[q]);
+                const h8 hi = *(const TVL_LDS h8 *)(hb + q * 1024 + 16 * lane);
+                const h8 lo = *(const TVL_LDS h8 *)(hb + HPART + q * 1024 + 16 * lane);
+                t = mfma16h(a, hi, t);
+                t = mfma16h(a, lo, t);
+            }
+            cf[rg] = t;
+        }
+        return inv;
+    }
+
+    template <int ST, int HS>
+    __device__ __forceinline__ bool step(int &c, int nfull, f4 (&xr)[2][XL], f4 (&acc)[RG],
+                                         f4 (&t1)[RG], f4 (&t2)[RG], int &n1) const
+    {
+        const f4 z = {0.f, 0.f, 0.f, 0.f};
+        __builtin_amdgcn_sched_barrier(0);
+        // vmcnt(NL): the weights of c and this wavefront's x of c + 1 have
+        // landed; the weights of c + 1 may still be in flight
+        __builtin_amdgcn_s_waitcnt((NL & 15) | ((NL >> 4) << 14) | 0x0F70);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        load_xs(min(c + 2, nfull - 1), xr[HS]); // x of c, split last step: free
+        Base::template issue<(ST + 2) % 3>((c + 2) * CC, c + 2 < nfull);
+        __builtin_amdgcn_sched_barrier(0);
+        // the matrix-core steps of chunk c first, speculatively on the split
+        // parts (a chunk too wide for them, rare, is redone on the fp32
+        // matrix cores and these products dropped), so that neither the flag
+        // test nor the split of x of c + 1 (past the end: never read) stands
+        // before them; the split runs while they do (in both branches, so that
+        // the products stay in the accumulators until added)
+        f4 cf[RG];
+        const float inv = products_split<ST, HS>(cf);
+        if (__builtin_expect(wide_chunk<HS>(), 0)) {
+            products_fp32<ST>(c, cf);
+            split<1 - HS>(xr[1 - HS]);
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg)
+                acc[rg] += cf[rg];
+        } else {
+            __builtin_amdgcn_sched_barrier(0);
+            split<1 - HS>(xr[1 - HS]);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg)
+                acc[rg] += cf[rg] * inv;
+        }
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg) {
+            t1[rg] += acc[rg];
+            acc[rg] = z;
+        }
+        if (++n1 == kMfmaLevel) {
+#pragma unroll
+            for (int rg = 0; rg < RG; ++rg) {
+                t2[rg] += t1[rg];
+                t1[rg] = z;
+            }
+            n1 = 0;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        return ++c == nfull;
+    }
+
+    __device__ __forceinline__ void run(f4 (&out)[RG]) const
+    {
+        const f4 z = {0.f, 0.f, 0.f, 0.f};
+        f4 acc[RG], t1[RG], t2[RG];
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+            acc[rg] = t1[rg] = t2[rg] = z;
+        const int nfull = this->kn / CC;
+        int c = 0, n1 = 0;
+        // the previous tile's readers of the shared split stages are done
+        __builtin_amdgcn_s_barrier();
+        if (nfull > 0) {
+            f4 xr[2][XL];
+            load_xs(0, xr[0]);
+            Base::template issue<0>(0, true);
+            load_xs(min(1, nfull - 1), xr[1]);
+            Base::template issue<1>(CC, nfull > 1);
+            __builtin_amdgcn_sched_barrier(0);
+            // this wavefront's x of chunk 0 has landed (the weights of 0 and
+            // 1 and the x of 1 may still be in flight)
+            constexpr int W0 = 2 * NL + XL;
+            __builtin_amdgcn_s_waitcnt((W0 & 15) | ((W0 >> 4) << 14) | 0x0F70);
+            __builtin_amdgcn_sched_barrier(0);
+            split<0>(xr[0]);
+            for (;;) {
+                if (step<0, 0>(c, nfull, xr, acc, t1, t2, n1)) break;
+                if (step<1, 1>(c, nfull, xr, acc, t1, t2, n1)) break;
+                if (step<2, 0>(c, nfull, xr, acc, t1, t2, n1)) break;
+                if (step<0, 1>(c, nfull, xr, acc, t1, t2, n1)) break;
+                if (step<1, 0>(c, nfull, xr, acc, t1, t2, n1)) break;
+                if (step<2, 1>(c, nfull, xr, acc, t1, t2, n1)) break;
+            }
+            __builtin_amdgcn_s_waitcnt(0x0F70); // the empty loads too
+        }
+        if (c * CC < this->kn) // private: weights stage 0, x in registers
+            Base::tail(c * CC, acc);
+#pragma unroll
+        for (int rg = 0; rg < RG; ++rg)
+            out[rg] = t2[rg] + (t1[rg] + acc[rg]);
+    }
+};
+
 // One row tile with x shared by the block; every wavefront runs it to the
-// end (see above).  lds: the block's LDS (weight stages, then x stages).
+// end (see above).  lds: the block's LDS (weight stages, then the shared x
+// or split-x stages).
+template <typename T, int RG, int CC, int WV, bool HX>
+struct XsRowsOf {
+    using type = MfmaDmaXsRows<T, RG, CC, WV, HX>;
+    static constexpr int kShared = 3 * type::XSTAGE; // LDS bytes after the weight stages
+};
+template <int RG, int CC, int WV>
+struct XsRowsOf<_Float16, RG, CC, WV, true> {
+    using type = MfmaXsHxRows<RG, CC, WV>;
+    static constexpr int kShared = 2 * type::HSTAGE;
+};
+
 template <typename T, int RG, int WV, int CC, bool HX>
 __device__ __forceinline__ void tile_mfma_dma_xs(const DevItem &it, int row0, TVL_LDS char *lds)
 {
-    using Rows = MfmaDmaXsRows<T, RG, CC, WV, HX>;
+    using Rows = typename XsRowsOf<T, RG, CC, WV, HX>::type;
     if (it.ldw > Rows::MAXLDW || it.ldx > Rows::MAXLDX) { // the item decides, no barrier
         tile_mfma16<T, RG, 4, WV>(it, row0);
         return;
@@ -1610,8 +1932,8 @@ __device__ __forceinline__ void tile_mfma_dma_xs(const DevItem &it, int row0, TV
 template <typename T, int RG, int WV, int CC, bool HX>
 constexpr int dma_xs_lds()
 {
-    using Rows = MfmaDmaXsRows<T, RG, CC, WV, HX>;
-    return WV * 3 * Rows::STAGE + 3 * Rows::XSTAGE;
+    using Of = XsRowsOf<T, RG, CC, WV, HX>;
+    return WV * 3 * Of::type::STAGE + Of::kShared;
 }
 
 // launches of one weight dtype (T); HX with fp16 only

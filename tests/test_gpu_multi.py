@@ -326,7 +326,8 @@ def test_split_x_wide_chunks():
 def test_multi_huge_x_stride(ldx):
     """x strides at the shared-x forms' limit (4 x vectors of one 64-column
     chunk row in a buffer descriptor's 31-bit size) and one past it (those
-    launches fall back to the direct-load form): 5 vectors of 0.5 GiB each (a
+    launches fall back to the direct-load form; the split-x shared form reads
+    x through plain pointers and runs as is): 5 vectors of 0.5 GiB each (a
     partial group of 4), fp32 and fp16 weights, every launch shape."""
     M, K, nb = 100, 300, 5
     rng = np.random.default_rng(ldx % 1000)
