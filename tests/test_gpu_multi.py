@@ -5,6 +5,8 @@ definition, applied per vector), with the GEMV parity norm.
 """
 from __future__ import annotations
 
+import sys
+
 import numpy as np
 import pytest
 
@@ -189,6 +191,7 @@ def test_beam_sweep110m_default(nb):
     plan = tvl.tvl_sweep_plan_create([d.item() for d in ms])
     plan.run()
     torch.cuda.synchronize()
+    worst = 0.0
     for d in ms:
         m = d.spec
         Y = d.Y.cpu().numpy()
@@ -197,6 +200,9 @@ def test_beam_sweep110m_default(nb):
             ref, S = host_oracle.gemv(Wh, m.x(b), 0)
             r = oracle.check(Y[b], ref, S, 1e-5)
             assert r["bad"] == 0, (m.name, nb, b, r)
+            worst = max(worst, r["max_err"])
+    print(f"beam{nb}_110m: every output, max normalised error {worst:.3e}", file=sys.stderr,
+          flush=True)
     plan.destroy()
 
 
@@ -214,6 +220,7 @@ def test_beam_70b_layer_default(nb):
     plan = tvl.tvl_sweep_plan_create([d.item() for d in ms])
     plan.run()
     torch.cuda.synchronize()
+    worst = 0.0
     for d in ms:
         m = d.spec
         Wh = m.weights()
@@ -222,7 +229,10 @@ def test_beam_70b_layer_default(nb):
             ref, S = host_oracle.gemv(Wh, m.x(b), 1)
             r = oracle.check(Y[b], ref, S, 1e-5)
             assert r["bad"] == 0, (m.name, nb, b, r)
+            worst = max(worst, r["max_err"])
         del Wh
+    print(f"beam{nb}_70b: every output, max normalised error {worst:.3e}", file=sys.stderr,
+          flush=True)
     plan.destroy()
     del ms
     torch.cuda.empty_cache()
