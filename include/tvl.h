@@ -144,8 +144,12 @@ typedef enum tvl_status {
  *     items only (op == TVL_OP_GEMV, g == NULL, nrhs <= 1).
  * One launch (plan or batch) may hold plain fp32/fp16 items together with
  * ONE of: RMSNorm/SwiGLU items, several-vector items, quantised items.
- * Items with g != NULL, op != TVL_OP_GEMV, nrhs > 1 or quantised weights run
- * in direct-x mode and cannot be K-split. */
+ * Items with g != NULL, op != TVL_OP_GEMV or nrhs > 1 run in direct-x mode;
+ * they and quantised items cannot be K-split.  Quantised items read x
+ * directly too, or, with TVL_FLAG_X_LDS, from a copy of x that each
+ * workgroup stages in LDS once per row tile (x of the largest quantised K in
+ * the launch, in whole KiB, must fit a workgroup's 160 KB: K <= 40,960;
+ * else TVL_ERR_SHAPE); plain items in such a launch still read x directly. */
 typedef struct tvl_item {
     const void *W;      /* device, M whole rows of ldw elements of `dtype`   */
     int64_t ldw;        /* row stride in elements                             */
@@ -216,8 +220,10 @@ typedef struct tvl_item {
  * pointers, x strides) longer than these forms' buffer descriptors can
  * address (a load's 2, 4 or 8 rows within 2^31 bytes) run the direct-load
  * 16x16x4 form.
- * Launches holding block-quantised items (direct-x only; R rows per group of
- * lanes, see tvl_dtype): (2,4,2) (4,4,1) (4,4,2) (4,1,2) (8,4,1) (8,2,1) */
+ * Launches holding block-quantised items (R rows per group of lanes, see
+ * tvl_dtype): direct-x (2,4,2) (4,4,1) (4,4,2) (4,1,2) (8,4,1) (8,2,1);
+ * x in LDS (TVL_FLAG_X_LDS; a tuning that sets only the flag keeps the
+ * default rows and waves) (4,4,1) (8,4,1) (8,2,1). */
 typedef struct tvl_tuning {
     int32_t rows_per_wave;
     int32_t waves_per_block;

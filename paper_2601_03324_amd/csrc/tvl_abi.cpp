@@ -31,6 +31,7 @@ struct tvl_plan {
     int multiB = 0; // > 0: several-vector plan holding B x vectors
     int wmode = 0;  // weight dtypes: 0 fp32 only, 1 fp16 only, 2 both
     bool quant = false; // some item has block-quantised weights
+    int qxbytes = 0;    // quantised plan with x in LDS: dynamic LDS per workgroup
     Shape shape{4, 4, 2, tvl::kXLds};
     int ks_cap = 0;
     int ntiles = 0;
@@ -62,6 +63,7 @@ tvl_status fail_hip(hipError_t e, const char *what)
 constexpr int64_t kMaxDim = 2147483647LL; // M and tile counts fit in int32
 constexpr int64_t kMaxK = 1LL << 30;       // K plus one LDS slice still fits in int32
 constexpr int64_t kMaxQuantK = 1LL << 24;  // quantised K and ldw (bytes)
+constexpr int64_t kMaxLdsBytes = 160 * 1024; // LDS per workgroup (gfx950)
 
 // Bytes per ldw unit: quantised rows are measured in bytes.
 int elem_size(int32_t dt) { return dt == TVL_F16 ? 2 : (dt == TVL_F32 ? 4 : 1); }
@@ -402,11 +404,18 @@ Shape default_fused_shape(double bytes_f16, double bytes_f32)
 // lane group, except for 8-bit launches of under 1 GB of codes, which get 4
 // (twice the wavefronts for a launch too short to reach full bandwidth;
 // 110M token: 5.64 against 5.34-5.38 TB/s; 7B: 6.34 against 6.51, 4-bit 7B:
-// 4.16 against 5.73, 4-bit 110M: 3.14 against 3.82).  qbytes: code bytes of
-// the launch's quantised items; q4: any of them 4-bit.
-Shape default_quant_shape(double qbytes, bool q4)
+// 4.16 against 5.73, 4-bit 110M: 3.14 against 3.82).  4-bit launches of
+// >= 1 GB of codes (8-lane groups) read x from LDS, staged once per row
+// tile, when it fits three workgroups per CU (K <= 13,312): their x loads
+// were as many as their code loads (7B 4-bit token: 6.61 against 6.35
+// TB/s; the 8-bit 7B token 6.96 against 7.01 and the 110M tokens -1 to -2 %
+// with x in LDS, so they keep direct x).  qbytes: code bytes of the launch's
+// quantised items; q4: any of them 4-bit; kq: their largest K.
+Shape default_quant_shape(double qbytes, bool q4, int64_t kq)
 {
     if (!q4 && qbytes < 1e9) return Shape{4, 4, 1, tvl::kXDirect};
+    if (q4 && qbytes >= 1e9 && tvl::quant_x_lds_bytes(kq) <= 52 * 1024)
+        return Shape{8, 4, 1, tvl::kXLds};
     return Shape{8, 4, 1, tvl::kXDirect};
 }
 
@@ -430,13 +439,15 @@ Shape default_shape_items(const tvl_item *items, int32_t n)
     }
     bool quant = false, q4 = false;
     double qbytes = 0;
+    int64_t kq = 1;
     for (int32_t i = 0; i < n; ++i)
         if (is_quant(items[i].dtype)) {
             quant = true;
             q4 = q4 || items[i].dtype == TVL_Q4;
             qbytes += (double)items[i].M * (double)items[i].K * quant_bits(items[i].dtype) / 8;
+            kq = std::max<int64_t>(kq, items[i].K);
         }
-    if (quant) return default_quant_shape(qbytes, q4);
+    if (quant) return default_quant_shape(qbytes, q4, kq);
     if (nmax > 1) return default_multi_shape(multi_B(nmax), b16 == 0, b32 == 0);
     if (fused) return default_fused_shape(b16, b32);
     return default_shape(b16, b32, b32 > 0 ? row32 / b32 : 0.0, true);
@@ -473,6 +484,35 @@ tvl_status pick_shape(const tvl_tuning *t, Shape def, Shape *out, bool plain = t
                                  "not an instantiated %s shape",
                     s.R, s.W, s.U, s.xmode == tvl::kXLds ? "LDS-x" : "direct-x");
     *out = s;
+    return TVL_OK;
+}
+
+// Shape of a launch with quantised items: as pick_shape, but a tuning that
+// forces only the x mode keeps the default rows and waves (they exist in both
+// modes).  With x in LDS, xbytes is the dynamic LDS its largest quantised K
+// needs, which must fit a workgroup's LDS.
+tvl_status pick_quant_shape(const tvl_tuning *t, Shape def, int64_t kq, Shape *out, int *xbytes,
+                            const char *who)
+{
+    tvl_status st = pick_shape(t, def, out, false);
+    if (st != TVL_OK) return st;
+    if (t && !t->rows_per_wave && !t->waves_per_block && !t->unroll) {
+        out->R = def.R;
+        out->W = def.W;
+        out->U = def.U;
+    }
+    if (!tvl::quant_shape_supported(*out))
+        return fail(TVL_ERR_ARG, "%s: no quantised-weight kernel for (%d, %d, %d) %s", who, out->R,
+                    out->W, out->U, out->xmode == tvl::kXLds ? "LDS-x" : "direct-x");
+    *xbytes = 0;
+    if (out->xmode == tvl::kXLds) {
+        const int64_t b = tvl::quant_x_lds_bytes(kq);
+        if (b > kMaxLdsBytes)
+            return fail(TVL_ERR_SHAPE, "%s: quantised weights with x in LDS: x of K=%lld needs "
+                                       "%lld bytes, more than a workgroup's %lld (use direct x)",
+                        who, (long long)kq, (long long)b, (long long)kMaxLdsBytes);
+        *xbytes = (int)b;
+    }
     return TVL_OK;
 }
 
@@ -580,18 +620,23 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
     bool special = false;
     for (int32_t i = 0; i < n; ++i)
         special = special || is_fused(items[i]) || is_multi(items[i]) || is_quant(items[i].dtype);
-    Shape shape;
-    tvl_status st = pick_shape(tuning, default_shape_items(items, n), &shape, !special);
-    if (st != TVL_OK) return st;
     // every argument check before the first HIP call
     bool fused = false, quant = false, f32 = false, f16 = false;
     int nmax = 1;
+    int64_t kq = 1; // largest quantised K
     for (int32_t i = 0; i < n; ++i) {
         fused = fused || is_fused(items[i]);
         quant = quant || is_quant(items[i].dtype);
         nmax = std::max<int>(nmax, (int)nvec(items[i]));
         (items[i].dtype == TVL_F16 ? f16 : f32) = true;
+        if (is_quant(items[i].dtype)) kq = std::max<int64_t>(kq, items[i].K);
     }
+    Shape shape;
+    int qxbytes = 0;
+    tvl_status st = quant ? pick_quant_shape(tuning, default_shape_items(items, n), kq, &shape,
+                                             &qxbytes, "plan")
+                          : pick_shape(tuning, default_shape_items(items, n), &shape, !special);
+    if (st != TVL_OK) return st;
     const int multiB = nmax > 1 ? multi_B(nmax) : 0;
     if (nmax > 1) {
         if (fused)
@@ -602,9 +647,6 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
                                      "vectors",
                         shape.R, shape.W, shape.U, multiB);
     }
-    if (quant && !tvl::quant_shape_supported(shape))
-        return fail(TVL_ERR_ARG, "plan: no quantised-weight kernel for (%d, %d, %d)", shape.R,
-                    shape.W, shape.U);
     if (fused && !tvl::fused_shape_supported(shape))
         return fail(TVL_ERR_ARG, "plan: items with RMSNorm or SwiGLU need a direct-x shape with "
                                  "fused support; (%d, %d, %d) %s has none",
@@ -621,6 +663,7 @@ tvl_status plan_build(const tvl_item *items, int32_t n, const tvl_tuning *tuning
     p->items.assign(items, items + n);
     p->fused = fused;
     p->quant = quant;
+    p->qxbytes = qxbytes;
     p->multiB = multiB;
     p->wmode = f32 && f16 ? 2 : f16 ? 1 : 0;
     // output rows per tile: a SwiGLU tile streams R rows of W and of W3 per
@@ -706,7 +749,7 @@ tvl_status plan_launch(const tvl_plan *p, hipStream_t st)
     if (p->ntiles == 0) return TVL_OK;
     const hipError_t e =
         p->quant    ? tvl::launch_sweep_quant(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid,
-                                              st)
+                                              p->qxbytes, st)
         : p->multiB ? tvl::launch_sweep_multi(p->shape, p->multiB, p->wmode, p->d_items,
                                               p->d_tiles, p->ntiles, p->grid, st)
         : p->fused ? tvl::launch_sweep_fused(p->shape, p->d_items, p->d_tiles, p->ntiles, p->grid,
@@ -775,17 +818,13 @@ tvl_status gemv_impl(const void *W, int64_t ldw, int32_t dtype, const float *x, 
     if (is_quant(dtype)) {
         if (tuning && tuning->ksplit > 1)
             return fail(TVL_ERR_ARG, "%s: quantised weights have no K split", who);
-        if (tuning && (tuning->flags & TVL_FLAG_X_LDS))
-            return fail(TVL_ERR_ARG, "%s: quantised weights read x directly (direct-x)", who);
         Shape qs;
-        st = pick_shape(tuning,
-                        default_quant_shape((double)M * (double)K * quant_bits(dtype) / 8,
-                                            dtype == TVL_Q4),
-                        &qs, false);
+        int qxbytes = 0;
+        st = pick_quant_shape(tuning,
+                              default_quant_shape((double)M * (double)K * quant_bits(dtype) / 8,
+                                                  dtype == TVL_Q4, K),
+                              K, &qs, &qxbytes, who);
         if (st != TVL_OK) return st;
-        if (!tvl::quant_shape_supported(qs))
-            return fail(TVL_ERR_ARG, "%s: no quantised-weight kernel for (%d, %d, %d)", who,
-                        qs.R, qs.W, qs.U);
         int qdev = 0;
         DevInfo qinfo;
         st = current_device(&qdev, &qinfo);
@@ -796,7 +835,7 @@ tvl_status gemv_impl(const void *W, int64_t ldw, int32_t dtype, const float *x, 
             st = noalloc_setup(qdev, stream, &p, &c);
             if (st != TVL_OK) return st;
         }
-        const hipError_t qe = tvl::launch_item_quant(qs, dev_item(it), stream);
+        const hipError_t qe = tvl::launch_item_quant(qs, dev_item(it), qxbytes, stream);
         if (qe != hipSuccess) return fail_hip(qe, "quantised gemv launch");
         return TVL_OK;
     }

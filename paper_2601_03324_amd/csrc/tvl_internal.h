@@ -130,11 +130,19 @@ hipError_t launch_sweep_fused(const Shape &s, const DevItem *items, const DevTil
 // One item (any op) as one launch: grid = its row tiles, item by value.
 hipError_t launch_item(const Shape &s, const DevItem &item, hipStream_t st);
 
-// Plans or items with block-quantised weights (any plain item, direct-x).
+// Plans or items with block-quantised weights (any plain item).  Direct-x,
+// or (xmode kXLds) the quantised items' x staged once per row tile in LDS,
+// xbytes = quant_x_lds_bytes(largest quantised K) of dynamic LDS per
+// workgroup; plain items read x directly either way.
 bool quant_shape_supported(const Shape &s);
 hipError_t launch_sweep_quant(const Shape &s, const DevItem *items, const DevTile *tiles,
-                              int ntiles, int grid, hipStream_t st);
-hipError_t launch_item_quant(const Shape &s, const DevItem &item, hipStream_t st);
+                              int ntiles, int grid, int xbytes, hipStream_t st);
+hipError_t launch_item_quant(const Shape &s, const DevItem &item, int xbytes, hipStream_t st);
+
+// LDS bytes for x of K columns in the quantised kernels' layout: whole
+// 1 KiB blocks of 256 columns (the staging loads' unit; the ragged last load
+// of a row reads at most to the end of its 32-column run).
+inline int64_t quant_x_lds_bytes(int64_t K) { return (K + 255) / 256 * 1024; }
 
 // Several x vectors per item (B = 2, 4, 8 or 16 >= every item's nrhs;
 // direct-x).  Shapes with R >= 8 run on the matrix cores (any B); wmode tells

@@ -27,6 +27,18 @@ namespace {
 //
 // Short rows: a wavefront splits into 64 / G groups of G lanes, one row per
 // group (G from quant_lanes), so a 384-byte row still fills its lanes.
+//
+// x, direct or through LDS.  All 64 / G groups of a wavefront read the same
+// x, and each lane reads 128 bytes of it per 16-byte code load (4-bit), so x
+// load instructions are as many as code loads.  With x staged in LDS (XL)
+// they leave the vector-memory path to the codes: each workgroup copies the
+// row tile's x into LDS once, by buffer loads that write LDS themselves
+// (1 KiB per wavefront load, no VGPRs, one wait), between two barriers, and
+// the lanes read it from there.  Within each 1 KiB block the 16-byte pieces
+// of each 128-byte row r are XOR-swizzled (piece t stored at t ^ r), so the
+// lanes of a group, whose x runs start 128 (4-bit) or 64 (8-bit) bytes
+// apart, read 8 distinct 16-byte bank groups per step.
+#define TVL_LDS __attribute__((address_space(3)))
 __device__ __forceinline__ float sbyte(unsigned v, int b) { return (float)(int)(signed char)(v >> (8 * b)); }
 
 // 8-bit: sum_j q_j x_j over the 16 columns of one 16-byte weight vector
@@ -93,7 +105,16 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, in
 }
 constexpr int kBufNT = 2; // cache policy: non-temporal (streamed once)
 
-template <int BITS, int G, int R, int U>
+// the f4 of x at column col (a multiple of 4) in the swizzled LDS layout:
+// f4 j lives at 16-byte slot (j with its low 3 bits XORed by bits 5:3)
+__device__ __forceinline__ f4 lds_x4(const TVL_LDS float *xl, int col)
+{
+    const int j = col >> 2;
+    const int slot = (j & ~7) | ((j ^ (j >> 3)) & 7);
+    return *(const TVL_LDS f4 *)(xl + 4 * slot);
+}
+
+template <int BITS, int G, int R, int U, bool XL = false>
 struct QuantRows {
     static constexpr int N = 128 / BITS;       // columns per 16-byte load
     static constexpr int NX = N / 4;           // float4 of x per load
@@ -109,6 +130,7 @@ struct QuantRows {
     int sblk;                          // bytes between 4-row blocks of the scale plane
     int vx;
     int kn, nv, nfull, seg;
+    const TVL_LDS float *xl; // XL: the tile's x in LDS
 
     // lrow[r]: the lane's r-th row relative to the wave's first row (in range:
     // rows past M are clamped by the caller); srow0: the lane's first row in
@@ -117,11 +139,11 @@ struct QuantRows {
     __device__ __forceinline__ QuantRows(const unsigned char *codes0, int64_t code_bytes,
                                          const float *plane, int64_t plane_bytes, int64_t ldw,
                                          int ng, const int (&lrow)[R], int srow0, const float *x,
-                                         int K, int seg_)
+                                         int K, int seg_, const TVL_LDS float *xl_ = nullptr)
         : wr(make_rsrc(codes0, code_bytes)), sr(make_rsrc(plane, plane_bytes)),
           xr(make_rsrc(x, ((int64_t)K * 4 + 15) & ~(int64_t)15)),
           vs(16 * ((srow0 / 4) * ng + seg_ * N / 64) + 4 * (srow0 % 4)), sblk(16 * ng),
-          vx(seg_ * N * 4), kn(K), nv((K + N - 1) / N), nfull(K / CH), seg(seg_)
+          vx(seg_ * N * 4), kn(K), nv((K + N - 1) / N), nfull(K / CH), seg(seg_), xl(xl_)
     {
 #pragma unroll
         for (int r = 0; r < R; ++r)
@@ -156,13 +178,21 @@ struct QuantRows {
     }
     __device__ __forceinline__ f4 xload(int c, int k) const
     {
-        return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(xr, vx + 16 * k, c * XB, 0));
+        if constexpr (XL)
+            return lds_x4(xl, c * CH + seg * N + 4 * k);
+        else
+            return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(xr, vx + 16 * k, c * XB, 0));
     }
     // The same load with the whole offset in the range-checked VGPR part:
-    // past the end of x (rounded to 16 bytes) it returns zeros, no branch.
+    // past the end of x (rounded to 16 bytes) it returns zeros, no branch
+    // (XL: past K the staged segment holds what the last 16-byte load of x
+    // brought, and the caller masks it).
     __device__ __forceinline__ f4 xload_checked(int c, int k) const
     {
-        return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(xr, vx + 16 * k + c * XB, 0, 0));
+        if constexpr (XL)
+            return lds_x4(xl, c * CH + seg * N + 4 * k);
+        else
+            return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(xr, vx + 16 * k + c * XB, 0, 0));
     }
 
     __device__ __forceinline__ void accumulate(float &acc, const u4 w, float sc, const f4 (&xv)[NX]) const
@@ -197,10 +227,9 @@ struct QuantRows {
         }
     }
 
-    // Full chunks in batches of U (all loads of a batch issued first).
-    __device__ __forceinline__ void run_batched(float (&acc)[R]) const
+    // Full chunks from c in batches of U (all loads of a batch issued first).
+    __device__ __forceinline__ void run_batched(float (&acc)[R], int c = 0) const
     {
-        int c = 0;
         for (; c + U <= nfull; c += U) {
             u4 w[U][R];
             float sc[U][R];
@@ -228,6 +257,25 @@ struct QuantRows {
     __device__ __forceinline__ void run(float (&acc)[R]) const
     {
         run_batched(acc);
+        run_tail(acc);
+    }
+
+    // U = 1, chunk 0's codes already loaded (w0, sc0; when nfull > 0)
+    __device__ __forceinline__ void run_preloaded(float (&acc)[R], const u4 (&w0)[R],
+                                                  const float (&sc0)[R]) const
+    {
+        static_assert(U == 1, "one chunk per batch");
+        if (nfull > 0) { // wavefront-uniform
+            f4 xv[NX];
+            load_x(0, xv);
+            compute(acc, w0, sc0, xv);
+            run_batched(acc, 1);
+        }
+        run_tail(acc);
+    }
+
+    __device__ __forceinline__ void run_tail(float (&acc)[R]) const
+    {
         const int c = nfull;
         if (c * G < nv) { // ragged last chunk: x past kn is zero (codes are finite)
             const int v = c * G + seg;
@@ -263,8 +311,32 @@ __device__ __forceinline__ float reduce_group(float (&v)[R], int lane)
 // One quantised row tile: WV wavefronts, each 64 / G row groups x R rows.
 // Group p of a wavefront takes the R consecutive rows wrow0 + p * R + r, so
 // its R scales of a group sit side by side in the scale plane's 4-row blocks.
-template <int BITS, int G, int R, int WV, int U>
-__device__ __forceinline__ void tile_quant_g(const DevItem &it, int row0)
+// XL: copy x[0, K) into the workgroup's LDS (the layout of lds_x4), then a
+// barrier before this tile's readers (the caller has taken one after the
+// previous tile's); every wavefront of the workgroup takes both.  Wavefront
+// w loads 1 KiB blocks w, w + WV, ...: lane l = 8 r + t of a block's load
+// fills slot l with f4 8 r + (t ^ r) of the block.  The descriptor covers K
+// rounded up to 16 bytes, as for direct x: the last piece may hold up to 3
+// values past K (the ragged last chunk masks them), and pieces past it read
+// as zeros.
+template <int WV>
+__device__ __forceinline__ void stage_x_quant(const DevItem &it, TVL_LDS float *xl)
+{
+    const __amdgpu_buffer_rsrc_t xr = make_rsrc(it.x, ((int64_t)it.K * 4 + 15) & ~(int64_t)15);
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int r = lane >> 3, t = lane & 7;
+    const int voff = 16 * (8 * r + (t ^ r));
+    const int nblk = (it.K + 255) / 256;
+    for (int b = wave; b < nblk; b += WV) // wavefront-uniform
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (TVL_LDS void *)(xl + 256 * b), 16, voff,
+                                                 1024 * b, 0, 0);
+    __builtin_amdgcn_s_waitcnt(0x0F70); // vmcnt(0): the LDS writes of these loads
+    __syncthreads();
+}
+
+template <int BITS, int G, int R, int WV, int U, bool XL>
+__device__ __forceinline__ void tile_quant_g(const DevItem &it, int row0, TVL_LDS float *xl)
 {
     constexpr int P = kWave / G;
     int lane = threadIdx.x & (kWave - 1);
@@ -275,7 +347,15 @@ __device__ __forceinline__ void tile_quant_g(const DevItem &it, int row0)
     asm volatile("" : "+v"(lane));
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int wrow0 = row0 + wave * (P * R);
-    if (wrow0 >= it.M) return;
+    if constexpr (XL) {
+        __syncthreads(); // the previous tile's readers of x are done
+        if (wrow0 >= it.M) { // wavefront-uniform: no rows, but its share of x
+            stage_x_quant<WV>(it, xl);
+            return;
+        }
+    } else if (wrow0 >= it.M) {
+        return;
+    }
     const int sub = lane / G, seg = lane % G;
     const unsigned char *codes = static_cast<const unsigned char *>(it.W);
     const int Mp = (it.M + 3) / 4 * 4;
@@ -290,10 +370,24 @@ __device__ __forceinline__ void tile_quant_g(const DevItem &it, int row0)
     for (int r = 0; r < R; ++r)
         acc[r] = 0.f;
     const int ng = (it.K + 63) / 64;
-    const QuantRows<BITS, G, R, U> qr(codes + (int64_t)wrow0 * it.ldw, (int64_t)rows_left * it.ldw,
-                                      plane, (int64_t)4 * Mp * ng, it.ldw, ng, lrow,
-                                      wrow0 + sub * R, it.x, it.K, seg);
-    qr.run(acc);
+    const QuantRows<BITS, G, R, U, XL> qr(codes + (int64_t)wrow0 * it.ldw,
+                                          (int64_t)rows_left * it.ldw, plane, (int64_t)4 * Mp * ng,
+                                          it.ldw, ng, lrow, wrow0 + sub * R, it.x, it.K, seg, xl);
+    if constexpr (XL) {
+        // the first chunk's codes in flight while x is staged (the wait for
+        // the x loads, issued after them, covers both).  Loaded whether or
+        // not the row has a full chunk (then unused): a 16-byte load per row
+        // at the lane's offset, inside the range-checked descriptor.
+        u4 w0[R];
+        float sc0[R];
+        qr.load_codes(0, w0, sc0);
+        __builtin_amdgcn_sched_barrier(0);
+        stage_x_quant<WV>(it, xl);
+        __builtin_amdgcn_sched_barrier(0);
+        qr.run_preloaded(acc, w0, sc0);
+    } else {
+        qr.run(acc);
+    }
     const float v = reduce_group<R, G>(acc, lane);
     constexpr int S = G / R; // lanes holding each row's total
     if (seg % S == 0) {
@@ -302,66 +396,74 @@ __device__ __forceinline__ void tile_quant_g(const DevItem &it, int row0)
     }
 }
 
-template <int BITS, int R, int WV, int U>
-__device__ __forceinline__ void tile_quant(const DevItem &it, int row0)
+template <int BITS, int R, int WV, int U, bool XL>
+__device__ __forceinline__ void tile_quant(const DevItem &it, int row0, TVL_LDS float *xl)
 {
     switch (it.lanes) {
-    case 8: tile_quant_g<BITS, 8, R, WV, U>(it, row0); break;
-    case 16: tile_quant_g<BITS, 16, R, WV, U>(it, row0); break;
-    case 32: tile_quant_g<BITS, 32, R, WV, U>(it, row0); break;
-    default: tile_quant_g<BITS, 64, R, WV, U>(it, row0); break;
+    case 8: tile_quant_g<BITS, 8, R, WV, U, XL>(it, row0, xl); break;
+    case 16: tile_quant_g<BITS, 16, R, WV, U, XL>(it, row0, xl); break;
+    case 32: tile_quant_g<BITS, 32, R, WV, U, XL>(it, row0, xl); break;
+    default: tile_quant_g<BITS, 64, R, WV, U, XL>(it, row0, xl); break;
     }
 }
 
-// Any plain item (fp32, fp16, 8-bit or 4-bit weights), direct-x.
-template <int R, int WV, int U>
-__device__ __forceinline__ void tile_plain_any(const DevItem &it, int row0)
+// Any plain item (fp32, fp16, 8-bit or 4-bit weights); XL: the quantised
+// ones with x in LDS (the others read x directly).  The choice depends only
+// on the item: every wavefront of a workgroup takes the same path.
+template <int R, int WV, int U, bool XL>
+__device__ __forceinline__ void tile_plain_any(const DevItem &it, int row0, TVL_LDS float *xl)
 {
     switch (it.dtype) {
-    case 3: tile_quant<4, R, WV, U>(it, row0); break;
-    case 2: tile_quant<8, R, WV, U>(it, row0); break;
+    case 3: tile_quant<4, R, WV, U, XL>(it, row0, xl); break;
+    case 2: tile_quant<8, R, WV, U, XL>(it, row0, xl); break;
     case 1: tile_fused<_Float16, R, WV, U, false, false>(it, row0); break;
     default: tile_fused<float, R, WV, U, false, false>(it, row0); break;
     }
 }
 
-template <int R, int WV, int U>
+// XL: dynamic LDS of quant_x_lds_bytes(largest quantised K) per workgroup
+template <int R, int WV, int U, bool XL>
 __global__ __launch_bounds__(WV *kWave) void k_sweep_quant(const DevItem *__restrict__ items,
                                                             const DevTile *__restrict__ tiles,
                                                             int ntiles)
 {
-    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    extern __shared__ f4 qx_lds[];
+    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) { // workgroup-uniform
         const DevTile tl = tiles[t];
         const DevItem it = items[tl.item];
-        tile_plain_any<R, WV, U>(it, tl.row0);
+        tile_plain_any<R, WV, U, XL>(it, tl.row0, (TVL_LDS float *)qx_lds);
         __builtin_amdgcn_s_waitcnt(0x0F70); // as in k_sweep
     }
 }
 
-template <int R, int WV, int U>
+template <int R, int WV, int U, bool XL>
 __global__ __launch_bounds__(WV *kWave) void k_item_quant(const DevItem it)
 {
-    tile_plain_any<R, WV, U>(it, (int)blockIdx.x * (R * WV * (kWave / it.lanes)));
+    extern __shared__ f4 qx_lds[];
+    tile_plain_any<R, WV, U, XL>(it, (int)blockIdx.x * (R * WV * (kWave / it.lanes)),
+                                 (TVL_LDS float *)qx_lds);
 }
 
-// (R, waves per block, U) for plans holding block-quantised weights.
+// (R, waves per block, U) for plans holding block-quantised weights:
+// direct-x, and with x staged in LDS.
 #define TVL_QUANT_SHAPES(X)                                                                       \
     X(2, 4, 2) X(4, 4, 1) X(4, 4, 2) X(4, 1, 2) X(8, 4, 1) X(8, 2, 1)
+#define TVL_QUANT_LDS_SHAPES(X) X(4, 4, 1) X(8, 4, 1) X(8, 2, 1)
 
-template <int R, int WV, int U>
+template <int R, int WV, int U, bool XL>
 struct InstQuant {
     static hipError_t sweep(const DevItem *items, const DevTile *tiles, int ntiles, int grid,
-                            hipStream_t st)
+                            int xbytes, hipStream_t st)
     {
-        hipLaunchKernelGGL((k_sweep_quant<R, WV, U>), dim3(grid), dim3(WV * kWave), 0, st, items,
-                           tiles, ntiles);
+        hipLaunchKernelGGL((k_sweep_quant<R, WV, U, XL>), dim3(grid), dim3(WV * kWave),
+                           XL ? xbytes : 0, st, items, tiles, ntiles);
         return hipGetLastError();
     }
-    static hipError_t item(const DevItem &it, hipStream_t st)
+    static hipError_t item(const DevItem &it, int xbytes, hipStream_t st)
     {
         const int rows = R * WV * (kWave / it.lanes);
         const dim3 grid((it.M + rows - 1) / rows), block(WV * kWave);
-        hipLaunchKernelGGL((k_item_quant<R, WV, U>), grid, block, 0, st, it);
+        hipLaunchKernelGGL((k_item_quant<R, WV, U, XL>), grid, block, XL ? xbytes : 0, st, it);
         return hipGetLastError();
     }
 };
@@ -371,28 +473,43 @@ struct InstQuant {
 bool quant_shape_supported(const Shape &s)
 {
 #define X(R_, W_, U_)                                                                             \
-    if (s.R == R_ && s.W == W_ && s.U == U_) return s.xmode == kXDirect;
+    if (s.xmode == kXDirect && s.R == R_ && s.W == W_ && s.U == U_) return true;
     TVL_QUANT_SHAPES(X)
+#undef X
+#define X(R_, W_, U_)                                                                             \
+    if (s.xmode == kXLds && s.R == R_ && s.W == W_ && s.U == U_) return true;
+    TVL_QUANT_LDS_SHAPES(X)
 #undef X
     return false;
 }
 
 hipError_t launch_sweep_quant(const Shape &s, const DevItem *items, const DevTile *tiles,
-                              int ntiles, int grid, hipStream_t st)
+                              int ntiles, int grid, int xbytes, hipStream_t st)
 {
 #define X(R_, W_, U_)                                                                             \
-    if (s.R == R_ && s.W == W_ && s.U == U_)                                                     \
-        return InstQuant<R_, W_, U_>::sweep(items, tiles, ntiles, grid, st);
+    if (s.xmode == kXDirect && s.R == R_ && s.W == W_ && s.U == U_)                              \
+        return InstQuant<R_, W_, U_, false>::sweep(items, tiles, ntiles, grid, 0, st);
     TVL_QUANT_SHAPES(X)
+#undef X
+#define X(R_, W_, U_)                                                                             \
+    if (s.xmode == kXLds && s.R == R_ && s.W == W_ && s.U == U_)                                 \
+        return InstQuant<R_, W_, U_, true>::sweep(items, tiles, ntiles, grid, xbytes, st);
+    TVL_QUANT_LDS_SHAPES(X)
 #undef X
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_item_quant(const Shape &s, const DevItem &item, hipStream_t st)
+hipError_t launch_item_quant(const Shape &s, const DevItem &item, int xbytes, hipStream_t st)
 {
 #define X(R_, W_, U_)                                                                             \
-    if (s.R == R_ && s.W == W_ && s.U == U_) return InstQuant<R_, W_, U_>::item(item, st);
+    if (s.xmode == kXDirect && s.R == R_ && s.W == W_ && s.U == U_)                              \
+        return InstQuant<R_, W_, U_, false>::item(item, 0, st);
     TVL_QUANT_SHAPES(X)
+#undef X
+#define X(R_, W_, U_)                                                                             \
+    if (s.xmode == kXLds && s.R == R_ && s.W == W_ && s.U == U_)                                 \
+        return InstQuant<R_, W_, U_, true>::item(item, xbytes, st);
+    TVL_QUANT_LDS_SHAPES(X)
 #undef X
     return hipErrorInvalidValue;
 }

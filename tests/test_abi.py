@@ -162,7 +162,11 @@ REJECTS = [
     (dict(W=0), NULL), (dict(x=0), NULL), (dict(y=0), NULL),
     (dict(dt=4), DTYPE), (dict(dt=-1), DTYPE),
     (dict(dt=2, ldw=640), SHAPE), (dict(dt=3, ldw=256), SHAPE), (dict(dt=2, ldw=896, tuning=dict(ksplit=2)), ARG),
-    (dict(dt=3, ldw=512, tuning=dict(flags=1)), ARG),
+    # quantised weights with x in LDS: only (4,4,1) (8,4,1) (8,2,1), and x of
+    # K columns in whole KiB within 160 KB (K <= 40,960)
+    (dict(dt=3, ldw=512, tuning=dict(rows_per_wave=2, waves_per_block=4, unroll=2, flags=1)),
+     ARG),
+    (dict(dt=3, K=40961, ldw=20608, tuning=dict(flags=1)), SHAPE),
     (dict(dt=2, K=(1 << 24) + 128, ldw=(1 << 24) + 128), SHAPE),
     (dict(dt=3, ldw=(1 << 24) + 128), SHAPE),
     (dict(M=0), SHAPE), (dict(K=0), SHAPE), (dict(M=-5), SHAPE), (dict(M=1 << 31), SHAPE),
@@ -184,6 +188,23 @@ def test_gemv_rejects(kw, st, fn):
     assert gemv(fn=fn, **kw) == st
     assert tvl.tvl_last_error() != ""
     assert tvl.tvl_status_str(st).startswith(tvl.STATUS[st])
+
+
+def test_quantised_x_in_lds_accepted():
+    """Quantised weights with x in LDS pass validation up to the LDS limit and
+    reach the device query (no GPU here); a flag-only tuning keeps the default
+    rows and waves, which have an LDS-x form."""
+    for K, ldw in ((768, 384), (11008, 5504), (40960, 20480)):
+        for tuning in (dict(flags=1), dict(rows_per_wave=8, waves_per_block=2, unroll=1,
+                                           flags=1)):
+            assert gemv(dt=3, K=K, ldw=ldw, tuning=tuning) in (OK, HIP), (K, tuning)
+    arr, n = tvl.make_items([dict(W=A, ldw=5504, x=B, y=C, M=768, K=11008, dtype=3)])
+    h = ctypes.c_void_p()
+    t = tvl.tvl_tuning(flags=1)
+    assert L.tvl_sweep_plan_create(arr, n, ctypes.byref(t), ctypes.byref(h)) in (OK, HIP)
+    arr, n = tvl.make_items([dict(W=A, ldw=20608, x=B, y=C, M=8, K=40961, dtype=3)])
+    assert L.tvl_sweep_plan_create(arr, n, ctypes.byref(t), ctypes.byref(h)) == SHAPE
+    assert "LDS" in tvl.tvl_last_error()
 
 
 def test_alias_boundaries_are_exact():

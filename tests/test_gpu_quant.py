@@ -30,6 +30,7 @@ TOL = 1e-5
 DEV = "cuda"
 BITS = {tvl.TVL_Q8: 8, tvl.TVL_Q4: 4}
 QUANT_SHAPES = [(2, 4, 2), (4, 4, 1), (4, 4, 2), (4, 1, 2), (8, 4, 1), (8, 2, 1)]
+QUANT_LDS_SHAPES = [(4, 4, 1), (8, 4, 1), (8, 2, 1)]  # x staged in LDS (TVL_FLAG_X_LDS)
 RAGGED = [(1, 1), (3, 17), (17, 3), (64, 63), (65, 65), (257, 255), (1000, 1000), (33, 4095),
           (130, 11008), (5, 28672), (2048, 768), (768, 2048), (9, 2049), (31, 1023)]
 
@@ -86,6 +87,76 @@ def test_quant_shapes(shape, dt):
         yref, S = oracle.gemv_q(Wq, BITS[dt], ldw, M, K, x)
         t = dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
         check(run_item(Wq, ldw, dt, x, M, K, t), yref, S, f"{shape} {M}x{K}")
+
+
+@pytest.mark.parametrize("shape", QUANT_LDS_SHAPES,
+                         ids=[f"R{r}W{w}U{u}" for r, w, u in QUANT_LDS_SHAPES])
+@pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
+def test_quant_x_in_lds(shape, dt):
+    """x staged in LDS per row tile: ragged K (not a multiple of 4, 32 or a
+    chunk), every lane-group size (K = 255 .. 11008 gives G = 8 .. 64), rows
+    past M, and NaN in the floats right after x (the staging's last 16-byte
+    load brings them into LDS; the ragged last chunk must mask them)."""
+    r, w, u = shape
+    t = dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=1)
+    for M, K in ((37, 5000), (130, 768), (7, 4097), (70, 1536), (300, 640), (9, 11008),
+                 (1, 1), (3, 17), (65, 65), (257, 255), (33, 4095), (5, 2049), (31, 1023)):
+        Wq, ldw, x = quant_case(M * 31 + K + r * 100 + w, M, K, dt)
+        yref, S = oracle.gemv_q(Wq, BITS[dt], ldw, M, K, x)
+        Wd = tvl.upload_quant(Wq, M, K, dt, ldw, DEV)
+        xbuf = torch.full((64 + K + 64,), float("nan"), dtype=torch.float32, device=DEV)
+        xd = xbuf[64:64 + K]  # NaN right after x: staged, never used
+        xd.copy_(torch.from_numpy(x))
+        y = torch.full((M,), float("nan"), dtype=torch.float32, device=DEV)
+        tvl.tvl_gemv_ex(Wd.buf, ldw, dt, xd, y, M, K, t)
+        torch.cuda.synchronize()
+        check(y.cpu().numpy(), yref, S, f"LDS-x {shape} {M}x{K}")
+
+
+def test_quant_x_in_lds_plan_mixed():
+    """A plan of 8-bit, 4-bit, fp32 and fp16 items with only the LDS-x flag
+    set (default rows and waves): the quantised items read x from LDS, the
+    plain ones directly; every output, two runs, bit-identical."""
+    rng = np.random.default_rng(4242)
+    cases, items, keep = [], [], []
+    for i, (M, K, dt) in enumerate([(768, 768, tvl.TVL_Q8), (2048, 768, tvl.TVL_Q4),
+                                    (768, 2048, tvl.TVL_Q4), (33, 4095, tvl.TVL_Q8),
+                                    (500, 300, tvl.TVL_F32), (257, 255, tvl.TVL_F16),
+                                    (1, 1, tvl.TVL_Q4), (300, 11008, tvl.TVL_Q4)]):
+        x = rng.standard_normal(K).astype(np.float32)
+        if dt in BITS:
+            Wq, ldw, _ = quant_case(2000 + i, M, K, dt)
+            Wd = tvl.upload_quant(Wq, M, K, dt, ldw, DEV)
+            yref, S = oracle.gemv_q(Wq, BITS[dt], ldw, M, K, x)
+        else:
+            Wf = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+            if dt == tvl.TVL_F32:
+                Wd = tvl.upload_matrix(Wf, dt, DEV)
+                yref, S = oracle.gemv_f32(Wf, x)
+            else:
+                Wh = synth.f32_to_f16_bits(Wf)
+                Wd = tvl.upload_matrix(Wh, dt, DEV)
+                yref, S = oracle.gemv_f16(Wh, x)
+        xd = torch.from_numpy(x).to(DEV)
+        y = torch.full((M,), float("nan"), dtype=torch.float32, device=DEV)
+        keep.append((Wd, xd))
+        items.append((Wd.ptr, Wd.ldw, xd, y, M, K, dt))
+        cases.append((y, yref, S, f"item {i} {M}x{K} dt={dt}"))
+    plan = tvl.tvl_sweep_plan_create(items, dict(flags=1))
+    outs = []
+    try:
+        for rep in range(2):
+            for y, *_ in cases:
+                y.fill_(float("nan"))
+            plan.run()
+            torch.cuda.synchronize()
+            outs.append([y.cpu().numpy().copy() for y, *_ in cases])
+            for y, yref, S, what in cases:
+                check(y.cpu().numpy(), yref, S, f"LDS-x rep {rep} {what}")
+    finally:
+        plan.destroy()
+    for a, b, (_, _, _, what) in zip(outs[0], outs[1], cases):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), what
 
 
 @pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
