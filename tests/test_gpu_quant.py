@@ -113,6 +113,28 @@ def test_quant_x_in_lds(shape, dt):
         check(y.cpu().numpy(), yref, S, f"LDS-x {shape} {M}x{K}")
 
 
+@pytest.mark.parametrize("K", [16385, 28672, 40960])
+def test_quant_x_in_lds_large_k(K):
+    """x in LDS beyond 64 KB of dynamic LDS (K > 16,384) up to the 160 KB
+    limit (K = 40,960), 4-bit and 8-bit, single GEMV and plan."""
+    for dt in (tvl.TVL_Q4, tvl.TVL_Q8):
+        M = 67
+        Wq, ldw, x = quant_case(K + dt, M, K, dt)
+        yref, S = oracle.gemv_q(Wq, BITS[dt], ldw, M, K, x)
+        y = run_item(Wq, ldw, dt, x, M, K, dict(flags=1))
+        check(y, yref, S, f"LDS-x K={K} dt={dt}")
+        Wd = tvl.upload_quant(Wq, M, K, dt, ldw, DEV)
+        xd = torch.from_numpy(x).to(DEV)
+        yd = torch.full((M,), float("nan"), dtype=torch.float32, device=DEV)
+        plan = tvl.tvl_sweep_plan_create([(Wd.ptr, Wd.ldw, xd, yd, M, K, dt)], dict(flags=1))
+        try:
+            plan.run()
+            torch.cuda.synchronize()
+        finally:
+            plan.destroy()
+        check(yd.cpu().numpy(), yref, S, f"LDS-x plan K={K} dt={dt}")
+
+
 def test_quant_x_in_lds_plan_mixed():
     """A plan of 8-bit, 4-bit, fp32 and fp16 items with only the LDS-x flag
     set (default rows and waves): the quantised items read x from LDS, the
