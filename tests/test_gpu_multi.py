@@ -332,6 +332,36 @@ def test_split_x_wide_chunks():
         assert oracle.check(Y[b], refs[b][0], refs[b][1], 1e-5)["bad"] == 0, b
 
 
+@pytest.mark.parametrize("nb", [5, 8, 16])
+def test_split_x_forms_agree_bitwise(nb):
+    """The split-x forms compute the same per-vector scale, split and
+    matrix-core steps per chunk whether each wavefront splits x itself (U =
+    13x) or each splits a share once per block (U = 30x): for the same chunk
+    width every shape gives the same bits, including chunks that take the
+    fp32 path and the ragged last chunk."""
+    M, K = 300, 1000
+    rng = np.random.default_rng(77 + nb)
+    W = synth.f32_to_f16_bits((rng.standard_normal((M, K)) * 0.02).astype(np.float32))
+    X = rng.standard_normal((nb, K)).astype(np.float32)
+    X[0, 130] = 2.0 ** 50  # a wide chunk (128 columns: chunk 1; 64 columns: chunk 2)
+    X[nb - 1, 900:] *= 1e-30
+    buf, ldw = dev_matrix(W, 1)
+    for cc in (128, 64):
+        shapes = ([t for t in MFMA_HX if t[2] % 10 == (3 if cc == 128 else 2)]
+                  + [t for t in MFMA_XS if t[2] > 300 and t[2] % 10 == (3 if cc == 128 else 2)])
+        outs = []
+        for r, w, u in shapes:
+            Y = run(buf, ldw, 1, X, M, K, nb, M, dict(rows_per_wave=r, waves_per_block=w,
+                                                       unroll=u, flags=2))
+            outs.append(((r, w, u), Y.view(np.uint32).copy()))
+        for shape, Y in outs[1:]:
+            assert np.array_equal(Y, outs[0][1]), (cc, outs[0][0], shape)
+        refs = [oracle.gemv_f16(W, X[b]) for b in range(nb)]
+        Y = outs[0][1].view(np.float32)
+        for b in range(nb):
+            assert oracle.check(Y[b], refs[b][0], refs[b][1], 1e-5)["bad"] == 0, (cc, b)
+
+
 @pytest.mark.parametrize("ldx", [(1 << 27) - 64, 1 << 27], ids=["xs-limit", "fallback"])
 def test_multi_huge_x_stride(ldx):
     """x strides at the shared-x forms' limit (4 x vectors of one 64-column
