@@ -1608,10 +1608,14 @@ __device__ __forceinline__ float group_max(float v)
 // matrix-core steps: so each wavefront splits only vectors VPW w .. VPW w +
 // VPW - 1 (LPV lanes per vector, CPL columns per lane), one chunk ahead, from
 // x it loads into registers, and writes the two fp16 parts straight into the
-// B-operand layout in LDS (MFMA lane L = 16 g + j at 32-column step s finds
-// columns 32 s + 8 g .. + 7 of vector j at byte s * 1024 + 16 L of a part),
-// with each vector's 2^-k and a flag per wavefront for a chunk too wide for
-// the split (kSplitMin).  After the next step's barrier every wavefront reads
+// B-operand layout in LDS: MFMA lane L = 16 g + j at 32-column step s finds
+// columns 32 s + 8 g .. + 7 of vector j in the 256-byte row s * 4 + g of a
+// part, at 16-byte slot j ^ h(s, g), h = (4 s + g) * 4 / NS.  Without the XOR
+// the 16 lanes writing one vector's columns would all hit one slot position
+// (16-way bank conflicts); with it writers and readers each touch 16
+// distinct slots per 256 bytes (checked on the CPU for every shape).  With
+// the parts go each vector's 2^-k and a flag per wavefront for a chunk too
+// wide for the split (kSplitMin).  After the next step's barrier every wavefront reads
 // its B operands there.  Each value is scaled and split exactly as in the
 // per-wavefront form (the same per-vector maximum), and the matrix-core
 // steps are the same, so the results are the same bit for bit; a chunk any
@@ -1646,8 +1650,16 @@ struct MfmaXsHxRows : MfmaDmaRows<_Float16, RG, CC, 3, true> {
     int64_t ldx;
     int nb, wave;
     TVL_LDS char *hl; // the block's two split stages
-    const float *xs; // this lane's vector (clamped to nb - 1) at its first column
-    int woff;        // byte offset of the lane's first column in a part
+    const float *xs;             // this lane's vector (clamped to nb - 1) at its first column
+    static constexpr int PC = CPL < 8 ? CPL : 8; // columns per LDS write
+    int woff[CPL / PC];          // byte offset in a part of each write of the lane
+    int roff[NS];                // byte offset in a part of the B operand of each step
+
+    // the 16-byte slot of (step s, 8-column group g, vector v) in a part
+    static __device__ __forceinline__ int slot(int s, int g, int v)
+    {
+        return s * 1024 + g * 256 + 16 * (v ^ ((4 * s + g) * (4 / NS)));
+    }
 
     __device__ __forceinline__ MfmaXsHxRows(const _Float16 *W_, int64_t ldw_, int wrow0, int M,
                                             const float *x, int64_t ldx_, int nb_, int K,
@@ -1660,7 +1672,14 @@ struct MfmaXsHxRows : MfmaDmaRows<_Float16, RG, CC, 3, true> {
         // form: same scale and range decisions, columns never stored
         const int v = VPW * wave_ + lane_ / LPV, col = (lane_ % LPV) * CPL;
         xs = x + (int64_t)min(v, nb_ - 1) * ldx_ + col;
-        woff = (col / 32) * 1024 + (16 * ((col % 32) / 8) + v) * 16 + 2 * (col % 8);
+#pragma unroll
+        for (int p = 0; p < CPL / PC; ++p) { // the next 8 columns: group g + 1
+            const int c8 = col + p * PC;
+            woff[p] = slot(c8 / 32, (c8 % 32) / 8, v) + 2 * (c8 % 8);
+        }
+#pragma unroll
+        for (int q = 0; q < NS; ++q)
+            roff[q] = slot(q, lane_ >> 4, lane_ & 15);
     }
 
     // this lane's x of chunk c
@@ -1708,7 +1727,6 @@ struct MfmaXsHxRows : MfmaDmaRows<_Float16, RG, CC, 3, true> {
             ((TVL_LDS float *)(hb + HSCALE))[VPW * wave + lane / LPV] = __builtin_ldexpf(1.f, -k);
         // hi = f16(x 2^k), lo = f16(x 2^k - hi), CPL values, in pieces of up
         // to 8 columns (one B-operand slot each)
-        constexpr int PC = CPL < 8 ? CPL : 8;
 #pragma unroll
         for (int p = 0; p < CPL / PC; ++p) {
             _Float16 hv[PC], lv[PC];
@@ -1719,7 +1737,7 @@ struct MfmaXsHxRows : MfmaDmaRows<_Float16, RG, CC, 3, true> {
                 hv[e] = vh;
                 lv[e] = (_Float16)__builtin_fmaf(xv, sc, -(float)vh);
             }
-            const int off = woff + p * 256; // the next 8 columns: slot g + 1
+            const int off = woff[p];
             if constexpr (PC == 8) {
                 *(TVL_LDS h8 *)(hb + off) = h8{hv[0], hv[1], hv[2], hv[3], hv[4], hv[5], hv[6], hv[7]};
                 *(TVL_LDS h8 *)(hb + HPART + off) =
@@ -1781,8 +1799,8 @@ struct MfmaXsHxRows : MfmaDmaRows<_Float16, RG, CC, 3, true> {
             for (int q = 0; q < NS; ++q) {
                 const h8 a = *(const TVL_LDS h8 *)(this->lds + ST * STAGE + rg * 16 * Base::RB +
                                                   this->raddr[q]);
-                const h8 hi = *(const TVL_LDS h8 *)(hb + q * 1024 + 16 * lane);
-                const h8 lo = *(const TVL_LDS h8 *)(hb + HPART + q * 1024 + 16 * lane);
+                const h8 hi = *(const TVL_LDS h8 *)(hb + roff[q]);
+                const h8 lo = *(const TVL_LDS h8 *)(hb + HPART + roff[q]);
                 t = mfma16h(a, hi, t);
                 t = mfma16h(a, lo, t);
             }
