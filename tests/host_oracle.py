@@ -21,7 +21,7 @@ _POOL = None
 
 
 def host_threads() -> int:
-    """Threads this process may use (the machine's CPU share), at most 16."""
+    """Threads this process may use (its CPU affinity), at most 16."""
     try:
         n = len(os.sched_getaffinity(0))
     except AttributeError:
