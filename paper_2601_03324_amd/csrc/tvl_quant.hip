@@ -318,7 +318,7 @@ __device__ __forceinline__ float reduce_group(float (&v)[R], int lane)
 // fills slot l with f4 8 r + (t ^ r) of the block.  The descriptor covers K
 // rounded up to 16 bytes, as for direct x: the last piece may hold up to 3
 // values past K (the ragged last chunk masks them), and pieces past it read
-// as zeros.
+// as zeros without touching memory.
 template <int WV>
 __device__ __forceinline__ void stage_x_quant(const DevItem &it, TVL_LDS float *xl)
 {
@@ -328,9 +328,11 @@ __device__ __forceinline__ void stage_x_quant(const DevItem &it, TVL_LDS float *
     const int r = lane >> 3, t = lane & 7;
     const int voff = 16 * (8 * r + (t ^ r));
     const int nblk = (it.K + 255) / 256;
+    // (the block offset goes in the per-lane offset, which the descriptor's
+    // range check covers; the scalar offset is not checked)
     for (int b = wave; b < nblk; b += WV) // wavefront-uniform
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (TVL_LDS void *)(xl + 256 * b), 16, voff,
-                                                 1024 * b, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (TVL_LDS void *)(xl + 256 * b), 16,
+                                                 voff + 1024 * b, 0, 0, 0);
     __builtin_amdgcn_s_waitcnt(0x0F70); // vmcnt(0): the LDS writes of these loads
     __syncthreads();
 }
