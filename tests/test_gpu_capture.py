@@ -17,6 +17,7 @@ import numpy as np
 import pytest
 
 import oracle
+import synth
 
 pytestmark = pytest.mark.gpu
 
@@ -110,3 +111,53 @@ def test_capture_survives_eviction_and_workspace_growth():
     del g
     torch.cuda.synchronize()
     tvl.tvl_release_workspaces()
+
+
+def test_capture_quantised_x_in_lds():
+    """A plan of 4-bit and 8-bit items with x staged in LDS (dynamic LDS per
+    launch) captured into a HIP graph: every replay, with eager work and
+    synchronisations between replays, equals the eager result bit for bit."""
+    rng = np.random.default_rng(31)
+    s = torch.cuda.Stream()
+    sid = int(s.cuda_stream)
+    items, outs, keep = [], [], []
+    for M, K, dt in ((300, 4096, tvl.TVL_Q4), (129, 11008, tvl.TVL_Q4), (77, 768, tvl.TVL_Q8)):
+        w = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+        bits = 4 if dt == tvl.TVL_Q4 else 8
+        ldw = tvl.tvl_row_stride(K, dt)
+        Wq = synth.quantize_rows(w, bits, ldw=ldw)
+        Wd = tvl.upload_quant(Wq, M, K, dt, ldw, DEV)
+        x = rng.standard_normal(K).astype(np.float32)
+        xd = torch.from_numpy(x).to(DEV)
+        y = torch.full((M,), float("nan"), device=DEV)
+        keep.append((Wd, xd, Wq, x, M, K, bits, ldw))
+        items.append((Wd.ptr, Wd.ldw, xd, y, M, K, dt))
+        outs.append(y)
+    plan = tvl.tvl_sweep_plan_create(items, dict(flags=1))
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        plan.run(sid)
+    s.synchronize()
+    eager = [y.clone() for y in outs]
+    for (_, _, Wq, x, M, K, bits, ldw), y in zip(keep, eager):
+        yref, S = oracle.gemv_q(Wq, bits, ldw, M, K, x)
+        assert oracle.check(y.cpu().numpy(), yref, S, 1e-5)["bad"] == 0, (M, K, bits)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        plan.run(sid)
+    for rep in range(3):
+        for y in outs:
+            y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for y, e in zip(outs, eager):
+            assert torch.equal(y, e), rep
+        with torch.cuda.stream(s):  # eager work between replays
+            plan.run(sid)
+        s.synchronize()
+        for y, e in zip(outs, eager):
+            assert torch.equal(y, e), rep
+    del g
+    torch.cuda.synchronize()
+    plan.destroy()
