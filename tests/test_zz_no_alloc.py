@@ -110,3 +110,26 @@ def test_noalloc_rejects_splits_beyond_the_scratch(M, tuning):
     assert b"static scratch" in tvl.lib.tvl_last_error()
     torch.cuda.synchronize()
     assert torch.isnan(y).all()  # nothing was enqueued
+
+
+@pytest.mark.parametrize("dt,tuning", [(3, dict(flags=1)), (3, None), (2, None)],
+                         ids=["q4-x-in-lds", "q4", "q8"])
+def test_noalloc_quantised(dt, tuning):
+    """Quantised weights need no scratch: tvl_gemv_noalloc gives the same
+    bits as tvl_gemv_ex (x staged in LDS: dynamic LDS, not an allocation),
+    two calls, the second smaller, both within the oracle's bar."""
+    import synth
+    bits = 4 if dt == 3 else 8
+    for n, (M, K) in enumerate(((640, 4096), (70, 1000))):
+        log(f"noalloc quantised: call {n + 1}: M={M} K={K} dtype={dt} tuning={tuning}")
+        rng = np.random.default_rng(M + K + dt)
+        w = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+        ldw = tvl.tvl_row_stride(K, dt)
+        Wq = synth.quantize_rows(w, bits, ldw=ldw)
+        Wd = tvl.upload_quant(Wq, M, K, dt, ldw, DEV)
+        x = rng.standard_normal(K).astype(np.float32)
+        y_ex = run(tvl.tvl_gemv_ex, Wd.buf, ldw, dt, x, M, K, tuning)
+        y_na = run(tvl.tvl_gemv_noalloc, Wd.buf, ldw, dt, x, M, K, tuning)
+        assert np.array_equal(y_ex.view(np.uint32), y_na.view(np.uint32)), (M, K, dt)
+        yref, S = oracle.gemv_q(Wq, bits, ldw, M, K, x)
+        assert oracle.check(y_na, yref, S, 1e-5)["bad"] == 0, (M, K, dt)
