@@ -1076,6 +1076,10 @@ typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 // x.  For x ~ N(0, 1), ~0.3 % of 128-column chunks of 16 vectors take the
 // fp32 path (each costs four times the matrix-core steps of a split chunk).
 constexpr float kSplitMin = 0x1p-7f;
+// (The range test reads each x value's bits with __float_as_uint on the
+// element's value: this compiler lowers __builtin_bit_cast of a vector
+// element such as xb[q][e] to the bits of element 0, which would test only
+// every fourth column.)
 
 __device__ __forceinline__ f4 mfma16h(h8 a, h8 b, f4 c)
 {
@@ -1256,7 +1260,7 @@ struct MfmaDmaRows {
             for (int q = 0; q < NQ; ++q)
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    mn = min(mn, (__builtin_bit_cast(uint32_t, xb[q][e]) << 1) - 2u);
+                    mn = min(mn, (__float_as_uint(xb[q][e]) << 1) - 2u);
             const bool wide = mn < (__builtin_bit_cast(uint32_t, thr) << 1) - 2u;
             if (__builtin_amdgcn_ballot_w64(wide) != 0) { // wave-uniform
                 // fp32 matrix cores: step e multiplies column 8 g + e of the
@@ -1716,7 +1720,7 @@ struct MfmaXsHxRows : MfmaDmaRows<_Float16, RG, CC, 3, true> {
             for (int u = 0; u < XL; ++u)
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    mn = min(mn, (__builtin_bit_cast(uint32_t, xr[u][e]) << 1) - 2u);
+                    mn = min(mn, (__float_as_uint(xr[u][e]) << 1) - 2u);
             wide = mn < (__builtin_bit_cast(uint32_t, thr) << 1) - 2u;
         }
         const int any = __builtin_amdgcn_ballot_w64(wide) != 0; // all lanes take part

@@ -332,6 +332,34 @@ def test_split_x_wide_chunks():
         assert oracle.check(Y[b], refs[b][0], refs[b][1], 1e-5)["bad"] == 0, b
 
 
+def test_split_x_wide_chunks_every_column_position():
+    """The range test must look at every column: chunks whose only small
+    nonzero entries sit at one position modulo 4 (1, 2, 3 or 0), beside one
+    huge entry under a zero weight and zeros elsewhere.  Split as is, the
+    small entries would round to zero (normalised error 1).  Every split-x
+    shape and the default, 16 vectors, fp32 bar."""
+    M, K, nb = 200, 1024, 16
+    rng = np.random.default_rng(4)
+    Wf = np.abs(rng.standard_normal((M, K)) * 0.02).astype(np.float32) + 1e-3
+    X = np.zeros((nb, K), np.float32)
+    for b in range(nb):
+        pos, c0 = b % 4, (b % 8) * 128  # one chunk of 128 (two of 64) per vector
+        big = c0 + (pos + 2) % 4  # the huge entry, never at the small ones' position
+        X[b, c0 + pos:c0 + 128:4] = 1.0 if b < 8 else 3e-3
+        X[b, big] = 2.0 ** 40 if b < 8 else 1e30
+        Wf[:, big] = 0.0
+        X[b, (c0 + 512) % K:(c0 + 512) % K + 128] = rng.standard_normal(128)  # a normal chunk
+    W = synth.f32_to_f16_bits(Wf)
+    refs = [oracle.gemv_f16(W, X[b]) for b in range(nb)]
+    buf, ldw = dev_matrix(W, 1)
+    for t in [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
+              for r, w, u in MFMA_HX + [t for t in MFMA_XS if t[2] > 300]] + [None]:
+        Y = run(buf, ldw, 1, X, M, K, nb, M, t)
+        for b in range(nb):
+            res = oracle.check(Y[b], refs[b][0], refs[b][1], 1e-5)
+            assert res["bad"] == 0, (t, b, b % 4, res)
+
+
 @pytest.mark.parametrize("nb", [5, 8, 16])
 def test_split_x_forms_agree_bitwise(nb):
     """The split-x forms compute the same per-vector scale, split and
