@@ -360,6 +360,35 @@ def test_split_x_wide_chunks_every_column_position():
             assert res["bad"] == 0, (t, b, b % 4, res)
 
 
+def test_split_x_extreme_finite_x():
+    """Every finite x: chunks near the fp32 maximum (3e38), of subnormals
+    (1e-39, 1e-44), of both beside ordinary values, and of zeros; small
+    weights keep every product and sum finite.  fp32 bar through every
+    split-x shape and the default, 16 vectors."""
+    M, K, nb = 100, 768, 16
+    rng = np.random.default_rng(5)
+    W = synth.f32_to_f16_bits((rng.standard_normal((M, K)) * 0.02).astype(np.float32))
+    X = rng.standard_normal((nb, K)).astype(np.float32)
+    X[0, :128] = 3e38 * np.sign(rng.standard_normal(128)).astype(np.float32)
+    X[1, :128] = np.float32(1e-39) * rng.standard_normal(128).astype(np.float32)
+    X[2, :128] = np.float32(1e-44)  # subnormals down to a few ulps of the smallest
+    X[3, 128:256] = 0.0
+    X[3, 130] = 3e38                 # the maximum beside zeros
+    X[4, 256:384] *= np.float32(1e-39)
+    X[4, 300] = 2.5e38               # subnormals beside the maximum: the fp32 path
+    X[5, 384:512] = np.float32(1.4e-45)  # the smallest subnormal
+    X[6] = 0.0
+    refs = [oracle.gemv_f16(W, X[b]) for b in range(nb)]
+    assert all(np.all(np.isfinite(r[0])) for r in refs)
+    buf, ldw = dev_matrix(W, 1)
+    for t in [dict(rows_per_wave=r, waves_per_block=w, unroll=u, flags=2)
+              for r, w, u in MFMA_HX + [t for t in MFMA_XS if t[2] > 300]] + [None]:
+        Y = run(buf, ldw, 1, X, M, K, nb, M, t)
+        for b in range(nb):
+            res = oracle.check(Y[b], refs[b][0], refs[b][1], 1e-5)
+            assert res["bad"] == 0, (t, b, res)
+
+
 @pytest.mark.parametrize("nb", [5, 8, 16])
 def test_split_x_forms_agree_bitwise(nb):
     """The split-x forms compute the same per-vector scale, split and
