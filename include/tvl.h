@@ -83,7 +83,10 @@ extern "C" {
  *                 (i/4)*4*ng + 4*g + i%4, ng = ceil(K/64), rows padded to
  *                 Mp = M rounded up to a multiple of 4 (entries of rows
  *                 i >= M are padding, never used);
- *   w_ij = s_{i,j/64} * q_ij        (converted exactly; fp32 accumulation).
+ *   w_ij = s_{i,j/64} * q_ij        (converted exactly; fp32 accumulation;
+ *                                    4-bit scales below 2^124: the 4-bit
+ *                                    kernels apply 16 s, so larger scales,
+ *                                    from weights beyond ~1.5e38, overflow).
  * Keeping the scales out of the code rows keeps every fetched 128-byte line
  * full; the 4-row blocks put the scales of 4 neighbouring rows side by side
  * (one 16-byte load) and the groups of a block in consecutive 16 bytes.  Code bytes past column K are

@@ -217,6 +217,31 @@ def test_quant_exact_on_integers(dt):
         assert np.array_equal(y.astype(np.float64), yref), f"{M}x{K}"
 
 
+@pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
+def test_quant_extreme_scales(dt):
+    """Huge weights (scales up to 1e37 / 7: the 4-bit kernels fold the codes'
+    1/16 into the scale, so a scale must stay below 2^124) with tiny x, and
+    tiny weights (subnormal scales) with huge x: every product and sum stays
+    finite and normal, so the results must meet the bar; default and every
+    shape (direct x and x in LDS)."""
+    rng = np.random.default_rng(9 + dt)
+    M, K = 64, 1000
+    tunings = [None] + [dict(rows_per_wave=r, waves_per_block=w_, unroll=u, flags=2)
+                        for r, w_, u in QUANT_SHAPES] + \
+        [dict(rows_per_wave=r, waves_per_block=w_, unroll=u, flags=1)
+         for r, w_, u in QUANT_LDS_SHAPES]
+    huge = np.clip(rng.standard_normal((M, K)) * 3e36, -1e37, 1e37).astype(np.float32)
+    tiny = (rng.standard_normal((M, K)) * 2e-38).astype(np.float32)
+    for w, xs in ((huge, 1e-8), (tiny, 1e30)):
+        x = (rng.standard_normal(K) * xs).astype(np.float32)
+        ldw = tvl.tvl_row_stride(K, dt)
+        Wq = synth.quantize_rows(w, BITS[dt], ldw=ldw)
+        yref, S = oracle.gemv_q(Wq, BITS[dt], ldw, M, K, x)
+        assert np.all(np.isfinite(yref))
+        for t in tunings:
+            check(run_item(Wq, ldw, dt, x, M, K, t), yref, S, f"extreme scales x~{xs} {t}")
+
+
 def test_quant_plan_mixed_with_float_items():
     """One plan over 8-bit, 4-bit, fp32 and fp16 items, run twice."""
     rng = np.random.default_rng(99)
