@@ -287,12 +287,13 @@ int multi_B(int n) { return n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16; }
 // LDS-staged and 3.68 for the direct-load form).  Launches with only fp16 weights (one
 // 70B-shaped layer), 5-16 vectors: the streamed form on the fp16 matrix
 // cores with x split in two fp16 parts once per block and shared by the
-// block's four wavefronts (16 rows each, 128-column chunks; 8 vectors: 5.94
-// TB/s against 5.61-5.75 for 2 or 8 wavefronts or 32 rows, 5.73 with x per
+// block's four wavefronts (16 rows each, 128-column chunks; 8 vectors: 6.15
+// TB/s against 5.67-5.98 for 2 or 8 wavefronts or 32 rows, 5.73 with x per
 // wavefront (32 rows), 4.64 on the fp32 matrix cores and 4.48 for 4 x 4 x 1;
-// 16: 5.80 against 4.84 with x per wavefront and 3.60 for the LDS-staged
-// form, where each converted fp16 chunk costs as many fp32 matrix-core steps
-// as an fp32 chunk of twice the bytes).  Launches mixing
+// 16: 6.01 against 5.68-5.82 for 2 or 8 wavefronts or 32 rows, 4.84 with x
+// per wavefront and 3.60 for the LDS-staged form, where each converted fp16
+// chunk costs as many fp32 matrix-core steps as an fp32 chunk of twice the
+// bytes).  Launches mixing
 // fp32 and fp16 weights: the streamed form with x per wavefront (32 rows)
 // with 5-8 vectors, the LDS-staged form with 16 rows beyond.
 Shape default_multi_shape(int B, bool all_f32, bool all_f16)
