@@ -1,6 +1,6 @@
-"""Launch shapes of the several-vector and fused kernels (include/tvl.h,
-tvl_tuning), shared by the GPU parity tests and the CPU check that the
-header, the library and the tests list the same shapes.
+"""Launch shapes of the several-vector, fused and quantised kernels
+(include/tvl.h, tvl_tuning), shared by the GPU parity tests and the CPU check
+that the header, the library and the tests list the same shapes.
 
 VALU form: (R, waves per block, U, B) with B x vectors per launch; matrix-core
 forms: (rows per wavefront, waves per block, U), any nrhs <= 16.
@@ -32,3 +32,7 @@ MFMA_XS = [(16, 4, 202), (32, 2, 202), (32, 4, 202), (16, 2, 203), (16, 4, 203),
 # launches holding RMSNorm or SwiGLU items: (R, waves per block, U), even R
 FUSED_SHAPES = [(2, 4, 2), (2, 4, 3), (2, 4, 4), (2, 1, 4), (4, 1, 2), (4, 1, 4), (4, 4, 2),
                 (2, 1, 8), (8, 4, 1), (8, 2, 1), (4, 4, 3)]
+# launches holding block-quantised items: (R, waves per block, U), direct x
+# and x staged in LDS (TVL_FLAG_X_LDS)
+QUANT_SHAPES = [(2, 4, 2), (4, 4, 1), (4, 4, 2), (4, 1, 2), (8, 4, 1), (8, 2, 1)]
+QUANT_LDS_SHAPES = [(4, 4, 1), (8, 4, 1), (8, 2, 1)]

@@ -17,6 +17,7 @@ import pytest
 
 import oracle
 import synth
+from multi_shapes import QUANT_LDS_SHAPES, QUANT_SHAPES  # direct x; x staged in LDS
 
 pytestmark = pytest.mark.gpu
 
@@ -29,8 +30,6 @@ from paper_2601_03324_amd import tvl  # noqa: E402
 TOL = 1e-5
 DEV = "cuda"
 BITS = {tvl.TVL_Q8: 8, tvl.TVL_Q4: 4}
-QUANT_SHAPES = [(2, 4, 2), (4, 4, 1), (4, 4, 2), (4, 1, 2), (8, 4, 1), (8, 2, 1)]
-QUANT_LDS_SHAPES = [(4, 4, 1), (8, 4, 1), (8, 2, 1)]  # x staged in LDS (TVL_FLAG_X_LDS)
 RAGGED = [(1, 1), (3, 17), (17, 3), (64, 63), (65, 65), (257, 255), (1000, 1000), (33, 4095),
           (130, 11008), (5, 28672), (2048, 768), (768, 2048), (9, 2049), (31, 1023)]
 
