@@ -86,6 +86,27 @@ def test_multi_vectors(M, K, dt, nrhs):
             assert r["bad"] == 0, (M, K, nrhs, b, t, r)
 
 
+@pytest.mark.parametrize("dt,nrhs", [(0, 16), (0, 3), (1, 8)], ids=["f32-16", "f32-3", "f16-8"])
+def test_multi_million_rows(dt, nrhs):
+    """2^20 + 3 rows of 72 columns (ragged) with several vectors, through the
+    library's default form (shared x on the matrix cores, the VALU form, and
+    split x on the fp16 matrix cores), every output of every vector against
+    the oracle."""
+    M, K = (1 << 20) + 3, 72
+    rng = np.random.default_rng((1 << 20) + 10 * dt + nrhs)
+    Wf = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    W = Wf if dt == 0 else synth.f32_to_f16_bits(Wf)
+    del Wf
+    X = rng.standard_normal((nrhs, K)).astype(np.float32)
+    refs = [host_oracle.gemv(W, X[b], dt) for b in range(nrhs)]
+    buf, ldw = dev_matrix(W, dt)
+    del W
+    Y = run(buf, ldw, dt, X, M, K, nrhs, M + 5, None)
+    for b in range(nrhs):
+        r = oracle.check(Y[b], refs[b][0], refs[b][1], TOL[dt])
+        assert r["bad"] == 0, (M, K, nrhs, b, r)
+
+
 def test_multi_matches_single_bitwise_on_integers():
     """Integer data: every vector's result is exact, so it equals the
     single-vector result bit for bit."""

@@ -314,6 +314,37 @@ def test_sweep110m_plan_batch_and_grid():
     plan.destroy()
 
 
+@pytest.mark.parametrize("dt", [0, 1], ids=["f32", "f16"])
+def test_two_million_rows_every_output(dt):
+    """2^21 + 17 rows of 40 columns (ragged, NaN in each row's padding): the
+    largest grids and tile tables of the tests (131,073 tiles of 16 rows in a
+    plan; single GEMVs in both x modes, 8 rows per wavefront and a K split
+    over all rows), every output against the oracle."""
+    M, K = (1 << 21) + 17, 40
+    rng = np.random.default_rng((1 << 21) + dt)
+    Wf = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    W = Wf if dt == 0 else synth.f32_to_f16_bits(Wf)
+    del Wf
+    x = rng.standard_normal(K).astype(np.float32)
+    yref, S = host_oracle.gemv(W, x, dt)
+    buf, ldw = dev_matrix(W, dt)
+    del W
+    for v in (None, dict(flags=1), dict(flags=2), dict(ksplit=2),
+              dict(rows_per_wave=8, waves_per_block=4, unroll=1, flags=2)):
+        log(f"{M} rows dt={dt} {vname(v)}")
+        y = run_gemv(buf, ldw, dt, x, M, K, v)
+        assert_parity(y, yref, S, dt, f"{M}x{K} {vname(v)}")
+    xd = torch.from_numpy(x).to(DEV)
+    yd = torch.full((M,), float("nan"), device=DEV)
+    plan = tvl.tvl_sweep_plan_create([(buf, ldw, xd, yd, M, K, dt)])
+    try:
+        plan.run()
+        torch.cuda.synchronize()
+        assert_parity(yd.cpu().numpy(), yref, S, dt, f"{M}x{K} plan {plan.info()}")
+    finally:
+        plan.destroy()
+
+
 def test_sweep_mixed_dtypes_and_ragged():
     rng = np.random.default_rng(11)
     specs = [(1, 1, 0), (3, 17, 1), (257, 255, 0), (65, 1000, 1), (1000, 65, 0),

@@ -181,6 +181,29 @@ def test_quant_x_in_lds_plan_mixed():
 
 
 @pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
+def test_quant_two_million_rows(dt):
+    """2^21 + 5 rows of 100 columns (two scale groups, the last one ragged;
+    a scale plane of 2,097,152 + 8 rows in 4-row blocks): the default, x in
+    LDS, another shape and a plan, every output against the oracle."""
+    M, K = (1 << 21) + 5, 100
+    log(f"quant {M} rows dtype={dt}")
+    Wq, ldw, x = quant_case((1 << 21) + dt, M, K, dt)
+    yref, S = oracle.gemv_q(Wq, BITS[dt], ldw, M, K, x)
+    for t in (None, dict(flags=1), dict(rows_per_wave=4, waves_per_block=4, unroll=1, flags=2)):
+        check(run_item(Wq, ldw, dt, x, M, K, t), yref, S, f"{M}x{K} {t}")
+    Wd = tvl.upload_quant(Wq, M, K, dt, ldw, DEV)
+    xd = torch.from_numpy(x).to(DEV)
+    yd = torch.full((M,), float("nan"), dtype=torch.float32, device=DEV)
+    plan = tvl.tvl_sweep_plan_create([(Wd.ptr, Wd.ldw, xd, yd, M, K, dt)])
+    try:
+        plan.run()
+        torch.cuda.synchronize()
+    finally:
+        plan.destroy()
+    check(yd.cpu().numpy(), yref, S, f"{M}x{K} plan")
+
+
+@pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
 def test_quant_wide_rows_and_junk_padding(dt):
     """ldw beyond the minimum, padding full of junk codes: never read into y."""
     for M, K, extra in ((65, 1000, 128), (3, 130, 1024), (100, 4095, 384)):
