@@ -345,6 +345,27 @@ def test_two_million_rows_every_output(dt):
         plan.destroy()
 
 
+def test_empty_sweeps_are_no_ops():
+    """A plan of no items has no tiles and runs as a no-op (no launch), also
+    under each kind of tuning; an empty batch sweep returns at once; the
+    stream stays usable and a following GEMV is exact."""
+    for tuning in (None, dict(flags=1), dict(flags=2),
+                   dict(rows_per_wave=4, waves_per_block=4, unroll=1, flags=2)):
+        plan = tvl.tvl_sweep_plan_create([], tuning)
+        try:
+            assert plan.info()["ntiles"] == 0
+            plan.run()
+            plan.run()
+        finally:
+            plan.destroy()
+    tvl.tvl_gemv_batch_sweep([])
+    torch.cuda.synchronize()
+    W = np.eye(64, dtype=np.float32)
+    x = np.arange(64, dtype=np.float32)
+    buf, ldw = dev_matrix(W, 0)
+    assert np.array_equal(run_gemv(buf, ldw, 0, x, 64, 64), x)
+
+
 def test_sweep_mixed_dtypes_and_ragged():
     rng = np.random.default_rng(11)
     specs = [(1, 1, 0), (3, 17, 1), (257, 255, 0), (65, 1000, 1), (1000, 65, 0),
