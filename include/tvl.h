@@ -328,7 +328,10 @@ TVL_API tvl_status tvl_gemv_batch_sweep(const tvl_item *items, int32_t n,
 
 /* Sweep plan: validate `items`, build the tile table (tiles of R*W output
  * rows; R/2*W for SwiGLU items; R*W*64/G for quantised items whose rows use
- * G lanes each; ordered by bytes per tile, largest first) and upload it once.  The item
+ * G lanes each; ordered by bytes per tile, largest first; in plans with
+ * several-vector or quantised items, each item's tiles are kept on as few
+ * of the GPU's XCDs as the largest-first order allows, so each XCD's L2
+ * fetches fewer x vectors) and upload it once.  The item
  * list is copied; the W, x, y buffers it names must stay valid for every
  * run.  `tuning` may be NULL.  The plan belongs to the device current at
  * creation.  Not while a stream of that device is being captured (the table
@@ -336,7 +339,8 @@ TVL_API tvl_status tvl_gemv_batch_sweep(const tvl_item *items, int32_t n,
 TVL_API tvl_status tvl_sweep_plan_create(const tvl_item *items, int32_t n,
                                          const tvl_tuning *tuning,
                                          tvl_plan **plan);
-/* Run a plan: exactly one kernel launch on `stream`. */
+/* Run a plan: exactly one kernel launch on `stream` (none for a plan of no
+ * items). */
 TVL_API tvl_status tvl_sweep_plan_run(const tvl_plan *plan, hipStream_t stream);
 /* Number of tiles and the launch grid of a plan (either pointer may be NULL). */
 TVL_API tvl_status tvl_sweep_plan_info(const tvl_plan *plan, int64_t *ntiles,
