@@ -12,6 +12,7 @@ plan while the stream is capturing is refused and enqueues nothing.
 from __future__ import annotations
 
 import ctypes
+import zlib
 
 import numpy as np
 import pytest
@@ -161,3 +162,99 @@ def test_capture_quantised_x_in_lds():
     del g
     torch.cuda.synchronize()
     plan.destroy()
+
+
+def f16_bits(w):
+    return torch.from_numpy(synth.f32_to_f16_bits(w).view(np.int16)).to(DEV)
+
+
+def plan_kind(kind, rng):
+    """(item dicts, outputs, kept buffers, tuning) of one plan kind."""
+    items, outs, keep = [], [], []
+
+    def out(n):
+        y = torch.full((n,), float("nan"), device=DEV)
+        outs.append(y)
+        return y
+
+    def vec(n):
+        v = torch.from_numpy(rng.standard_normal(n).astype(np.float32)).to(DEV)
+        keep.append(v)
+        return v
+
+    def mat(M, K, dt):
+        w = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+        d = torch.from_numpy(w).to(DEV) if dt == 0 else f16_bits(w)
+        keep.append(d)
+        return d
+
+    tuning = None
+    if kind in ("plain", "plain-lds"):
+        for M, K, dt in ((768, 768, 0), (2048, 768, 0), (300, 1024, 1), (129, 4096, 0)):
+            items.append(dict(W=mat(M, K, dt), ldw=K, x=vec(K), y=out(M), M=M, K=K, dtype=dt))
+        tuning = dict(flags=1) if kind == "plain-lds" else None
+    elif kind == "fused":
+        K = 768
+        g = vec(K)
+        items.append(dict(W=mat(768, K, 0), ldw=K, x=vec(K), y=out(768), M=768, K=K, dtype=0,
+                          g=g, eps=1e-5))
+        items.append(dict(W=mat(2048, K, 0), ldw=K, x=vec(K), y=out(2048), M=2048, K=K, dtype=0,
+                          op=tvl.TVL_OP_SWIGLU, W3=mat(2048, K, 0), g=g, eps=1e-5))
+        items.append(dict(W=mat(512, 2048, 1), ldw=2048, x=vec(2048), y=out(512), M=512,
+                          K=2048, dtype=1))
+    else:  # several vectors: fp32 on the shared-x matrix-core form, fp16 with
+        # split x, mixed weights, and the vector ALUs
+        nb, dts = {"multi-f32-16": (16, (0, 0)), "multi-f16-8": (8, (1, 1)),
+                   "multi-mixed-8": (8, (0, 1)), "multi-4": (4, (0, 1))}[kind]
+        for (M, K), dt in zip(((768, 768), (2048, 2048)), dts):
+            ldx, ldy = K + 4, M + 8
+            X = vec(nb * ldx)
+            Y = torch.full((nb * ldy,), float("nan"), device=DEV)
+            outs.append(Y)
+            items.append(dict(W=mat(M, K, dt), ldw=K, x=X, y=Y, M=M, K=K, dtype=dt, nrhs=nb,
+                              ldx=ldx, ldy=ldy))
+    return items, outs, keep, tuning
+
+
+@pytest.mark.parametrize("kind", ["plain", "plain-lds", "fused", "multi-f32-16", "multi-f16-8",
+                                  "multi-mixed-8", "multi-4"])
+def test_capture_every_plan_kind(kind):
+    """A plan of each kind (plain fp32/fp16 in both x modes, RMSNorm and
+    SwiGLU items, several vectors through each default form: shared x with
+    weights streamed into LDS, split x on the fp16 matrix cores, mixed
+    weights, the vector ALUs) run twice inside one captured HIP graph: five
+    replays, with eager runs and synchronisations between them, each equal
+    to the eager result bit for bit."""
+    rng = np.random.default_rng(zlib.crc32(kind.encode()))
+    items, outs, keep, tuning = plan_kind(kind, rng)
+    s = torch.cuda.Stream()
+    sid = int(s.cuda_stream)
+    plan = tvl.tvl_sweep_plan_create(items, tuning)
+    try:
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            plan.run(sid)
+        s.synchronize()
+        eager = [y.clone() for y in outs]
+        assert all(bool(torch.isfinite(e).any()) for e in eager)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            plan.run(sid)
+            plan.run(sid)
+        for rep in range(5):
+            for y in outs:
+                y.fill_(float("nan"))
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            for y, e in zip(outs, eager):  # bit patterns: unwritten gaps stay NaN
+                assert torch.equal(y.view(torch.int32), e.view(torch.int32)), (kind, rep)
+            with torch.cuda.stream(s):  # eager work between replays
+                plan.run(sid)
+            s.synchronize()
+            for y, e in zip(outs, eager):
+                assert torch.equal(y.view(torch.int32), e.view(torch.int32)), (kind, rep)
+        del g
+        torch.cuda.synchronize()
+    finally:
+        plan.destroy()
