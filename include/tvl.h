@@ -21,6 +21,11 @@
  *     16-byte load may touch it).  Elements K..ldw-1 of a row are padding;
  *     their values are never used (they may even hold NaN).
  *   - y is overwritten ("xout = W @ x"); its previous contents are ignored.
+ *   - Non-finite x: a NaN in x makes every output NaN; an infinite x_j gives
+ *     y_i = +-inf by the sign of W_ij, or NaN where W_ij = 0, as IEEE
+ *     arithmetic does, in every form whose products are fp32 (all forms but
+ *     the fp16 matrix-core form with split x, which is specified for finite
+ *     x only; see tvl_item).
  *   - Summation order differs from the sequential loop (Sec. 5.2 accepts the
  *     drift of reordered fused multiply-add accumulation).  Each output is
  *     the sum of 256 interleaved fp32 partial sums (64 lanes x 4) joined by

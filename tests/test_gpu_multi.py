@@ -107,6 +107,35 @@ def test_multi_million_rows(dt, nrhs):
         assert r["bad"] == 0, (M, K, nrhs, b, r)
 
 
+@pytest.mark.parametrize("dt,nrhs", [(0, 3), (0, 8), (0, 16), (1, 3)],
+                         ids=["f32-3", "f32-8", "f32-16", "f16-3"])
+def test_multi_inf_in_x_gives_ieee_results(dt, nrhs):
+    """+inf in one column of one vector: that vector's outputs are +inf,
+    -inf or NaN exactly as IEEE arithmetic gives them (the sign of the
+    weight in that column, NaN where it is 0), the other vectors' stay
+    finite; every form with fp32 products (the vector ALUs, the fp32
+    matrix cores; fp16 weights on the vector ALUs).  The fp16 matrix-core
+    form with split x holds for finite x only."""
+    rng = np.random.default_rng(41 + 10 * dt + nrhs)
+    M, K = 301, 1001
+    ts = tunings(nrhs) if dt == 0 else [t for t in tunings(nrhs)
+                                        if t is None or t["unroll"] < 10]
+    for col in (0, 517, K - 1):
+        Wf = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+        Wf[:, col] = np.tile(np.float32([0.5, -0.25, 0.0]), M // 3 + 1)[:M]
+        W = Wf if dt == 0 else synth.f32_to_f16_bits(Wf)
+        X = rng.standard_normal((nrhs, K)).astype(np.float32)
+        X[1, col] = np.inf
+        want = np.tile(np.int8([1, -1, 0]), M // 3 + 1)[:M]
+        buf, ldw = dev_matrix(W, dt)
+        for t in ts:
+            Y = run(buf, ldw, dt, X, M, K, nrhs, M + 3, t)
+            cls = np.where(np.isnan(Y), 0, np.where(np.isinf(Y), np.sign(Y), 2)).astype(np.int8)
+            assert np.array_equal(cls[1], want), (col, t)
+            others = np.delete(cls, 1, axis=0)
+            assert np.all(others == 2), (col, t)
+
+
 def test_multi_matches_single_bitwise_on_integers():
     """Integer data: every vector's result is exact, so it equals the
     single-vector result bit for bit."""

@@ -235,6 +235,39 @@ def test_nan_in_x_propagates():
         assert np.all(np.isnan(y)), vname(v)
 
 
+def ieee_class(y):
+    """-1 / +1 for -inf / +inf, 0 for NaN, 2 for finite."""
+    return np.where(np.isnan(y), 0, np.where(np.isinf(y), np.sign(y), 2)).astype(np.int8)
+
+
+def inf_case(rng, M, K, col):
+    """Weights whose column `col` is positive, negative or zero by row, x with
+    +inf there: y_i is +inf, -inf or NaN (0 * inf) by IEEE whatever the
+    order of the sum (the other terms are finite)."""
+    W = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    W[:, col] = np.tile(np.float32([0.5, -0.25, 0.0]), M // 3 + 1)[:M]
+    x = rng.standard_normal(K).astype(np.float32)
+    x[col] = np.inf
+    want = np.tile(np.int8([1, -1, 0]), M // 3 + 1)[:M]
+    return W, x, want
+
+
+@pytest.mark.parametrize("dt", [0, 1], ids=["f32", "f16"])
+def test_inf_in_x_gives_ieee_results(dt):
+    """+inf in x: every plain variant gives +inf, -inf or NaN exactly where
+    IEEE arithmetic does (the sign of the weight in that column; NaN where
+    it is 0), with the inf in the first, a middle and the ragged last chunk."""
+    rng = np.random.default_rng(77 + dt)
+    M, K = 301, 1001
+    for col in (0, 517, K - 1):
+        W, x, want = inf_case(rng, M, K, col)
+        Wd = W if dt == 0 else synth.f32_to_f16_bits(W)
+        buf, ldw = dev_matrix(Wd, dt)
+        for v in VARIANTS:
+            y = run_gemv(buf, ldw, dt, x, M, K, v)
+            assert np.array_equal(ieee_class(y), want), (col, vname(v))
+
+
 def test_output_overwritten_and_rerun_bitwise():
     """y is overwritten whatever it held; 10 reruns of each variant are
     bitwise identical (the K-split combine has a fixed order)."""

@@ -204,6 +204,31 @@ def test_quant_two_million_rows(dt):
 
 
 @pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
+def test_quant_inf_in_x_gives_ieee_results(dt):
+    """+inf in x: rows whose code in that column is positive, negative or 0
+    give +inf, -inf or NaN (0 * inf), as IEEE arithmetic on the decoded
+    weights does; every shape, direct x and x in LDS."""
+    rng = np.random.default_rng(5 + dt)
+    M, K = 301, 1001
+    tunings = [None] + [dict(rows_per_wave=r, waves_per_block=w_, unroll=u, flags=2)
+                        for r, w_, u in QUANT_SHAPES] + \
+        [dict(rows_per_wave=r, waves_per_block=w_, unroll=u, flags=1)
+         for r, w_, u in QUANT_LDS_SHAPES]
+    for col in (0, 517, K - 1):
+        w = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+        w[:, col] = np.tile(np.float32([0.05, -0.05, 0.0]), M // 3 + 1)[:M]
+        x = rng.standard_normal(K).astype(np.float32)
+        x[col] = np.inf
+        ldw = tvl.tvl_row_stride(K, dt)
+        Wq = synth.quantize_rows(w, BITS[dt], ldw=ldw)
+        want = np.tile(np.int8([1, -1, 0]), M // 3 + 1)[:M]
+        for t in tunings:
+            y = run_item(Wq, ldw, dt, x, M, K, t)
+            cls = np.where(np.isnan(y), 0, np.where(np.isinf(y), np.sign(y), 2)).astype(np.int8)
+            assert np.array_equal(cls, want), (col, t)
+
+
+@pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
 def test_quant_wide_rows_and_junk_padding(dt):
     """ldw beyond the minimum, padding full of junk codes: never read into y."""
     for M, K, extra in ((65, 1000, 128), (3, 130, 1024), (100, 4095, 384)):
