@@ -25,7 +25,8 @@
  *     y_i = +-inf by the sign of W_ij, or NaN where W_ij = 0, as IEEE
  *     arithmetic does, in every form whose products are fp32 (all forms but
  *     the fp16 matrix-core form with split x, which is specified for finite
- *     x only; see tvl_item).
+ *     x only; see tvl_item).  With RMSNorm (tvl_item) the normalised x is
+ *     NaN at j and 0 elsewhere, so every output is NaN.
  *   - Summation order differs from the sequential loop (Sec. 5.2 accepts the
  *     drift of reordered fused multiply-add accumulation).  Each output is
  *     the sum of 256 interleaved fp32 partial sums (64 lanes x 4) joined by

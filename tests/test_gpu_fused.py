@@ -112,6 +112,49 @@ def test_swiglu_item(M, K, norm, dt):
         check_swiglu(y.cpu().numpy(), href, bound, dt, f"swiglu {M}x{K} norm={norm} {t}")
 
 
+def ieee_class(y):
+    """-1 / +1 for -inf / +inf, 0 for NaN, 2 for finite."""
+    y = np.asarray(y, np.float64)
+    return np.where(np.isnan(y), 0, np.where(np.isinf(y), np.sign(y), 2)).astype(np.int8)
+
+
+@pytest.mark.parametrize("dt", [0, 1], ids=["f32", "f16"])
+def test_fused_inf_in_x_matches_the_oracle(dt):
+    """+inf in x, fused items: with RMSNorm the normalised x is NaN at that
+    column and 0 elsewhere, so every output is NaN; a SwiGLU pair without
+    RMSNorm gives silu(a) * b with a, b = +-inf or NaN by the weights' signs
+    (silu(-inf) is NaN, silu(+inf) = +inf).  The GPU's +inf / -inf / NaN /
+    finite pattern must equal the oracle's, every fused shape."""
+    rng = np.random.default_rng(606 + dt)
+    M, K, col = 301, 1001, 517
+    W1 = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    W3 = (rng.standard_normal((M, K)) * 0.02).astype(np.float32)
+    W1[:, col] = np.tile(np.float32([0.5, -0.25, 0.0]), M // 3 + 1)[:M]
+    W3[:, col] = np.tile(np.float32([0.5, 0.5, -0.5, 0.0]), M // 4 + 1)[:M]
+    if dt == 1:
+        W1, W3 = synth.f32_to_f16_bits(W1), synth.f32_to_f16_bits(W3)
+    x = rng.standard_normal(K).astype(np.float32)
+    x[col] = np.inf
+    g = rng.uniform(0.5, 1.5, K).astype(np.float32)
+    yref, _ = oracle.rmsnorm_gemv(W1, x, g, 1e-5)
+    href = oracle.swiglu_ffn_in(W1, W3, x, None, 1e-5)[0]
+    assert np.all(np.isnan(yref))
+    want = ieee_class(href)
+    assert set(np.unique(want)) == {-1, 0, 1}
+    b1, ldw = dev_matrix(W1, dt)
+    b3, _ = dev_matrix(W3, dt)
+    xd, gd = torch.from_numpy(x).to(DEV), torch.from_numpy(g).to(DEV)
+    for t in TUNINGS:
+        y = torch.full((M,), 0.0, device=DEV)
+        tvl.tvl_gemv_item(dict(W=b1, ldw=ldw, x=xd, y=y, M=M, K=K, dtype=dt, g=gd, eps=1e-5), t)
+        h = torch.full((M,), 0.0, device=DEV)
+        tvl.tvl_gemv_item(dict(W=b1, ldw=ldw, x=xd, y=h, M=M, K=K, dtype=dt,
+                               op=tvl.TVL_OP_SWIGLU, W3=b3), t)
+        torch.cuda.synchronize()
+        assert np.all(np.isnan(y.cpu().numpy())), t
+        assert np.array_equal(ieee_class(h.cpu().numpy()), want), t
+
+
 def test_fused_closed_forms():
     """Exact cases: identity W after RMSNorm of a +-1 vector (mean square 1,
     eps 0) gives g * x bitwise; a zero W3 row gives h = 0; a saturated gate
