@@ -136,6 +136,27 @@ def test_multi_inf_in_x_gives_ieee_results(dt, nrhs):
             assert np.all(others == 2), (col, t)
 
 
+@pytest.mark.parametrize("dt", [0, 1], ids=["f32", "f16"])
+@pytest.mark.parametrize("nrhs", [3, 8, 16])
+def test_multi_subnormal_x(nrhs, dt):
+    """Weights of small integers and subnormal x (k 2^-140): every product
+    and partial sum is exact only if subnormals are kept; every form must
+    equal the oracle bit for bit (with fp16 weights on the fp16 matrix
+    cores each chunk's range is too wide for the split: the chunk runs on
+    the fp32 matrix cores)."""
+    rng = np.random.default_rng(1400 + nrhs + 7 * dt)
+    M, K = 301, 1001
+    Wi = rng.integers(-4, 5, (M, K)).astype(np.float32)
+    W = Wi if dt == 0 else synth.f32_to_f16_bits(Wi)
+    X = (rng.integers(-100, 101, (nrhs, K)) * 2.0 ** -140).astype(np.float32)
+    refs = [oracle.gemv_f32(Wi, X[b])[0] for b in range(nrhs)]
+    buf, ldw = dev_matrix(W, dt)
+    for t in tunings(nrhs):
+        Y = run(buf, ldw, dt, X, M, K, nrhs, M + 3, t)
+        for b in range(nrhs):
+            assert np.array_equal(Y[b].astype(np.float64), refs[b]), (nrhs, b, t)
+
+
 def test_multi_matches_single_bitwise_on_integers():
     """Integer data: every vector's result is exact, so it equals the
     single-vector result bit for bit."""

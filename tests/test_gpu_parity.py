@@ -268,6 +268,27 @@ def test_inf_in_x_gives_ieee_results(dt):
             assert np.array_equal(ieee_class(y), want), (col, vname(v))
 
 
+@pytest.mark.parametrize("dt", [0, 1], ids=["f32", "f16"])
+def test_subnormal_x_not_flushed(dt):
+    """x_j = k_j 2^-140 (fp32 subnormals) and integer weights: every product
+    and every partial sum is a multiple of 2^-149 below 2^-116, so the sums
+    are exact in fp32 only if subnormal x, products and partial sums are
+    kept (not flushed to zero); each plain variant must equal the oracle
+    bit for bit."""
+    rng = np.random.default_rng(140 + dt)
+    M, K = 257, 1001
+    Wi = rng.integers(-4, 5, (M, K)).astype(np.float32)
+    W = Wi if dt == 0 else synth.f32_to_f16_bits(Wi)
+    x = (rng.integers(-100, 101, K) * 2.0 ** -140).astype(np.float32)
+    assert np.all(np.abs(x[x != 0]) < np.finfo(np.float32).tiny)
+    yref, _ = ref(W, x, dt)
+    assert np.any(yref != 0)
+    buf, ldw = dev_matrix(W, dt)
+    for v in VARIANTS:
+        y = run_gemv(buf, ldw, dt, x, M, K, v)
+        assert np.array_equal(y.astype(np.float64), yref), vname(v)
+
+
 def test_output_overwritten_and_rerun_bitwise():
     """y is overwritten whatever it held; 10 reruns of each variant are
     bitwise identical (the K-split combine has a fixed order)."""
