@@ -240,8 +240,9 @@ def test_quant_wide_rows_and_junk_padding(dt):
 
 @pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
 def test_quant_exact_on_integers(dt):
-    """Codes over the full range, power-of-two scales, integer x: the result
-    is exact, so it must equal the oracle bit for bit."""
+    """Codes over the full range, power-of-two scales, integer x (and the
+    same x scaled into the fp32 subnormals): the result is exact, so it must
+    equal the oracle bit for bit."""
     bits = BITS[dt]
     for M, K in ((77, 4096), (5, 3000), (300, 129)):
         rng = np.random.default_rng(M * K + bits)
@@ -262,6 +263,14 @@ def test_quant_exact_on_integers(dt):
         yref, _ = oracle.gemv_q(Wq, bits, ldw, M, K, x)
         y = run_item(Wq, ldw, dt, x, M, K)
         assert np.array_equal(y.astype(np.float64), yref), f"{M}x{K}"
+        # the same with subnormal x (k 2^-140): exact only if subnormal x,
+        # products and partial sums are kept, direct x and x in LDS
+        xs = (x * 2.0 ** -140).astype(np.float32)
+        yref, _ = oracle.gemv_q(Wq, bits, ldw, M, K, xs)
+        assert np.array_equal(yref.astype(np.float32).astype(np.float64), yref)
+        for t in (None, dict(flags=1), dict(flags=2)):
+            y = run_item(Wq, ldw, dt, xs, M, K, t)
+            assert np.array_equal(y.astype(np.float64), yref), f"{M}x{K} subnormal x {t}"
 
 
 @pytest.mark.parametrize("dt", [tvl.TVL_Q8, tvl.TVL_Q4], ids=["q8", "q4"])
