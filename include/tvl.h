@@ -232,7 +232,7 @@ typedef struct tvl_item {
  * Launches holding block-quantised items (R rows per group of lanes, see
  * tvl_dtype): direct-x (2,4,2) (4,4,1) (4,4,2) (4,1,2) (8,4,1) (8,2,1);
  * x in LDS (TVL_FLAG_X_LDS; a tuning that sets only the flag keeps the
- * default rows and waves) (4,4,1) (8,4,1) (8,2,1). */
+ * default rows and waves) (4,4,1) (8,4,1) (8,2,1) (4,4,2). */
 typedef struct tvl_tuning {
     int32_t rows_per_wave;
     int32_t waves_per_block;

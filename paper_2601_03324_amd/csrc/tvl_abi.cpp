@@ -405,18 +405,22 @@ Shape default_fused_shape(double bytes_f16, double bytes_f32)
 // lane group, except for 8-bit launches of under 1 GB of codes, which get 4
 // (twice the wavefronts for a launch too short to reach full bandwidth;
 // 110M token: 5.64 against 5.34-5.38 TB/s; 7B: 6.34 against 6.51, 4-bit 7B:
-// 4.16 against 5.73, 4-bit 110M: 3.14 against 3.82).  4-bit launches of
-// >= 1 GB of codes (8-lane groups) read x from LDS, staged once per row
-// tile, when it fits three workgroups per CU (K <= 13,312): their x loads
-// were as many as their code loads (7B 4-bit token: 6.61 against 6.35
-// TB/s; the 8-bit 7B token 6.96 against 7.01 and the 110M tokens -1 to -2 %
-// with x in LDS, so they keep direct x).  qbytes: code bytes of the launch's
-// quantised items; q4: any of them 4-bit; kq: their largest K.
+// 4.16 against 5.73, 4-bit 110M: 3.14 against 3.82).  Launches of >= 1 GB
+// of codes read x from LDS, staged once per row tile, when it fits three
+// workgroups per CU (K <= 13,312): 4-bit ones (8-lane groups, whose x loads
+// were as many as their code loads) at 8 rows, one chunk in flight (7B
+// 4-bit token: 6.61 against 6.35 TB/s); 8-bit ones at 4 rows with two
+// chunks in flight, which x in LDS leaves room for in registers (7B 8-bit
+// token: 7.12-7.13 against 7.00-7.01 TB/s at (8, 4, 1) with direct x, 6.96
+// at (8, 4, 1) with x in LDS, 6.54 at (4, 4, 2) with direct x).  The 110M
+// tokens are 1-2 % slower with x in LDS and keep direct x.  qbytes: code
+// bytes of the launch's quantised items; q4: any of them 4-bit; kq: their
+// largest K.
 Shape default_quant_shape(double qbytes, bool q4, int64_t kq)
 {
     if (!q4 && qbytes < 1e9) return Shape{4, 4, 1, tvl::kXDirect};
-    if (q4 && qbytes >= 1e9 && tvl::quant_x_lds_bytes(kq) <= 52 * 1024)
-        return Shape{8, 4, 1, tvl::kXLds};
+    if (qbytes >= 1e9 && tvl::quant_x_lds_bytes(kq) <= 52 * 1024)
+        return q4 ? Shape{8, 4, 1, tvl::kXLds} : Shape{4, 4, 2, tvl::kXLds};
     return Shape{8, 4, 1, tvl::kXDirect};
 }
 

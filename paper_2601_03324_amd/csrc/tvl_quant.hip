@@ -227,9 +227,12 @@ struct QuantRows {
         }
     }
 
-    // Full chunks from c in batches of U (all loads of a batch issued first).
+    // Full chunks from c in batches of U (all code loads of a batch issued
+    // first; x with them, or with x in LDS and U > 1 read just before each
+    // chunk's decode, so that it holds no VGPRs while the codes are in flight).
     __device__ __forceinline__ void run_batched(float (&acc)[R], int c = 0) const
     {
+        constexpr bool LAZY_X = XL && U > 1;
         for (; c + U <= nfull; c += U) {
             u4 w[U][R];
             float sc[U][R];
@@ -237,12 +240,14 @@ struct QuantRows {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 load_codes(c + u, w[u], sc[u]);
-                load_x(c + u, xv[u]);
+                if constexpr (!LAZY_X) load_x(c + u, xv[u]);
             }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int u = 0; u < U; ++u)
+            for (int u = 0; u < U; ++u) {
+                if constexpr (LAZY_X) load_x(c + u, xv[u]);
                 compute(acc, w[u], sc[u], xv[u]);
+            }
         }
         for (; c < nfull; ++c) {
             u4 w[R];
@@ -375,7 +380,7 @@ __device__ __forceinline__ void tile_quant_g(const DevItem &it, int row0, TVL_LD
     const QuantRows<BITS, G, R, U, XL> qr(codes + (int64_t)wrow0 * it.ldw,
                                           (int64_t)rows_left * it.ldw, plane, (int64_t)4 * Mp * ng,
                                           it.ldw, ng, lrow, wrow0 + sub * R, it.x, it.K, seg, xl);
-    if constexpr (XL) {
+    if constexpr (XL && U == 1) {
         // the first chunk's codes in flight while x is staged (the wait for
         // the x loads, issued after them, covers both).  Loaded whether or
         // not the row has a full chunk (then unused): a 16-byte load per row
@@ -387,6 +392,9 @@ __device__ __forceinline__ void tile_quant_g(const DevItem &it, int row0, TVL_LD
         stage_x_quant<WV>(it, xl);
         __builtin_amdgcn_sched_barrier(0);
         qr.run_preloaded(acc, w0, sc0);
+    } else if constexpr (XL) {
+        stage_x_quant<WV>(it, xl);
+        qr.run(acc);
     } else {
         qr.run(acc);
     }
@@ -450,7 +458,7 @@ __global__ __launch_bounds__(WV *kWave) void k_item_quant(const DevItem it)
 // direct-x, and with x staged in LDS.
 #define TVL_QUANT_SHAPES(X)                                                                       \
     X(2, 4, 2) X(4, 4, 1) X(4, 4, 2) X(4, 1, 2) X(8, 4, 1) X(8, 2, 1)
-#define TVL_QUANT_LDS_SHAPES(X) X(4, 4, 1) X(8, 4, 1) X(8, 2, 1)
+#define TVL_QUANT_LDS_SHAPES(X) X(4, 4, 1) X(8, 4, 1) X(8, 2, 1) X(4, 4, 2)
 
 template <int R, int WV, int U, bool XL>
 struct InstQuant {

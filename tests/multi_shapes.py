@@ -35,4 +35,4 @@ FUSED_SHAPES = [(2, 4, 2), (2, 4, 3), (2, 4, 4), (2, 1, 4), (4, 1, 2), (4, 1, 4)
 # launches holding block-quantised items: (R, waves per block, U), direct x
 # and x staged in LDS (TVL_FLAG_X_LDS)
 QUANT_SHAPES = [(2, 4, 2), (4, 4, 1), (4, 4, 2), (4, 1, 2), (8, 4, 1), (8, 2, 1)]
-QUANT_LDS_SHAPES = [(4, 4, 1), (8, 4, 1), (8, 2, 1)]
+QUANT_LDS_SHAPES = [(4, 4, 1), (8, 4, 1), (8, 2, 1), (4, 4, 2)]

@@ -162,7 +162,7 @@ REJECTS = [
     (dict(W=0), NULL), (dict(x=0), NULL), (dict(y=0), NULL),
     (dict(dt=4), DTYPE), (dict(dt=-1), DTYPE),
     (dict(dt=2, ldw=640), SHAPE), (dict(dt=3, ldw=256), SHAPE), (dict(dt=2, ldw=896, tuning=dict(ksplit=2)), ARG),
-    # quantised weights with x in LDS: only (4,4,1) (8,4,1) (8,2,1), and x of
+    # quantised weights with x in LDS: only (4,4,1) (8,4,1) (8,2,1) (4,4,2), and x of
     # K columns in whole KiB within 160 KB (K <= 40,960)
     (dict(dt=3, ldw=512, tuning=dict(rows_per_wave=2, waves_per_block=4, unroll=2, flags=1)),
      ARG),
